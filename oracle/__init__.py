@@ -1,0 +1,6 @@
+"""CPU oracle for the centroid + residual LoRA apply (test infrastructure only).
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s ``cpu_baseline``
+leg may import this package.  The product path never imports or calls it.
+"""
+from .ref import adapter_bytes, apply, decode, plan  # noqa: F401
