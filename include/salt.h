@@ -1,0 +1,188 @@
+/*
+ * libsalt -- batched centroid + residual LoRA apply for MI355X (gfx950).
+ *
+ * The serving-time composition of SALT ("Pin Once, Swap Light", Sec. 3.3): the
+ * weight served to request i is W_base + gamma * Wbar + delta_i, where the domain
+ * centroid Wbar is a high-rank LoRA that stays pinned in GPU memory (Sec. 3.1)
+ * and the user residual delta_i is a rank <= 2 LoRA that is swapped in from host
+ * memory on demand (Sec. 3.1, Sec. 4.4).  With y already holding x * W_base, the
+ * library adds, for every token t of a mixed batch,
+ *
+ *     y_t += gamma_t * (x_t A_{c_t}) B_{c_t}  +  (x_t A_{u_t}) B_{u_t}
+ *
+ * (row vectors; A is in x r, B is r x out; c_t = centroid id, u_t = residual slot).
+ *
+ * Conventions for every entry point
+ *   - Returns a salt_status; no exception or abort crosses the ABI.
+ *   - An invalid call (SALT_ERR_INVALID_ARG, _OUT_OF_RANGE, _NOT_PINNED,
+ *     _SLOT_EMPTY) changes no state.  A failing HIP call returns SALT_ERR_HIP and
+ *     poisons the context: every later call on it returns SALT_ERR_BAD_STATE.
+ *     salt_last_error() gives a message for the last failure.
+ *   - A context is externally synchronised (not thread-safe).
+ *   - "stream" arguments are hipStream_t values passed as void*; NULL is the
+ *     legacy default stream.  Work is enqueued asynchronously unless stated.
+ *   - Adapter layout is rank-major: A is stored transposed, At[r][in], and B as
+ *     B[r][out], both row-major in the context dtype.  Concatenating a centroid
+ *     and a residual (the single r_c + r_u adapter of Sec. 3.3) is then a stack
+ *     of rows.
+ *   - in_dim and out_dim must be multiples of 8; x, y and every host buffer must
+ *     be 16-byte aligned.
+ */
+#ifndef SALT_H_
+#define SALT_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SALT_VERSION 1
+
+#if defined(__GNUC__)
+#define SALT_API __attribute__((visibility("default")))
+#else
+#define SALT_API
+#endif
+
+typedef enum {
+  SALT_OK = 0,
+  SALT_ERR_INVALID_ARG = 1,   /* null pointer, bad size, misaligned buffer        */
+  SALT_ERR_OUT_OF_RANGE = 2,  /* table / centroid / slot / rank / token count     */
+  SALT_ERR_OUT_OF_MEMORY = 3, /* device or pinned allocation failed               */
+  SALT_ERR_NOT_PINNED = 4,    /* residual blob is not page-locked host memory     */
+  SALT_ERR_SLOT_EMPTY = 5,    /* a map references a slot that was never loaded    */
+  SALT_ERR_HIP = 6,           /* a HIP runtime call failed; the context is poisoned */
+  SALT_ERR_BAD_STATE = 7      /* poisoned context, stale plan, unpinned centroids */
+} salt_status;
+
+typedef enum { SALT_F32 = 0, SALT_BF16 = 1 } salt_dtype;
+
+/* One adapted linear projection ("table"): x[T][in_dim] -> y[T][out_dim]. */
+typedef struct {
+  int32_t in_dim;
+  int32_t out_dim;
+} salt_shape;
+
+typedef struct {
+  salt_dtype dtype;          /* storage type of x, y and every adapter; math is fp32 */
+  int32_t n_tables;          /* >= 1: projections served by this context            */
+  const salt_shape* tables;  /* [n_tables]; copied by salt_create                  */
+  int32_t n_centroids;       /* C in [0, 64]: centroid library size (Sec. 3.2)     */
+  int32_t r_c;               /* centroid rank in [0, 128] (0 iff C == 0)           */
+  int32_t n_slots;           /* residual slot-pool size, >= 1                      */
+  int32_t r_u_max;           /* largest residual rank a slot holds, in [0, 16]     */
+  int32_t max_tokens;        /* largest batch a plan accepts, in [1, 1 << 20]      */
+  int32_t device;            /* HIP device ordinal                                  */
+} salt_config;
+
+typedef struct salt_ctx salt_ctx;
+typedef struct salt_plan salt_plan;
+
+/* ---- context ----------------------------------------------------------------
+ * salt_create validates cfg, then allocates on cfg->device: the centroid store
+ * (per table, At[C][r_c][in] and B[C][r_c][out]), the residual slot pool
+ * (n_slots slots of salt_residual_bytes(ctx, r_u_max) bytes each) and a side
+ * stream for residual swaps.  The context owns all of these; salt_destroy waits
+ * for the context's outstanding work and frees them.  Fails with
+ * SALT_ERR_OUT_OF_MEMORY (nothing leaked) if the pool does not fit. */
+SALT_API salt_status salt_create(const salt_config* cfg, salt_ctx** out);
+SALT_API void salt_destroy(salt_ctx* ctx);
+
+/* Pin centroids c0 .. c0+n-1 of one table into device memory (Sec. 3.1: the
+ * centroid is pre-loaded and pinned; Sec. 3.3: done once at node start-up).
+ *   At_host: [n][r_c][in] host array (pageable is fine), B_host: [n][r_c][out].
+ * Blocking: the copy has completed when the call returns and the host arrays may
+ * be freed.  salt_apply on a table refuses to run (SALT_ERR_BAD_STATE) until all
+ * n_centroids of that table have been pinned at least once. */
+SALT_API salt_status salt_pin_centroids(salt_ctx* ctx, int32_t table, int32_t c0, int32_t n,
+                               const void* At_host, const void* B_host);
+
+/* Size in bytes of one user's residual blob of rank r_u over all tables of the
+ * context: r_u * sum_t(in_t + out_t) * element size (the per-adapter swap size
+ * of Table 1 and the appendix tables).  Returns 0 for an invalid rank. */
+SALT_API size_t salt_residual_bytes(const salt_ctx* ctx, int32_t r_u);
+/* Same count without a context (host-only; no HIP call). */
+SALT_API size_t salt_residual_bytes_for(salt_dtype dtype, int32_t n_tables, const salt_shape* tables,
+                               int32_t r_u);
+
+/* Swap one user's residual into a slot of the HBM pool (Sec. 3.1: only the
+ * residual is swapped; Sec. 4.4: the H2D PCIe transfer this minimises).
+ *   blob: page-locked host memory (salt_host_alloc / hipHostMalloc), laid out as,
+ *         for each table in order, At_u[r_u][in] followed by B_u[r_u][out];
+ *         bytes must equal salt_residual_bytes(ctx, r_u).  r_u == 0 empties the
+ *         residual term of the slot (bytes == 0, blob may be NULL).
+ * Asynchronous: one hipMemcpyAsync on the context's side stream.  The copy first
+ * waits for every enqueued salt_apply whose plan references this slot, so an
+ * in-flight apply still sees the slot's previous residual.  Every later
+ * salt_apply whose plan references the slot waits for this copy.  The blob must
+ * stay valid and unmodified until the copy completes (salt_wait_loads).
+ * Errors: SALT_ERR_OUT_OF_RANGE (slot, r_u > r_u_max), SALT_ERR_INVALID_ARG
+ * (bytes mismatch), SALT_ERR_NOT_PINNED (pageable blob; no synchronous fallback). */
+SALT_API salt_status salt_load_residual(salt_ctx* ctx, int32_t slot, int32_t r_u, const void* blob,
+                               size_t bytes);
+
+/* Block the host until every residual swap enqueued so far has completed. */
+SALT_API salt_status salt_wait_loads(salt_ctx* ctx);
+
+/* Page-locked host buffers for residual blobs (hipHostMalloc / hipHostFree). */
+SALT_API salt_status salt_host_alloc(size_t bytes, void** out);
+SALT_API void salt_host_free(void* p);
+
+/* ---- plans --------------------------------------------------------------------
+ * A plan is the canonical grouping of one batch (Sec. 3.3: the frontend groups
+ * requests by their centroid): tokens ordered by (centroid id, residual slot,
+ * token index) ascending, -1 first.  Built once per batch on the device, then
+ * reused by every table's salt_apply.  A plan owns device buffers sized for
+ * max_tokens, including the apply's scratch, so applies that share a plan must
+ * be ordered on one stream; use one plan per concurrently running stream. */
+SALT_API salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out);
+SALT_API void salt_plan_destroy(salt_ctx* ctx, salt_plan* plan);
+
+/* Stage a batch's maps (host arrays, pageable or pinned, read before return):
+ *   tok_c[T]: centroid id in [-1, C)        (-1: no centroid term)
+ *   tok_u[T]: residual slot in [-1, n_slots) (-1: no residual term)
+ *   tok_gamma[T]: centroid scale per token (Sec. 3.3's discrete gamma bins), or
+ *                 NULL for gamma = 1.  Must be finite.
+ * Validates the maps on the host (SALT_ERR_OUT_OF_RANGE, SALT_ERR_SLOT_EMPTY for
+ * a slot never loaded), snapshots the residual rank of every referenced slot and
+ * enqueues one H2D copy of the packed maps on `stream`.  0 <= T <= max_tokens;
+ * T == 0 gives an empty plan whose applies do nothing. */
+SALT_API salt_status salt_plan_set_maps(salt_ctx* ctx, salt_plan* plan, int32_t T, const int32_t* tok_c,
+                               const int32_t* tok_u, const float* tok_gamma, void* stream);
+
+/* Build the plan on the device from the staged maps (enqueued on `stream`):
+ * the sorted order, the segments of equal (centroid, slot) and the groups of
+ * equal centroid.  Integer work; the result is bit-exact and unique. */
+SALT_API salt_status salt_plan_build(salt_ctx* ctx, salt_plan* plan, void* stream);
+
+/* Copy a built plan to host arrays (synchronises `stream`).  Sizes: perm[T],
+ * seg_off[n_seg + 1], seg_c[n_seg], seg_u[n_seg], grp_off[n_grp + 1] where
+ * n_seg, n_grp <= T; pass arrays of T + 1 entries.  Any pointer may be NULL. */
+SALT_API salt_status salt_plan_download(salt_ctx* ctx, const salt_plan* plan, void* stream, int32_t* perm,
+                               int32_t* seg_off, int32_t* seg_c, int32_t* seg_u, int32_t* grp_off,
+                               int32_t* n_seg, int32_t* n_grp);
+
+/* ---- the hot path ---------------------------------------------------------------
+ * y[t] += gamma_t * (x[t] A_{c_t}) B_{c_t} + (x[t] A_{u_t}) B_{u_t} for one table,
+ * every token of a built plan (Sec. 3.3's served weight minus W_base).
+ *   x: device [T][in_dim], y: device [T][out_dim], context dtype, row-major,
+ *      16-byte aligned; y is read and written once per element, rounded once
+ *      (round-to-nearest-even) from fp32 y + fp32 delta.
+ * Accumulation is fp32.  Enqueued on `stream` after the swaps of every slot the
+ * plan references.  Errors: SALT_ERR_OUT_OF_RANGE (table), SALT_ERR_BAD_STATE
+ * (centroids of the table not pinned; a referenced slot was reloaded with a
+ * different rank after salt_plan_set_maps). */
+SALT_API salt_status salt_apply(salt_ctx* ctx, int32_t table, const salt_plan* plan, const void* x, void* y,
+                       void* stream);
+
+/* ---- diagnostics -------------------------------------------------------------------- */
+SALT_API const char* salt_status_str(salt_status s);
+SALT_API const char* salt_last_error(const salt_ctx* ctx);
+SALT_API int32_t salt_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SALT_H_ */

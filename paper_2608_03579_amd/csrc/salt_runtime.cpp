@@ -1,0 +1,578 @@
+// libsalt host runtime: the C ABI of include/salt.h.
+//
+// Owns the pinned centroid store, the residual slot pool, the side stream that
+// swaps residuals in, plan buffers, and the stream/event bookkeeping that keeps a
+// swap from overwriting a slot an in-flight apply still reads (Sec. 3.1 / 3.3:
+// pin the centroid once, swap only the rank <= 2 residual).
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/salt.h"
+#include "salt_internal.h"
+
+using salt::ApplyArgs;
+using salt::PlanBuffers;
+
+namespace {
+
+constexpr int kEvRing = 1024;         // reader / loader event rings
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+size_t esize_of(salt_dtype d) { return d == SALT_F32 ? 4 : 2; }
+
+// A ring of events with monotone sequence numbers.  Before slot k % N is
+// re-recorded, the event it held (sequence k - N) is synchronised, so every
+// sequence <= `done` is known complete.
+struct EventRing {
+  std::vector<hipEvent_t> ev;
+  int64_t next = 0;   // sequence number of the next record
+  int64_t done = -1;  // all sequences <= done have completed
+};
+
+}  // namespace
+
+struct salt_plan {
+  PlanBuffers dev{};
+  int4* staging = nullptr;          // pinned host copy of the maps
+  hipEvent_t staged = nullptr;      // recorded after the H2D copy of the maps
+  bool staged_pending = false;
+  int32_t T = 0;
+  bool built = false;
+  std::vector<int32_t> slots;       // distinct referenced slots
+  std::vector<int32_t> slot_rank;   // rank of each at set_maps time
+  int32_t n_centroid_groups_ub = 0;
+};
+
+struct salt_ctx {
+  salt_config cfg{};
+  std::vector<salt_shape> tables;
+  std::vector<int64_t> tab_prefix;       // sum of (in + out) over earlier tables
+  int64_t sum_io = 0;
+  size_t esize = 2;
+  int device = 0;
+  // device memory
+  std::vector<char*> cent_at, cent_b;    // per table
+  std::vector<uint8_t> cent_pinned;      // per table x centroid
+  char* pool = nullptr;
+  size_t slot_stride = 0;
+  hipStream_t side = nullptr;
+  // bookkeeping
+  std::vector<int32_t> slot_rank;        // -1 = never loaded
+  std::vector<int64_t> slot_reader;      // apply sequence of the last reader
+  std::vector<int64_t> slot_loader;      // load sequence of the last swap
+  EventRing readers, loaders;
+  std::vector<salt_plan*> plans;
+  bool poisoned = false;
+  std::string err;
+};
+
+namespace {
+
+// message of the last salt_create failure on this thread (salt_last_error(NULL))
+thread_local std::string g_create_err;
+
+salt_status fail(salt_ctx* c, salt_status s, const char* fmt, ...) {
+  if (c) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    c->err = buf;
+  }
+  return s;
+}
+
+salt_status hip_fail(salt_ctx* c, hipError_t e, const char* what) {
+  if (c) {
+    c->poisoned = true;
+    c->err = std::string(what) + ": " + hipGetErrorString(e);
+  }
+  return SALT_ERR_HIP;
+}
+
+#define SALT_HIP(ctx, call)                                   \
+  do {                                                        \
+    hipError_t e_ = (call);                                   \
+    if (e_ != hipSuccess) return hip_fail((ctx), e_, #call);  \
+  } while (0)
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+hipError_t ring_record(EventRing& r, hipStream_t s, int64_t* seq_out) {
+  const int64_t seq = r.next;
+  const int k = (int)(seq % (int64_t)r.ev.size());
+  if (seq >= (int64_t)r.ev.size() && seq - (int64_t)r.ev.size() > r.done) {
+    hipError_t e = hipEventSynchronize(r.ev[k]);
+    if (e != hipSuccess) return e;
+    r.done = seq - (int64_t)r.ev.size();
+  }
+  hipError_t e = hipEventRecord(r.ev[k], s);
+  if (e != hipSuccess) return e;
+  r.next = seq + 1;
+  *seq_out = seq;
+  return hipSuccess;
+}
+
+// Make `s` wait for sequence `seq` of ring `r` unless it is known complete.
+hipError_t ring_wait(EventRing& r, hipStream_t s, int64_t seq) {
+  if (seq < 0 || seq <= r.done) return hipSuccess;
+  return hipStreamWaitEvent(s, r.ev[(int)(seq % (int64_t)r.ev.size())], 0);
+}
+
+void free_plan_buffers(salt_plan* p) {
+  PlanBuffers& b = p->dev;
+  void* ptrs[] = {b.maps, b.perm, b.srt, b.srt_c, b.seg_off, b.seg_c, b.seg_u,
+                  b.grp_off, b.grp_tok, b.grp_c, b.meta, b.counter, b.partials};
+  for (void* q : ptrs)
+    if (q) (void)hipFree(q);
+  if (p->staging) (void)hipHostFree(p->staging);
+  if (p->staged) (void)hipEventDestroy(p->staged);
+}
+
+void destroy_ctx_memory(salt_ctx* c) {
+  for (char* p : c->cent_at)
+    if (p) (void)hipFree(p);
+  for (char* p : c->cent_b)
+    if (p) (void)hipFree(p);
+  if (c->pool) (void)hipFree(c->pool);
+  for (hipEvent_t e : c->readers.ev)
+    if (e) (void)hipEventDestroy(e);
+  for (hipEvent_t e : c->loaders.ev)
+    if (e) (void)hipEventDestroy(e);
+  if (c->side) (void)hipStreamDestroy(c->side);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* salt_status_str(salt_status s) {
+  switch (s) {
+    case SALT_OK: return "ok";
+    case SALT_ERR_INVALID_ARG: return "invalid argument";
+    case SALT_ERR_OUT_OF_RANGE: return "out of range";
+    case SALT_ERR_OUT_OF_MEMORY: return "out of memory";
+    case SALT_ERR_NOT_PINNED: return "residual blob is not page-locked";
+    case SALT_ERR_SLOT_EMPTY: return "slot was never loaded";
+    case SALT_ERR_HIP: return "HIP runtime error";
+    case SALT_ERR_BAD_STATE: return "bad state";
+  }
+  return "unknown status";
+}
+
+const char* salt_last_error(const salt_ctx* ctx) { return ctx ? ctx->err.c_str() : g_create_err.c_str(); }
+
+int32_t salt_version(void) { return SALT_VERSION; }
+
+size_t salt_residual_bytes_for(salt_dtype dtype, int32_t n_tables, const salt_shape* tables,
+                               int32_t r_u) {
+  if (!tables || n_tables <= 0 || r_u < 0 || (dtype != SALT_F32 && dtype != SALT_BF16)) return 0;
+  size_t sum = 0;
+  for (int i = 0; i < n_tables; ++i) {
+    if (tables[i].in_dim <= 0 || tables[i].out_dim <= 0) return 0;
+    sum += (size_t)tables[i].in_dim + (size_t)tables[i].out_dim;
+  }
+  return (size_t)r_u * sum * esize_of(dtype);
+}
+
+size_t salt_residual_bytes(const salt_ctx* ctx, int32_t r_u) {
+  if (!ctx || r_u < 0 || r_u > ctx->cfg.r_u_max) return 0;
+  return (size_t)r_u * (size_t)ctx->sum_io * ctx->esize;
+}
+
+salt_status salt_host_alloc(size_t bytes, void** out) {
+  if (!out || bytes == 0) return SALT_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (hipHostMalloc(out, bytes, hipHostMallocDefault) != hipSuccess) {
+    *out = nullptr;
+    return SALT_ERR_OUT_OF_MEMORY;
+  }
+  return SALT_OK;
+}
+
+void salt_host_free(void* p) {
+  if (p) (void)hipHostFree(p);
+}
+
+salt_status salt_create(const salt_config* cfg, salt_ctx** out) {
+  if (!cfg || !out) return SALT_ERR_INVALID_ARG;
+  *out = nullptr;
+  g_create_err = "invalid configuration";
+  if (cfg->dtype != SALT_F32 && cfg->dtype != SALT_BF16) return SALT_ERR_INVALID_ARG;
+  if (cfg->n_tables < 1 || !cfg->tables) return SALT_ERR_INVALID_ARG;
+  if (cfg->n_centroids < 0 || cfg->n_centroids > 64 || cfg->r_c < 0 || cfg->r_c > 128 ||
+      (cfg->n_centroids == 0) != (cfg->r_c == 0))
+    return SALT_ERR_OUT_OF_RANGE;
+  if (cfg->n_slots < 1 || cfg->n_slots > (1 << 20) || cfg->r_u_max < 0 || cfg->r_u_max > 16)
+    return SALT_ERR_OUT_OF_RANGE;
+  if (cfg->max_tokens < 1 || cfg->max_tokens > (1 << 20)) return SALT_ERR_OUT_OF_RANGE;
+  for (int i = 0; i < cfg->n_tables; ++i) {
+    const salt_shape s = cfg->tables[i];
+    if (s.in_dim <= 0 || s.out_dim <= 0 || s.in_dim % 8 || s.out_dim % 8 || s.in_dim > (1 << 20) ||
+        s.out_dim > (1 << 20))
+      return SALT_ERR_INVALID_ARG;
+  }
+  salt_ctx* c = new (std::nothrow) salt_ctx();
+  if (!c) return SALT_ERR_OUT_OF_MEMORY;
+  c->cfg = *cfg;
+  c->tables.assign(cfg->tables, cfg->tables + cfg->n_tables);
+  c->cfg.tables = c->tables.data();
+  c->esize = esize_of(cfg->dtype);
+  c->device = cfg->device;
+  int64_t acc = 0;
+  for (const salt_shape& s : c->tables) {
+    c->tab_prefix.push_back(acc);
+    acc += (int64_t)s.in_dim + s.out_dim;
+  }
+  c->sum_io = acc;
+
+  auto bail = [&](salt_status st, hipError_t e, const char* what) {
+    if (st == SALT_ERR_HIP) hip_fail(c, e, what);
+    else c->err = "device allocation failed";
+    g_create_err = c->err;
+    destroy_ctx_memory(c);
+    delete c;
+    return st;
+  };
+  hipError_t e = hipSetDevice(cfg->device);
+  if (e != hipSuccess) return bail(SALT_ERR_HIP, e, "hipSetDevice");
+  e = salt::kernels_init(cfg->device);
+  if (e != hipSuccess) return bail(SALT_ERR_HIP, e, "kernels_init");
+  const size_t C = (size_t)cfg->n_centroids, rc = (size_t)cfg->r_c;
+  c->cent_at.assign(cfg->n_tables, nullptr);
+  c->cent_b.assign(cfg->n_tables, nullptr);
+  c->cent_pinned.assign((size_t)cfg->n_tables * C, 0);
+  if (C > 0) {
+    for (int t = 0; t < cfg->n_tables; ++t) {
+      const salt_shape s = c->tables[t];
+      if (hipMalloc((void**)&c->cent_at[t], C * rc * s.in_dim * c->esize) != hipSuccess ||
+          hipMalloc((void**)&c->cent_b[t], C * rc * s.out_dim * c->esize) != hipSuccess) {
+        (void)hipGetLastError();
+        return bail(SALT_ERR_OUT_OF_MEMORY, hipSuccess, "");
+      }
+    }
+  }
+  c->slot_stride = round_up(std::max<size_t>(1, salt_residual_bytes(c, cfg->r_u_max)), kAlign);
+  if (hipMalloc((void**)&c->pool, c->slot_stride * (size_t)cfg->n_slots) != hipSuccess) {
+    (void)hipGetLastError();
+    return bail(SALT_ERR_OUT_OF_MEMORY, hipSuccess, "");
+  }
+  e = hipStreamCreateWithFlags(&c->side, hipStreamNonBlocking);
+  if (e != hipSuccess) return bail(SALT_ERR_HIP, e, "hipStreamCreateWithFlags");
+  c->readers.ev.assign(kEvRing, nullptr);
+  c->loaders.ev.assign(kEvRing, nullptr);
+  for (int i = 0; i < kEvRing; ++i) {
+    if ((e = hipEventCreateWithFlags(&c->readers.ev[i], hipEventDisableTiming)) != hipSuccess ||
+        (e = hipEventCreateWithFlags(&c->loaders.ev[i], hipEventDisableTiming)) != hipSuccess)
+      return bail(SALT_ERR_HIP, e, "hipEventCreateWithFlags");
+  }
+  c->slot_rank.assign(cfg->n_slots, -1);
+  c->slot_reader.assign(cfg->n_slots, -1);
+  c->slot_loader.assign(cfg->n_slots, -1);
+  g_create_err.clear();
+  *out = c;
+  return SALT_OK;
+}
+
+void salt_destroy(salt_ctx* ctx) {
+  if (!ctx) return;
+  (void)hipSetDevice(ctx->device);
+  (void)hipDeviceSynchronize();
+  for (salt_plan* p : ctx->plans) {
+    free_plan_buffers(p);
+    delete p;
+  }
+  destroy_ctx_memory(ctx);
+  delete ctx;
+}
+
+salt_status salt_pin_centroids(salt_ctx* ctx, int32_t table, int32_t c0, int32_t n,
+                               const void* At_host, const void* B_host) {
+  if (!ctx) return SALT_ERR_INVALID_ARG;
+  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  if (table < 0 || table >= ctx->cfg.n_tables)
+    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "table %d not in [0, %d)", table, ctx->cfg.n_tables);
+  if (n < 0 || c0 < 0 || c0 + n > ctx->cfg.n_centroids)
+    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "centroids [%d, %d) not in [0, %d)", c0, c0 + n,
+                ctx->cfg.n_centroids);
+  if (n == 0) return SALT_OK;
+  if (!At_host || !B_host) return fail(ctx, SALT_ERR_INVALID_ARG, "null centroid array");
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  const salt_shape s = ctx->tables[table];
+  const size_t rc = ctx->cfg.r_c, es = ctx->esize;
+  const size_t a_bytes = (size_t)n * rc * s.in_dim * es, b_bytes = (size_t)n * rc * s.out_dim * es;
+  SALT_HIP(ctx, hipMemcpy(ctx->cent_at[table] + (size_t)c0 * rc * s.in_dim * es, At_host, a_bytes,
+                          hipMemcpyHostToDevice));
+  SALT_HIP(ctx, hipMemcpy(ctx->cent_b[table] + (size_t)c0 * rc * s.out_dim * es, B_host, b_bytes,
+                          hipMemcpyHostToDevice));
+  for (int i = c0; i < c0 + n; ++i) ctx->cent_pinned[(size_t)table * ctx->cfg.n_centroids + i] = 1;
+  return SALT_OK;
+}
+
+salt_status salt_load_residual(salt_ctx* ctx, int32_t slot, int32_t r_u, const void* blob,
+                               size_t bytes) {
+  if (!ctx) return SALT_ERR_INVALID_ARG;
+  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  if (slot < 0 || slot >= ctx->cfg.n_slots)
+    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "slot %d not in [0, %d)", slot, ctx->cfg.n_slots);
+  if (r_u < 0 || r_u > ctx->cfg.r_u_max)
+    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "rank %d not in [0, %d]", r_u, ctx->cfg.r_u_max);
+  const size_t want = salt_residual_bytes(ctx, r_u);
+  if (bytes != want)
+    return fail(ctx, SALT_ERR_INVALID_ARG, "blob is %zu bytes, rank %d needs %zu", bytes, r_u, want);
+  if (want > 0) {
+    if (!blob || !aligned16(blob)) return fail(ctx, SALT_ERR_INVALID_ARG, "null or misaligned blob");
+    hipPointerAttribute_t attr;
+    hipError_t e = hipPointerGetAttributes(&attr, blob);
+    if (e != hipSuccess || attr.type != hipMemoryTypeHost) {
+      (void)hipGetLastError();
+      return fail(ctx, SALT_ERR_NOT_PINNED, "blob %p is not page-locked host memory", blob);
+    }
+  }
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  // the swap may not overwrite what an enqueued apply still reads
+  SALT_HIP(ctx, ring_wait(ctx->readers, ctx->side, ctx->slot_reader[slot]));
+  if (want > 0)
+    SALT_HIP(ctx, hipMemcpyAsync(ctx->pool + (size_t)slot * ctx->slot_stride, blob, want,
+                                 hipMemcpyHostToDevice, ctx->side));
+  int64_t seq;
+  SALT_HIP(ctx, ring_record(ctx->loaders, ctx->side, &seq));
+  ctx->slot_loader[slot] = seq;
+  ctx->slot_rank[slot] = r_u;
+  return SALT_OK;
+}
+
+salt_status salt_wait_loads(salt_ctx* ctx) {
+  if (!ctx) return SALT_ERR_INVALID_ARG;
+  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  SALT_HIP(ctx, hipStreamSynchronize(ctx->side));
+  ctx->loaders.done = ctx->loaders.next - 1;
+  return SALT_OK;
+}
+
+salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out) {
+  if (!ctx || !out) return SALT_ERR_INVALID_ARG;
+  *out = nullptr;
+  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  salt_plan* p = new (std::nothrow) salt_plan();
+  if (!p) return SALT_ERR_OUT_OF_MEMORY;
+  const size_t T = (size_t)ctx->cfg.max_tokens;
+  const size_t R = (size_t)ctx->cfg.r_c + ctx->cfg.r_u_max;
+  PlanBuffers& b = p->dev;
+  // split-K partials: enough for (splits x tokens) up to max(8 * max_tokens, 64K)
+  b.partial_cap = std::max<size_t>(8 * T, 65536) * std::max<size_t>(R, 1);
+  bool ok = hipMalloc((void**)&b.maps, T * sizeof(int4)) == hipSuccess &&
+            hipMalloc((void**)&b.perm, T * 4) == hipSuccess &&
+            hipMalloc((void**)&b.srt, T * sizeof(int4)) == hipSuccess &&
+            hipMalloc((void**)&b.srt_c, T * 4) == hipSuccess &&
+            hipMalloc((void**)&b.seg_off, (T + 1) * 4) == hipSuccess &&
+            hipMalloc((void**)&b.seg_c, T * 4) == hipSuccess &&
+            hipMalloc((void**)&b.seg_u, T * 4) == hipSuccess &&
+            hipMalloc((void**)&b.grp_off, (T + 1) * 4) == hipSuccess &&
+            hipMalloc((void**)&b.grp_tok, (T + 1) * 4) == hipSuccess &&
+            hipMalloc((void**)&b.grp_c, T * 4) == hipSuccess &&
+            hipMalloc((void**)&b.meta, 16 * 4) == hipSuccess &&
+            hipMalloc((void**)&b.counter, 64 * 4) == hipSuccess &&
+            hipMalloc((void**)&b.partials, b.partial_cap * 4) == hipSuccess &&
+            hipHostMalloc((void**)&p->staging, T * sizeof(int4), hipHostMallocDefault) == hipSuccess;
+  if (!ok) {
+    (void)hipGetLastError();
+    free_plan_buffers(p);
+    delete p;
+    return fail(ctx, SALT_ERR_OUT_OF_MEMORY, "plan buffers for %zu tokens do not fit", T);
+  }
+  hipError_t e = hipEventCreateWithFlags(&p->staged, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipMemset(b.counter, 0, 64 * 4);
+  if (e == hipSuccess) e = hipMemset(b.meta, 0, 16 * 4);
+  if (e != hipSuccess) {
+    free_plan_buffers(p);
+    delete p;
+    return hip_fail(ctx, e, "plan init");
+  }
+  ctx->plans.push_back(p);
+  *out = p;
+  return SALT_OK;
+}
+
+void salt_plan_destroy(salt_ctx* ctx, salt_plan* plan) {
+  if (!ctx || !plan) return;
+  auto it = std::find(ctx->plans.begin(), ctx->plans.end(), plan);
+  if (it == ctx->plans.end()) return;
+  (void)hipSetDevice(ctx->device);
+  (void)hipDeviceSynchronize();
+  ctx->plans.erase(it);
+  free_plan_buffers(plan);
+  delete plan;
+}
+
+salt_status salt_plan_set_maps(salt_ctx* ctx, salt_plan* plan, int32_t T, const int32_t* tok_c,
+                               const int32_t* tok_u, const float* tok_gamma, void* stream) {
+  if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
+  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  if (T < 0 || T > ctx->cfg.max_tokens)
+    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "T = %d not in [0, %d]", T, ctx->cfg.max_tokens);
+  if (T > 0 && (!tok_c || !tok_u)) return fail(ctx, SALT_ERR_INVALID_ARG, "null map");
+  const int C = ctx->cfg.n_centroids, S = ctx->cfg.n_slots;
+  for (int t = 0; t < T; ++t) {
+    if (tok_c[t] < -1 || tok_c[t] >= C)
+      return fail(ctx, SALT_ERR_OUT_OF_RANGE, "tok_c[%d] = %d not in [-1, %d)", t, tok_c[t], C);
+    if (tok_u[t] < -1 || tok_u[t] >= S)
+      return fail(ctx, SALT_ERR_OUT_OF_RANGE, "tok_u[%d] = %d not in [-1, %d)", t, tok_u[t], S);
+    if (tok_u[t] >= 0 && ctx->slot_rank[tok_u[t]] < 0)
+      return fail(ctx, SALT_ERR_SLOT_EMPTY, "tok_u[%d] = %d: slot never loaded", t, tok_u[t]);
+    if (tok_gamma && !std::isfinite(tok_gamma[t]))
+      return fail(ctx, SALT_ERR_INVALID_ARG, "tok_gamma[%d] is not finite", t);
+  }
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  hipStream_t s = (hipStream_t)stream;
+  // the staging buffer may still feed the previous copy
+  if (plan->staged_pending) {
+    SALT_HIP(ctx, hipEventSynchronize(plan->staged));
+    plan->staged_pending = false;
+  }
+  std::vector<int32_t> slots;
+  int cmin = C, cmax = -2;
+  for (int t = 0; t < T; ++t) {
+    const int u = tok_u[t];
+    const float g = tok_gamma ? tok_gamma[t] : 1.0f;
+    int32_t gbits;
+    std::memcpy(&gbits, &g, 4);
+    plan->staging[t] = make_int4(tok_c[t], u, u >= 0 ? ctx->slot_rank[u] : 0, gbits);
+    if (u >= 0) slots.push_back(u);
+    cmin = std::min(cmin, tok_c[t]);
+    cmax = std::max(cmax, tok_c[t]);
+  }
+  std::sort(slots.begin(), slots.end());
+  slots.erase(std::unique(slots.begin(), slots.end()), slots.end());
+  plan->slots = slots;
+  plan->slot_rank.resize(slots.size());
+  for (size_t i = 0; i < slots.size(); ++i) plan->slot_rank[i] = ctx->slot_rank[slots[i]];
+  plan->T = T;
+  plan->built = false;
+  plan->n_centroid_groups_ub = (T > 0) ? std::min(T, cmax - cmin + 1) : 0;
+  if (T > 0) {
+    SALT_HIP(ctx, hipMemcpyAsync(plan->dev.maps, plan->staging, (size_t)T * sizeof(int4),
+                                 hipMemcpyHostToDevice, s));
+    SALT_HIP(ctx, hipEventRecord(plan->staged, s));
+    plan->staged_pending = true;
+  }
+  return SALT_OK;
+}
+
+salt_status salt_plan_build(salt_ctx* ctx, salt_plan* plan, void* stream) {
+  if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
+  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  SALT_HIP(ctx, salt::launch_plan(plan->dev, plan->T, ctx->cfg.n_centroids, (hipStream_t)stream));
+  plan->built = true;
+  return SALT_OK;
+}
+
+salt_status salt_plan_download(salt_ctx* ctx, const salt_plan* plan, void* stream, int32_t* perm,
+                               int32_t* seg_off, int32_t* seg_c, int32_t* seg_u, int32_t* grp_off,
+                               int32_t* n_seg, int32_t* n_grp) {
+  if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
+  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  if (!plan->built) return fail(ctx, SALT_ERR_BAD_STATE, "plan was not built");
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  hipStream_t s = (hipStream_t)stream;
+  SALT_HIP(ctx, hipStreamSynchronize(s));
+  const int T = plan->T;
+  int32_t meta[3] = {0, 0, 0};
+  if (T > 0) SALT_HIP(ctx, hipMemcpy(meta, plan->dev.meta, sizeof meta, hipMemcpyDeviceToHost));
+  const int ns = meta[0], ng = meta[1];
+  if (n_seg) *n_seg = ns;
+  if (n_grp) *n_grp = ng;
+  if (T == 0) {
+    if (seg_off) seg_off[0] = 0;
+    if (grp_off) grp_off[0] = 0;
+    return SALT_OK;
+  }
+  if (perm) SALT_HIP(ctx, hipMemcpy(perm, plan->dev.perm, (size_t)T * 4, hipMemcpyDeviceToHost));
+  if (seg_off) SALT_HIP(ctx, hipMemcpy(seg_off, plan->dev.seg_off, (size_t)(ns + 1) * 4, hipMemcpyDeviceToHost));
+  if (seg_c) SALT_HIP(ctx, hipMemcpy(seg_c, plan->dev.seg_c, (size_t)ns * 4, hipMemcpyDeviceToHost));
+  if (seg_u) SALT_HIP(ctx, hipMemcpy(seg_u, plan->dev.seg_u, (size_t)ns * 4, hipMemcpyDeviceToHost));
+  if (grp_off) SALT_HIP(ctx, hipMemcpy(grp_off, plan->dev.grp_off, (size_t)(ng + 1) * 4, hipMemcpyDeviceToHost));
+  return SALT_OK;
+}
+
+salt_status salt_apply(salt_ctx* ctx, int32_t table, const salt_plan* plan, const void* x, void* y,
+                       void* stream) {
+  if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
+  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  if (table < 0 || table >= ctx->cfg.n_tables)
+    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "table %d not in [0, %d)", table, ctx->cfg.n_tables);
+  if (!plan->built) return fail(ctx, SALT_ERR_BAD_STATE, "plan was not built");
+  const int T = plan->T;
+  if (T == 0) return SALT_OK;
+  if (!x || !y || !aligned16(x) || !aligned16(y))
+    return fail(ctx, SALT_ERR_INVALID_ARG, "null or misaligned x / y");
+  const int C = ctx->cfg.n_centroids;
+  for (int i = 0; i < C; ++i)
+    if (!ctx->cent_pinned[(size_t)table * C + i])
+      return fail(ctx, SALT_ERR_BAD_STATE, "centroid %d of table %d was never pinned", i, table);
+  int64_t need_load = -1;
+  for (size_t i = 0; i < plan->slots.size(); ++i) {
+    const int s = plan->slots[i];
+    if (ctx->slot_rank[s] != plan->slot_rank[i])
+      return fail(ctx, SALT_ERR_BAD_STATE,
+                  "slot %d was reloaded with rank %d after the plan's maps were set (rank %d)", s,
+                  ctx->slot_rank[s], plan->slot_rank[i]);
+    need_load = std::max(need_load, ctx->slot_loader[s]);
+  }
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  hipStream_t s = (hipStream_t)stream;
+  SALT_HIP(ctx, ring_wait(ctx->loaders, s, need_load));
+
+  const salt_shape sh = ctx->tables[table];
+  ApplyArgs a{};
+  a.x = x;
+  a.y = y;
+  a.cent_at = C ? ctx->cent_at[table] : nullptr;
+  a.cent_b = C ? ctx->cent_b[table] : nullptr;
+  a.pool = ctx->pool;
+  a.slot_stride = ctx->slot_stride;
+  a.tab_prefix = ctx->tab_prefix[table];
+  a.srt = plan->dev.srt;
+  a.grp_tok = plan->dev.grp_tok;
+  a.grp_c = plan->dev.grp_c;
+  a.meta = plan->dev.meta;
+  a.partials = plan->dev.partials;
+  a.T = T;
+  a.in_dim = sh.in_dim;
+  a.out_dim = sh.out_dim;
+  a.r_c = ctx->cfg.r_c;
+  a.r_u_max = ctx->cfg.r_u_max;
+  a.R = std::max(1, a.r_c + a.r_u_max);
+  // tiles: at most ceil(T / M) plus one partial tile per centroid group
+  const int M = salt::kTileM;
+  const int tiles_ub = (T + M - 1) / M + plan->n_centroid_groups_ub;
+  // split K so that about 1024 blocks work on the shrink, in multiples of 64
+  const int kmax = (sh.in_dim + 63) / 64;
+  int S = std::max(1, std::min(kmax, (1024 + tiles_ub - 1) / tiles_ub));
+  while (S > 1 && (size_t)S * T * a.R > plan->dev.partial_cap) --S;
+  int Kc = ((sh.in_dim + S - 1) / S + 63) / 64 * 64;
+  S = (sh.in_dim + Kc - 1) / Kc;
+  a.S = S;
+  a.Kc = Kc;
+  a.NC = 128;
+  SALT_HIP(ctx, salt::launch_apply(a, ctx->cfg.dtype == SALT_BF16, tiles_ub, s));
+  int64_t seq;
+  SALT_HIP(ctx, ring_record(ctx->readers, s, &seq));
+  for (int slot : plan->slots) ctx->slot_reader[slot] = seq;
+  return SALT_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,136 @@
+"""GPU parity: libsalt (through the C ABI) against the fp64 CPU oracle.
+
+Plans must match the oracle bit for bit.  Outputs must satisfy
+|y - ref| <= 1e-2 * (1 + |ref|) element-wise for bf16 (fp32 accumulation), and
+1e-5 * (1 + |ref|) for the fp32 Tiny workload; the integer-valued variants must be
+bit-exact.  Every case prints its name before the GPU work starts.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_03579_amd import synth
+from tests.gpu_harness import TOL_F32, TOL_NORTH_STAR, Run, close_enough
+
+pytestmark = pytest.mark.gpu
+
+
+def _tol(w):
+    return TOL_F32 if w.dtype == "f32" else TOL_NORTH_STAR
+
+
+def _check_plan(run):
+    p = run.plan.download(run.stream)
+    want = oracle.plan(run.maps[0], run.maps[1])
+    for k in ("perm", "seg_off", "seg_c", "seg_u", "grp_off"):
+        assert np.array_equal(p[k], want[k]), (k, p[k][:16], want[k][:16])
+
+
+def _check_table(run, table, rows=None, exact=False):
+    got = run.apply(table)
+    got = oracle.decode(got, run.w.dtype)
+    ref = run.oracle_table(table, rows)
+    if rows is not None:
+        got = got[np.asarray(rows)]
+    if exact:
+        assert np.array_equal(got, ref), f"table {table}: {np.sum(got != ref)} exact mismatches"
+        return
+    ok, worst, nbad = close_enough(got, ref, _tol(run.w))
+    assert ok, f"table {table}: {nbad} elements out of tolerance, worst {worst:.3f}x the bound"
+
+
+def _announce(name):
+    print(f"\n[gpu case] {name}", flush=True)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("y0", ["zero", "normal"])
+def test_tiny_fp32(seed, y0):
+    _announce(f"tiny fp32 seed={seed} y0={y0}")
+    run = Run(synth.make(1, seed, y0=y0))
+    try:
+        run.set_and_build()
+        _check_plan(run)
+        _check_table(run, 0)
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_llama32_qproj_decode(seed):
+    _announce(f"cfg2 q_proj decode seed={seed}")
+    run = Run(synth.make(2, seed, y0="normal" if seed == 1 else "zero"))
+    try:
+        run.set_and_build()
+        _check_plan(run)
+        _check_table(run, 0)
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 5])
+def test_exact_integer_bit_exact(cfg):
+    _announce(f"exact integer cfg={cfg}")
+    w = synth.make(cfg, 3, exact=True, y0="int")
+    run = Run(w)
+    try:
+        run.set_and_build()
+        _check_plan(run)
+        for t in range(len(w.tables)):
+            _check_table(run, t, exact=True)
+    finally:
+        run.close()
+
+
+def test_gamma_bins():
+    _announce("gamma bins cfg1 + cfg2")
+    for cfg in (1, 2):
+        run = Run(synth.make(cfg, 4, gamma="bins"))
+        try:
+            run.set_and_build()
+            _check_table(run, 0)
+        finally:
+            run.close()
+
+
+def test_llama31_decode_with_swaps():
+    _announce("cfg4 llama3.1-8b decode T=256 with 32 swapped residuals")
+    w = synth.make(4, 0)
+    run = Run(w)
+    try:
+        for s in w.meta["swap_slots"]:
+            run.load(int(s), 1)
+        run.set_and_build()
+        _check_plan(run)
+        for t in range(len(w.tables)):
+            _check_table(run, t)
+    finally:
+        run.close()
+
+
+@pytest.mark.parametrize("baseline", [False, True])
+def test_zipf_multitenant(baseline):
+    _announce(f"cfg5 zipf T=512 baseline={baseline}")
+    w = synth.make(5, 0, baseline=baseline)
+    run = Run(w)
+    try:
+        run.set_and_build()
+        _check_plan(run)
+        for t in range(len(w.tables)):
+            _check_table(run, t)
+    finally:
+        run.close()
+
+
+def test_prefill_reduced():
+    _announce("cfg3 prefill 1 layer, T=2048")
+    w = synth.make(3, 0, layers=1, T=2048)
+    run = Run(w)
+    try:
+        run.set_and_build()
+        _check_plan(run)
+        rows = list(range(0, w.T, 7)) + [w.T - 1]
+        for t in range(len(w.tables)):
+            _check_table(run, t, rows=rows)
+    finally:
+        run.close()
