@@ -1,0 +1,322 @@
+#!/usr/bin/env python3
+"""Throughput of the batched centroid + residual LoRA apply on one MI355X.
+
+    python bench.py [--steps K] [--warmup W] [--workload qproj|prefill|decode8b|zipf]
+
+Prints ONE JSON line.  A step is one pass of the hot path over one batch: the
+device plan build (grouping by centroid) followed by ``salt_apply`` on every
+table of the workload.  Inputs (x, y, maps, pinned centroids, resident
+residuals) are in HBM before the timed region starts.
+
+Default workload: Llama-3.2-3B q_proj (3072 -> 3072), bf16 decode batch of 64
+tokens, 4 centroids r=32, 64 residual slots r=2 (one token per user).  One such
+apply moves about 4.3 MB, which fits in the 256 MB Infinity Cache, so the bench
+rotates over ``--rot`` copies of every buffer (tables, slot pool, x, y, plans):
+consecutive steps touch disjoint memory, as consecutive projections of a real
+decode step would, and bytes come from HBM.
+
+Timing: HIP events on the stream the kernels run on, around the K timed steps;
+then, for the roofline, events around each apply of a second pass to get the
+apply's own average duration.  ``cpu_baseline`` times the fp64 oracle on a
+bounded sample of the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBPS = 8000.0   # MI355X HBM3E
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def apply_bytes(w, plan_maps, table):
+    """Algorithmic HBM bytes of one apply: x once, y read + write once, each
+    referenced centroid's A and B once, each referenced residual at its own rank
+    once, and the per-token plan records (16 B each)."""
+    tok_c, tok_u = plan_maps
+    _, n_in, n_out = w.tables[table]
+    es = w.esize
+    T = len(tok_c)
+    cents = np.unique(tok_c[tok_c >= 0])
+    slots = np.unique(tok_u[tok_u >= 0])
+    b = T * n_in * es + 2 * T * n_out * es
+    b += len(cents) * w.r_c * (n_in + n_out) * es
+    b += int(sum(int(w.slot_rank[s]) for s in slots)) * (n_in + n_out) * es
+    b += T * 16
+    return b
+
+
+def apply_flops(w, plan_maps, table):
+    tok_c, tok_u = plan_maps
+    _, n_in, n_out = w.tables[table]
+    r = np.where(tok_c >= 0, w.r_c, 0) + np.where(tok_u >= 0, w.slot_rank[np.maximum(tok_u, 0)], 0)
+    return int(2 * (n_in + n_out) * r.sum())
+
+
+# ---------------------------------------------------------------------------
+# CPU baseline: the oracle as it stands, bounded sample, on this host
+# ---------------------------------------------------------------------------
+def cpu_baseline(w, budget_s=12.0):
+    import oracle
+    try:
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=1)
+    except Exception:   # pragma: no cover
+        limiter = None
+    d = w.dtype
+    n_tab = len(w.tables)
+    data = []
+    for t in range(n_tab):
+        x = oracle.decode(w.x(t), d)
+        y0 = oracle.decode(w.y0(t), d)
+        cat, cb = (oracle.decode(a, d) for a in w.centroids(t)) if w.n_centroids else (None, None)
+        res = {int(s): tuple(oracle.decode(a, d) for a in w.residual(int(s), t)) for s in w.referenced_slots()}
+        data.append((x, y0, cat, cb, res))
+    tokens = 0
+    t0 = time.perf_counter()
+    passes = 0
+    while True:
+        oracle.plan(w.tok_c, w.tok_u)
+        for t in range(n_tab):
+            x, y0, cat, cb, res = data[t]
+            oracle.apply(x, y0, cat, cb, res, w.tok_c, w.tok_u, w.gamma)
+        tokens += w.T
+        passes += 1
+        if time.perf_counter() - t0 >= budget_s:
+            break
+    dt = time.perf_counter() - t0
+    if limiter is not None:
+        limiter.unregister() if hasattr(limiter, "unregister") else None
+    return {"value": tokens / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{passes} full passes (plan + {n_tab} table apply) of the same batch, "
+                      f"{dt:.1f} s, fp64 numpy, BLAS limited to 1 thread, host cpu: {os.cpu_count()} logical"}
+
+
+# ---------------------------------------------------------------------------
+# GPU bench
+# ---------------------------------------------------------------------------
+def build_replicated(w, rot, hip, salt):
+    """A context whose tables are ``rot`` copies of the workload's tables, with
+    every centroid pinned and every referenced residual loaded."""
+    shapes = [(i, o) for _, i, o in w.tables] * rot
+    ctx = salt.Context(w.dtype, shapes, w.n_centroids, w.r_c, w.n_slots, w.r_u_max, max(1, w.T))
+    n_tab = len(w.tables)
+    if w.n_centroids:
+        for t in range(n_tab):
+            at, b = w.centroids(t)
+            for k in range(rot):
+                ctx.pin_centroids(k * n_tab + t, at, b)
+    for s in w.referenced_slots():
+        s = int(s)
+        r = int(w.slot_rank[s])
+        blob = w.residual_blob(s)
+        ctx.load_residual(s, r, np.tile(blob, rot) if r else None)
+    ctx.wait_loads()
+    return ctx
+
+
+def swap_timing(w, hip, salt, n=32):
+    """H2D swap of n residual blobs (rank r_u_max of the workload vs rank 16),
+    pinned host memory, on the context's side stream."""
+    out = {}
+    shapes = [(i, o) for _, i, o in w.tables]
+    for r in sorted({max(1, w.r_u_max), 16}):
+        ctx = salt.Context(w.dtype, shapes, 0, 0, n, r, 1)
+        nbytes = ctx.residual_bytes(r)
+        bufs = [salt.HostBuffer(nbytes) for _ in range(n)]
+        for b in bufs:
+            b.view(np.uint8)[:] = 1
+        ev0, ev1 = hip.Event(), hip.Event()
+        best = None
+        for rep in range(5):
+            hip.synchronize()
+            t0 = time.perf_counter()
+            for i, b in enumerate(bufs):
+                st = ctx.load_residual_ptr(i, r, b.ptr, nbytes)
+                assert st == 0, st
+            ctx.wait_loads()
+            dt = time.perf_counter() - t0
+            best = dt if best is None else min(best, dt)
+        out[f"r{r}"] = {"blobs": n, "bytes_per_blob": nbytes, "ms": best * 1e3,
+                        "GBps": n * nbytes / best / 1e9}
+        for b in bufs:
+            b.free()
+        ctx.close()
+    return out
+
+
+def run_gpu(w, args, hip, salt):
+    rot = args.rot
+    n_tab = len(w.tables)
+    log(f"workload: {w.name}; T={w.T}, tables={n_tab}, rotation={rot}")
+    ctx = build_replicated(w, rot, hip, salt)
+    stream = hip.Stream()
+    # x and y per table copy: rotation keeps the working set above the MALL
+    xs, ys = [], []
+    for t in range(n_tab):
+        x = w.x(t)
+        y = w.y0(t)
+        for k in range(rot):
+            xs.append(hip.DeviceArray.from_host(x))
+            ys.append(hip.DeviceArray.from_host(y))
+    # one plan per rotation slot; every plan holds the same batch's maps
+    plans = []
+    for k in range(rot):
+        p = ctx.plan()
+        p.set_maps(w.tok_c, w.tok_u, w.gamma, stream.h)
+        plans.append(p)
+    stream.synchronize()
+
+    def step(k):
+        slot = k % rot
+        p = plans[slot]
+        p.build(stream.h)
+        for t in range(n_tab):
+            tab = slot * n_tab + t
+            ctx.apply(tab, p, xs[tab].ptr, ys[tab].ptr, stream.h)
+
+    for k in range(args.warmup):
+        step(k)
+    stream.synchronize()
+    e0, e1 = hip.Event(), hip.Event()
+    hip.synchronize()
+    e0.record(stream)
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(k)
+    e1.record(stream)
+    e1.synchronize()
+    wall = time.perf_counter() - t0
+    hip.synchronize()
+    ms_total = e0.elapsed_ms(e1)
+    ms_step = ms_total / args.steps
+    log(f"timed {args.steps} steps: {ms_total:.3f} ms GPU ({wall * 1e3:.1f} ms wall), {ms_step * 1e3:.2f} us/step")
+
+    # apply-only durations: events around each apply, same stream, same rotation
+    n_meas = min(args.steps, 2000)
+    evs = [(hip.Event(), hip.Event()) for _ in range(n_tab)]
+    per_tab = np.zeros(n_tab)
+    for k in range(n_meas):
+        slot = k % rot
+        p = plans[slot]
+        p.build(stream.h)
+        for t in range(n_tab):
+            tab = slot * n_tab + t
+            a, b = evs[t]
+            a.record(stream)
+            ctx.apply(tab, p, xs[tab].ptr, ys[tab].ptr, stream.h)
+            b.record(stream)
+        stream.synchronize()
+        for t in range(n_tab):
+            per_tab[t] += evs[t][0].elapsed_ms(evs[t][1])
+    per_tab /= n_meas
+    maps = (w.tok_c, w.tok_u)
+    bytes_tab = np.array([apply_bytes(w, maps, t) for t in range(n_tab)], dtype=np.float64)
+    flops_tab = np.array([apply_flops(w, maps, t) for t in range(n_tab)], dtype=np.float64)
+    dom = int(np.argmax(per_tab))
+    achieved = bytes_tab[dom] / (per_tab[dom] * 1e-3) / 1e9
+    step_bytes = float(bytes_tab.sum())
+
+    swap = swap_timing(w, hip, salt) if args.swap else None
+    for p in plans:
+        p.close()
+    ctx.close()
+    return {
+        "ms_per_step": ms_step,
+        "tokens_per_s": w.T / (ms_step * 1e-3),
+        "step_GBps": step_bytes / (ms_step * 1e-3) / 1e9,
+        "apply_us": {w.tables[t][0]: round(per_tab[t] * 1e3, 3) for t in range(n_tab)},
+        "apply_bytes": {w.tables[t][0]: int(bytes_tab[t]) for t in range(n_tab)},
+        "apply_flops": {w.tables[t][0]: int(flops_tab[t]) for t in range(n_tab)},
+        "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                     "kernel": f"salt_apply on {w.tables[dom][0]} (plan + shrink + expand of one table; "
+                               f"events bracket the apply's launches)",
+                     "bytes_per_launch": int(bytes_tab[dom]), "avg_us": per_tab[dom] * 1e3},
+        "swap": swap,
+    }
+
+
+WORKLOADS = {
+    "qproj": dict(cfg=2, rot=128),
+    "decode8b": dict(cfg=4, rot=4),
+    "zipf": dict(cfg=5, rot=4),
+    "zipf-baseline": dict(cfg=5, rot=4, baseline=True),
+}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=2000)
+    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--workload", default="qproj", choices=sorted(WORKLOADS))
+    ap.add_argument("--rot", type=int, default=None)
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-swap", dest="swap", action="store_false")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only: the apply has no cross-GPU path in this build "
+              f"(asked for --gpus {args.gpus})", file=sys.stderr)
+        sys.exit(2)
+    spec = WORKLOADS[args.workload]
+    if args.rot is None:
+        args.rot = spec["rot"]
+
+    from paper_2608_03579_amd import synth
+    w = synth.make(spec["cfg"], 0, baseline=spec.get("baseline", False))
+
+    from paper_2608_03579_amd import hip, salt
+    if hip.device_count() < 1:
+        print("no HIP device visible", file=sys.stderr)
+        sys.exit(1)
+    hip.set_device(0)
+    res = run_gpu(w, args, hip, salt)
+
+    cpu = None
+    if not args.no_cpu:
+        log("cpu baseline (oracle) ...")
+        cpu = cpu_baseline(w)
+
+    out = {
+        "metric": "Centroid+residual LoRA apply: tokens/s and achieved HBM GB/s, Llama-3.2-3B",
+        "value": res["tokens_per_s"],
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": res["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": w.name, "T": w.T,
+                   "tables": [f"{n} {i}->{o}" for n, i, o in w.tables],
+                   "centroids": f"{w.n_centroids} x r{w.r_c}",
+                   "residual_slots": f"{w.n_slots} x r<={w.r_u_max}",
+                   "accumulation": "fp32", "rotation": args.rot,
+                   "step": "salt_plan_build + salt_apply per table, maps staged in HBM beforehand"},
+        "achieved_GBps_step": res["step_GBps"],
+        "apply_us": res["apply_us"],
+        "apply_bytes": res["apply_bytes"],
+        "roofline": res["roofline"],
+        "cpu_baseline": cpu,
+        "swap_h2d": res["swap"],
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -70,7 +70,7 @@ typedef struct {
   int32_t n_tables;          /* >= 1: projections served by this context            */
   const salt_shape* tables;  /* [n_tables]; copied by salt_create                  */
   int32_t n_centroids;       /* C in [0, 64]: centroid library size (Sec. 3.2)     */
-  int32_t r_c;               /* centroid rank in [0, 128] (0 iff C == 0)           */
+  int32_t r_c;               /* centroid rank in [0, 128], a multiple of 8 (0 iff C == 0) */
   int32_t n_slots;           /* residual slot-pool size, >= 1                      */
   int32_t r_u_max;           /* largest residual rank a slot holds, in [0, 16]     */
   int32_t max_tokens;        /* largest batch a plan accepts, in [1, 1 << 20]      */
@@ -170,12 +170,23 @@ SALT_API salt_status salt_plan_download(salt_ctx* ctx, const salt_plan* plan, vo
  *   x: device [T][in_dim], y: device [T][out_dim], context dtype, row-major,
  *      16-byte aligned; y is read and written once per element, rounded once
  *      (round-to-nearest-even) from fp32 y + fp32 delta.
- * Accumulation is fp32.  Enqueued on `stream` after the swaps of every slot the
+ * Accumulation is fp32: the centroid contractions run on bf16 MFMA with fp32
+ * accumulation (the expand splits the fp32 v into two bf16 terms), the residual
+ * contractions on fp32 vector ALUs.  One kernel launch; the plan's scratch
+ * (split-K partials, v, per-tile flags) is reused, so applies of one plan must be
+ * ordered on one stream.  Enqueued on `stream` after the swaps of every slot the
  * plan references.  Errors: SALT_ERR_OUT_OF_RANGE (table), SALT_ERR_BAD_STATE
  * (centroids of the table not pinned; a referenced slot was reloaded with a
  * different rank after salt_plan_set_maps). */
-SALT_API salt_status salt_apply(salt_ctx* ctx, int32_t table, const salt_plan* plan, const void* x, void* y,
+SALT_API salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y,
                        void* stream);
+
+/* Synchronise `stream`, then report in *n_errors the number of apply blocks of
+ * this plan that gave up waiting for their tile since the last salt_plan_build
+ * (their slice of y was left unchanged; 0 in normal operation).  Also checks
+ * that the device-built tiling matches the host's (SALT_ERR_BAD_STATE if not). */
+SALT_API salt_status salt_plan_errors(salt_ctx* ctx, const salt_plan* plan, void* stream,
+                                      int32_t* n_errors);
 
 /* ---- diagnostics -------------------------------------------------------------------- */
 SALT_API const char* salt_status_str(salt_status s);

@@ -8,48 +8,68 @@
 
 namespace salt {
 
-// Device buffers of one plan.  Sorted-position arrays are indexed by the
-// position of a token in the canonical (centroid, slot, token) order.
+// Slots of the per-plan meta word array.
+enum Meta { kMetaNSeg = 0, kMetaNGrp = 1, kMetaT = 2, kMetaNTiles = 3, kMetaErr = 4, kMetaWords = 16 };
+
+// Device buffers of one plan.  "Sorted position" is the position of a token in
+// the canonical (centroid, slot, token) order.
 struct PlanBuffers {
-  int4* maps;        // [max_T] staged maps: (c, u, r, gamma bits) per token
-  int32_t* perm;     // [max_T] token index at each sorted position
-  int4* srt;         // [max_T] (token, u, r, gamma bits) at each sorted position
-  int32_t* srt_c;    // [max_T] centroid id at each sorted position
-  int32_t* seg_off;  // [max_T + 1]
-  int32_t* seg_c;    // [max_T]
-  int32_t* seg_u;    // [max_T]
-  int32_t* grp_off;  // [max_T + 1] segment index where each centroid group starts
-  int32_t* grp_tok;  // [max_T + 1] sorted position where each centroid group starts
-  int32_t* grp_c;    // [max_T] centroid id of each group
-  int32_t* meta;     // [16]: [0] n_seg, [1] n_grp, [2] T
-  uint32_t* counter; // [64] arrival counters, zero between launches
-  float* partials;   // [partial_cap] fp32 split-K partial sums of the shrink
-  size_t partial_cap;
+  int4* maps;         // [max_T] staged maps: (c, u, r, gamma bits) per token
+  int32_t* perm;      // [max_T] token index at each sorted position
+  int4* srt;          // [max_T] (token, u, r, gamma bits) at each sorted position
+  int32_t* srt_c;     // [max_T] centroid id at each sorted position
+  int32_t* seg_off;   // [max_T + 1]
+  int32_t* seg_c;     // [max_T]
+  int32_t* seg_u;     // [max_T]
+  int32_t* grp_off;   // [max_T + 1] segment index where each centroid group starts
+  int32_t* grp_tok;   // [max_T + 1] sorted position where each centroid group starts
+  int32_t* grp_c;     // [max_T] centroid id of each group
+  int4* tiles;        // [tile_cap]: per tile (i0, n, c, 0) then M token records
+  uint32_t* arrive;   // [max tiles] shrink blocks that finished a tile in this apply
+  uint32_t* ready;    // [max tiles] epoch of the apply whose v of the tile is complete
+  int32_t* meta;      // [kMetaWords]
+  uint32_t* counter;  // [64] arrival counter of the multi-block plan build
+  float* partials;    // [partial_cap] split-K partial sums of the shrink
+  float* v;           // [max_T][R] reduced v = x [A_c | A_u] (gamma applied)
+  size_t partial_cap; // floats
+  size_t tile_cap;    // int4 entries
+  int32_t tiles_max;  // entries of arrive / ready
 };
 
-// Everything one salt_apply launch needs, passed by value.
+struct PlanArgs {
+  PlanBuffers b;
+  int32_t T;
+  int32_t M;          // tokens per tile (16, 32 or 64)
+};
+
+// Everything one apply launch needs, passed by value.
 struct ApplyArgs {
   const void* x;            // [T][in]
   void* y;                  // [T][out]
-  const void* cent_at;      // [C][r_c][in] of this table
-  const void* cent_b;       // [C][r_c][out] of this table
-  const char* pool;         // slot pool base
+  const void* cent_at;      // [C][r_c][in]  centroid A, transposed
+  const void* cent_bt;      // [C][out][r_c] centroid B, transposed (internal layout)
+  const char* pool;         // residual slot pool
   size_t slot_stride;       // bytes between slots
-  int64_t tab_prefix;       // sum of (in + out) over earlier tables, in elements per rank
-  const int4* srt;
-  const int32_t* grp_tok;
-  const int32_t* grp_c;
-  const int32_t* meta;
+  int64_t tab_prefix;       // sum of (in + out) over earlier tables (elements per rank)
+  const int4* tiles;
   float* partials;          // [S][T][R]
+  float* v;                 // [T][R]
+  uint32_t* arrive;
+  uint32_t* ready;
+  int32_t* meta;
+  uint32_t epoch;           // 1, 2, ... per apply of the plan since its build
   int32_t T, in_dim, out_dim, r_c, r_u_max, R;
-  int32_t S, Kc, NC;        // K-splits, K per split, columns per expand block
+  int32_t n_tiles, S, Kc, n_col;
 };
 
-hipError_t launch_plan(const PlanBuffers& b, int32_t T, int32_t n_centroids, hipStream_t s);
-hipError_t launch_apply(const ApplyArgs& a, int dtype_bf16, int32_t tiles_ub, hipStream_t s);
 hipError_t kernels_init(int device);
+hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
+hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s);
 
-// Tile size (tokens of one centroid group) of the VALU apply kernels.
-constexpr int kTileM = 16;
+// Columns of y per expand block.
+constexpr int kNC = 128;
+// Largest supported ranks.
+constexpr int kMaxRc = 128;
+constexpr int kMaxRu = 16;
 
 }  // namespace salt

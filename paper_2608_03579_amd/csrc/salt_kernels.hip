@@ -1,79 +1,176 @@
-// HIP kernels of libsalt for gfx950 (MI355X): device plan builder and the
-// centroid + residual apply (gathered split-K shrink, expand with fused y update).
+// HIP kernels of libsalt for gfx950 (MI355X): the device plan builder and the
+// fused centroid + residual apply.
 //
-// The apply computes, per token t of a plan (Sec. 3.3 served weight minus W_base):
-//     v_t = x_t [A_c | A_u]                (shrink: one rank-(r_c + r_u) contraction)
-//     v_t[0:r_c] *= gamma_t                (centroid scale, Sec. 3.3)
-//     y_t = rne(y_t + v_t [B_c ; B_u])     (expand + accumulate, fp32 math)
-// Tokens are processed in tiles of up to kTileM tokens that share one centroid,
-// so each tile streams its centroid's A/B chunk once for all of its tokens.
+// Per token t of a plan (the served weight of Sec. 3.3 minus W_base):
+//     v_t = x_t [A_c | A_u]              shrink: one rank-(r_c + r_u) contraction
+//     v_t[0:r_c] *= gamma_t              centroid scale (Sec. 3.3)
+//     y_t = rne(y_t + v_t [B_c ; B_u])   expand and accumulate, fp32 math
+//
+// Tokens are cut into tiles of M = 16, 32 or 64 sorted tokens that share one
+// centroid.  For a tile, the centroid part of the shrink, [M x in] . [in x r_c],
+// and of the expand, [M x r_c] . [r_c x out], are dense skinny GEMMs and run on
+// MFMA (v_mfma_f32_16x16x32_bf16); the residual part differs per token, has
+// rank <= 2 (<= 16 for plain LoRA baselines) and runs on the vector ALUs, with
+// lane shuffles for the reductions.
+//
+// One launch per apply holds two kinds of blocks.  Shrink blocks (the first
+// n_tiles * S block ids) each reduce one tile over one K range into split-K
+// partials; the last of a tile's S blocks to arrive sums them in a fixed order,
+// applies gamma, stores v and publishes the apply's epoch in the tile's ready
+// word (release).  Expand blocks (the rest) prefetch their y, B_c and B_u
+// slices, then wait (acquire) for their tile's ready word, and update y.
+// Blocks are dispatched in id order, so every shrink block has started before
+// any expand block waits on it, and shrink blocks never wait: the wait always
+// ends.  It is still bounded; a block that gives up records an error in the
+// plan's meta words and leaves its slice of y untouched.
 #include "salt_internal.h"
 
 namespace salt {
 namespace {
 
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+
+constexpr uint32_t kSpinMax = 1u << 24;   // ~0.5 s of polling before giving up
+
 // ---------------------------------------------------------------------------
-// element access: 8 consecutive elements <-> 8 floats
+// element types: bf16 (uint16 storage) and fp32, 8 elements per vector
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// fp32 -> bf16, round to nearest even (NaN stays a quiet NaN).
+// fp32 -> bf16 bits, round to nearest even (NaN stays a quiet NaN).
 __device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
   if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
   return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
 }
 
-__device__ __forceinline__ void ld8(const uint16_t* p, float* o) {
-  const uint4 v = *reinterpret_cast<const uint4*>(p);
-  o[0] = bf_lo(v.x); o[1] = bf_hi(v.x); o[2] = bf_lo(v.y); o[3] = bf_hi(v.y);
-  o[4] = bf_lo(v.z); o[5] = bf_hi(v.z); o[6] = bf_lo(v.w); o[7] = bf_hi(v.w);
-}
-__device__ __forceinline__ void ld8(const float* p, float* o) {
-  const float4 a = *reinterpret_cast<const float4*>(p);
-  const float4 b = *reinterpret_cast<const float4*>(p + 4);
-  o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
-  o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
-}
-__device__ __forceinline__ void st8(uint16_t* p, const float* v) {
-  uint4 w;
-  w.x = f32_to_bf16_rne(v[0]) | (f32_to_bf16_rne(v[1]) << 16);
-  w.y = f32_to_bf16_rne(v[2]) | (f32_to_bf16_rne(v[3]) << 16);
-  w.z = f32_to_bf16_rne(v[4]) | (f32_to_bf16_rne(v[5]) << 16);
-  w.w = f32_to_bf16_rne(v[6]) | (f32_to_bf16_rne(v[7]) << 16);
-  *reinterpret_cast<uint4*>(p) = w;
-}
-__device__ __forceinline__ void st8(float* p, const float* v) {
-  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
-  *reinterpret_cast<float4*>(p + 4) = make_float4(v[4], v[5], v[6], v[7]);
-}
+template <typename E>
+struct Ops;
+
+template <>
+struct Ops<uint16_t> {
+  using Vec = uint4;
+  static __device__ __forceinline__ Vec zero() { return make_uint4(0u, 0u, 0u, 0u); }
+  static __device__ __forceinline__ Vec load(const uint16_t* p) {
+    return *reinterpret_cast<const uint4*>(p);
+  }
+  static __device__ __forceinline__ void to_f32(const Vec& v, float* o) {
+    o[0] = bf_lo(v.x); o[1] = bf_hi(v.x); o[2] = bf_lo(v.y); o[3] = bf_hi(v.y);
+    o[4] = bf_lo(v.z); o[5] = bf_hi(v.z); o[6] = bf_lo(v.w); o[7] = bf_hi(v.w);
+  }
+  static __device__ __forceinline__ void store(uint16_t* p, const float* f) {
+    uint4 w;
+    w.x = f32_to_bf16_rne(f[0]) | (f32_to_bf16_rne(f[1]) << 16);
+    w.y = f32_to_bf16_rne(f[2]) | (f32_to_bf16_rne(f[3]) << 16);
+    w.z = f32_to_bf16_rne(f[4]) | (f32_to_bf16_rne(f[5]) << 16);
+    w.w = f32_to_bf16_rne(f[6]) | (f32_to_bf16_rne(f[7]) << 16);
+    *reinterpret_cast<uint4*>(p) = w;
+  }
+  // acc + sum_e a[e] * b[e], products exact in fp32
+  static __device__ __forceinline__ float dot(const Vec& a, const Vec& b, float acc) {
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a.x), __builtin_bit_cast(bf16x2, b.x), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a.y), __builtin_bit_cast(bf16x2, b.y), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a.z), __builtin_bit_cast(bf16x2, b.z), acc, false);
+    acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_bit_cast(bf16x2, a.w), __builtin_bit_cast(bf16x2, b.w), acc, false);
+    return acc;
+  }
+  // One 16x16x32 step: lane l brings row (l & 15) of the left operand and column
+  // (l & 15) of the right one, 8 consecutive k each.
+  static __device__ __forceinline__ f32x4 mma(const Vec& a, const Vec& b, f32x4 c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a),
+                                                   __builtin_bit_cast(bf16x8, b), c, 0, 0, 0);
+  }
+  // Same with an fp32 right operand: v = hi + lo with hi, lo bf16, so the
+  // product keeps about 16 significant bits of v (two MFMA steps).
+  static __device__ __forceinline__ f32x4 mma_f32rhs(const Vec& a, const float* v, f32x4 c) {
+    uint32_t h[8], l[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      h[e] = f32_to_bf16_rne(v[e]);
+      l[e] = f32_to_bf16_rne(v[e] - __uint_as_float(h[e] << 16));
+    }
+    const uint4 hi = make_uint4(h[0] | (h[1] << 16), h[2] | (h[3] << 16), h[4] | (h[5] << 16), h[6] | (h[7] << 16));
+    const uint4 lo = make_uint4(l[0] | (l[1] << 16), l[2] | (l[3] << 16), l[4] | (l[5] << 16), l[6] | (l[7] << 16));
+    c = mma(a, hi, c);
+    return mma(a, lo, c);
+  }
+};
+
+template <>
+struct Ops<float> {
+  struct Vec {
+    float4 lo, hi;
+  };
+  static __device__ __forceinline__ Vec zero() {
+    return Vec{make_float4(0.f, 0.f, 0.f, 0.f), make_float4(0.f, 0.f, 0.f, 0.f)};
+  }
+  static __device__ __forceinline__ Vec load(const float* p) {
+    return Vec{*reinterpret_cast<const float4*>(p), *reinterpret_cast<const float4*>(p + 4)};
+  }
+  static __device__ __forceinline__ void to_f32(const Vec& v, float* o) {
+    o[0] = v.lo.x; o[1] = v.lo.y; o[2] = v.lo.z; o[3] = v.lo.w;
+    o[4] = v.hi.x; o[5] = v.hi.y; o[6] = v.hi.z; o[7] = v.hi.w;
+  }
+  static __device__ __forceinline__ void store(float* p, const float* f) {
+    *reinterpret_cast<float4*>(p) = make_float4(f[0], f[1], f[2], f[3]);
+    *reinterpret_cast<float4*>(p + 4) = make_float4(f[4], f[5], f[6], f[7]);
+  }
+  static __device__ __forceinline__ float dot(const Vec& a, const Vec& b, float acc) {
+    float x[8], y[8];
+    to_f32(a, x);
+    to_f32(b, y);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc = fmaf(x[e], y[e], acc);
+    return acc;
+  }
+  // Eight 16x16x4 fp32 steps: in step e, lane group g = l >> 4 supplies k = 8g + e,
+  // so the eight steps together cover the same 32 k as one bf16 step.
+  static __device__ __forceinline__ f32x4 mma(const Vec& a, const Vec& b, f32x4 c) {
+    float x[8], y[8];
+    to_f32(a, x);
+    to_f32(b, y);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) c = __builtin_amdgcn_mfma_f32_16x16x4f32(x[e], y[e], c, 0, 0, 0);
+    return c;
+  }
+  static __device__ __forceinline__ f32x4 mma_f32rhs(const Vec& a, const float* v, f32x4 c) {
+    float x[8];
+    to_f32(a, x);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) c = __builtin_amdgcn_mfma_f32_16x16x4f32(x[e], v[e], c, 0, 0, 0);
+    return c;
+  }
+};
 
 // ---------------------------------------------------------------------------
 // plan
 // ---------------------------------------------------------------------------
-constexpr int kPlanThreads = 256;
+constexpr int kPlanSmallT = 1024;     // one 1024-thread block sorts in LDS
+constexpr int kPlanThreads = 256;     // multi-block rank counting
 constexpr int kPlanTokPerBlock = 64;  // four lanes count the rank of one token
 constexpr int kPlanChunk = 2048;      // keys staged in LDS per pass
+constexpr int kMaxGroups = 72;        // centroid groups: C + 1 <= 65
 
 // Total order key (centroid, slot, token), -1 ids first: each field is shifted by
-// one so that -1 becomes 0.  Fields are 21 bits wide (T, slots, centroids < 2^21 - 1).
+// one so that -1 becomes 0.  Fields are 21 bits wide.
 __device__ __forceinline__ uint64_t plan_key(int c, int u, int t) {
   return (uint64_t(uint32_t(c + 1)) << 42) | (uint64_t(uint32_t(u + 1)) << 21) |
          uint64_t(uint32_t(t));
 }
 
-// Exclusive count of `pred` over the 256 threads of a block, and the block total.
+// Exclusive count of `pred` over the threads of the block, and the total.
 __device__ __forceinline__ int block_excl_count(bool pred, int* s_wave, int& total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
   const uint64_t m = __ballot(pred);
   const int in_wave = (int)__builtin_amdgcn_mbcnt_hi(
       (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
   if (lane == 0) s_wave[wave] = __popcll(m);
   __syncthreads();
   int off = 0, tot = 0;
-#pragma unroll
-  for (int w = 0; w < kPlanThreads / 64; ++w) {
+  for (int w = 0; w < nw; ++w) {
     const int c = s_wave[w];
     off += (w < wave) ? c : 0;
     tot += c;
@@ -83,13 +180,143 @@ __device__ __forceinline__ int block_excl_count(bool pred, int* s_wave, int& tot
   return off + in_wave;
 }
 
-// Rank of every token in the (c, u, t) order by counting smaller keys, then the
-// last block to arrive cuts the sorted order into segments and groups.
-__global__ void __launch_bounds__(kPlanThreads) k_plan(PlanBuffers b, int T) {
+struct PlanShared {
+  int s_wave[16];
+  int g_start[kMaxGroups + 1];
+  int g_c[kMaxGroups];
+  int g_tile[kMaxGroups + 1];
+  int n_seg, n_grp, n_tiles;
+};
+
+// Segments, groups and tiles from the sorted order.  Runs in one block;
+// srt / srt_c are read from LDS (small batches) or global memory.
+__device__ void plan_finish(const PlanArgs& a, const int4* srt, const int32_t* srt_c, PlanShared& sh) {
+  const PlanBuffers& b = a.b;
+  const int T = a.T, M = a.M, tid = threadIdx.x, nt = blockDim.x;
+  int seg_base = 0, grp_base = 0;
+  for (int base = 0; base < T; base += nt) {
+    const int i = base + tid;
+    int c = 0, u = 0;
+    bool ns = false, ng = false;
+    if (i < T) {
+      c = srt_c[i];
+      u = srt[i].y;
+      if (i == 0) {
+        ns = ng = true;
+      } else {
+        const int cp = srt_c[i - 1], up = srt[i - 1].y;
+        ng = (c != cp);
+        ns = ng || (u != up);
+      }
+    }
+    int seg_tot, grp_tot;
+    const int sr = block_excl_count(ns, sh.s_wave, seg_tot);
+    const int gr = block_excl_count(ng, sh.s_wave, grp_tot);
+    if (ns) {
+      const int s = seg_base + sr;
+      b.seg_off[s] = i;
+      b.seg_c[s] = c;
+      b.seg_u[s] = u;
+    }
+    if (ng) {
+      const int g = grp_base + gr;
+      b.grp_off[g] = seg_base + sr;
+      b.grp_tok[g] = i;
+      b.grp_c[g] = c;
+      if (g < kMaxGroups) {
+        sh.g_start[g] = i;
+        sh.g_c[g] = c;
+      }
+    }
+    seg_base += seg_tot;
+    grp_base += grp_tot;
+  }
+  if (tid == 0) {
+    const int ng = grp_base < kMaxGroups ? grp_base : kMaxGroups;
+    sh.g_start[ng] = T;
+    int acc = 0;
+    for (int g = 0; g < ng; ++g) {
+      sh.g_tile[g] = acc;
+      acc += (sh.g_start[g + 1] - sh.g_start[g] + M - 1) / M;
+    }
+    sh.g_tile[ng] = acc;
+    sh.n_seg = seg_base;
+    sh.n_grp = ng;
+    sh.n_tiles = acc;
+    b.seg_off[seg_base] = T;
+    b.grp_off[grp_base] = seg_base;
+    b.grp_tok[grp_base] = T;
+  }
+  __syncthreads();
+  const int ng = sh.n_grp, n_tiles = sh.n_tiles;
+  const bool fits = (size_t)n_tiles * (M + 1) <= b.tile_cap && n_tiles <= b.tiles_max && grp_base < kMaxGroups;
+  if (fits) {
+    for (int e = tid; e < n_tiles * (M + 1); e += nt) {
+      const int tau = e / (M + 1), k = e % (M + 1);
+      int lo = 0, hi = ng - 1;  // last group whose first tile <= tau
+      while (lo < hi) {
+        const int mid = (lo + hi + 1) >> 1;
+        if (sh.g_tile[mid] <= tau) lo = mid;
+        else hi = mid - 1;
+      }
+      const int i0 = sh.g_start[lo] + (tau - sh.g_tile[lo]) * M;
+      const int n = min(M, sh.g_start[lo + 1] - i0);
+      int4 rec;
+      if (k == 0) rec = make_int4(i0, n, sh.g_c[lo], 0);
+      else if (k - 1 < n) rec = srt[i0 + k - 1];
+      else rec = make_int4(0, -1, 0, 0);
+      b.tiles[e] = rec;
+    }
+    for (int t = tid; t < n_tiles; t += nt) {
+      b.arrive[t] = 0u;
+      b.ready[t] = 0u;
+    }
+  }
+  if (tid == 0) {
+    b.meta[kMetaNSeg] = sh.n_seg;
+    b.meta[kMetaNGrp] = grp_base;
+    b.meta[kMetaT] = T;
+    b.meta[kMetaNTiles] = fits ? n_tiles : -1;
+    b.meta[kMetaErr] = 0;
+  }
+}
+
+// Batches of up to kPlanSmallT tokens: one block, everything in LDS.
+__global__ void __launch_bounds__(kPlanSmallT) k_plan_small(PlanArgs a) {
+  __shared__ uint64_t skey[kPlanSmallT];
+  __shared__ int4 s_srt[kPlanSmallT];
+  __shared__ int32_t s_c[kPlanSmallT];
+  __shared__ PlanShared sh;
+  const int T = a.T, t = threadIdx.x;
+  int4 m = make_int4(0, 0, 0, 0);
+  uint64_t my = ~0ull;
+  if (t < T) {
+    m = a.b.maps[t];
+    my = plan_key(m.x, m.y, t);
+    skey[t] = my;
+  }
+  __syncthreads();
+  if (t < T) {
+    int cnt = 0;
+    for (int i = 0; i < T; ++i) cnt += (skey[i] < my) ? 1 : 0;
+    s_srt[cnt] = make_int4(t, m.y, m.z, m.w);
+    s_c[cnt] = m.x;
+    a.b.perm[cnt] = t;
+    a.b.srt[cnt] = make_int4(t, m.y, m.z, m.w);
+    a.b.srt_c[cnt] = m.x;
+  }
+  __syncthreads();
+  plan_finish(a, s_srt, s_c, sh);
+}
+
+// Larger batches: rank by counting smaller keys across blocks; the last block to
+// arrive finishes the plan from global memory.
+__global__ void __launch_bounds__(kPlanThreads) k_plan_large(PlanArgs a) {
   __shared__ uint64_t skey[kPlanChunk];
-  __shared__ int s_wave[kPlanThreads / 64];
+  __shared__ PlanShared sh;
   __shared__ int s_last;
-  const int tid = threadIdx.x;
+  const PlanBuffers& b = a.b;
+  const int T = a.T, tid = threadIdx.x;
   const int t = blockIdx.x * kPlanTokPerBlock + (tid >> 2);
   const int q = tid & 3;
   int4 mine = make_int4(0, 0, 0, 0);
@@ -116,279 +343,323 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan(PlanBuffers b, int T) {
     b.srt[cnt] = make_int4(t, mine.y, mine.z, mine.w);
     b.srt_c[cnt] = mine.x;
   }
-
-  // the last block to arrive sees every block's scatter
-  __threadfence();
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
   __syncthreads();
-  if (tid == 0) s_last = (atomicAdd(b.counter, 1u) == gridDim.x - 1) ? 1 : 0;
+  if (tid == 0) {
+    const uint32_t old = __hip_atomic_fetch_add(b.counter, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+    s_last = (old == gridDim.x - 1) ? 1 : 0;
+  }
   __syncthreads();
   if (!s_last) return;
-  __threadfence();
-
-  int seg_base = 0, grp_base = 0;
-  for (int base = 0; base < T; base += kPlanThreads) {
-    const int i = base + tid;
-    int c = 0, u = 0;
-    bool ns = false, ng = false;
-    if (i < T) {
-      c = b.srt_c[i];
-      u = b.srt[i].y;
-      if (i == 0) {
-        ns = ng = true;
-      } else {
-        const int cp = b.srt_c[i - 1], up = b.srt[i - 1].y;
-        ng = (c != cp);
-        ns = ng || (u != up);
-      }
-    }
-    int seg_tot, grp_tot;
-    const int sr = block_excl_count(ns, s_wave, seg_tot);
-    const int gr = block_excl_count(ng, s_wave, grp_tot);
-    if (ns) {
-      const int s = seg_base + sr;
-      b.seg_off[s] = i;
-      b.seg_c[s] = c;
-      b.seg_u[s] = u;
-    }
-    if (ng) {
-      const int g = grp_base + gr;
-      b.grp_off[g] = seg_base + sr;
-      b.grp_tok[g] = i;
-      b.grp_c[g] = c;
-    }
-    seg_base += seg_tot;
-    grp_base += grp_tot;
-  }
-  if (tid == 0) {
-    b.seg_off[seg_base] = T;
-    b.grp_off[grp_base] = seg_base;
-    b.grp_tok[grp_base] = T;
-    b.meta[0] = seg_base;
-    b.meta[1] = grp_base;
-    b.meta[2] = T;
-    *b.counter = 0u;
-  }
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  plan_finish(a, b.srt, b.srt_c, sh);
+  if (tid == 0) __hip_atomic_store(b.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // ---------------------------------------------------------------------------
-// tiles: groups of equal centroid cut into runs of at most M sorted tokens
+// apply
 // ---------------------------------------------------------------------------
-struct TileInfo {
-  int i0, n, c;
-};
+__host__ __device__ constexpr int tile_bytes(int M) { return ((M + 1) * 16 + 255) / 256 * 256; }
 
-// Wave 0 finds tile `tile` (in group order); writes n = 0 if there is none.
-__device__ void find_tile(const int32_t* grp_tok, const int32_t* grp_c, const int32_t* meta,
-                          int M, int tile, TileInfo* out) {
-  const int lane = threadIdx.x & 63;
-  if (lane == 0) out->n = 0;
-  const int n_grp = meta[1];
-  int carry = 0;
-  for (int gb = 0; gb < n_grp; gb += 64) {
-    const int g = gb + lane;
-    int start = 0, len = 0, cnt = 0;
-    if (g < n_grp) {
-      start = grp_tok[g];
-      len = grp_tok[g + 1] - start;
-      cnt = (len + M - 1) / M;
-    }
-    int incl = cnt;
-#pragma unroll
-    for (int off = 1; off < 64; off <<= 1) {
-      const int v = __shfl_up(incl, off);
-      if (lane >= off) incl += v;
-    }
-    const int excl = carry + incl - cnt;
-    if (g < n_grp && tile >= excl && tile < excl + cnt) {
-      const int k = tile - excl;
-      out->i0 = start + k * M;
-      out->n = min(M, len - k * M);
-      out->c = grp_c[g];
-    }
-    carry += __shfl(incl, 63);
-  }
-}
-
-// ---------------------------------------------------------------------------
-// shrink: split-K partial sums of v = x [A_c | A_u] for one tile and one K range
-// ---------------------------------------------------------------------------
-constexpr int kKS = 64;               // K sub-chunk staged in LDS
-constexpr int kLds = kKS + 1;         // padded row stride (floats), avoids bank conflicts
-constexpr int kMaxR = 128 + 16;       // r_c + r_u_max upper bound
-constexpr int kQ = (kTileM * kMaxR + 255) / 256;
-constexpr int kLdsBudget = 120 * 1024;   // largest dynamic LDS any apply launch requests
-
-template <typename E>
-__global__ void __launch_bounds__(256) k_shrink(ApplyArgs a) {
-  extern __shared__ float lds[];
-  __shared__ TileInfo s_tile;
-  __shared__ int s_row[kTileM], s_r[kTileM];
-  __shared__ const E* s_au[kTileM];
-  const int tid = threadIdx.x;
-  if (tid < 64) find_tile(a.grp_tok, a.grp_c, a.meta, kTileM, blockIdx.x, &s_tile);
+// Shrink block: tile `tau`, K range `s` of the apply.
+template <typename E, int MB, int RU>
+__device__ void shrink_block(const ApplyArgs& a, int tau, int s, char* lds) {
+  using O = Ops<E>;
+  using Vec = typename O::Vec;
+  constexpr int M = 16 * MB, KW = 4 / MB;
+  int4* s_tile = reinterpret_cast<int4*>(lds);
+  float* s_part = reinterpret_cast<float*>(lds + tile_bytes(M));   // [KW][M][R]
+  __shared__ int s_last;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int4* trec = a.tiles + (size_t)tau * (M + 1);
+  for (int i = tid; i < M + 1; i += 256) s_tile[i] = trec[i];
   __syncthreads();
-  const int n = s_tile.n;
-  if (n == 0) return;
-  const int i0 = s_tile.i0, c = s_tile.c;
-  if (tid < n) {
-    const int4 e = a.srt[i0 + tid];
-    const int r = (e.y >= 0) ? e.z : 0;
-    s_row[tid] = e.x;
-    s_r[tid] = r;
-    s_au[tid] = r ? reinterpret_cast<const E*>(a.pool + (size_t)e.y * a.slot_stride) +
-                        (int64_t)r * a.tab_prefix
-                  : nullptr;
-  }
-  __syncthreads();
+  const int i0 = s_tile[0].x, n = s_tile[0].y, c = s_tile[0].z;
+  const int R = a.R, in = a.in_dim, rc = a.r_c;
+  const bool has_c = c >= 0 && rc > 0;
+  const int mb = wave % MB, kq = wave / MB;
+  const int tl = mb * 16 + (lane & 15);        // token of this lane within the tile
+  const int kseg = (lane >> 4) * 8;             // k offset of this lane inside a 32-wide step
+  const int4 tk = s_tile[1 + tl];
+  const bool tok_ok = tl < n;
+  const int ru = (tok_ok && tk.y >= 0) ? tk.z : 0;
+  const E* xrow = reinterpret_cast<const E*>(a.x) + (size_t)(tok_ok ? tk.x : 0) * in;
+  const E* au = ru ? reinterpret_cast<const E*>(a.pool + (size_t)tk.y * a.slot_stride) + (int64_t)ru * a.tab_prefix
+                   : nullptr;
+  const E* at_c = reinterpret_cast<const E*>(a.cent_at) + (size_t)(has_c ? c : 0) * rc * in;
+  const int NB = (rc + 15) >> 4;                // 16-rank blocks of the centroid
 
-  const int R = a.R, rc = (c >= 0) ? a.r_c : 0, rum = a.r_u_max, in = a.in_dim;
-  float* X = lds;                        // [kTileM][kLds]
-  float* AC = X + kTileM * kLds;         // [r_c][kLds]
-  float* AU = AC + a.r_c * kLds;         // [kTileM * r_u_max][kLds]
-  const E* at_c = reinterpret_cast<const E*>(a.cent_at) + (size_t)(c >= 0 ? c : 0) * a.r_c * in;
-  const int k0 = blockIdx.y * a.Kc, k1 = min(in, k0 + a.Kc);
+  const int kw_len = a.Kc / KW;                 // a multiple of 32
+  const int kbeg = s * a.Kc + kq * kw_len;
+  const int kend = min(in, kbeg + kw_len);
 
-  float acc[kQ];
+  f32x4 acc[kMaxRc / 16];
 #pragma unroll
-  for (int q = 0; q < kQ; ++q) acc[q] = 0.f;
+  for (int nb = 0; nb < kMaxRc / 16; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float accu[RU];
+#pragma unroll
+  for (int j = 0; j < RU; ++j) accu[j] = 0.f;
 
-  for (int kb = k0; kb < k1; kb += kKS) {
-    const int kw = min(kKS, k1 - kb);
-    __syncthreads();
-    for (int v = tid; v < kTileM * (kKS / 8); v += 256) {
-      const int i = v / (kKS / 8), kk = (v % (kKS / 8)) * 8;
-      float tmp[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-      if (i < n && kk < kw) ld8(reinterpret_cast<const E*>(a.x) + (size_t)s_row[i] * in + kb + kk, tmp);
+  for (int k = kbeg; k < kend; k += 32) {
+    const int kk = k + kseg;
+    const bool kin = kk < kend;
+    const Vec xa = (tok_ok && kin) ? O::load(xrow + kk) : O::zero();
+    if (has_c) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) X[i * kLds + kk + e] = tmp[e];
-    }
-    for (int v = tid; v < rc * (kKS / 8); v += 256) {
-      const int j = v / (kKS / 8), kk = (v % (kKS / 8)) * 8;
-      float tmp[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-      if (kk < kw) ld8(at_c + (size_t)j * in + kb + kk, tmp);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) AC[j * kLds + kk + e] = tmp[e];
-    }
-    for (int v = tid; v < kTileM * rum * (kKS / 8); v += 256) {
-      const int row = v / (kKS / 8), kk = (v % (kKS / 8)) * 8;
-      const int i = row / rum, j = row % rum;
-      float tmp[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-      if (i < n && j < s_r[i] && kk < kw) ld8(s_au[i] + (size_t)j * in + kb + kk, tmp);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) AU[row * kLds + kk + e] = tmp[e];
-    }
-    __syncthreads();
-#pragma unroll
-    for (int q = 0; q < kQ; ++q) {
-      const int o = tid + 256 * q;
-      if (o < n * R) {
-        const int i = o / R, j = o % R;
-        const float* ar = nullptr;
-        if (j < rc) ar = AC + j * kLds;
-        else if (j >= a.r_c && j - a.r_c < s_r[i]) ar = AU + (i * rum + (j - a.r_c)) * kLds;
-        if (ar) {
-          const float* xr = X + i * kLds;
-          float s = 0.f;
-#pragma unroll 16
-          for (int kk = 0; kk < kKS; ++kk) s += xr[kk] * ar[kk];
-          acc[q] += s;
+      for (int nb = 0; nb < kMaxRc / 16; ++nb) {
+        if (nb < NB) {
+          const int j = nb * 16 + (lane & 15);
+          const Vec bv = (kin && j < rc) ? O::load(at_c + (size_t)j * in + kk) : O::zero();
+          acc[nb] = O::mma(xa, bv, acc[nb]);
         }
       }
     }
-  }
-  float* P = a.partials + ((size_t)blockIdx.y * a.T + i0) * R;
 #pragma unroll
-  for (int q = 0; q < kQ; ++q) {
-    const int o = tid + 256 * q;
-    if (o < n * R) P[o] = acc[q];
-  }
-}
-
-// ---------------------------------------------------------------------------
-// expand: y rows of one tile, one column chunk: y += v [g*B_c ; B_u]
-// ---------------------------------------------------------------------------
-template <typename E>
-__global__ void __launch_bounds__(256) k_expand(ApplyArgs a) {
-  extern __shared__ float lds[];
-  __shared__ TileInfo s_tile;
-  __shared__ int s_row[kTileM], s_r[kTileM];
-  __shared__ float s_g[kTileM];
-  __shared__ const E* s_bu[kTileM];
-  const int tid = threadIdx.x;
-  if (tid < 64) find_tile(a.grp_tok, a.grp_c, a.meta, kTileM, blockIdx.x, &s_tile);
-  __syncthreads();
-  const int n = s_tile.n;
-  if (n == 0) return;
-  const int i0 = s_tile.i0, c = s_tile.c;
-  const int R = a.R, rc = (c >= 0) ? a.r_c : 0, out = a.out_dim, NC = a.NC;
-  if (tid < n) {
-    const int4 e = a.srt[i0 + tid];
-    const int r = (e.y >= 0) ? e.z : 0;
-    s_row[tid] = e.x;
-    s_r[tid] = r;
-    s_g[tid] = __int_as_float(e.w);
-    s_bu[tid] = r ? reinterpret_cast<const E*>(a.pool + (size_t)e.y * a.slot_stride) +
-                        (int64_t)r * (a.tab_prefix + a.in_dim)
-                  : nullptr;
-  }
-  __syncthreads();
-
-  float* V = lds;                  // [kTileM][R]
-  float* BC = V + kTileM * R;      // [r_c][NC]
-  for (int idx = tid; idx < n * R; idx += 256) {
-    const float* P = a.partials + (size_t)i0 * R + idx;
-    float s = 0.f;
-    for (int sp = 0; sp < a.S; ++sp) s += P[(size_t)sp * a.T * R];
-    const int i = idx / R, j = idx % R;
-    if (j < a.r_c) s *= s_g[i];
-    V[idx] = s;
-  }
-  const int n0 = blockIdx.y * NC;
-  const int ncols = min(NC, out - n0);
-  const E* bc = reinterpret_cast<const E*>(a.cent_b) + (size_t)(c >= 0 ? c : 0) * a.r_c * out;
-  for (int v = tid; v < rc * (NC / 8); v += 256) {
-    const int j = v / (NC / 8), cc = (v % (NC / 8)) * 8;
-    float tmp[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    if (cc < ncols) ld8(bc + (size_t)j * out + n0 + cc, tmp);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) BC[j * NC + cc + e] = tmp[e];
-  }
-  __syncthreads();
-
-  const int CG = NC / 8, TL = 256 / CG;
-  const int cg = tid % CG, tl = tid / CG;
-  if (tl >= TL || cg * 8 >= ncols) return;
-  const int col = n0 + cg * 8;
-  for (int i = tl; i < n; i += TL) {
-    float acc[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    const float* vi = V + i * R;
-    for (int j = 0; j < rc; ++j) {
-      const float vj = vi[j];
-      const float* b = BC + j * NC + cg * 8;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += vj * b[e];
+    for (int j = 0; j < RU; ++j) {
+      if (j < ru && kin) accu[j] = O::dot(xa, O::load(au + (size_t)j * in + kk), accu[j]);
     }
-    for (int j = 0; j < s_r[i]; ++j) {
-      float b[8];
-      ld8(s_bu[i] + (size_t)j * out + col, b);
-      const float vj = vi[a.r_c + j];
+  }
+  // residual: lanes l, l^16, l^32, l^48 hold the four k offsets of one token
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += vj * b[e];
+  for (int j = 0; j < RU; ++j) {
+    accu[j] += __shfl_xor(accu[j], 16);
+    accu[j] += __shfl_xor(accu[j], 32);
+  }
+  // this wave's partial -> LDS [kq][token][j]
+  float* P = s_part + (size_t)kq * M * R;
+#pragma unroll
+  for (int nb = 0; nb < kMaxRc / 16; ++nb) {
+    if (nb < NB) {
+      const int j = nb * 16 + (lane & 15);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int t = mb * 16 + 4 * (lane >> 4) + e;
+        if (j < rc) P[t * R + j] = has_c ? acc[nb][e] : 0.f;
+      }
     }
-    E* yp = reinterpret_cast<E*>(a.y) + (size_t)s_row[i] * out + col;
-    float yv[8];
-    ld8(yp, yv);
+  }
+  if (lane < 16) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) yv[e] += acc[e];
-    st8(yp, yv);
+    for (int j = 0; j < RU; ++j)
+      if (j < a.r_u_max) P[tl * R + rc + j] = (j < ru) ? accu[j] : 0.f;
+  }
+  __syncthreads();
+
+  if (a.S == 1) {
+    // single K range: v directly, no partials
+    for (int idx = tid; idx < n * R; idx += 256) {
+      float v = 0.f;
+#pragma unroll
+      for (int q = 0; q < KW; ++q) v += s_part[(size_t)q * M * R + idx];
+      const int t = idx / R, j = idx - t * R;
+      if (j < rc) v *= __int_as_float(s_tile[1 + t].w);
+      a.v[(size_t)i0 * R + idx] = v;
+    }
+  } else {
+    float* G = a.partials + ((size_t)s * a.T + i0) * R;
+    for (int idx = tid; idx < n * R; idx += 256) {
+      float v = 0.f;
+#pragma unroll
+      for (int q = 0; q < KW; ++q) v += s_part[(size_t)q * M * R + idx];
+      G[idx] = v;
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+    __syncthreads();
+    if (tid == 0) {
+      const uint32_t old = __hip_atomic_fetch_add(a.arrive + tau, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+      const bool last = (old == (uint32_t)a.S - 1u);
+      if (last) __hip_atomic_store(a.arrive + tau, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      s_last = last ? 1 : 0;
+    }
+    __syncthreads();
+    if (!s_last) return;
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    const float* P0 = a.partials + (size_t)i0 * R;
+    const size_t stride = (size_t)a.T * R;
+    for (int idx = tid; idx < n * R; idx += 256) {
+      float v = 0.f;
+      for (int sp = 0; sp < a.S; ++sp) v += P0[sp * stride + idx];
+      const int t = idx / R, j = idx - t * R;
+      if (j < rc) v *= __int_as_float(s_tile[1 + t].w);
+      a.v[(size_t)i0 * R + idx] = v;
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+  __syncthreads();
+  if (tid == 0) __hip_atomic_store(a.ready + tau, a.epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Expand block: tile `tau`, columns [q * kNC, q * kNC + kNC) of y.
+template <typename E, int MB, int RU>
+__device__ void expand_block(const ApplyArgs& a, int tau, int q, char* lds) {
+  using O = Ops<E>;
+  using Vec = typename O::Vec;
+  constexpr int M = 16 * MB;
+  constexpr int CG = kNC / 8;                   // 8-column groups per block
+  constexpr int ITEMS = M * CG / 256;           // (token, column group) items per thread
+  constexpr int RP = RU < 2 ? RU : 2;           // residual ranks prefetched
+  constexpr int NBW = kNC / 16 / 4;             // 16-column blocks per wave
+  constexpr int KS = kMaxRc / 32;               // 32-rank steps, at most
+  int4* s_tile = reinterpret_cast<int4*>(lds);
+  float* s_v = reinterpret_cast<float*>(lds + tile_bytes(M));     // [M][R]
+  float* s_y = s_v + (size_t)M * a.R;                             // [M][kNC]
+  __shared__ int s_abort;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int4* trec = a.tiles + (size_t)tau * (M + 1);
+  for (int i = tid; i < M + 1; i += 256) s_tile[i] = trec[i];
+  __syncthreads();
+  const int i0 = s_tile[0].x, n = s_tile[0].y, c = s_tile[0].z;
+  const int R = a.R, out = a.out_dim, rc = a.r_c, in = a.in_dim;
+  const bool has_c = c >= 0 && rc > 0;
+  const int n0 = q * kNC;
+
+  // ---- prefetch: y and B_u slices of this thread's items, B_c^T operands ----
+  Vec yold[ITEMS];
+  Vec bu[ITEMS][RP > 0 ? RP : 1];
+#pragma unroll
+  for (int it = 0; it < ITEMS; ++it) {
+    const int idx = tid + 256 * it, t = idx / CG, col = n0 + (idx % CG) * 8;
+    const int4 tk = s_tile[1 + t];
+    const bool ok = t < n && col < out;
+    const int ru = (ok && tk.y >= 0) ? tk.z : 0;
+    yold[it] = ok ? O::load(reinterpret_cast<const E*>(a.y) + (size_t)tk.x * out + col) : O::zero();
+    const E* bup = ru ? reinterpret_cast<const E*>(a.pool + (size_t)tk.y * a.slot_stride) +
+                            (int64_t)ru * (a.tab_prefix + in)
+                      : nullptr;
+#pragma unroll
+    for (int j = 0; j < RP; ++j) bu[it][j] = (j < ru) ? O::load(bup + (size_t)j * out + col) : O::zero();
+  }
+  const int KSn = (rc + 31) >> 5;
+  Vec bct[NBW][KS];
+  const E* bt = reinterpret_cast<const E*>(a.cent_bt) + (size_t)(has_c ? c : 0) * out * rc;
+#pragma unroll
+  for (int w = 0; w < NBW; ++w) {
+    const int col = n0 + (wave + 4 * w) * 16 + (lane & 15);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int j = ks * 32 + (lane >> 4) * 8;
+      bct[w][ks] = (has_c && ks < KSn && col < out && j < rc) ? O::load(bt + (size_t)col * rc + j) : O::zero();
+    }
+  }
+
+  // ---- wait for the tile's v ----
+  if (tid == 0) {
+    uint32_t spins = 0;
+    int abort = 0;
+    while (__hip_atomic_load(a.ready + tau, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) != a.epoch) {
+      __builtin_amdgcn_s_sleep(2);
+      if (++spins > kSpinMax) {
+        atomicAdd(a.meta + kMetaErr, 1);
+        abort = 1;
+        break;
+      }
+    }
+    s_abort = abort;
+  }
+  __syncthreads();
+  if (s_abort) return;
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+  for (int idx = tid; idx < M * R; idx += 256) s_v[idx] = (idx < n * R) ? a.v[(size_t)i0 * R + idx] : 0.f;
+  __syncthreads();
+
+  // ---- centroid part on MFMA: y^T block [16 cols x 16 tokens] = B_c^T . v_c^T ----
+  if (has_c) {
+#pragma unroll
+    for (int w = 0; w < NBW; ++w) {
+      const int cb = (wave + 4 * w) * 16;       // first column of the block, local
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+        const int t = mb * 16 + (lane & 15);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          if (ks < KSn) {
+            const int j = ks * 32 + (lane >> 4) * 8;
+            float vv[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) vv[e] = (j + e < rc) ? s_v[t * R + j + e] : 0.f;
+            acc = O::mma_f32rhs(bct[w][ks], vv, acc);
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s_y[t * kNC + cb + 4 * (lane >> 4) + e] = acc[e];
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- residual part, add, round, store ----
+#pragma unroll
+  for (int it = 0; it < ITEMS; ++it) {
+    const int idx = tid + 256 * it, t = idx / CG, cl = (idx % CG) * 8, col = n0 + cl;
+    if (t >= n || col >= out) continue;
+    const int4 tk = s_tile[1 + t];
+    const int ru = tk.y >= 0 ? tk.z : 0;
+    float accv[8], yv[8];
+    if (has_c) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) accv[e] = s_y[t * kNC + cl + e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) accv[e] = 0.f;
+    }
+    const float* vt = s_v + t * R + rc;
+#pragma unroll
+    for (int j = 0; j < RU; ++j) {
+      if (j < ru) {
+        Vec bv;
+        if (j < RP) {
+          bv = bu[it][j < RP ? j : 0];
+        } else {
+          const E* bup = reinterpret_cast<const E*>(a.pool + (size_t)tk.y * a.slot_stride) +
+                         (int64_t)ru * (a.tab_prefix + in);
+          bv = O::load(bup + (size_t)j * out + col);
+        }
+        float b8[8];
+        O::to_f32(bv, b8);
+        const float vj = vt[j];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) accv[e] = fmaf(vj, b8[e], accv[e]);
+      }
+    }
+    O::to_f32(yold[it], yv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) yv[e] += accv[e];
+    O::store(reinterpret_cast<E*>(a.y) + (size_t)tk.x * out + col, yv);
   }
 }
 
-size_t shrink_lds(const ApplyArgs& a) {
-  return sizeof(float) * (size_t)(kTileM + a.r_c + kTileM * a.r_u_max) * kLds;
+template <typename E, int MB, int RU>
+__global__ void __launch_bounds__(256) k_apply(ApplyArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  const int b = blockIdx.x;
+  const int n_shrink = a.n_tiles * a.S;
+  if (b < n_shrink) {
+    shrink_block<E, MB, RU>(a, b % a.n_tiles, b / a.n_tiles, lds);
+  } else {
+    const int e = b - n_shrink;
+    expand_block<E, MB, RU>(a, e % a.n_tiles, e / a.n_tiles, lds);
+  }
 }
-size_t expand_lds(const ApplyArgs& a) {
-  return sizeof(float) * ((size_t)kTileM * a.R + (size_t)a.r_c * a.NC);
+
+size_t apply_lds(int M, int R) {
+  const size_t tb = (size_t)tile_bytes(M);
+  const size_t shrink = tb + sizeof(float) * 64 * (size_t)R;           // KW * M == 64
+  const size_t expand = tb + sizeof(float) * ((size_t)M * R + (size_t)M * kNC);
+  return shrink > expand ? shrink : expand;
+}
+
+template <typename E, int RU>
+hipError_t launch_typed(const ApplyArgs& a, int M, hipStream_t s) {
+  const dim3 grid(a.n_tiles * (a.S + a.n_col)), block(256);
+  const size_t lds = apply_lds(M, a.R);
+  switch (M) {
+    case 16: hipLaunchKernelGGL((k_apply<E, 1, RU>), grid, block, lds, s, a); break;
+    case 32: hipLaunchKernelGGL((k_apply<E, 2, RU>), grid, block, lds, s, a); break;
+    case 64: hipLaunchKernelGGL((k_apply<E, 4, RU>), grid, block, lds, s, a); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 }  // namespace
@@ -402,29 +673,26 @@ hipError_t kernels_init(int device) {
   int lds_max = 0;
   hipError_t e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, device);
   if (e != hipSuccess) return e;
-  if (lds_max < kLdsBudget) return hipErrorInvalidConfiguration;
+  if ((size_t)lds_max < apply_lds(64, kMaxRc + kMaxRu) + 1024) return hipErrorInvalidConfiguration;
   done[device] = true;
   return hipSuccess;
 }
 
-hipError_t launch_plan(const PlanBuffers& b, int32_t T, int32_t, hipStream_t s) {
-  if (T <= 0) return hipSuccess;
-  const int blocks = (T + kPlanTokPerBlock - 1) / kPlanTokPerBlock;
-  hipLaunchKernelGGL(k_plan, dim3(blocks), dim3(kPlanThreads), 0, s, b, T);
+hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
+  if (a.T <= 0) return hipSuccess;
+  if (a.T <= kPlanSmallT) {
+    hipLaunchKernelGGL(k_plan_small, dim3(1), dim3(kPlanSmallT), 0, s, a);
+  } else {
+    const int blocks = (a.T + kPlanTokPerBlock - 1) / kPlanTokPerBlock;
+    hipLaunchKernelGGL(k_plan_large, dim3(blocks), dim3(kPlanThreads), 0, s, a);
+  }
   return hipGetLastError();
 }
 
-hipError_t launch_apply(const ApplyArgs& a, int bf16, int32_t tiles_ub, hipStream_t s) {
-  if (a.T <= 0 || tiles_ub <= 0) return hipSuccess;
-  const dim3 g1(tiles_ub, a.S), g2(tiles_ub, (a.out_dim + a.NC - 1) / a.NC);
-  if (bf16) {
-    hipLaunchKernelGGL(k_shrink<uint16_t>, g1, dim3(256), shrink_lds(a), s, a);
-    hipLaunchKernelGGL(k_expand<uint16_t>, g2, dim3(256), expand_lds(a), s, a);
-  } else {
-    hipLaunchKernelGGL(k_shrink<float>, g1, dim3(256), shrink_lds(a), s, a);
-    hipLaunchKernelGGL(k_expand<float>, g2, dim3(256), expand_lds(a), s, a);
-  }
-  return hipGetLastError();
+hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s) {
+  if (a.T <= 0 || a.n_tiles <= 0) return hipSuccess;
+  if (a.r_u_max <= 2) return bf16 ? launch_typed<uint16_t, 2>(a, M, s) : launch_typed<float, 2>(a, M, s);
+  return bf16 ? launch_typed<uint16_t, kMaxRu>(a, M, s) : launch_typed<float, kMaxRu>(a, M, s);
 }
 
 }  // namespace salt

@@ -49,7 +49,11 @@ struct salt_plan {
   bool built = false;
   std::vector<int32_t> slots;       // distinct referenced slots
   std::vector<int32_t> slot_rank;   // rank of each at set_maps time
-  int32_t n_centroid_groups_ub = 0;
+  int32_t M = 16;                   // tokens per tile
+  int32_t n_tiles = 0;
+  int32_t n_groups_c = 0;           // groups with a centroid
+  int64_t sum_ru = 0;               // residual rank summed over tokens
+  uint32_t epoch = 0;               // applies since the last build
 };
 
 struct salt_ctx {
@@ -106,6 +110,18 @@ salt_status hip_fail(salt_ctx* c, hipError_t e, const char* what) {
     if (e_ != hipSuccess) return hip_fail((ctx), e_, #call);  \
   } while (0)
 
+// dst[i][o][j] = src[i][j][o] for n matrices of rc x out elements.
+template <typename W>
+void transpose_rank_major(const W* src, W* dst, size_t n, size_t rc, size_t out) {
+  for (size_t i = 0; i < n; ++i) {
+    const W* s = src + i * rc * out;
+    W* d = dst + i * out * rc;
+    for (size_t o0 = 0; o0 < out; o0 += 64)
+      for (size_t j = 0; j < rc; ++j)
+        for (size_t o = o0; o < std::min(out, o0 + 64); ++o) d[o * rc + j] = s[j * out + o];
+  }
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 hipError_t ring_record(EventRing& r, hipStream_t s, int64_t* seq_out) {
@@ -131,8 +147,8 @@ hipError_t ring_wait(EventRing& r, hipStream_t s, int64_t seq) {
 
 void free_plan_buffers(salt_plan* p) {
   PlanBuffers& b = p->dev;
-  void* ptrs[] = {b.maps, b.perm, b.srt, b.srt_c, b.seg_off, b.seg_c, b.seg_u,
-                  b.grp_off, b.grp_tok, b.grp_c, b.meta, b.counter, b.partials};
+  void* ptrs[] = {b.maps, b.perm, b.srt, b.srt_c, b.seg_off, b.seg_c, b.seg_u, b.grp_off,
+                  b.grp_tok, b.grp_c, b.tiles, b.arrive, b.ready, b.meta, b.counter, b.partials, b.v};
   for (void* q : ptrs)
     if (q) (void)hipFree(q);
   if (p->staging) (void)hipHostFree(p->staging);
@@ -210,10 +226,10 @@ salt_status salt_create(const salt_config* cfg, salt_ctx** out) {
   g_create_err = "invalid configuration";
   if (cfg->dtype != SALT_F32 && cfg->dtype != SALT_BF16) return SALT_ERR_INVALID_ARG;
   if (cfg->n_tables < 1 || !cfg->tables) return SALT_ERR_INVALID_ARG;
-  if (cfg->n_centroids < 0 || cfg->n_centroids > 64 || cfg->r_c < 0 || cfg->r_c > 128 ||
-      (cfg->n_centroids == 0) != (cfg->r_c == 0))
+  if (cfg->n_centroids < 0 || cfg->n_centroids > 64 || cfg->r_c < 0 || cfg->r_c > salt::kMaxRc ||
+      cfg->r_c % 8 != 0 || (cfg->n_centroids == 0) != (cfg->r_c == 0))
     return SALT_ERR_OUT_OF_RANGE;
-  if (cfg->n_slots < 1 || cfg->n_slots > (1 << 20) || cfg->r_u_max < 0 || cfg->r_u_max > 16)
+  if (cfg->n_slots < 1 || cfg->n_slots > (1 << 20) || cfg->r_u_max < 0 || cfg->r_u_max > salt::kMaxRu)
     return SALT_ERR_OUT_OF_RANGE;
   if (cfg->max_tokens < 1 || cfg->max_tokens > (1 << 20)) return SALT_ERR_OUT_OF_RANGE;
   for (int i = 0; i < cfg->n_tables; ++i) {
@@ -309,11 +325,18 @@ salt_status salt_pin_centroids(salt_ctx* ctx, int32_t table, int32_t c0, int32_t
   if (!At_host || !B_host) return fail(ctx, SALT_ERR_INVALID_ARG, "null centroid array");
   SALT_HIP(ctx, hipSetDevice(ctx->device));
   const salt_shape s = ctx->tables[table];
-  const size_t rc = ctx->cfg.r_c, es = ctx->esize;
-  const size_t a_bytes = (size_t)n * rc * s.in_dim * es, b_bytes = (size_t)n * rc * s.out_dim * es;
+  const size_t rc = ctx->cfg.r_c, es = ctx->esize, out = s.out_dim;
+  const size_t a_bytes = (size_t)n * rc * s.in_dim * es;
   SALT_HIP(ctx, hipMemcpy(ctx->cent_at[table] + (size_t)c0 * rc * s.in_dim * es, At_host, a_bytes,
                           hipMemcpyHostToDevice));
-  SALT_HIP(ctx, hipMemcpy(ctx->cent_b[table] + (size_t)c0 * rc * s.out_dim * es, B_host, b_bytes,
+  // B is kept transposed on the device, [C][out][r_c], so that the expand reads
+  // the 8 consecutive ranks of one output column with one 16-byte load
+  std::vector<char> bt((size_t)n * rc * out * es);
+  if (es == 2)
+    transpose_rank_major(static_cast<const uint16_t*>(B_host), reinterpret_cast<uint16_t*>(bt.data()), n, rc, out);
+  else
+    transpose_rank_major(static_cast<const uint32_t*>(B_host), reinterpret_cast<uint32_t*>(bt.data()), n, rc, out);
+  SALT_HIP(ctx, hipMemcpy(ctx->cent_b[table] + (size_t)c0 * rc * out * es, bt.data(), bt.size(),
                           hipMemcpyHostToDevice));
   for (int i = c0; i < c0 + n; ++i) ctx->cent_pinned[(size_t)table * ctx->cfg.n_centroids + i] = 1;
   return SALT_OK;
@@ -369,10 +392,14 @@ salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out) {
   salt_plan* p = new (std::nothrow) salt_plan();
   if (!p) return SALT_ERR_OUT_OF_MEMORY;
   const size_t T = (size_t)ctx->cfg.max_tokens;
-  const size_t R = (size_t)ctx->cfg.r_c + ctx->cfg.r_u_max;
+  const size_t R = std::max<size_t>(1, (size_t)ctx->cfg.r_c + ctx->cfg.r_u_max);
   PlanBuffers& b = p->dev;
-  // split-K partials: enough for (splits x tokens) up to max(8 * max_tokens, 64K)
-  b.partial_cap = std::max<size_t>(8 * T, 65536) * std::max<size_t>(R, 1);
+  // split-K partials for up to max(8 T, 64K) (split, token) pairs
+  b.partial_cap = std::max<size_t>(8 * T, 65536) * R;
+  // tiles: at most ceil(T / M) + one partial tile per centroid group (<= 65)
+  b.tiles_max = (int32_t)((T + 15) / 16 + 66);
+  b.tile_cap = 0;
+  for (size_t M : {16, 32, 64}) b.tile_cap = std::max(b.tile_cap, ((T + M - 1) / M + 66) * (M + 1));
   bool ok = hipMalloc((void**)&b.maps, T * sizeof(int4)) == hipSuccess &&
             hipMalloc((void**)&b.perm, T * 4) == hipSuccess &&
             hipMalloc((void**)&b.srt, T * sizeof(int4)) == hipSuccess &&
@@ -383,9 +410,13 @@ salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out) {
             hipMalloc((void**)&b.grp_off, (T + 1) * 4) == hipSuccess &&
             hipMalloc((void**)&b.grp_tok, (T + 1) * 4) == hipSuccess &&
             hipMalloc((void**)&b.grp_c, T * 4) == hipSuccess &&
-            hipMalloc((void**)&b.meta, 16 * 4) == hipSuccess &&
+            hipMalloc((void**)&b.tiles, b.tile_cap * sizeof(int4)) == hipSuccess &&
+            hipMalloc((void**)&b.arrive, (size_t)b.tiles_max * 4) == hipSuccess &&
+            hipMalloc((void**)&b.ready, (size_t)b.tiles_max * 4) == hipSuccess &&
+            hipMalloc((void**)&b.meta, salt::kMetaWords * 4) == hipSuccess &&
             hipMalloc((void**)&b.counter, 64 * 4) == hipSuccess &&
             hipMalloc((void**)&b.partials, b.partial_cap * 4) == hipSuccess &&
+            hipMalloc((void**)&b.v, T * R * 4) == hipSuccess &&
             hipHostMalloc((void**)&p->staging, T * sizeof(int4), hipHostMallocDefault) == hipSuccess;
   if (!ok) {
     (void)hipGetLastError();
@@ -395,7 +426,10 @@ salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out) {
   }
   hipError_t e = hipEventCreateWithFlags(&p->staged, hipEventDisableTiming);
   if (e == hipSuccess) e = hipMemset(b.counter, 0, 64 * 4);
-  if (e == hipSuccess) e = hipMemset(b.meta, 0, 16 * 4);
+  if (e == hipSuccess) e = hipMemset(b.meta, 0, salt::kMetaWords * 4);
+  if (e == hipSuccess) e = hipMemset(b.arrive, 0, (size_t)b.tiles_max * 4);
+  if (e == hipSuccess) e = hipMemset(b.ready, 0, (size_t)b.tiles_max * 4);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     free_plan_buffers(p);
     delete p;
@@ -443,25 +477,40 @@ salt_status salt_plan_set_maps(salt_ctx* ctx, salt_plan* plan, int32_t T, const 
     plan->staged_pending = false;
   }
   std::vector<int32_t> slots;
-  int cmin = C, cmax = -2;
+  std::vector<int32_t> per_c((size_t)C + 1, 0);   // tokens per centroid id (+1 for c = -1)
+  int64_t sum_ru = 0;
   for (int t = 0; t < T; ++t) {
     const int u = tok_u[t];
+    const int r = u >= 0 ? ctx->slot_rank[u] : 0;
     const float g = tok_gamma ? tok_gamma[t] : 1.0f;
     int32_t gbits;
     std::memcpy(&gbits, &g, 4);
-    plan->staging[t] = make_int4(tok_c[t], u, u >= 0 ? ctx->slot_rank[u] : 0, gbits);
+    plan->staging[t] = make_int4(tok_c[t], u, r, gbits);
     if (u >= 0) slots.push_back(u);
-    cmin = std::min(cmin, tok_c[t]);
-    cmax = std::max(cmax, tok_c[t]);
+    per_c[(size_t)tok_c[t] + 1]++;
+    sum_ru += r;
   }
   std::sort(slots.begin(), slots.end());
   slots.erase(std::unique(slots.begin(), slots.end()), slots.end());
   plan->slots = slots;
   plan->slot_rank.resize(slots.size());
   for (size_t i = 0; i < slots.size(); ++i) plan->slot_rank[i] = ctx->slot_rank[slots[i]];
+  // tile size from the mean group size; the tile count is exact
+  int n_groups = 0, n_groups_c = 0;
+  for (int g = 0; g <= C; ++g)
+    if (per_c[g]) {
+      ++n_groups;
+      n_groups_c += (g > 0);
+    }
+  const double mean = n_groups ? (double)T / n_groups : 0.0;
+  plan->M = mean <= 24.0 ? 16 : (mean <= 48.0 ? 32 : 64);
+  int n_tiles = 0;
+  for (int g = 0; g <= C; ++g) n_tiles += (per_c[g] + plan->M - 1) / plan->M;
+  plan->n_tiles = n_tiles;
+  plan->n_groups_c = n_groups_c;
+  plan->sum_ru = sum_ru;
   plan->T = T;
   plan->built = false;
-  plan->n_centroid_groups_ub = (T > 0) ? std::min(T, cmax - cmin + 1) : 0;
   if (T > 0) {
     SALT_HIP(ctx, hipMemcpyAsync(plan->dev.maps, plan->staging, (size_t)T * sizeof(int4),
                                  hipMemcpyHostToDevice, s));
@@ -475,8 +524,31 @@ salt_status salt_plan_build(salt_ctx* ctx, salt_plan* plan, void* stream) {
   if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
   if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
   SALT_HIP(ctx, hipSetDevice(ctx->device));
-  SALT_HIP(ctx, salt::launch_plan(plan->dev, plan->T, ctx->cfg.n_centroids, (hipStream_t)stream));
+  salt::PlanArgs pa{};
+  pa.b = plan->dev;
+  pa.T = plan->T;
+  pa.M = plan->M;
+  SALT_HIP(ctx, salt::launch_plan(pa, (hipStream_t)stream));
   plan->built = true;
+  plan->epoch = 0;
+  return SALT_OK;
+}
+
+salt_status salt_plan_errors(salt_ctx* ctx, const salt_plan* plan, void* stream, int32_t* n_errors) {
+  if (!ctx || !plan || !n_errors) return SALT_ERR_INVALID_ARG;
+  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  *n_errors = 0;
+  if (!plan->built || plan->T == 0) return SALT_OK;
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  SALT_HIP(ctx, hipStreamSynchronize((hipStream_t)stream));
+  int32_t meta[salt::kMetaWords];
+  SALT_HIP(ctx, hipMemcpy(meta, plan->dev.meta, sizeof meta, hipMemcpyDeviceToHost));
+  if (meta[salt::kMetaNTiles] != plan->n_tiles) {
+    *n_errors = 1;
+    return fail(ctx, SALT_ERR_BAD_STATE, "device plan has %d tiles, host expected %d",
+                meta[salt::kMetaNTiles], plan->n_tiles);
+  }
+  *n_errors = meta[salt::kMetaErr];
   return SALT_OK;
 }
 
@@ -508,7 +580,7 @@ salt_status salt_plan_download(salt_ctx* ctx, const salt_plan* plan, void* strea
   return SALT_OK;
 }
 
-salt_status salt_apply(salt_ctx* ctx, int32_t table, const salt_plan* plan, const void* x, void* y,
+salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y,
                        void* stream) {
   if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
   if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
@@ -541,34 +613,39 @@ salt_status salt_apply(salt_ctx* ctx, int32_t table, const salt_plan* plan, cons
   a.x = x;
   a.y = y;
   a.cent_at = C ? ctx->cent_at[table] : nullptr;
-  a.cent_b = C ? ctx->cent_b[table] : nullptr;
+  a.cent_bt = C ? ctx->cent_b[table] : nullptr;
   a.pool = ctx->pool;
   a.slot_stride = ctx->slot_stride;
   a.tab_prefix = ctx->tab_prefix[table];
-  a.srt = plan->dev.srt;
-  a.grp_tok = plan->dev.grp_tok;
-  a.grp_c = plan->dev.grp_c;
-  a.meta = plan->dev.meta;
+  a.tiles = plan->dev.tiles;
   a.partials = plan->dev.partials;
+  a.v = plan->dev.v;
+  a.arrive = plan->dev.arrive;
+  a.ready = plan->dev.ready;
+  a.meta = plan->dev.meta;
   a.T = T;
   a.in_dim = sh.in_dim;
   a.out_dim = sh.out_dim;
   a.r_c = ctx->cfg.r_c;
   a.r_u_max = ctx->cfg.r_u_max;
   a.R = std::max(1, a.r_c + a.r_u_max);
-  // tiles: at most ceil(T / M) plus one partial tile per centroid group
-  const int M = salt::kTileM;
-  const int tiles_ub = (T + M - 1) / M + plan->n_centroid_groups_ub;
-  // split K so that about 1024 blocks work on the shrink, in multiples of 64
-  const int kmax = (sh.in_dim + 63) / 64;
-  int S = std::max(1, std::min(kmax, (1024 + tiles_ub - 1) / tiles_ub));
+  a.n_tiles = plan->n_tiles;
+  // K split: blocks of ~64 KiB of shrink input, partial traffic kept under a
+  // fifth of it, each wave's K range a multiple of 32
+  const int M = plan->M, KW = 64 / M;
+  const double es = (double)ctx->esize;
+  const double shrink_bytes = es * sh.in_dim * ((double)T + (double)plan->n_groups_c * a.r_c + (double)plan->sum_ru);
+  int S = (int)std::ceil(shrink_bytes / ((double)a.n_tiles * 65536.0));
+  const int s_traffic = std::max(1, (int)(0.2 * shrink_bytes / ((double)T * a.R * 8.0)));
+  const int gran = 32 * KW;
+  S = std::max(1, std::min({S, s_traffic, (sh.in_dim + gran - 1) / gran}));
   while (S > 1 && (size_t)S * T * a.R > plan->dev.partial_cap) --S;
-  int Kc = ((sh.in_dim + S - 1) / S + 63) / 64 * 64;
-  S = (sh.in_dim + Kc - 1) / Kc;
-  a.S = S;
+  const int Kc = ((sh.in_dim + S - 1) / S + gran - 1) / gran * gran;
   a.Kc = Kc;
-  a.NC = 128;
-  SALT_HIP(ctx, salt::launch_apply(a, ctx->cfg.dtype == SALT_BF16, tiles_ub, s));
+  a.S = (sh.in_dim + Kc - 1) / Kc;
+  a.n_col = (sh.out_dim + salt::kNC - 1) / salt::kNC;
+  a.epoch = ++plan->epoch;
+  SALT_HIP(ctx, salt::launch_apply(a, ctx->cfg.dtype == SALT_BF16, M, s));
   int64_t seq;
   SALT_HIP(ctx, ring_record(ctx->readers, s, &seq));
   for (int slot : plan->slots) ctx->slot_reader[slot] = seq;

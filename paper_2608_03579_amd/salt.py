@@ -26,8 +26,8 @@ EXPORTS = (
     "salt_create", "salt_destroy", "salt_pin_centroids", "salt_residual_bytes",
     "salt_residual_bytes_for", "salt_load_residual", "salt_wait_loads", "salt_host_alloc",
     "salt_host_free", "salt_plan_create", "salt_plan_destroy", "salt_plan_set_maps",
-    "salt_plan_build", "salt_plan_download", "salt_apply", "salt_status_str", "salt_last_error",
-    "salt_version",
+    "salt_plan_build", "salt_plan_download", "salt_plan_errors", "salt_apply", "salt_status_str",
+    "salt_last_error", "salt_version",
 )
 
 
@@ -62,6 +62,7 @@ def _load() -> C.CDLL:
         "salt_plan_set_maps": (C.c_int, [P, P, I32, IP, IP, C.POINTER(C.c_float), VP]),
         "salt_plan_build": (C.c_int, [P, P, VP]),
         "salt_plan_download": (C.c_int, [P, P, VP, IP, IP, IP, IP, IP, IP, IP]),
+        "salt_plan_errors": (C.c_int, [P, P, VP, IP]),
         "salt_apply": (C.c_int, [P, I32, P, VP, VP, VP]),
         "salt_status_str": (C.c_char_p, [C.c_int]),
         "salt_last_error": (C.c_char_p, [P]),
@@ -243,6 +244,11 @@ class Plan:
 
     def build(self, stream: int = 0):
         self.ctx._check(lib.salt_plan_build(self.ctx.h, self.h, stream), "salt_plan_build")
+
+    def errors(self, stream: int = 0) -> int:
+        n = C.c_int32()
+        self.ctx._check(lib.salt_plan_errors(self.ctx.h, self.h, stream, C.byref(n)), "salt_plan_errors")
+        return int(n.value)
 
     def download(self, stream: int = 0) -> Dict[str, np.ndarray]:
         T = self.T

@@ -28,6 +28,7 @@ def _check_plan(run):
 
 def _check_table(run, table, rows=None, exact=False):
     got = run.apply(table)
+    assert run.plan.errors(run.stream) == 0, "apply blocks gave up waiting for their tile"
     got = oracle.decode(got, run.w.dtype)
     ref = run.oracle_table(table, rows)
     if rows is not None:
