@@ -25,15 +25,15 @@ struct PlanBuffers {
   int32_t* grp_tok;   // [max_T + 1] sorted position where each centroid group starts
   int32_t* grp_c;     // [max_T] centroid id of each group
   int4* tiles;        // [tile_cap]: per tile (i0, n, c, 0) then M token records
-  uint32_t* arrive;   // [max tiles] shrink blocks that finished a tile in this apply
-  uint32_t* ready;    // [max tiles] epoch of the apply whose v of the tile is complete
+  uint32_t* arrive;   // [max tiles * kCounterStride] shrink blocks done with each tile since the build
+  uint32_t* ready;    // [max tiles * kCounterStride] epoch of the last apply whose v of the tile is complete
+  float* v;           // [max_T][R] v = x [A_c | A_u], gamma applied
   int32_t* meta;      // [kMetaWords]
   uint32_t* counter;  // [64] arrival counter of the multi-block plan build
   float* partials;    // [partial_cap] split-K partial sums of the shrink
-  float* v;           // [max_T][R] reduced v = x [A_c | A_u] (gamma applied)
   size_t partial_cap; // floats
   size_t tile_cap;    // int4 entries
-  int32_t tiles_max;  // entries of arrive / ready
+  int32_t tiles_max;  // entries of arrive
 };
 
 struct PlanArgs {
@@ -57,6 +57,7 @@ struct ApplyArgs {
   uint32_t* arrive;
   uint32_t* ready;
   int32_t* meta;
+  uint32_t target;          // arrival count of every tile once this apply's shrink is done
   uint32_t epoch;           // 1, 2, ... per apply of the plan since its build
   int32_t T, in_dim, out_dim, r_c, r_u_max, R;
   int32_t n_tiles, S, Kc, n_col;
@@ -68,6 +69,17 @@ hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s);
 
 // Columns of y per expand block.
 constexpr int kNC = 128;
+// Per-tile arrival counters sit 256 bytes apart (no two share a cache line).
+constexpr int kCounterStride = 64;
+// Largest K split of one apply.
+constexpr int kMaxSplit = 32;
+
+// 32-wide K steps whose loads a shrink wave issues together: about 96 VGPRs of
+// operands (x, nbm A_c rows, ru A_u rows per step, vec_regs registers each).
+constexpr int shrink_batch(int vec_regs, int nbm, int ru) {
+  const int u = 96 / (vec_regs * (1 + nbm + ru));
+  return u < 1 ? 1 : (u > 4 ? 4 : u);
+}
 // Largest supported ranks.
 constexpr int kMaxRc = 128;
 constexpr int kMaxRu = 16;

@@ -15,10 +15,12 @@
 //
 // One launch per apply holds two kinds of blocks.  Shrink blocks (the first
 // n_tiles * S block ids) each reduce one tile over one K range into split-K
-// partials; the last of a tile's S blocks to arrive sums them in a fixed order,
-// applies gamma, stores v and publishes the apply's epoch in the tile's ready
-// word (release).  Expand blocks (the rest) prefetch their y, B_c and B_u
-// slices, then wait (acquire) for their tile's ready word, and update y.
+// partials and count their arrival on the tile; the last of a tile's S blocks
+// to arrive sums the partials in split order, scales the centroid part by
+// gamma, stores v and raises the tile's ready word to this apply's epoch.
+// Expand blocks (the rest) prefetch their y, B_c and B_u slices, wait for the
+// ready word, read v and update y.  Arrival counts and epochs only grow between
+// plan builds; the host passes the values this apply reaches.
 // Blocks are dispatched in id order, so every shrink block has started before
 // any expand block waits on it, and shrink blocks never wait: the wait always
 // ends.  It is still bounded; a block that gives up records an error in the
@@ -268,8 +270,8 @@ __device__ void plan_finish(const PlanArgs& a, const int4* srt, const int32_t* s
       b.tiles[e] = rec;
     }
     for (int t = tid; t < n_tiles; t += nt) {
-      b.arrive[t] = 0u;
-      b.ready[t] = 0u;
+      b.arrive[(size_t)t * kCounterStride] = 0u;
+      b.ready[(size_t)t * kCounterStride] = 0u;
     }
   }
   if (tid == 0) {
@@ -361,15 +363,82 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_large(PlanArgs a) {
 // ---------------------------------------------------------------------------
 __host__ __device__ constexpr int tile_bytes(int M) { return ((M + 1) * 16 + 255) / 256 * 256; }
 
-// Shrink block: tile `tau`, K range `s` of the apply.
-template <typename E, int MB, int RU>
+// Keeps a prefetched value in registers here: the compiler may not sink its load
+// below this point (e.g. past a wait loop).
+template <typename V>
+__device__ __forceinline__ void pin_regs(const V& v) {
+  static_assert(sizeof(V) % 4 == 0, "pin whole 32-bit words");
+  uint32_t w[sizeof(V) / 4];
+  __builtin_memcpy(w, &v, sizeof(V));
+#pragma unroll
+  for (int i = 0; i < (int)(sizeof(V) / 4); ++i) asm volatile("" ::"v"(w[i]));
+}
+
+// Hand-off of split-K partials between blocks, with no cache-wide fences.
+// Partials are written and read with device-coherent accesses (relaxed
+// agent-scope atomics: stores write through to the device-coherent level, loads
+// never return a stale cached copy).  A shrink block waits until its partial
+// stores have completed (s_waitcnt), meets its other waves, and only then bumps
+// the tile's arrival count; an expand block issues its partial loads only after
+// it has seen the count.  Completed device-coherent stores are visible to every
+// later device-coherent load, so the counter orders the data without writing
+// back or invalidating the L2.
+__device__ __forceinline__ void store_coherent(float* p, float v) {
+  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+__device__ __forceinline__ float load_coherent(const float* p) {
+  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// All waves' coherent stores have completed, then one thread adds 1 to
+// `counter`; returns (to every thread) the count after the addition.
+__device__ __forceinline__ uint32_t publish_add(uint32_t* counter, uint32_t* s_word) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0)
+    *s_word = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) + 1u;
+  __syncthreads();
+  return *s_word;
+}
+
+// All waves' coherent stores have completed, then one thread stores `value`.
+__device__ __forceinline__ void publish_store(uint32_t* word, uint32_t value) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  if (threadIdx.x == 0) __hip_atomic_store(word, value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Wait until `word` reaches `target` (wrap-safe), polling with coherent loads.
+// Returns false (and counts an error) if it gives up.
+__device__ __forceinline__ bool await_word(const uint32_t* word, uint32_t target, int32_t* err, int* s_flag) {
+  if (threadIdx.x == 0) {
+    uint32_t spins = 0;
+    int ok = 1;
+    while ((int32_t)(__hip_atomic_load(const_cast<uint32_t*>(word), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
+      __builtin_amdgcn_s_sleep(2);
+      if (++spins > kSpinMax) {
+        atomicAdd(err, 1);
+        ok = 0;
+        break;
+      }
+    }
+    *s_flag = ok;
+  }
+  __syncthreads();
+  return *s_flag != 0;
+}
+
+// Shrink block: tile `tau`, K range `s` of the apply.  Writes the tile's
+// split-K partial sums P[s][token][0 : r_c + r_u_max] and counts its arrival.
+template <typename E, int MB, int RU, int NBM>
 __device__ void shrink_block(const ApplyArgs& a, int tau, int s, char* lds) {
   using O = Ops<E>;
   using Vec = typename O::Vec;
   constexpr int M = 16 * MB, KW = 4 / MB;
+  constexpr int U = shrink_batch((int)(sizeof(Vec) / 4), NBM, RU);
   int4* s_tile = reinterpret_cast<int4*>(lds);
   float* s_part = reinterpret_cast<float*>(lds + tile_bytes(M));   // [KW][M][R]
-  __shared__ int s_last;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int4* trec = a.tiles + (size_t)tau * (M + 1);
   for (int i = tid; i < M + 1; i += 256) s_tile[i] = trec[i];
@@ -385,38 +454,47 @@ __device__ void shrink_block(const ApplyArgs& a, int tau, int s, char* lds) {
   const int ru = (tok_ok && tk.y >= 0) ? tk.z : 0;
   const E* xrow = reinterpret_cast<const E*>(a.x) + (size_t)(tok_ok ? tk.x : 0) * in;
   const E* au = ru ? reinterpret_cast<const E*>(a.pool + (size_t)tk.y * a.slot_stride) + (int64_t)ru * a.tab_prefix
-                   : nullptr;
-  const E* at_c = reinterpret_cast<const E*>(a.cent_at) + (size_t)(has_c ? c : 0) * rc * in;
-  const int NB = (rc + 15) >> 4;                // 16-rank blocks of the centroid
+                   : xrow;
+  const E* arow[NBM];                           // A_c^T row of this lane per 16-rank block
+  bool aok[NBM];
+#pragma unroll
+  for (int nb = 0; nb < NBM; ++nb) {
+    const int j = nb * 16 + (lane & 15);
+    aok[nb] = has_c && j < rc;
+    arow[nb] = reinterpret_cast<const E*>(a.cent_at) + ((size_t)(has_c ? c : 0) * rc + (aok[nb] ? j : 0)) * in;
+  }
 
   const int kw_len = a.Kc / KW;                 // a multiple of 32
   const int kbeg = s * a.Kc + kq * kw_len;
   const int kend = min(in, kbeg + kw_len);
 
-  f32x4 acc[kMaxRc / 16];
+  f32x4 acc[NBM];
 #pragma unroll
-  for (int nb = 0; nb < kMaxRc / 16; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int nb = 0; nb < NBM; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float accu[RU];
 #pragma unroll
   for (int j = 0; j < RU; ++j) accu[j] = 0.f;
 
-  for (int k = kbeg; k < kend; k += 32) {
-    const int kk = k + kseg;
-    const bool kin = kk < kend;
-    const Vec xa = (tok_ok && kin) ? O::load(xrow + kk) : O::zero();
-    if (has_c) {
+  for (int k0 = kbeg; k0 < kend; k0 += 32 * U) {
+    Vec xv[U], av[U][NBM], uv[U][RU];
 #pragma unroll
-      for (int nb = 0; nb < kMaxRc / 16; ++nb) {
-        if (nb < NB) {
-          const int j = nb * 16 + (lane & 15);
-          const Vec bv = (kin && j < rc) ? O::load(at_c + (size_t)j * in + kk) : O::zero();
-          acc[nb] = O::mma(xa, bv, acc[nb]);
-        }
-      }
+    for (int u = 0; u < U; ++u) {
+      const int kk = k0 + 32 * u + kseg;
+      const bool kin = kk < kend;
+      xv[u] = (tok_ok && kin) ? O::load(xrow + kk) : O::zero();
+#pragma unroll
+      for (int nb = 0; nb < NBM; ++nb) av[u][nb] = (aok[nb] && kin) ? O::load(arow[nb] + kk) : O::zero();
+#pragma unroll
+      for (int j = 0; j < RU; ++j) uv[u][j] = (j < ru && kin) ? O::load(au + (size_t)j * in + kk) : O::zero();
     }
 #pragma unroll
-    for (int j = 0; j < RU; ++j) {
-      if (j < ru && kin) accu[j] = O::dot(xa, O::load(au + (size_t)j * in + kk), accu[j]);
+    for (int u = 0; u < U; ++u) {
+      if (has_c) {
+#pragma unroll
+        for (int nb = 0; nb < NBM; ++nb) acc[nb] = O::mma(xv[u], av[u][nb], acc[nb]);
+      }
+#pragma unroll
+      for (int j = 0; j < RU; ++j) accu[j] = O::dot(xv[u], uv[u][j], accu[j]);
     }
   }
   // residual: lanes l, l^16, l^32, l^48 hold the four k offsets of one token
@@ -428,69 +506,76 @@ __device__ void shrink_block(const ApplyArgs& a, int tau, int s, char* lds) {
   // this wave's partial -> LDS [kq][token][j]
   float* P = s_part + (size_t)kq * M * R;
 #pragma unroll
-  for (int nb = 0; nb < kMaxRc / 16; ++nb) {
-    if (nb < NB) {
-      const int j = nb * 16 + (lane & 15);
+  for (int nb = 0; nb < NBM; ++nb) {
+    const int j = nb * 16 + (lane & 15);
+    if (j < rc) {
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int t = mb * 16 + 4 * (lane >> 4) + e;
-        if (j < rc) P[t * R + j] = has_c ? acc[nb][e] : 0.f;
-      }
+      for (int e = 0; e < 4; ++e) P[(mb * 16 + 4 * (lane >> 4) + e) * R + j] = acc[nb][e];
     }
   }
   if (lane < 16) {
 #pragma unroll
     for (int j = 0; j < RU; ++j)
-      if (j < a.r_u_max) P[tl * R + rc + j] = (j < ru) ? accu[j] : 0.f;
+      if (j < a.r_u_max) P[tl * R + rc + j] = accu[j];
   }
   __syncthreads();
-
+  const int nR = n * R;
+  float* V = a.v + (size_t)i0 * R;             // v rows of this tile
   if (a.S == 1) {
-    // single K range: v directly, no partials
-    for (int idx = tid; idx < n * R; idx += 256) {
+    // one K range: this block writes v itself
+    for (int idx = tid; idx < nR; idx += 256) {
       float v = 0.f;
 #pragma unroll
       for (int q = 0; q < KW; ++q) v += s_part[(size_t)q * M * R + idx];
       const int t = idx / R, j = idx - t * R;
       if (j < rc) v *= __int_as_float(s_tile[1 + t].w);
-      a.v[(size_t)i0 * R + idx] = v;
+      store_coherent(V + idx, v);
     }
   } else {
     float* G = a.partials + ((size_t)s * a.T + i0) * R;
-    for (int idx = tid; idx < n * R; idx += 256) {
+    for (int idx = tid; idx < nR; idx += 256) {
       float v = 0.f;
 #pragma unroll
       for (int q = 0; q < KW; ++q) v += s_part[(size_t)q * M * R + idx];
-      G[idx] = v;
+      store_coherent(G + idx, v);
     }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-    __syncthreads();
-    if (tid == 0) {
-      const uint32_t old = __hip_atomic_fetch_add(a.arrive + tau, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
-      const bool last = (old == (uint32_t)a.S - 1u);
-      if (last) __hip_atomic_store(a.arrive + tau, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      s_last = last ? 1 : 0;
-    }
-    __syncthreads();
-    if (!s_last) return;
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+    __shared__ uint32_t s_count;
+    if (publish_add(a.arrive + (size_t)tau * kCounterStride, &s_count) != a.target) return;
+    // the last of the tile's S blocks: sum the splits in order, scale by gamma
     const float* P0 = a.partials + (size_t)i0 * R;
     const size_t stride = (size_t)a.T * R;
-    for (int idx = tid; idx < n * R; idx += 256) {
-      float v = 0.f;
-      for (int sp = 0; sp < a.S; ++sp) v += P0[sp * stride + idx];
-      const int t = idx / R, j = idx - t * R;
-      if (j < rc) v *= __int_as_float(s_tile[1 + t].w);
-      a.v[(size_t)i0 * R + idx] = v;
+    constexpr int Q = 4, SG = 8;                 // entries x splits in flight per thread
+    for (int base = 0; base < nR; base += 256 * Q) {
+      float v[Q] = {0.f, 0.f, 0.f, 0.f};
+      for (int s0 = 0; s0 < a.S; s0 += SG) {
+        float p[Q][SG];
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          const int idx = base + tid + 256 * q;
+#pragma unroll
+          for (int e = 0; e < SG; ++e)
+            p[q][e] = (idx < nR && s0 + e < a.S) ? load_coherent(P0 + (s0 + e) * stride + idx) : 0.f;
+        }
+#pragma unroll
+        for (int q = 0; q < Q; ++q)
+#pragma unroll
+          for (int e = 0; e < SG; ++e) v[q] += p[q][e];
+      }
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int idx = base + tid + 256 * q;
+        if (idx < nR) {
+          const int t = idx / R, j = idx - t * R;
+          store_coherent(V + idx, j < rc ? v[q] * __int_as_float(s_tile[1 + t].w) : v[q]);
+        }
+      }
     }
   }
-  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
-  __syncthreads();
-  if (tid == 0) __hip_atomic_store(a.ready + tau, a.epoch, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+  publish_store(a.ready + (size_t)tau * kCounterStride, a.epoch);
 }
 
 // Expand block: tile `tau`, columns [q * kNC, q * kNC + kNC) of y.
-template <typename E, int MB, int RU>
+template <typename E, int MB, int RU, int NBM>
 __device__ void expand_block(const ApplyArgs& a, int tau, int q, char* lds) {
   using O = Ops<E>;
   using Vec = typename O::Vec;
@@ -499,11 +584,11 @@ __device__ void expand_block(const ApplyArgs& a, int tau, int q, char* lds) {
   constexpr int ITEMS = M * CG / 256;           // (token, column group) items per thread
   constexpr int RP = RU < 2 ? RU : 2;           // residual ranks prefetched
   constexpr int NBW = kNC / 16 / 4;             // 16-column blocks per wave
-  constexpr int KS = kMaxRc / 32;               // 32-rank steps, at most
+  constexpr int KS = (NBM + 1) / 2;             // 32-rank steps
   int4* s_tile = reinterpret_cast<int4*>(lds);
   float* s_v = reinterpret_cast<float*>(lds + tile_bytes(M));     // [M][R]
   float* s_y = s_v + (size_t)M * a.R;                             // [M][kNC]
-  __shared__ int s_abort;
+  __shared__ int s_flag;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int4* trec = a.tiles + (size_t)tau * (M + 1);
   for (int i = tid; i < M + 1; i += 256) s_tile[i] = trec[i];
@@ -529,7 +614,6 @@ __device__ void expand_block(const ApplyArgs& a, int tau, int q, char* lds) {
 #pragma unroll
     for (int j = 0; j < RP; ++j) bu[it][j] = (j < ru) ? O::load(bup + (size_t)j * out + col) : O::zero();
   }
-  const int KSn = (rc + 31) >> 5;
   Vec bct[NBW][KS];
   const E* bt = reinterpret_cast<const E*>(a.cent_bt) + (size_t)(has_c ? c : 0) * out * rc;
 #pragma unroll
@@ -538,28 +622,28 @@ __device__ void expand_block(const ApplyArgs& a, int tau, int q, char* lds) {
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const int j = ks * 32 + (lane >> 4) * 8;
-      bct[w][ks] = (has_c && ks < KSn && col < out && j < rc) ? O::load(bt + (size_t)col * rc + j) : O::zero();
+      bct[w][ks] = (has_c && col < out && j < rc) ? O::load(bt + (size_t)col * rc + j) : O::zero();
     }
   }
 
-  // ---- wait for the tile's v ----
-  if (tid == 0) {
-    uint32_t spins = 0;
-    int abort = 0;
-    while (__hip_atomic_load(a.ready + tau, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) != a.epoch) {
-      __builtin_amdgcn_s_sleep(2);
-      if (++spins > kSpinMax) {
-        atomicAdd(a.meta + kMetaErr, 1);
-        abort = 1;
-        break;
-      }
-    }
-    s_abort = abort;
+#pragma unroll
+  for (int it = 0; it < ITEMS; ++it) {
+    pin_regs(yold[it]);
+#pragma unroll
+    for (int j = 0; j < RP; ++j) pin_regs(bu[it][j]);
   }
-  __syncthreads();
-  if (s_abort) return;
-  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  for (int idx = tid; idx < M * R; idx += 256) s_v[idx] = (idx < n * R) ? a.v[(size_t)i0 * R + idx] : 0.f;
+#pragma unroll
+  for (int w = 0; w < NBW; ++w)
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) pin_regs(bct[w][ks]);
+
+  // ---- wait for the tile's v ----
+  if (!await_word(a.ready + (size_t)tau * kCounterStride, a.epoch, a.meta + kMetaErr, &s_flag)) return;
+  {
+    const float* V = a.v + (size_t)i0 * R;
+    const int nR = n * R, MR = M * R;
+    for (int idx = tid; idx < MR; idx += 256) s_v[idx] = idx < nR ? load_coherent(V + idx) : 0.f;
+  }
   __syncthreads();
 
   // ---- centroid part on MFMA: y^T block [16 cols x 16 tokens] = B_c^T . v_c^T ----
@@ -573,13 +657,11 @@ __device__ void expand_block(const ApplyArgs& a, int tau, int q, char* lds) {
         const int t = mb * 16 + (lane & 15);
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
-          if (ks < KSn) {
-            const int j = ks * 32 + (lane >> 4) * 8;
-            float vv[8];
+          const int j = ks * 32 + (lane >> 4) * 8;
+          float vv[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) vv[e] = (j + e < rc) ? s_v[t * R + j + e] : 0.f;
-            acc = O::mma_f32rhs(bct[w][ks], vv, acc);
-          }
+          for (int e = 0; e < 8; ++e) vv[e] = (j + e < rc) ? s_v[t * R + j + e] : 0.f;
+          acc = O::mma_f32rhs(bct[w][ks], vv, acc);
         }
 #pragma unroll
         for (int e = 0; e < 4; ++e) s_y[t * kNC + cb + 4 * (lane >> 4) + e] = acc[e];
@@ -629,16 +711,16 @@ __device__ void expand_block(const ApplyArgs& a, int tau, int q, char* lds) {
   }
 }
 
-template <typename E, int MB, int RU>
+template <typename E, int MB, int RU, int NBM>
 __global__ void __launch_bounds__(256) k_apply(ApplyArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int b = blockIdx.x;
   const int n_shrink = a.n_tiles * a.S;
   if (b < n_shrink) {
-    shrink_block<E, MB, RU>(a, b % a.n_tiles, b / a.n_tiles, lds);
+    shrink_block<E, MB, RU, NBM>(a, b % a.n_tiles, b / a.n_tiles, lds);
   } else {
     const int e = b - n_shrink;
-    expand_block<E, MB, RU>(a, e % a.n_tiles, e / a.n_tiles, lds);
+    expand_block<E, MB, RU, NBM>(a, e % a.n_tiles, e / a.n_tiles, lds);
   }
 }
 
@@ -649,17 +731,28 @@ size_t apply_lds(int M, int R) {
   return shrink > expand ? shrink : expand;
 }
 
-template <typename E, int RU>
-hipError_t launch_typed(const ApplyArgs& a, int M, hipStream_t s) {
+template <typename E, int RU, int NBM>
+hipError_t launch_nbm(const ApplyArgs& a, int M, hipStream_t s) {
   const dim3 grid(a.n_tiles * (a.S + a.n_col)), block(256);
   const size_t lds = apply_lds(M, a.R);
-  switch (M) {
-    case 16: hipLaunchKernelGGL((k_apply<E, 1, RU>), grid, block, lds, s, a); break;
-    case 32: hipLaunchKernelGGL((k_apply<E, 2, RU>), grid, block, lds, s, a); break;
-    case 64: hipLaunchKernelGGL((k_apply<E, 4, RU>), grid, block, lds, s, a); break;
-    default: return hipErrorInvalidValue;
+  if (M == 16) {
+    hipLaunchKernelGGL((k_apply<E, 1, RU, NBM>), grid, block, lds, s, a);
+  } else if constexpr (sizeof(E) == 2) {
+    if (M == 32) hipLaunchKernelGGL((k_apply<E, 2, RU, NBM>), grid, block, lds, s, a);
+    else if (M == 64) hipLaunchKernelGGL((k_apply<E, 4, RU, NBM>), grid, block, lds, s, a);
+    else return hipErrorInvalidValue;
+  } else {
+    return hipErrorInvalidValue;
   }
   return hipGetLastError();
+}
+
+// NBM: 16-rank blocks of the centroid held per lane (r_c <= 16 * NBM)
+template <typename E, int RU>
+hipError_t launch_typed(const ApplyArgs& a, int M, hipStream_t s) {
+  if (a.r_c <= 32) return launch_nbm<E, RU, 2>(a, M, s);
+  if (a.r_c <= 64) return launch_nbm<E, RU, 4>(a, M, s);
+  return launch_nbm<E, RU, 8>(a, M, s);
 }
 
 }  // namespace
@@ -689,10 +782,19 @@ hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
+// RU: residual ranks held per lane (1, 2 or kMaxRu).  fp32 plans use 16-token
+// tiles only.
 hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s) {
   if (a.T <= 0 || a.n_tiles <= 0) return hipSuccess;
-  if (a.r_u_max <= 2) return bf16 ? launch_typed<uint16_t, 2>(a, M, s) : launch_typed<float, 2>(a, M, s);
-  return bf16 ? launch_typed<uint16_t, kMaxRu>(a, M, s) : launch_typed<float, kMaxRu>(a, M, s);
+  if (!bf16) {
+    if (M != 16) return hipErrorInvalidValue;
+    if (a.r_u_max <= 1) return launch_typed<float, 1>(a, M, s);
+    if (a.r_u_max <= 2) return launch_typed<float, 2>(a, M, s);
+    return launch_typed<float, kMaxRu>(a, M, s);
+  }
+  if (a.r_u_max <= 1) return launch_typed<uint16_t, 1>(a, M, s);
+  if (a.r_u_max <= 2) return launch_typed<uint16_t, 2>(a, M, s);
+  return launch_typed<uint16_t, kMaxRu>(a, M, s);
 }
 
 }  // namespace salt

@@ -53,7 +53,8 @@ struct salt_plan {
   int32_t n_tiles = 0;
   int32_t n_groups_c = 0;           // groups with a centroid
   int64_t sum_ru = 0;               // residual rank summed over tokens
-  uint32_t epoch = 0;               // applies since the last build
+  uint32_t arrivals = 0;            // per-tile arrival count after the last enqueued apply
+  uint32_t epoch = 0;               // applies enqueued since the last build
 };
 
 struct salt_ctx {
@@ -411,12 +412,12 @@ salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out) {
             hipMalloc((void**)&b.grp_tok, (T + 1) * 4) == hipSuccess &&
             hipMalloc((void**)&b.grp_c, T * 4) == hipSuccess &&
             hipMalloc((void**)&b.tiles, b.tile_cap * sizeof(int4)) == hipSuccess &&
-            hipMalloc((void**)&b.arrive, (size_t)b.tiles_max * 4) == hipSuccess &&
-            hipMalloc((void**)&b.ready, (size_t)b.tiles_max * 4) == hipSuccess &&
+            hipMalloc((void**)&b.arrive, (size_t)b.tiles_max * salt::kCounterStride * 4) == hipSuccess &&
+            hipMalloc((void**)&b.ready, (size_t)b.tiles_max * salt::kCounterStride * 4) == hipSuccess &&
+            hipMalloc((void**)&b.v, T * R * 4) == hipSuccess &&
             hipMalloc((void**)&b.meta, salt::kMetaWords * 4) == hipSuccess &&
             hipMalloc((void**)&b.counter, 64 * 4) == hipSuccess &&
             hipMalloc((void**)&b.partials, b.partial_cap * 4) == hipSuccess &&
-            hipMalloc((void**)&b.v, T * R * 4) == hipSuccess &&
             hipHostMalloc((void**)&p->staging, T * sizeof(int4), hipHostMallocDefault) == hipSuccess;
   if (!ok) {
     (void)hipGetLastError();
@@ -427,8 +428,8 @@ salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out) {
   hipError_t e = hipEventCreateWithFlags(&p->staged, hipEventDisableTiming);
   if (e == hipSuccess) e = hipMemset(b.counter, 0, 64 * 4);
   if (e == hipSuccess) e = hipMemset(b.meta, 0, salt::kMetaWords * 4);
-  if (e == hipSuccess) e = hipMemset(b.arrive, 0, (size_t)b.tiles_max * 4);
-  if (e == hipSuccess) e = hipMemset(b.ready, 0, (size_t)b.tiles_max * 4);
+  if (e == hipSuccess) e = hipMemset(b.arrive, 0, (size_t)b.tiles_max * salt::kCounterStride * 4);
+  if (e == hipSuccess) e = hipMemset(b.ready, 0, (size_t)b.tiles_max * salt::kCounterStride * 4);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     free_plan_buffers(p);
@@ -503,7 +504,7 @@ salt_status salt_plan_set_maps(salt_ctx* ctx, salt_plan* plan, int32_t T, const 
       n_groups_c += (g > 0);
     }
   const double mean = n_groups ? (double)T / n_groups : 0.0;
-  plan->M = mean <= 24.0 ? 16 : (mean <= 48.0 ? 32 : 64);
+  plan->M = (ctx->cfg.dtype == SALT_F32 || mean <= 24.0) ? 16 : (mean <= 48.0 ? 32 : 64);
   int n_tiles = 0;
   for (int g = 0; g <= C; ++g) n_tiles += (per_c[g] + plan->M - 1) / plan->M;
   plan->n_tiles = n_tiles;
@@ -530,6 +531,7 @@ salt_status salt_plan_build(salt_ctx* ctx, salt_plan* plan, void* stream) {
   pa.M = plan->M;
   SALT_HIP(ctx, salt::launch_plan(pa, (hipStream_t)stream));
   plan->built = true;
+  plan->arrivals = 0;
   plan->epoch = 0;
   return SALT_OK;
 }
@@ -619,9 +621,9 @@ salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
   a.tab_prefix = ctx->tab_prefix[table];
   a.tiles = plan->dev.tiles;
   a.partials = plan->dev.partials;
-  a.v = plan->dev.v;
   a.arrive = plan->dev.arrive;
   a.ready = plan->dev.ready;
+  a.v = plan->dev.v;
   a.meta = plan->dev.meta;
   a.T = T;
   a.in_dim = sh.in_dim;
@@ -630,20 +632,26 @@ salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
   a.r_u_max = ctx->cfg.r_u_max;
   a.R = std::max(1, a.r_c + a.r_u_max);
   a.n_tiles = plan->n_tiles;
-  // K split: blocks of ~64 KiB of shrink input, partial traffic kept under a
-  // fifth of it, each wave's K range a multiple of 32
+  // K split.  Small (decode) batches are latency bound: spread the shrink input
+  // over many blocks (~16 KiB each) so no CU streams much more than its share,
+  // and let partial traffic reach half of the input.  Large (prefill) batches
+  // are bandwidth bound: ~64 KiB blocks, partial traffic under a fifth.
   const int M = plan->M, KW = 64 / M;
   const double es = (double)ctx->esize;
   const double shrink_bytes = es * sh.in_dim * ((double)T + (double)plan->n_groups_c * a.r_c + (double)plan->sum_ru);
-  int S = (int)std::ceil(shrink_bytes / ((double)a.n_tiles * 65536.0));
-  const int s_traffic = std::max(1, (int)(0.2 * shrink_bytes / ((double)T * a.R * 8.0)));
+  const bool small = T <= 1024;
+  const double block_bytes = small ? 16384.0 : 65536.0;
+  const int s_bytes = (int)std::ceil(shrink_bytes / ((double)a.n_tiles * block_bytes));
+  const int s_traffic = std::max(1, (int)((small ? 0.5 : 0.2) * shrink_bytes / ((double)T * a.R * 8.0)));
   const int gran = 32 * KW;
-  S = std::max(1, std::min({S, s_traffic, (sh.in_dim + gran - 1) / gran}));
+  int S = std::max(1, std::min({s_bytes, s_traffic, salt::kMaxSplit, (sh.in_dim + gran - 1) / gran}));
   while (S > 1 && (size_t)S * T * a.R > plan->dev.partial_cap) --S;
   const int Kc = ((sh.in_dim + S - 1) / S + gran - 1) / gran * gran;
   a.Kc = Kc;
-  a.S = (sh.in_dim + Kc - 1) / Kc;
+  a.S = (sh.in_dim + Kc - 1) / Kc;   // <= S
   a.n_col = (sh.out_dim + salt::kNC - 1) / salt::kNC;
+  if (a.S > 1) plan->arrivals += (uint32_t)a.S;
+  a.target = plan->arrivals;
   a.epoch = ++plan->epoch;
   SALT_HIP(ctx, salt::launch_apply(a, ctx->cfg.dtype == SALT_BF16, M, s));
   int64_t seq;
