@@ -163,27 +163,44 @@ __device__ __forceinline__ uint64_t plan_key(int c, int u, int t) {
          uint64_t(uint32_t(t));
 }
 
-// Exclusive count of `pred` over the threads of the block, and the total.
-__device__ __forceinline__ int block_excl_count(bool pred, int* s_wave, int& total) {
+// Exclusive counts of two predicates over the threads of the block, and their
+// totals: per-wave ballots, then one wave scans the per-wave counts.
+__device__ __forceinline__ void block_excl_count2(bool p0, bool p1, int* s_wave, int& r0, int& r1, int& tot0,
+                                                  int& tot1) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
-  const uint64_t m = __ballot(pred);
-  const int in_wave = (int)__builtin_amdgcn_mbcnt_hi(
-      (uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-  if (lane == 0) s_wave[wave] = __popcll(m);
-  __syncthreads();
-  int off = 0, tot = 0;
-  for (int w = 0; w < nw; ++w) {
-    const int c = s_wave[w];
-    off += (w < wave) ? c : 0;
-    tot += c;
+  const uint64_t m0 = __ballot(p0), m1 = __ballot(p1);
+  const int in0 = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m0 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m0, 0u));
+  const int in1 = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(m1 >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m1, 0u));
+  if (lane == 0) {
+    s_wave[wave] = __popcll(m0);
+    s_wave[16 + wave] = __popcll(m1);
   }
   __syncthreads();
-  total = tot;
-  return off + in_wave;
+  if (wave == 0) {
+    // lanes 0..15: counts of predicate 0, lanes 16..31: predicate 1 (nw <= 16)
+    const int w = lane & 15;
+    int c = (lane < 32 && w < nw) ? s_wave[(lane >> 4) * 16 + w] : 0;
+    int incl = c;
+#pragma unroll
+    for (int off = 1; off < 16; off <<= 1) {
+      const int v = __shfl_up(incl, off, 16);
+      if (w >= off) incl += v;
+    }
+    if (lane < 32) {
+      s_wave[32 + lane] = incl - c;                       // exclusive prefix per wave
+      if (w == 15) s_wave[64 + (lane >> 4)] = incl;       // totals
+    }
+  }
+  __syncthreads();
+  r0 = s_wave[32 + wave] + in0;
+  r1 = s_wave[48 + wave] + in1;
+  tot0 = s_wave[64];
+  tot1 = s_wave[65];
+  __syncthreads();
 }
 
 struct PlanShared {
-  int s_wave[16];
+  int s_wave[72];
   int g_start[kMaxGroups + 1];
   int g_c[kMaxGroups];
   int g_tile[kMaxGroups + 1];
@@ -211,9 +228,8 @@ __device__ void plan_finish(const PlanArgs& a, const int4* srt, const int32_t* s
         ns = ng || (u != up);
       }
     }
-    int seg_tot, grp_tot;
-    const int sr = block_excl_count(ns, sh.s_wave, seg_tot);
-    const int gr = block_excl_count(ng, sh.s_wave, grp_tot);
+    int seg_tot, grp_tot, sr, gr;
+    block_excl_count2(ns, ng, sh.s_wave, sr, gr, seg_tot, grp_tot);
     if (ns) {
       const int s = seg_base + sr;
       b.seg_off[s] = i;
@@ -283,28 +299,37 @@ __device__ void plan_finish(const PlanArgs& a, const int4* srt, const int32_t* s
   }
 }
 
-// Batches of up to kPlanSmallT tokens: one block, everything in LDS.
+// Batches of up to kPlanSmallT tokens: one block, everything in LDS.  The
+// block has plan_small_threads(T) threads; each token's rank is counted by
+// blockDim / T lanes (a power of two) and summed with lane shuffles.
 __global__ void __launch_bounds__(kPlanSmallT) k_plan_small(PlanArgs a) {
   __shared__ uint64_t skey[kPlanSmallT];
+  __shared__ int4 s_maps[kPlanSmallT];
   __shared__ int4 s_srt[kPlanSmallT];
   __shared__ int32_t s_c[kPlanSmallT];
   __shared__ PlanShared sh;
-  const int T = a.T, t = threadIdx.x;
-  int4 m = make_int4(0, 0, 0, 0);
-  uint64_t my = ~0ull;
-  if (t < T) {
-    m = a.b.maps[t];
-    my = plan_key(m.x, m.y, t);
-    skey[t] = my;
+  const int T = a.T, tid = threadIdx.x;
+  if (tid < T) {
+    const int4 m = a.b.maps[tid];
+    s_maps[tid] = m;
+    skey[tid] = plan_key(m.x, m.y, tid);
   }
   __syncthreads();
-  if (t < T) {
-    int cnt = 0;
-    for (int i = 0; i < T; ++i) cnt += (skey[i] < my) ? 1 : 0;
-    s_srt[cnt] = make_int4(t, m.y, m.z, m.w);
+  int lpt = 1;
+  while (lpt < 16 && lpt * 2 * T <= (int)blockDim.x) lpt *= 2;
+  const int t = tid / lpt, sub = tid % lpt;
+  const uint64_t my = t < T ? skey[t] : ~0ull;
+  int cnt = 0;
+#pragma unroll 8
+  for (int i = sub; i < T; i += lpt) cnt += (skey[i] < my) ? 1 : 0;
+  for (int off = 1; off < lpt; off <<= 1) cnt += __shfl_xor(cnt, off);
+  if (t < T && sub == 0) {
+    const int4 m = s_maps[t];
+    const int4 rec = make_int4(t, m.y, m.z, m.w);
+    s_srt[cnt] = rec;
     s_c[cnt] = m.x;
     a.b.perm[cnt] = t;
-    a.b.srt[cnt] = make_int4(t, m.y, m.z, m.w);
+    a.b.srt[cnt] = rec;
     a.b.srt_c[cnt] = m.x;
   }
   __syncthreads();
@@ -774,7 +799,9 @@ hipError_t kernels_init(int device) {
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
   if (a.T <= kPlanSmallT) {
-    hipLaunchKernelGGL(k_plan_small, dim3(1), dim3(kPlanSmallT), 0, s, a);
+    // 256 threads up to T = 256 (several lanes per token), else one per token
+    const int threads = a.T <= 256 ? 256 : (a.T + 63) / 64 * 64;
+    hipLaunchKernelGGL(k_plan_small, dim3(1), dim3(threads), 0, s, a);
   } else {
     const int blocks = (a.T + kPlanTokPerBlock - 1) / kPlanTokPerBlock;
     hipLaunchKernelGGL(k_plan_large, dim3(blocks), dim3(kPlanThreads), 0, s, a);
