@@ -16,9 +16,12 @@ consecutive steps touch disjoint memory, as consecutive projections of a real
 decode step would, and bytes come from HBM.
 
 Timing: HIP events on the stream the kernels run on, around the K timed steps;
-then, for the roofline, events around each apply of a second pass to get the
-apply's own average duration.  ``cpu_baseline`` times the fp64 oracle on a
-bounded sample of the same workload on this host.
+then, for the roofline, events around a second timed region of back-to-back
+applies (plans already built) give the apply kernel's average duration.
+``cpu_baseline`` times the fp64 oracle on a bounded sample of the same workload
+on this host.  Other workloads (--workload): the 28-layer Llama-3.2-3B prefill
+(T = 8192), the Llama-3.1-8B decode (T = 256) and the Zipf multi-tenant batch
+(T = 512) with its rank-16 LoRA baseline.
 """
 from __future__ import annotations
 
@@ -68,6 +71,9 @@ def apply_flops(w, plan_maps, table):
 # CPU baseline: the oracle as it stands, bounded sample, on this host
 # ---------------------------------------------------------------------------
 def cpu_baseline(w, budget_s=12.0):
+    """Tokens/s of the oracle: plan once per batch, then every table's apply,
+    in chunks of at most 64 tokens so that a bounded sample of a large batch
+    still covers every table.  BLAS limited to one thread."""
     import oracle
     try:
         from threadpoolctl import threadpool_limits
@@ -76,6 +82,7 @@ def cpu_baseline(w, budget_s=12.0):
         limiter = None
     d = w.dtype
     n_tab = len(w.tables)
+    chunk = min(w.T, 64)
     data = []
     for t in range(n_tab):
         x = oracle.decode(w.x(t), d)
@@ -83,45 +90,51 @@ def cpu_baseline(w, budget_s=12.0):
         cat, cb = (oracle.decode(a, d) for a in w.centroids(t)) if w.n_centroids else (None, None)
         res = {int(s): tuple(oracle.decode(a, d) for a in w.residual(int(s), t)) for s in w.referenced_slots()}
         data.append((x, y0, cat, cb, res))
-    tokens = 0
+    pairs = 0            # (token, table) pairs computed
     t0 = time.perf_counter()
-    passes = 0
+    start = 0
     while True:
-        oracle.plan(w.tok_c, w.tok_u)
+        if start == 0:
+            oracle.plan(w.tok_c, w.tok_u)
+        rows = list(range(start, min(w.T, start + chunk)))
         for t in range(n_tab):
             x, y0, cat, cb, res = data[t]
-            oracle.apply(x, y0, cat, cb, res, w.tok_c, w.tok_u, w.gamma)
-        tokens += w.T
-        passes += 1
-        if time.perf_counter() - t0 >= budget_s:
+            oracle.apply(x, y0, cat, cb, res, w.tok_c, w.tok_u, w.gamma, rows=rows)
+        pairs += len(rows) * n_tab
+        start = (start + chunk) % w.T
+        if time.perf_counter() - t0 >= budget_s and start == 0 or time.perf_counter() - t0 >= 3 * budget_s:
             break
     dt = time.perf_counter() - t0
-    if limiter is not None:
-        limiter.unregister() if hasattr(limiter, "unregister") else None
-    return {"value": tokens / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{passes} full passes (plan + {n_tab} table apply) of the same batch, "
-                      f"{dt:.1f} s, fp64 numpy, BLAS limited to 1 thread, host cpu: {os.cpu_count()} logical"}
+    if limiter is not None and hasattr(limiter, "unregister"):
+        limiter.unregister()
+    return {"value": pairs / n_tab / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
+            "sample": f"{pairs // n_tab} tokens through all {n_tab} tables (plan + apply, chunks of {chunk} "
+                      f"tokens) in {dt:.1f} s; fp64 numpy, BLAS limited to 1 thread; "
+                      f"host has {os.cpu_count()} logical cpus"}
 
 
 # ---------------------------------------------------------------------------
 # GPU bench
 # ---------------------------------------------------------------------------
-def build_replicated(w, rot, hip, salt):
+def build_replicated(w, dw, rot, hip, salt):
     """A context whose tables are ``rot`` copies of the workload's tables, with
-    every centroid pinned and every referenced residual loaded."""
+    every centroid pinned and every referenced residual loaded.  Adapter values
+    come from ``dw``, whose tables repeat to give ``w``'s (the same workload with
+    fewer layers for the 28-layer prefill; ``w`` itself otherwise)."""
     shapes = [(i, o) for _, i, o in w.tables] * rot
     ctx = salt.Context(w.dtype, shapes, w.n_centroids, w.r_c, w.n_slots, w.r_u_max, max(1, w.T))
-    n_tab = len(w.tables)
+    n_tab, n_dat = len(w.tables), len(dw.tables)
+    reps = (n_tab // n_dat) * rot
     if w.n_centroids:
-        for t in range(n_tab):
-            at, b = w.centroids(t)
-            for k in range(rot):
-                ctx.pin_centroids(k * n_tab + t, at, b)
+        for t in range(n_dat):
+            at, b = dw.centroids(t)
+            for k in range(reps):
+                ctx.pin_centroids(k * n_dat + t, at, b)
     for s in w.referenced_slots():
         s = int(s)
         r = int(w.slot_rank[s])
-        blob = w.residual_blob(s)
-        ctx.load_residual(s, r, np.tile(blob, rot) if r else None)
+        blob = dw.residual_blob(s)
+        ctx.load_residual(s, r, np.tile(blob, reps) if r else None)
     ctx.wait_loads()
     return ctx
 
@@ -131,6 +144,8 @@ def swap_timing(w, hip, salt, n=32):
     pinned host memory, on the context's side stream."""
     out = {}
     shapes = [(i, o) for _, i, o in w.tables]
+    per16 = salt.residual_bytes_for(salt.BF16 if w.dtype == "bf16" else salt.F32, shapes, 16)
+    n = n or max(4, min(32, (256 << 20) // max(1, per16)))
     for r in sorted({max(1, w.r_u_max), 16}):
         ctx = salt.Context(w.dtype, shapes, 0, 0, n, r, 1)
         nbytes = ctx.residual_bytes(r)
@@ -156,20 +171,27 @@ def swap_timing(w, hip, salt, n=32):
     return out
 
 
-def run_gpu(w, args, hip, salt):
+def run_gpu(w, dw, args, hip, salt):
     rot = args.rot
-    n_tab = len(w.tables)
+    n_tab, n_dat = len(w.tables), len(dw.tables)
     log(f"workload: {w.name}; T={w.T}, tables={n_tab}, rotation={rot}")
-    ctx = build_replicated(w, rot, hip, salt)
+    ctx = build_replicated(w, dw, rot, hip, salt)
     stream = hip.Stream()
-    # x and y per table copy: rotation keeps the working set above the MALL
-    xs, ys = [], []
-    for t in range(n_tab):
-        x = w.x(t)
-        y = w.y0(t)
-        for k in range(rot):
-            xs.append(hip.DeviceArray.from_host(x))
-            ys.append(hip.DeviceArray.from_host(y))
+    # x and y per table copy (rotation keeps the working set above the MALL);
+    # values repeat with the data tables, memory does not
+    xs, ys = [None] * (n_tab * rot), [None] * (n_tab * rot)
+    for t in range(n_dat):
+        x0 = hip.DeviceArray.from_host(dw.x(t))
+        y0 = hip.DeviceArray.from_host(dw.y0(t))
+        for k in range(rot * (n_tab // n_dat)):
+            i = k * n_dat + t
+            xs[i] = hip.DeviceArray(x0.shape, x0.dtype)
+            ys[i] = hip.DeviceArray(y0.shape, y0.dtype)
+            xs[i].copy_from(x0)
+            ys[i].copy_from(y0)
+        hip.synchronize()
+        x0.free()
+        y0.free()
     # one plan per rotation slot; every plan holds the same batch's maps
     plans = []
     for k in range(rot):
@@ -203,32 +225,41 @@ def run_gpu(w, args, hip, salt):
     ms_step = ms_total / args.steps
     log(f"timed {args.steps} steps: {ms_total:.3f} ms GPU ({wall * 1e3:.1f} ms wall), {ms_step * 1e3:.2f} us/step")
 
-    # apply-only durations: events around each apply, same stream, same rotation
-    n_meas = min(args.steps, 2000)
-    evs = [(hip.Event(), hip.Event()) for _ in range(n_tab)]
-    per_tab = np.zeros(n_tab)
-    for k in range(n_meas):
-        slot = k % rot
-        p = plans[slot]
-        p.build(stream.h)
-        for t in range(n_tab):
-            tab = slot * n_tab + t
-            a, b = evs[t]
-            a.record(stream)
-            ctx.apply(tab, p, xs[tab].ptr, ys[tab].ptr, stream.h)
-            b.record(stream)
-        stream.synchronize()
-        for t in range(n_tab):
-            per_tab[t] += evs[t][0].elapsed_ms(evs[t][1])
-    per_tab /= n_meas
+    # roofline: the apply kernel's own duration, from a second timed region of
+    # back-to-back applies (plans already built), events on the kernel's stream
     maps = (w.tok_c, w.tok_u)
     bytes_tab = np.array([apply_bytes(w, maps, t) for t in range(n_tab)], dtype=np.float64)
     flops_tab = np.array([apply_flops(w, maps, t) for t in range(n_tab)], dtype=np.float64)
-    dom = int(np.argmax(per_tab))
+    n_meas = max(1, min(args.steps, 4000) // n_tab)
+    per_tab = np.zeros(n_tab)
+    for t in range(n_tab):
+        a, b = hip.Event(), hip.Event()
+        a.record(stream)
+        for k in range(n_meas):
+            slot = k % rot
+            tab = slot * n_tab + t
+            ctx.apply(tab, plans[slot], xs[tab].ptr, ys[tab].ptr, stream.h)
+        b.record(stream)
+        b.synchronize()
+        per_tab[t] = a.elapsed_ms(b) / n_meas
+    errors = sum(p.errors(stream.h) for p in plans)
+    if errors:
+        raise RuntimeError(f"{errors} apply blocks gave up waiting; results invalid")
+    dom = int(np.argmax(per_tab * 1.0))
     achieved = bytes_tab[dom] / (per_tab[dom] * 1e-3) / 1e9
     step_bytes = float(bytes_tab.sum())
+    log(f"apply durations (us): " + ", ".join(f"{w.tables[t][0]} {per_tab[t] * 1e3:.2f}" for t in range(n_tab)))
 
     swap = swap_timing(w, hip, salt) if args.swap else None
+    if args.copy_mb:
+        log(f"copy calibration: {args.copy_mb} MiB device-to-device")
+        a_ = hip.DeviceArray((args.copy_mb << 20,), np.uint8)
+        b_ = hip.DeviceArray((args.copy_mb << 20,), np.uint8)
+        for _ in range(3):
+            b_.copy_from(a_, stream)
+        stream.synchronize()
+        a_.free()
+        b_.free()
     for p in plans:
         p.close()
     ctx.close()
@@ -241,26 +272,29 @@ def run_gpu(w, args, hip, salt):
         "apply_flops": {w.tables[t][0]: int(flops_tab[t]) for t in range(n_tab)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
-                     "kernel": f"salt_apply on {w.tables[dom][0]} (plan + shrink + expand of one table; "
-                               f"events bracket the apply's launches)",
-                     "bytes_per_launch": int(bytes_tab[dom]), "avg_us": per_tab[dom] * 1e3},
+                     "kernel": f"k_apply (salt_apply, one launch) on {w.tables[dom][0]}",
+                     "bytes_per_launch": int(bytes_tab[dom]), "avg_us": per_tab[dom] * 1e3,
+                     "timing": f"HIP events around {n_meas} back-to-back applies on the kernel's stream"},
         "swap": swap,
     }
 
 
 WORKLOADS = {
-    "qproj": dict(cfg=2, rot=128),
-    "decode8b": dict(cfg=4, rot=4),
-    "zipf": dict(cfg=5, rot=4),
-    "zipf-baseline": dict(cfg=5, rot=4, baseline=True),
+    "qproj": dict(cfg=2, rot=128, steps=2000, warmup=200),
+    "prefill": dict(cfg=3, rot=1, steps=10, warmup=2),
+    "decode8b": dict(cfg=4, rot=4, steps=500, warmup=50),
+    "zipf": dict(cfg=5, rot=4, steps=500, warmup=50),
+    "zipf-baseline": dict(cfg=5, rot=4, baseline=True, steps=200, warmup=20),
 }
 
 
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=2000)
-    ap.add_argument("--warmup", type=int, default=200)
+    ap.add_argument("--steps", type=int, default=None)
+    ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--copy-mb", type=int, default=0,
+                    help="also run a device-to-device copy of this many MiB (counter calibration)")
     ap.add_argument("--workload", default="qproj", choices=sorted(WORKLOADS))
     ap.add_argument("--rot", type=int, default=None)
     ap.add_argument("--no-cpu", action="store_true")
@@ -273,21 +307,28 @@ def main():
     spec = WORKLOADS[args.workload]
     if args.rot is None:
         args.rot = spec["rot"]
+    if args.steps is None:
+        args.steps = spec["steps"]
+    if args.warmup is None:
+        args.warmup = spec["warmup"]
 
     from paper_2608_03579_amd import synth
     w = synth.make(spec["cfg"], 0, baseline=spec.get("baseline", False))
+    # the 28-layer prefill draws adapter and activation values for one layer and
+    # repeats them over the layers (distinct memory per table)
+    dw = synth.make(3, 0, layers=1) if spec["cfg"] == 3 else w
 
     from paper_2608_03579_amd import hip, salt
     if hip.device_count() < 1:
         print("no HIP device visible", file=sys.stderr)
         sys.exit(1)
     hip.set_device(0)
-    res = run_gpu(w, args, hip, salt)
+    res = run_gpu(w, dw, args, hip, salt)
 
     cpu = None
     if not args.no_cpu:
         log("cpu baseline (oracle) ...")
-        cpu = cpu_baseline(w)
+        cpu = cpu_baseline(dw if spec["cfg"] == 3 else w)
 
     out = {
         "metric": "Centroid+residual LoRA apply: tokens/s and achieved HBM GB/s, Llama-3.2-3B",

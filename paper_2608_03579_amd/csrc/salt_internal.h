@@ -27,7 +27,7 @@ struct PlanBuffers {
   int4* tiles;        // [tile_cap]: per tile (i0, n, c, 0) then M token records
   uint32_t* arrive;   // [max tiles * kCounterStride] shrink blocks done with each tile since the build
   uint32_t* ready;    // [max tiles * kCounterStride] epoch of the last apply whose v of the tile is complete
-  float* v;           // [max_T][R] v = x [A_c | A_u], gamma applied
+  float* v;           // [max_T][R] v = x [A_c | A_u], gamma applied (R padded to 4)
   int32_t* meta;      // [kMetaWords]
   uint32_t* counter;  // [64] arrival counter of the multi-block plan build
   float* partials;    // [partial_cap] split-K partial sums of the shrink
@@ -60,15 +60,23 @@ struct ApplyArgs {
   uint32_t target;          // arrival count of every tile once this apply's shrink is done
   uint32_t epoch;           // 1, 2, ... per apply of the plan since its build
   int32_t T, in_dim, out_dim, r_c, r_u_max, R;
-  int32_t n_tiles, S, Kc, n_col;
+  int32_t n_tiles, S, Kc;
+  int32_t n_col;            // expand blocks per tile
+  int32_t cpb;              // kNC-column chunks per expand block
 };
 
 hipError_t kernels_init(int device);
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s);
 
-// Columns of y per expand block.
+// Columns of y per expand chunk.
 constexpr int kNC = 128;
+
+// Row stride of the partials and of v: r_c + r_u_max rounded up to whole float4s.
+constexpr int padded_rank(int r_c, int r_u_max) {
+  const int r = r_c + r_u_max;
+  return r < 4 ? 4 : (r + 3) / 4 * 4;
+}
 // Per-tile arrival counters sit 256 bytes apart (no two share a cache line).
 constexpr int kCounterStride = 64;
 // Largest K split of one apply.

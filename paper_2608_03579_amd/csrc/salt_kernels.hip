@@ -35,6 +35,8 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr uint32_t kSpinMax = 1u << 24;   // ~0.5 s of polling before giving up
+constexpr int kYS = kNC + 4;              // LDS row stride of the expand's y tile (floats)
+constexpr int kVS = kMaxRc + 8;           // LDS row stride of the bf16 v operands (elements)
 
 // ---------------------------------------------------------------------------
 // element types: bf16 (uint16 storage) and fp32, 8 elements per vector
@@ -400,19 +402,26 @@ __device__ __forceinline__ void pin_regs(const V& v) {
 }
 
 // Hand-off of split-K partials between blocks, with no cache-wide fences.
-// Partials are written and read with device-coherent accesses (relaxed
-// agent-scope atomics: stores write through to the device-coherent level, loads
-// never return a stale cached copy).  A shrink block waits until its partial
+// Partials and v are written and read with device-coherent 16-byte buffer
+// accesses (cache policy sc1: stores write through to the device-coherent
+// level, loads never return a stale cached copy).  A shrink block waits until its partial
 // stores have completed (s_waitcnt), meets its other waves, and only then bumps
 // the tile's arrival count; an expand block issues its partial loads only after
 // it has seen the count.  Completed device-coherent stores are visible to every
 // later device-coherent load, so the counter orders the data without writing
 // back or invalidating the L2.
-__device__ __forceinline__ void store_coherent(float* p, float v) {
-  __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+constexpr int kCoherent = 16;                 // buffer cache policy: sc1 (device scope)
+constexpr int kRawBufferWord3 = 0x00020000;   // gfx9 raw buffer resource, dword 3
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kRawBufferWord3);
 }
-__device__ __forceinline__ float load_coherent(const float* p) {
-  return __hip_atomic_load(const_cast<float*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 load4_coherent(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, kCoherent));
+}
+__device__ __forceinline__ void store4_coherent(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, float4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)byte_off, 0, kCoherent);
 }
 
 // All waves' coherent stores have completed, then one thread adds 1 to
@@ -454,14 +463,27 @@ __device__ __forceinline__ bool await_word(const uint32_t* word, uint32_t target
   return *s_flag != 0;
 }
 
+// v entries idx .. idx+3 of a tile (row-major [token][R]): the centroid ranks
+// j < r_c are scaled by the token's gamma.
+__device__ __forceinline__ float4 scale_centroid(float4 v, int idx, int R, int rc, const int4* s_tile) {
+  const int t = idx / R, j = idx - t * R;      // the 4 entries share a row (R % 4 == 0)
+  const float g = __int_as_float(s_tile[1 + t].w);
+  if (j + 0 < rc) v.x *= g;
+  if (j + 1 < rc) v.y *= g;
+  if (j + 2 < rc) v.z *= g;
+  if (j + 3 < rc) v.w *= g;
+  return v;
+}
+
 // Shrink block: tile `tau`, K range `s` of the apply.  Writes the tile's
 // split-K partial sums P[s][token][0 : r_c + r_u_max] and counts its arrival.
 template <typename E, int MB, int RU, int NBM>
-__device__ void shrink_block(const ApplyArgs& a, int tau, int s, char* lds) {
+__device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s, char* lds) {
   using O = Ops<E>;
   using Vec = typename O::Vec;
   constexpr int M = 16 * MB, KW = 4 / MB;
-  constexpr int U = shrink_batch((int)(sizeof(Vec) / 4), NBM, RU);
+  constexpr int U0 = shrink_batch((int)(sizeof(Vec) / 4), NBM, RU) / 2;
+  constexpr int U = U0 < 1 ? 1 : U0;            // steps per register buffer
   int4* s_tile = reinterpret_cast<int4*>(lds);
   float* s_part = reinterpret_cast<float*>(lds + tile_bytes(M));   // [KW][M][R]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -500,26 +522,40 @@ __device__ void shrink_block(const ApplyArgs& a, int tau, int s, char* lds) {
 #pragma unroll
   for (int j = 0; j < RU; ++j) accu[j] = 0.f;
 
-  for (int k0 = kbeg; k0 < kend; k0 += 32 * U) {
-    Vec xv[U], av[U][NBM], uv[U][RU];
+  // two register buffers of U steps each: the loads of batch b + 1 are in
+  // flight while batch b is multiplied
+  Vec xv[2][U], av[2][U][NBM], uv[2][U][RU];
+  auto load_batch = [&](Vec (&x_)[U], Vec (&a_)[U][NBM], Vec (&u_)[U][RU], int k0) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       const int kk = k0 + 32 * u + kseg;
       const bool kin = kk < kend;
-      xv[u] = (tok_ok && kin) ? O::load(xrow + kk) : O::zero();
+      x_[u] = (tok_ok && kin) ? O::load(xrow + kk) : O::zero();
 #pragma unroll
-      for (int nb = 0; nb < NBM; ++nb) av[u][nb] = (aok[nb] && kin) ? O::load(arow[nb] + kk) : O::zero();
+      for (int nb = 0; nb < NBM; ++nb) a_[u][nb] = (aok[nb] && kin) ? O::load(arow[nb] + kk) : O::zero();
 #pragma unroll
-      for (int j = 0; j < RU; ++j) uv[u][j] = (j < ru && kin) ? O::load(au + (size_t)j * in + kk) : O::zero();
+      for (int j = 0; j < RU; ++j) u_[u][j] = (j < ru && kin) ? O::load(au + (size_t)j * in + kk) : O::zero();
     }
+  };
+  auto mul_batch = [&](const Vec (&x_)[U], const Vec (&a_)[U][NBM], const Vec (&u_)[U][RU]) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
       if (has_c) {
 #pragma unroll
-        for (int nb = 0; nb < NBM; ++nb) acc[nb] = O::mma(xv[u], av[u][nb], acc[nb]);
+        for (int nb = 0; nb < NBM; ++nb) acc[nb] = O::mma(x_[u], a_[u][nb], acc[nb]);
       }
 #pragma unroll
-      for (int j = 0; j < RU; ++j) accu[j] = O::dot(xv[u], uv[u][j], accu[j]);
+      for (int j = 0; j < RU; ++j) accu[j] = O::dot(x_[u], u_[u][j], accu[j]);
+    }
+  };
+  const int nbat = (kend - kbeg + 32 * U - 1) / (32 * U);
+  if (nbat > 0) load_batch(xv[0], av[0], uv[0], kbeg);
+  for (int b = 0; b < nbat; b += 2) {
+    if (b + 1 < nbat) load_batch(xv[1], av[1], uv[1], kbeg + (b + 1) * 32 * U);
+    mul_batch(xv[0], av[0], uv[0]);
+    if (b + 1 < nbat) {
+      if (b + 2 < nbat) load_batch(xv[0], av[0], uv[0], kbeg + (b + 2) * 32 * U);
+      mul_batch(xv[1], av[1], uv[1]);
     }
   }
   // residual: lanes l, l^16, l^32, l^48 hold the four k offsets of one token
@@ -542,77 +578,148 @@ __device__ void shrink_block(const ApplyArgs& a, int tau, int s, char* lds) {
 #pragma unroll
     for (int j = 0; j < RU; ++j)
       if (j < a.r_u_max) P[tl * R + rc + j] = accu[j];
+    for (int j = rc + a.r_u_max; j < R; ++j) P[tl * R + j] = 0.f;   // row padding
   }
   __syncthreads();
-  const int nR = n * R;
-  float* V = a.v + (size_t)i0 * R;             // v rows of this tile
+  // R is a multiple of 4: rows are whole float4 vectors
+  const int nR4 = n * R / 4;
+  const __amdgpu_buffer_rsrc_t rv = coherent_rsrc(a.v + (size_t)i0 * R, (uint32_t)(nR4 * 16));
   if (a.S == 1) {
     // one K range: this block writes v itself
-    for (int idx = tid; idx < nR; idx += 256) {
-      float v = 0.f;
+    for (int i4 = tid; i4 < nR4; i4 += 256) {
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-      for (int q = 0; q < KW; ++q) v += s_part[(size_t)q * M * R + idx];
-      const int t = idx / R, j = idx - t * R;
-      if (j < rc) v *= __int_as_float(s_tile[1 + t].w);
-      store_coherent(V + idx, v);
+      for (int q = 0; q < KW; ++q) {
+        const float4 p = *reinterpret_cast<const float4*>(s_part + (size_t)q * M * R + 4 * i4);
+        v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+      }
+      store4_coherent(rv, 16u * i4, scale_centroid(v, 4 * i4, R, rc, s_tile));
     }
   } else {
-    float* G = a.partials + ((size_t)s * a.T + i0) * R;
-    for (int idx = tid; idx < nR; idx += 256) {
-      float v = 0.f;
+    const __amdgpu_buffer_rsrc_t rp =
+        coherent_rsrc(a.partials + ((size_t)s * a.T + i0) * R, (uint32_t)(nR4 * 16));
+    for (int i4 = tid; i4 < nR4; i4 += 256) {
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
 #pragma unroll
-      for (int q = 0; q < KW; ++q) v += s_part[(size_t)q * M * R + idx];
-      store_coherent(G + idx, v);
+      for (int q = 0; q < KW; ++q) {
+        const float4 p = *reinterpret_cast<const float4*>(s_part + (size_t)q * M * R + 4 * i4);
+        v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+      }
+      store4_coherent(rp, 16u * i4, v);
     }
     __shared__ uint32_t s_count;
     if (publish_add(a.arrive + (size_t)tau * kCounterStride, &s_count) != a.target) return;
     // the last of the tile's S blocks: sum the splits in order, scale by gamma
-    const float* P0 = a.partials + (size_t)i0 * R;
-    const size_t stride = (size_t)a.T * R;
-    constexpr int Q = 4, SG = 8;                 // entries x splits in flight per thread
-    for (int base = 0; base < nR; base += 256 * Q) {
-      float v[Q] = {0.f, 0.f, 0.f, 0.f};
+    const size_t split_bytes = (size_t)a.T * R * 4;
+    const __amdgpu_buffer_rsrc_t rall = coherent_rsrc(a.partials + (size_t)i0 * R,
+                                                      (uint32_t)((a.S - 1) * split_bytes + nR4 * 16));
+    constexpr int Q = 2, SG = 8;                 // vectors x splits in flight per thread
+    for (int base = 0; base < nR4; base += 256 * Q) {
+      float4 v[Q];
+#pragma unroll
+      for (int q = 0; q < Q; ++q) v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
       for (int s0 = 0; s0 < a.S; s0 += SG) {
-        float p[Q][SG];
+        float4 p[Q][SG];
 #pragma unroll
         for (int q = 0; q < Q; ++q) {
-          const int idx = base + tid + 256 * q;
+          const int i4 = base + tid + 256 * q;
 #pragma unroll
           for (int e = 0; e < SG; ++e)
-            p[q][e] = (idx < nR && s0 + e < a.S) ? load_coherent(P0 + (s0 + e) * stride + idx) : 0.f;
+            p[q][e] = (i4 < nR4 && s0 + e < a.S)
+                          ? load4_coherent(rall, (uint32_t)((s0 + e) * split_bytes + 16u * i4))
+                          : make_float4(0.f, 0.f, 0.f, 0.f);
         }
 #pragma unroll
         for (int q = 0; q < Q; ++q)
 #pragma unroll
-          for (int e = 0; e < SG; ++e) v[q] += p[q][e];
+          for (int e = 0; e < SG; ++e) {
+            v[q].x += p[q][e].x; v[q].y += p[q][e].y; v[q].z += p[q][e].z; v[q].w += p[q][e].w;
+          }
       }
 #pragma unroll
       for (int q = 0; q < Q; ++q) {
-        const int idx = base + tid + 256 * q;
-        if (idx < nR) {
-          const int t = idx / R, j = idx - t * R;
-          store_coherent(V + idx, j < rc ? v[q] * __int_as_float(s_tile[1 + t].w) : v[q]);
-        }
+        const int i4 = base + tid + 256 * q;
+        if (i4 < nR4) store4_coherent(rv, 16u * i4, scale_centroid(v[q], 4 * i4, R, rc, s_tile));
       }
     }
   }
   publish_store(a.ready + (size_t)tau * kCounterStride, a.epoch);
 }
 
-// Expand block: tile `tau`, columns [q * kNC, q * kNC + kNC) of y.
+// Operands of one expand chunk (kNC columns of y for the tile's tokens) that a
+// thread holds in registers: y and B_u slices of its (token, 8-column) items and
+// the B_c^T operands of its wave's MFMA column blocks.
 template <typename E, int MB, int RU, int NBM>
-__device__ void expand_block(const ApplyArgs& a, int tau, int q, char* lds) {
+struct ExpandRegs {
+  using Vec = typename Ops<E>::Vec;
+  static constexpr int M = 16 * MB;
+  static constexpr int CG = kNC / 8;            // 8-column groups per chunk
+  static constexpr int ITEMS = M * CG / 256;    // (token, column group) items per thread
+  static constexpr int RP = RU < 2 ? RU : 2;    // residual ranks held in registers
+  static constexpr int NBW = kNC / 16 / 4;      // 16-column MFMA blocks per wave
+  static constexpr int KS = (NBM + 1) / 2;      // 32-rank MFMA steps
+  Vec yold[ITEMS];
+  Vec bu[ITEMS][RP > 0 ? RP : 1];
+  Vec bct[NBW][KS];
+
+  __device__ __forceinline__ void load(const ApplyArgs& a, const int4* s_tile, int n, bool has_c, int c, int n0) {
+    using O = Ops<E>;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int out = a.out_dim, rc = a.r_c;
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) {
+      const int idx = tid + 256 * it, t = idx / CG, col = n0 + (idx % CG) * 8;
+      const int4 tk = s_tile[1 + t];
+      const bool ok = t < n && col < out;
+      const int ru = (ok && tk.y >= 0) ? tk.z : 0;
+      yold[it] = ok ? O::load(reinterpret_cast<const E*>(a.y) + (size_t)tk.x * out + col) : O::zero();
+      const E* bup = ru ? reinterpret_cast<const E*>(a.pool + (size_t)tk.y * a.slot_stride) +
+                              (int64_t)ru * (a.tab_prefix + a.in_dim)
+                        : nullptr;
+#pragma unroll
+      for (int j = 0; j < RP; ++j) bu[it][j] = (j < ru) ? O::load(bup + (size_t)j * out + col) : O::zero();
+    }
+    const E* bt = reinterpret_cast<const E*>(a.cent_bt) + (size_t)(has_c ? c : 0) * out * rc;
+#pragma unroll
+    for (int w = 0; w < NBW; ++w) {
+      const int col = n0 + (wave + 4 * w) * 16 + (lane & 15);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int j = ks * 32 + (lane >> 4) * 8;
+        bct[w][ks] = (has_c && col < out && j < rc) ? O::load(bt + (size_t)col * rc + j) : O::zero();
+      }
+    }
+  }
+
+  __device__ __forceinline__ void pin() const {
+#pragma unroll
+    for (int it = 0; it < ITEMS; ++it) {
+      pin_regs(yold[it]);
+#pragma unroll
+      for (int j = 0; j < RP; ++j) pin_regs(bu[it][j]);
+    }
+#pragma unroll
+    for (int w = 0; w < NBW; ++w)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) pin_regs(bct[w][ks]);
+  }
+};
+
+// Expand block: tile `tau`, column chunks [q * cpb, q * cpb + cpb) of kNC
+// columns each.  The first chunk's operands are loaded before the wait.
+template <typename E, int MB, int RU, int NBM>
+__device__ __forceinline__ void expand_block(const ApplyArgs& a, int tau, int q, char* lds) {
   using O = Ops<E>;
   using Vec = typename O::Vec;
-  constexpr int M = 16 * MB;
-  constexpr int CG = kNC / 8;                   // 8-column groups per block
-  constexpr int ITEMS = M * CG / 256;           // (token, column group) items per thread
-  constexpr int RP = RU < 2 ? RU : 2;           // residual ranks prefetched
-  constexpr int NBW = kNC / 16 / 4;             // 16-column blocks per wave
-  constexpr int KS = (NBM + 1) / 2;             // 32-rank steps
+  using Regs = ExpandRegs<E, MB, RU, NBM>;
+  constexpr int M = Regs::M, CG = Regs::CG, ITEMS = Regs::ITEMS, RP = Regs::RP;
+  constexpr int NBW = Regs::NBW, KS = Regs::KS;
   int4* s_tile = reinterpret_cast<int4*>(lds);
   float* s_v = reinterpret_cast<float*>(lds + tile_bytes(M));     // [M][R]
-  float* s_y = s_v + (size_t)M * a.R;                             // [M][kNC]
+  float* s_y = s_v + (size_t)M * a.R;                             // [M][kYS]
+  // bf16: hi and lo halves of the centroid part of v, [M][kVS] each, built once
+  uint16_t* s_vh = reinterpret_cast<uint16_t*>(s_y + (size_t)M * kYS);
+  uint16_t* s_vl = s_vh + (size_t)M * kVS;
   __shared__ int s_flag;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int4* trec = a.tiles + (size_t)tau * (M + 1);
@@ -621,118 +728,111 @@ __device__ void expand_block(const ApplyArgs& a, int tau, int q, char* lds) {
   const int i0 = s_tile[0].x, n = s_tile[0].y, c = s_tile[0].z;
   const int R = a.R, out = a.out_dim, rc = a.r_c, in = a.in_dim;
   const bool has_c = c >= 0 && rc > 0;
-  const int n0 = q * kNC;
+  const int chunk0 = q * a.cpb;
 
-  // ---- prefetch: y and B_u slices of this thread's items, B_c^T operands ----
-  Vec yold[ITEMS];
-  Vec bu[ITEMS][RP > 0 ? RP : 1];
-#pragma unroll
-  for (int it = 0; it < ITEMS; ++it) {
-    const int idx = tid + 256 * it, t = idx / CG, col = n0 + (idx % CG) * 8;
-    const int4 tk = s_tile[1 + t];
-    const bool ok = t < n && col < out;
-    const int ru = (ok && tk.y >= 0) ? tk.z : 0;
-    yold[it] = ok ? O::load(reinterpret_cast<const E*>(a.y) + (size_t)tk.x * out + col) : O::zero();
-    const E* bup = ru ? reinterpret_cast<const E*>(a.pool + (size_t)tk.y * a.slot_stride) +
-                            (int64_t)ru * (a.tab_prefix + in)
-                      : nullptr;
-#pragma unroll
-    for (int j = 0; j < RP; ++j) bu[it][j] = (j < ru) ? O::load(bup + (size_t)j * out + col) : O::zero();
-  }
-  Vec bct[NBW][KS];
-  const E* bt = reinterpret_cast<const E*>(a.cent_bt) + (size_t)(has_c ? c : 0) * out * rc;
-#pragma unroll
-  for (int w = 0; w < NBW; ++w) {
-    const int col = n0 + (wave + 4 * w) * 16 + (lane & 15);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const int j = ks * 32 + (lane >> 4) * 8;
-      bct[w][ks] = (has_c && col < out && j < rc) ? O::load(bt + (size_t)col * rc + j) : O::zero();
-    }
-  }
-
-#pragma unroll
-  for (int it = 0; it < ITEMS; ++it) {
-    pin_regs(yold[it]);
-#pragma unroll
-    for (int j = 0; j < RP; ++j) pin_regs(bu[it][j]);
-  }
-#pragma unroll
-  for (int w = 0; w < NBW; ++w)
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) pin_regs(bct[w][ks]);
+  Regs regs;
+  regs.load(a, s_tile, n, has_c, c, chunk0 * kNC);
+  regs.pin();
 
   // ---- wait for the tile's v ----
   if (!await_word(a.ready + (size_t)tau * kCounterStride, a.epoch, a.meta + kMetaErr, &s_flag)) return;
   {
-    const float* V = a.v + (size_t)i0 * R;
-    const int nR = n * R, MR = M * R;
-    for (int idx = tid; idx < MR; idx += 256) s_v[idx] = idx < nR ? load_coherent(V + idx) : 0.f;
+    const int nR4 = n * R / 4, MR4 = M * R / 4;
+    const __amdgpu_buffer_rsrc_t rv = coherent_rsrc(a.v + (size_t)i0 * R, (uint32_t)(nR4 * 16));
+    for (int i4 = tid; i4 < MR4; i4 += 256)
+      reinterpret_cast<float4*>(s_v)[i4] = load4_coherent(rv, 16u * i4);   // past n rows: zeros
   }
   __syncthreads();
-
-  // ---- centroid part on MFMA: y^T block [16 cols x 16 tokens] = B_c^T . v_c^T ----
-  if (has_c) {
-#pragma unroll
-    for (int w = 0; w < NBW; ++w) {
-      const int cb = (wave + 4 * w) * 16;       // first column of the block, local
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-        const int t = mb * 16 + (lane & 15);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const int j = ks * 32 + (lane >> 4) * 8;
-          float vv[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) vv[e] = (j + e < rc) ? s_v[t * R + j + e] : 0.f;
-          acc = O::mma_f32rhs(bct[w][ks], vv, acc);
-        }
-#pragma unroll
-        for (int e = 0; e < 4; ++e) s_y[t * kNC + cb + 4 * (lane >> 4) + e] = acc[e];
-      }
+  if constexpr (sizeof(E) == 2) {
+    // v_c = hi + lo, both bf16 (hi = rne(v), lo = rne(v - hi)): about 16
+    // significant bits of v reach the MFMA; ranks past r_c are zero
+    for (int i = tid; i < M * KS * 32; i += 256) {
+      const int t = i / (KS * 32), j = i - t * (KS * 32);
+      const float v = j < rc ? s_v[t * R + j] : 0.f;
+      const uint32_t h = f32_to_bf16_rne(v);
+      s_vh[t * kVS + j] = (uint16_t)h;
+      s_vl[t * kVS + j] = (uint16_t)f32_to_bf16_rne(v - __uint_as_float(h << 16));
     }
+    __syncthreads();
   }
-  __syncthreads();
 
-  // ---- residual part, add, round, store ----
-#pragma unroll
-  for (int it = 0; it < ITEMS; ++it) {
-    const int idx = tid + 256 * it, t = idx / CG, cl = (idx % CG) * 8, col = n0 + cl;
-    if (t >= n || col >= out) continue;
-    const int4 tk = s_tile[1 + t];
-    const int ru = tk.y >= 0 ? tk.z : 0;
-    float accv[8], yv[8];
+  for (int cc = 0; cc < a.cpb; ++cc) {
+    const int n0 = (chunk0 + cc) * kNC;
+    if (n0 >= out) break;
+    if (cc > 0) {
+      regs.load(a, s_tile, n, has_c, c, n0);
+      __syncthreads();                          // s_y of the previous chunk fully consumed
+    }
+    // ---- centroid part on MFMA: y^T block [16 cols x 16 tokens] = B_c^T . v_c^T ----
     if (has_c) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) accv[e] = s_y[t * kNC + cl + e];
-    } else {
+      for (int w = 0; w < NBW; ++w) {
+        const int cb = (wave + 4 * w) * 16;     // first column of the block, local
 #pragma unroll
-      for (int e = 0; e < 8; ++e) accv[e] = 0.f;
-    }
-    const float* vt = s_v + t * R + rc;
+        for (int mb = 0; mb < MB; ++mb) {
+          f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+          const int t = mb * 16 + (lane & 15);
 #pragma unroll
-    for (int j = 0; j < RU; ++j) {
-      if (j < ru) {
-        Vec bv;
-        if (j < RP) {
-          bv = bu[it][j < RP ? j : 0];
-        } else {
-          const E* bup = reinterpret_cast<const E*>(a.pool + (size_t)tk.y * a.slot_stride) +
-                         (int64_t)ru * (a.tab_prefix + in);
-          bv = O::load(bup + (size_t)j * out + col);
+          for (int ks = 0; ks < KS; ++ks) {
+            const int j = ks * 32 + (lane >> 4) * 8;
+            if constexpr (sizeof(E) == 2) {
+              const uint4 hi = *reinterpret_cast<const uint4*>(s_vh + t * kVS + j);
+              const uint4 lo = *reinterpret_cast<const uint4*>(s_vl + t * kVS + j);
+              acc = O::mma(regs.bct[w][ks], hi, acc);
+              acc = O::mma(regs.bct[w][ks], lo, acc);
+            } else {
+              float vv[8];
+#pragma unroll
+              for (int e = 0; e < 8; ++e) vv[e] = (j + e < rc) ? s_v[t * R + j + e] : 0.f;
+              acc = O::mma_f32rhs(regs.bct[w][ks], vv, acc);
+            }
+          }
+#pragma unroll
+          for (int e = 0; e < 4; ++e) s_y[t * kYS + cb + 4 * (lane >> 4) + e] = acc[e];
         }
-        float b8[8];
-        O::to_f32(bv, b8);
-        const float vj = vt[j];
-#pragma unroll
-        for (int e = 0; e < 8; ++e) accv[e] = fmaf(vj, b8[e], accv[e]);
       }
     }
-    O::to_f32(yold[it], yv);
+    __syncthreads();
+
+    // ---- residual part, add, round, store ----
 #pragma unroll
-    for (int e = 0; e < 8; ++e) yv[e] += accv[e];
-    O::store(reinterpret_cast<E*>(a.y) + (size_t)tk.x * out + col, yv);
+    for (int it = 0; it < ITEMS; ++it) {
+      const int idx = tid + 256 * it, t = idx / CG, cl = (idx % CG) * 8, col = n0 + cl;
+      if (t >= n || col >= out) continue;
+      const int4 tk = s_tile[1 + t];
+      const int ru = tk.y >= 0 ? tk.z : 0;
+      float accv[8], yv[8];
+      if (has_c) {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) accv[e] = s_y[t * kYS + cl + e];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) accv[e] = 0.f;
+      }
+      const float* vt = s_v + t * R + rc;
+#pragma unroll
+      for (int j = 0; j < RU; ++j) {
+        if (j < ru) {
+          Vec bv;
+          if (j < RP) {
+            bv = regs.bu[it][j < RP ? j : 0];
+          } else {
+            const E* bup = reinterpret_cast<const E*>(a.pool + (size_t)tk.y * a.slot_stride) +
+                           (int64_t)ru * (a.tab_prefix + in);
+            bv = O::load(bup + (size_t)j * out + col);
+          }
+          float b8[8];
+          O::to_f32(bv, b8);
+          const float vj = vt[j];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) accv[e] = fmaf(vj, b8[e], accv[e]);
+        }
+      }
+      O::to_f32(regs.yold[it], yv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) yv[e] += accv[e];
+      O::store(reinterpret_cast<E*>(a.y) + (size_t)tk.x * out + col, yv);
+    }
   }
 }
 
@@ -752,13 +852,13 @@ __global__ void __launch_bounds__(256) k_apply(ApplyArgs a) {
 size_t apply_lds(int M, int R) {
   const size_t tb = (size_t)tile_bytes(M);
   const size_t shrink = tb + sizeof(float) * 64 * (size_t)R;           // KW * M == 64
-  const size_t expand = tb + sizeof(float) * ((size_t)M * R + (size_t)M * kNC);
+  const size_t expand = tb + sizeof(float) * ((size_t)M * R + (size_t)M * kYS) + 2 * sizeof(uint16_t) * M * kVS;
   return shrink > expand ? shrink : expand;
 }
 
 template <typename E, int RU, int NBM>
 hipError_t launch_nbm(const ApplyArgs& a, int M, hipStream_t s) {
-  const dim3 grid(a.n_tiles * (a.S + a.n_col)), block(256);
+  const dim3 grid(a.n_tiles * (a.S + a.n_col)), block(256);   // n_col: column blocks of cpb chunks
   const size_t lds = apply_lds(M, a.R);
   if (M == 16) {
     hipLaunchKernelGGL((k_apply<E, 1, RU, NBM>), grid, block, lds, s, a);

@@ -393,7 +393,7 @@ salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out) {
   salt_plan* p = new (std::nothrow) salt_plan();
   if (!p) return SALT_ERR_OUT_OF_MEMORY;
   const size_t T = (size_t)ctx->cfg.max_tokens;
-  const size_t R = std::max<size_t>(1, (size_t)ctx->cfg.r_c + ctx->cfg.r_u_max);
+  const size_t R = salt::padded_rank(ctx->cfg.r_c, ctx->cfg.r_u_max);
   PlanBuffers& b = p->dev;
   // split-K partials for up to max(8 T, 64K) (split, token) pairs
   b.partial_cap = std::max<size_t>(8 * T, 65536) * R;
@@ -504,7 +504,7 @@ salt_status salt_plan_set_maps(salt_ctx* ctx, salt_plan* plan, int32_t T, const 
       n_groups_c += (g > 0);
     }
   const double mean = n_groups ? (double)T / n_groups : 0.0;
-  plan->M = (ctx->cfg.dtype == SALT_F32 || mean <= 24.0) ? 16 : (mean <= 48.0 ? 32 : 64);
+  plan->M = (ctx->cfg.dtype == SALT_F32 || mean <= 24.0) ? 16 : 32;
   int n_tiles = 0;
   for (int g = 0; g <= C; ++g) n_tiles += (per_c[g] + plan->M - 1) / plan->M;
   plan->n_tiles = n_tiles;
@@ -630,7 +630,7 @@ salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
   a.out_dim = sh.out_dim;
   a.r_c = ctx->cfg.r_c;
   a.r_u_max = ctx->cfg.r_u_max;
-  a.R = std::max(1, a.r_c + a.r_u_max);
+  a.R = salt::padded_rank(a.r_c, a.r_u_max);
   a.n_tiles = plan->n_tiles;
   // K split.  Small (decode) batches are latency bound: spread the shrink input
   // over many blocks (~16 KiB each) so no CU streams much more than its share,
@@ -644,12 +644,18 @@ salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
   const int s_bytes = (int)std::ceil(shrink_bytes / ((double)a.n_tiles * block_bytes));
   const int s_traffic = std::max(1, (int)((small ? 0.5 : 0.2) * shrink_bytes / ((double)T * a.R * 8.0)));
   const int gran = 32 * KW;
-  int S = std::max(1, std::min({s_bytes, s_traffic, salt::kMaxSplit, (sh.in_dim + gran - 1) / gran}));
+  // the last block of a tile sums S x M x R partials: keep that within ~64 KiB
+  const int s_reduce = std::max(1, (int)(65536 / ((size_t)M * a.R * 4)));
+  int S = std::max(1, std::min({s_bytes, s_traffic, s_reduce, salt::kMaxSplit, (sh.in_dim + gran - 1) / gran}));
   while (S > 1 && (size_t)S * T * a.R > plan->dev.partial_cap) --S;
   const int Kc = ((sh.in_dim + S - 1) / S + gran - 1) / gran * gran;
   a.Kc = Kc;
   a.S = (sh.in_dim + Kc - 1) / Kc;   // <= S
-  a.n_col = (sh.out_dim + salt::kNC - 1) / salt::kNC;
+  // expand: several kNC-column chunks per block when there are blocks to spare,
+  // so one block reads the tile's v once for more columns
+  const int chunks = (sh.out_dim + salt::kNC - 1) / salt::kNC;
+  a.cpb = std::max(1, std::min(4, (a.n_tiles * chunks) / 1024));
+  a.n_col = (chunks + a.cpb - 1) / a.cpb;
   if (a.S > 1) plan->arrivals += (uint32_t)a.S;
   a.target = plan->arrivals;
   a.epoch = ++plan->epoch;
