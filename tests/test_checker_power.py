@@ -1,0 +1,60 @@
+"""The parity gate |y - ref| <= 1e-2 (1 + |ref|) must reject plausible wrong
+outputs at the workloads' own scales (CPU only, oracle-generated mutants).
+
+Each mutant is what a kernel with one planted mistake would produce, rounded
+to bf16 like a real output; the correct output rounded the same way must pass.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_03579_amd import synth
+from tests.gpu_harness import TOL_NORTH_STAR, close_enough
+
+
+def to_bf16_values(a):
+    return oracle.decode(synth.f32_to_bf16_bits(a.astype(np.float32)), "bf16")
+
+
+def outputs(w, table, tok_c, tok_u, gamma, drop_residual=False, rows=None):
+    d = w.dtype
+    x = oracle.decode(w.x(table), d)
+    y0 = oracle.decode(w.y0(table), d)
+    cat, cb = (oracle.decode(a, d) for a in w.centroids(table))
+    res = {}
+    for s in set(int(u) for u in tok_u if u >= 0):
+        at, b = (oracle.decode(a, d) for a in w.residual(s, table))
+        res[s] = (at * 0, b * 0) if drop_residual else (at, b)
+    return oracle.apply(x, y0, cat, cb, res, tok_c, tok_u, gamma, rows=rows)
+
+
+CASES = [(2, {}), (4, dict(T=64)), (5, dict(T=96)), (2, dict(gamma="bins"))]
+
+
+@pytest.mark.parametrize("cfg,kw", CASES)
+def test_gate_rejects_planted_mistakes(cfg, kw):
+    w = synth.make(cfg, 0, **kw)
+    t = 0
+    rows = list(range(min(w.T, 48)))
+    ref = outputs(w, t, w.tok_c, w.tok_u, w.gamma, rows=rows)
+    assert close_enough(to_bf16_values(ref), ref, TOL_NORTH_STAR)[0]
+    C, S = w.n_centroids, w.n_slots
+    mutants = {
+        "y unchanged": oracle.decode(w.y0(t), w.dtype)[rows],
+        "residual dropped": outputs(w, t, w.tok_c, w.tok_u, w.gamma, drop_residual=True, rows=rows),
+        "centroid off by one": outputs(w, t, (w.tok_c + 1) % C, w.tok_u, w.gamma, rows=rows),
+        "centroid dropped": outputs(w, t, np.full_like(w.tok_c, -1), w.tok_u, w.gamma, rows=rows),
+    }
+    # a slot off by one only matters where the neighbouring slot is loaded
+    tu = w.tok_u.copy()
+    ref_slots = set(w.referenced_slots().tolist())
+    nxt = np.array([(u + 1) % S for u in tu])
+    ok = np.array([n in ref_slots and w.slot_rank[n] == w.slot_rank[u] for u, n in zip(tu, nxt)])
+    if ok.any():
+        tu[ok] = nxt[ok]
+        mutants["slot off by one"] = outputs(w, t, w.tok_c, tu, w.gamma, rows=rows)
+    if w.gamma is not None:
+        mutants["gamma ignored"] = outputs(w, t, w.tok_c, w.tok_u, None, rows=rows)
+    for name, m in mutants.items():
+        passed, worst, nbad = close_enough(to_bf16_values(m), ref, TOL_NORTH_STAR)
+        assert not passed, f"cfg {cfg}: the gate accepts '{name}' (worst {worst:.2f}x)"

@@ -1,0 +1,241 @@
+"""GPU edge cases, error paths and swap ordering of the libsalt C ABI.
+
+Every case prints its name before touching the GPU.  Expected values come from
+the CPU oracle on the same seeded inputs.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_03579_amd import synth
+from tests.gpu_harness import TOL_F32, TOL_NORTH_STAR, Run, close_enough
+
+pytestmark = pytest.mark.gpu
+
+
+def _announce(name):
+    print(f"\n[gpu case] {name}", flush=True)
+
+
+def _tol(w):
+    return TOL_F32 if w.dtype == "f32" else TOL_NORTH_STAR
+
+
+def _check(run, table=0, rows=None):
+    got = oracle.decode(run.apply(table), run.w.dtype)
+    assert run.plan.errors(run.stream) == 0
+    ref = run.oracle_table(table, rows)
+    if rows is not None:
+        got = got[np.asarray(rows)]
+    ok, worst, nbad = close_enough(got, ref, _tol(run.w))
+    assert ok, f"{nbad} elements out of tolerance, worst {worst:.3f}x"
+
+
+def _plan_matches(run):
+    p = run.plan.download(run.stream)
+    want = oracle.plan(run.maps[0], run.maps[1])
+    for k in want:
+        assert np.array_equal(p[k], want[k]), k
+
+
+@pytest.mark.parametrize("cfg", [1, 2])
+def test_term_absent_cases(cfg):
+    """c = -1 (residual only), u = -1 (centroid only), both -1 (y untouched)."""
+    _announce(f"absent terms cfg={cfg}")
+    w = synth.make(cfg, 5, y0="normal")
+    run = Run(w)
+    try:
+        T = w.T
+        rng = np.random.default_rng(9)
+        cases = {
+            "no centroid": (np.full(T, -1, np.int32), w.tok_u),
+            "no residual": (w.tok_c, np.full(T, -1, np.int32)),
+            "neither": (np.full(T, -1, np.int32), np.full(T, -1, np.int32)),
+            "mixed": (np.where(rng.random(T) < 0.3, -1, w.tok_c).astype(np.int32),
+                      np.where(rng.random(T) < 0.3, -1, w.tok_u).astype(np.int32)),
+        }
+        for name, (tc, tu) in cases.items():
+            run.set_and_build(tc, tu)
+            _plan_matches(run)
+            _check(run)
+        # both absent: bit-identical y
+        run.set_and_build(cases["neither"][0], cases["neither"][1])
+        assert np.array_equal(run.apply(0), w.y0(0))
+    finally:
+        run.close()
+
+
+def test_ragged_and_degenerate_batches():
+    _announce("ragged batch sizes, T = 0 and T = 1, one big centroid group")
+    w = synth.make(2, 6, y0="normal")
+    run = Run(w)
+    try:
+        for T in (1, 5, 17, 33, 63):
+            run.set_and_build(w.tok_c[:T], w.tok_u[:T])
+            _plan_matches(run)
+            got = oracle.decode(run.apply(0), w.dtype)[:T]
+            ref = run.oracle_table(0, rows=list(range(T)))
+            assert close_enough(got, ref, TOL_NORTH_STAR)[0], T
+            # rows past T are untouched
+            assert np.array_equal(run.apply(0)[T:], w.y0(0)[T:])
+        # one centroid for everyone: a group spanning several tiles
+        run.set_and_build(np.zeros(w.T, np.int32), w.tok_u)
+        _plan_matches(run)
+        _check(run)
+        # empty batch: plan is empty, apply is a no-op
+        run.set_and_build(np.zeros(0, np.int32), np.zeros(0, np.int32))
+        p = run.plan.download(run.stream)
+        assert p["perm"].size == 0 and p["seg_off"].tolist() == [0] and p["grp_off"].tolist() == [0]
+        assert np.array_equal(run.apply(0), w.y0(0))
+    finally:
+        run.close()
+
+
+def test_rank_zero_and_mixed_rank_slots():
+    _announce("rank-0 slots and ranks 1/2 in one batch")
+    w = synth.make(5, 2, layers=1, T=160)
+    run = Run(w)
+    try:
+        # empty the residual term of a few referenced slots
+        slots = w.referenced_slots()[:5]
+        for s in slots:
+            run.ctx.load_residual(int(s), 0, None)
+            run.w.slot_rank[int(s)] = 0
+        run.ctx.wait_loads()
+        run.set_and_build()
+        _plan_matches(run)
+        for t in (0, 6):
+            _check(run, t)
+    finally:
+        run.close()
+
+
+def test_repeated_applies_and_rebuilds():
+    """Arrival counters and epochs over many applies of one plan, then a rebuild
+    with a batch of a different tiling."""
+    _announce("40 applies on one plan, then rebuilds")
+    w = synth.make(2, 7)
+    run = Run(w)
+    try:
+        run.set_and_build()
+        x = w.x(0)
+        from tests.gpu_harness import to_dev
+        xd, yd = to_dev(x), to_dev(w.y0(0))
+        for _ in range(40):
+            run.ctx.apply(0, run.plan, xd.ptr, yd.ptr, run.stream)
+        run._stream.synchronize()
+        assert run.plan.errors(run.stream) == 0
+        got = oracle.decode(yd.to_host(), w.dtype)
+        one = run.oracle_table(0) - oracle.decode(w.y0(0), w.dtype)
+        ref = oracle.decode(w.y0(0), w.dtype) + 40 * one
+        # 40 bf16 roundings of the running y: allow 40x the per-step bound
+        assert np.all(np.abs(got - ref) <= 40 * TOL_NORTH_STAR * (1 + np.abs(ref)))
+        for seed in (8, 9):
+            w2 = synth.make(2, seed)
+            run.set_and_build(w2.tok_c, w2.tok_u)
+            _plan_matches(run)
+            _check(run)
+    finally:
+        run.close()
+
+
+def test_api_errors_change_no_state():
+    from paper_2608_03579_amd import salt
+    _announce("api error paths")
+    w = synth.make(2, 1)
+    run = Run(w)
+    try:
+        ctx, plan = run.ctx, run.plan
+        T = w.T
+        st = plan.set_maps_status
+        assert st(np.full(T, 4, np.int32), w.tok_u) == salt.ERR_OUT_OF_RANGE           # c >= C
+        assert st(w.tok_c, np.full(T, 64, np.int32)) == salt.ERR_OUT_OF_RANGE          # u >= n_slots
+        assert st(np.full(T, -2, np.int32), w.tok_u) == salt.ERR_OUT_OF_RANGE
+        assert st(np.zeros(T + 1, np.int32), np.zeros(T + 1, np.int32)) == salt.ERR_OUT_OF_RANGE   # > max_tokens
+        g = np.ones(T, np.float32)
+        g[3] = np.nan
+        assert st(w.tok_c, w.tok_u, g) == salt.ERR_INVALID_ARG
+        # residual loads: range, size, pageable memory
+        nb = ctx.residual_bytes(2)
+        blob = np.zeros(nb, np.uint8)
+        assert ctx.load_residual_ptr(64, 2, blob.ctypes.data, nb) == salt.ERR_OUT_OF_RANGE
+        assert ctx.load_residual_ptr(0, 3, blob.ctypes.data, nb) == salt.ERR_OUT_OF_RANGE
+        assert ctx.load_residual_ptr(0, 2, blob.ctypes.data, nb - 2) == salt.ERR_INVALID_ARG
+        assert ctx.load_residual_ptr(0, 2, blob.ctypes.data, nb) == salt.ERR_NOT_PINNED
+        # the calls above changed nothing: the real batch still applies correctly
+        run.set_and_build()
+        _check(run)
+        # apply: table out of range
+        from tests.gpu_harness import to_dev
+        xd, yd = to_dev(w.x(0)), to_dev(w.y0(0))
+        assert ctx.apply_status(1, plan, xd.ptr, yd.ptr, run.stream) == salt.ERR_OUT_OF_RANGE
+        # a slot of the plan reloaded with another rank: the plan is stale
+        s0 = int(w.tok_u[0])
+        ctx.load_residual(s0, 1, np.zeros(ctx.residual_bytes(1) // 2, np.uint16))
+        ctx.wait_loads()
+        assert ctx.apply_status(0, plan, xd.ptr, yd.ptr, run.stream) == salt.ERR_BAD_STATE
+        # never-loaded slot
+        fresh = salt.Context(w.dtype, [(3072, 3072)], 4, 32, 8, 2, 16)
+        p2 = fresh.plan()
+        assert p2.set_maps_status(np.zeros(2, np.int32), np.array([0, 1], np.int32)) == salt.ERR_SLOT_EMPTY
+        # centroids of the table never pinned
+        fresh.load_residual(0, 2, np.zeros(fresh.residual_bytes(2) // 2, np.uint16))
+        fresh.wait_loads()
+        p2.set_maps(np.zeros(2, np.int32), np.zeros(2, np.int32))
+        p2.build()
+        assert fresh.apply_status(0, p2, xd.ptr, yd.ptr, 0) == salt.ERR_BAD_STATE
+        p2.close()
+        fresh.close()
+    finally:
+        run.close()
+
+
+def test_swap_is_ordered_after_inflight_apply():
+    """Reloading a slot right after an apply is enqueued must not change what
+    that apply reads; the next apply sees the new residual."""
+    _announce("swap ordering against an in-flight apply")
+    w = synth.make(4, 3)
+    run = Run(w)
+    try:
+        run.set_and_build()
+        from tests.gpu_harness import to_dev
+        t = 4                                            # gate_proj 4096 -> 14336
+        xd, y1 = to_dev(w.x(t)), to_dev(w.y0(t))
+        run.ctx.apply(t, run.plan, xd.ptr, y1.ptr, run.stream)
+        swapped = [int(s) for s in w.meta["swap_slots"]]
+        for s in swapped:
+            run.load(s, 1)                               # enqueued behind the apply's reads
+        y2 = to_dev(w.y0(t))
+        run.ctx.apply(t, run.plan, xd.ptr, y2.ptr, run.stream)
+        run._stream.synchronize()
+        run.ctx.wait_loads()
+        got1 = oracle.decode(y1.to_host(), w.dtype)
+        got2 = oracle.decode(y2.to_host(), w.dtype)
+        ref2 = run.oracle_table(t)                       # gen 1 for the swapped slots
+        for s in swapped:
+            run.gen[s] = 0
+        ref1 = run.oracle_table(t)
+        assert close_enough(got1, ref1, TOL_NORTH_STAR)[0]
+        assert close_enough(got2, ref2, TOL_NORTH_STAR)[0]
+        assert not close_enough(got1, ref2, TOL_NORTH_STAR)[0]
+    finally:
+        run.close()
+
+
+def test_prefill_full_size_sampled():
+    """28-layer Llama-3.2-3B prefill at full size (196 tables, T = 8192), the
+    shapes and launch configuration bench.py times; sampled tables and rows."""
+    _announce("cfg3 full size: 196 tables, T=8192, sampled tables/rows")
+    w = synth.make(3, 0)
+    run = Run(w)
+    try:
+        run.set_and_build()
+        _plan_matches(run)
+        rng = np.random.default_rng(3)
+        seg = np.cumsum(w.meta["seg_lens"])
+        rows = sorted(set(rng.choice(w.T, 96, replace=False).tolist()) | {0, w.T - 1} |
+                      set((seg[:20] - 1).tolist()))
+        for t in (0, 1, 4, 6, 97, 195):
+            _check(run, t, rows=rows)
+    finally:
+        run.close()
