@@ -279,6 +279,32 @@ def run_gpu(w, dw, args, hip, salt):
     }
 
 
+# committed rocprofv3 counter summaries: HBM traffic per apply launch, valid
+# only for the kernel source they were taken on
+TRAFFIC_PROFILES = {
+    "qproj": "profiles/k_apply_llama32-3b_qproj_decode_T64_hbm_traffic.md",
+}
+
+
+def measured_traffic(workload):
+    """Bytes per launch from the committed counter summary of this workload, or
+    None when there is none or the kernel source changed since it was taken."""
+    import hashlib
+    rel = TRAFFIC_PROFILES.get(workload)
+    if rel is None or not os.path.exists(os.path.join(ROOT, rel)):
+        return None
+    fields = {}
+    for line in open(os.path.join(ROOT, rel)):
+        if ":" in line:
+            k, v = line.split(":", 1)
+            fields[k.strip()] = v.strip()
+    src = os.path.join(ROOT, "paper_2608_03579_amd", "csrc", "salt_kernels.hip")
+    h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
+    if fields.get("kernel_source_sha256_16") != h or "traffic_bytes_per_launch" not in fields:
+        return None
+    return int(fields["traffic_bytes_per_launch"])
+
+
 WORKLOADS = {
     "qproj": dict(cfg=2, rot=128, steps=2000, warmup=200),
     "prefill": dict(cfg=3, rot=1, steps=10, warmup=2),
@@ -324,6 +350,7 @@ def main():
         sys.exit(1)
     hip.set_device(0)
     res = run_gpu(w, dw, args, hip, salt)
+    res["roofline"]["traffic"] = measured_traffic(args.workload)
 
     cpu = None
     if not args.no_cpu:
