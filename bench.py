@@ -113,16 +113,26 @@ def cpu_baseline(w, budget_s=12.0):
                       f"host has {os.cpu_count()} logical cpus"}
 
 
+def tables_summary(w):
+    names = [f"{n} {i}->{o}" for n, i, o in w.tables]
+    layers = sorted({n.split(".")[0] for n, _, _ in w.tables}) if "." in w.tables[0][0] else []
+    if len(layers) > 1:
+        per = len(names) // len(layers)
+        return [f"{len(layers)} layers x " + ", ".join(x.split(".", 1)[1] for x in names[:per])]
+    return names
+
+
 # ---------------------------------------------------------------------------
 # GPU bench
 # ---------------------------------------------------------------------------
-def build_replicated(w, dw, rot, hip, salt):
+def build_replicated(w, dw, rot, hip, salt, deterministic=False):
     """A context whose tables are ``rot`` copies of the workload's tables, with
     every centroid pinned and every referenced residual loaded.  Adapter values
     come from ``dw``, whose tables repeat to give ``w``'s (the same workload with
     fewer layers for the 28-layer prefill; ``w`` itself otherwise)."""
     shapes = [(i, o) for _, i, o in w.tables] * rot
-    ctx = salt.Context(w.dtype, shapes, w.n_centroids, w.r_c, w.n_slots, w.r_u_max, max(1, w.T))
+    ctx = salt.Context(w.dtype, shapes, w.n_centroids, w.r_c, w.n_slots, w.r_u_max, max(1, w.T),
+                       deterministic=deterministic)
     n_tab, n_dat = len(w.tables), len(dw.tables)
     reps = (n_tab // n_dat) * rot
     if w.n_centroids:
@@ -175,7 +185,7 @@ def run_gpu(w, dw, args, hip, salt):
     rot = args.rot
     n_tab, n_dat = len(w.tables), len(dw.tables)
     log(f"workload: {w.name}; T={w.T}, tables={n_tab}, rotation={rot}")
-    ctx = build_replicated(w, dw, rot, hip, salt)
+    ctx = build_replicated(w, dw, rot, hip, salt, deterministic=args.deterministic)
     stream = hip.Stream()
     # x and y per table copy (rotation keeps the working set above the MALL);
     # values repeat with the data tables, memory does not
@@ -325,6 +335,8 @@ def main():
     ap.add_argument("--rot", type=int, default=None)
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-swap", dest="swap", action="store_false")
+    ap.add_argument("--deterministic", action="store_true",
+                    help="fixed-order split-K sums (SALT_DETERMINISTIC) instead of fp32 atomics")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only: the apply has no cross-GPU path in this build "
@@ -371,10 +383,11 @@ def main():
         "dtype": "bf16",
         "data": "synthetic",
         "config": {"workload": w.name, "T": w.T,
-                   "tables": [f"{n} {i}->{o}" for n, i, o in w.tables],
+                   "tables": tables_summary(w),
                    "centroids": f"{w.n_centroids} x r{w.r_c}",
                    "residual_slots": f"{w.n_slots} x r<={w.r_u_max}",
                    "accumulation": "fp32", "rotation": args.rot,
+                   "split_k_sum": "ordered" if args.deterministic else "fp32 atomics",
                    "step": "salt_plan_build + salt_apply per table, maps staged in HBM beforehand"},
         "achieved_GBps_step": res["step_GBps"],
         "apply_us": res["apply_us"],

@@ -75,7 +75,16 @@ typedef struct {
   int32_t r_u_max;           /* largest residual rank a slot holds, in [0, 16]     */
   int32_t max_tokens;        /* largest batch a plan accepts, in [1, 1 << 20]      */
   int32_t device;            /* HIP device ordinal                                  */
+  int32_t flags;             /* 0 or SALT_DETERMINISTIC                             */
 } salt_config;
+
+/* salt_config.flags.  By default an apply that splits the shrink contraction
+ * over several blocks sums their fp32 partial results with device atomics, in
+ * arrival order: y is correct to fp32 rounding, but two runs may differ in its
+ * last bits.  SALT_DETERMINISTIC sums the partials in a fixed order instead, so
+ * equal inputs give bit-identical y, at the cost of one more round trip through
+ * memory per apply. */
+#define SALT_DETERMINISTIC 1
 
 typedef struct salt_ctx salt_ctx;
 typedef struct salt_plan salt_plan;

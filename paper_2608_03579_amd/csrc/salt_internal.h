@@ -26,8 +26,11 @@ struct PlanBuffers {
   int32_t* grp_c;     // [max_T] centroid id of each group
   int4* tiles;        // [tile_cap]: per tile (i0, n, c, 0) then M token records
   uint32_t* arrive;   // [max tiles * kCounterStride] shrink blocks done with each tile since the build
-  uint32_t* ready;    // [max tiles * kCounterStride] epoch of the last apply whose v of the tile is complete
-  float* v;           // [max_T][R] v = x [A_c | A_u], gamma applied (R padded to 4)
+  uint32_t* ready;    // [max tiles * kReadyPerTile] epoch of the last apply whose v of the tile is
+                      // complete: word 0 (ordered sums), or word s * kReadyStride per K range s
+                      // (atomic sums)
+  float* v;           // [2][max_T][R] v = x [A_c | A_u] (R padded to 4); two buffers
+  size_t v_stride;    // floats between the two v buffers
   int32_t* meta;      // [kMetaWords]
   uint32_t* counter;  // [64] arrival counter of the multi-block plan build
   float* partials;    // [partial_cap] split-K partial sums of the shrink
@@ -38,8 +41,10 @@ struct PlanBuffers {
 
 struct PlanArgs {
   PlanBuffers b;
+  float* v_zero;      // [T][R] v buffer to clear, or null
   int32_t T;
   int32_t M;          // tokens per tile (16, 32 or 64)
+  int32_t R;          // row stride of v
 };
 
 // Everything one apply launch needs, passed by value.
@@ -52,8 +57,9 @@ struct ApplyArgs {
   size_t slot_stride;       // bytes between slots
   int64_t tab_prefix;       // sum of (in + out) over earlier tables (elements per rank)
   const int4* tiles;
-  float* partials;          // [S][T][R]
-  float* v;                 // [T][R]
+  float* partials;          // [S][T][R] (ordered sums only)
+  float* v;                 // [T][R] v of this apply, centroid part not yet scaled by gamma
+  float* v_clear;           // [T][R] v buffer of the next apply, cleared here (atomic sums only)
   uint32_t* arrive;
   uint32_t* ready;
   int32_t* meta;
@@ -63,6 +69,7 @@ struct ApplyArgs {
   int32_t n_tiles, S, Kc;
   int32_t n_col;            // expand blocks per tile
   int32_t cpb;              // kNC-column chunks per expand block
+  int32_t atomic_sum;       // 1: split partials are added into v with device atomics
 };
 
 hipError_t kernels_init(int device);
@@ -81,6 +88,10 @@ constexpr int padded_rank(int r_c, int r_u_max) {
 constexpr int kCounterStride = 64;
 // Largest K split of one apply.
 constexpr int kMaxSplit = 32;
+// Ready words: kMaxSplit per tile, 64 bytes apart, so that the S blocks of a
+// tile that raise them concurrently never write the same 64-byte sector.
+constexpr int kReadyStride = 16;
+constexpr int kReadyPerTile = kMaxSplit * kReadyStride;
 
 // 32-wide K steps whose loads a shrink wave issues together: about 96 VGPRs of
 // operands (x, nbm A_c rows, ru A_u rows per step, vec_regs registers each).

@@ -14,13 +14,16 @@
 // lane shuffles for the reductions.
 //
 // One launch per apply holds two kinds of blocks.  Shrink blocks (the first
-// n_tiles * S block ids) each reduce one tile over one K range into split-K
-// partials and count their arrival on the tile; the last of a tile's S blocks
-// to arrive sums the partials in split order, scales the centroid part by
-// gamma, stores v and raises the tile's ready word to this apply's epoch.
-// Expand blocks (the rest) prefetch their y, B_c and B_u slices, wait for the
-// ready word, read v and update y.  Arrival counts and epochs only grow between
-// plan builds; the host passes the values this apply reaches.
+// n_tiles * S block ids) each reduce one tile over one K range into a split-K
+// partial of v.  By default they add it into v with fp32 device atomics and
+// raise their own ready word of the tile to this apply's epoch; the expand
+// waits for all S words (one word per writer: no contended counter).  In the
+// deterministic mode they store the partial instead, and the last of a tile's
+// S blocks to arrive sums the partials in split order, stores v and raises the
+// tile's ready word to this apply's epoch.  Expand blocks (the rest) prefetch
+// their y, B_c and B_u slices, wait, read v, scale its centroid part by gamma
+// and update y.  Arrival counts and epochs only grow between plan builds; the
+// host passes the values this apply reaches.
 // Blocks are dispatched in id order, so every shrink block has started before
 // any expand block waits on it, and shrink blocks never wait: the wait always
 // ends.  It is still bounded; a block that gives up records an error in the
@@ -148,6 +151,30 @@ struct Ops<float> {
     return c;
   }
 };
+
+// Hand-off of split-K partials between blocks, with no cache-wide fences.
+// Partials and v are written and read with device-coherent 16-byte buffer
+// accesses (cache policy sc1: stores write through to the device-coherent
+// level, loads never return a stale cached copy) or added with device-scope
+// atomics, which are performed at that level.  A shrink block waits until its
+// stores or atomics have completed (s_waitcnt), meets its other waves, and only
+// then bumps the tile's arrival count; a block that consumes the data issues
+// its loads only after it has seen the count.  Completed device-coherent writes
+// are visible to every later device-coherent load, so the counter orders the
+// data without writing back or invalidating the L2.
+constexpr int kCoherent = 16;                 // buffer cache policy: sc1 (device scope)
+constexpr int kRawBufferWord3 = 0x00020000;   // gfx9 raw buffer resource, dword 3
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kRawBufferWord3);
+}
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ float4 load4_coherent(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
+  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, kCoherent));
+}
+__device__ __forceinline__ void store4_coherent(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, float4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)byte_off, 0, kCoherent);
+}
 
 // ---------------------------------------------------------------------------
 // plan
@@ -287,9 +314,10 @@ __device__ void plan_finish(const PlanArgs& a, const int4* srt, const int32_t* s
       else rec = make_int4(0, -1, 0, 0);
       b.tiles[e] = rec;
     }
-    for (int t = tid; t < n_tiles; t += nt) {
-      b.arrive[(size_t)t * kCounterStride] = 0u;
-      b.ready[(size_t)t * kCounterStride] = 0u;
+    for (int e = tid; e < n_tiles * kMaxSplit; e += nt) {
+      const size_t t = (size_t)(e / kMaxSplit), j = (size_t)(e % kMaxSplit);
+      if (j == 0) b.arrive[t * kCounterStride] = 0u;
+      b.ready[t * kReadyPerTile + j * kReadyStride] = 0u;
     }
   }
   if (tid == 0) {
@@ -299,6 +327,16 @@ __device__ void plan_finish(const PlanArgs& a, const int4* srt, const int32_t* s
     b.meta[kMetaNTiles] = fits ? n_tiles : -1;
     b.meta[kMetaErr] = 0;
   }
+}
+
+// Zeroes v_zero[0 : T][0 : R] (atomic split-K sums start from it), float4 `i`
+// for i = first, first + step, ...  Device-coherent stores, like every other
+// access to v.
+__device__ __forceinline__ void clear_v(const PlanArgs& a, int first, int step) {
+  if (!a.v_zero) return;
+  const int n4 = a.T * a.R / 4;
+  const __amdgpu_buffer_rsrc_t r = coherent_rsrc(a.v_zero, (uint32_t)n4 * 16u);
+  for (int i = first; i < n4; i += step) store4_coherent(r, 16u * (uint32_t)i, make_float4(0.f, 0.f, 0.f, 0.f));
 }
 
 // Batches of up to kPlanSmallT tokens: one block, everything in LDS.  The
@@ -336,6 +374,7 @@ __global__ void __launch_bounds__(kPlanSmallT) k_plan_small(PlanArgs a) {
   }
   __syncthreads();
   plan_finish(a, s_srt, s_c, sh);
+  clear_v(a, tid, blockDim.x);
 }
 
 // Larger batches: rank by counting smaller keys across blocks; the last block to
@@ -346,6 +385,7 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_large(PlanArgs a) {
   __shared__ int s_last;
   const PlanBuffers& b = a.b;
   const int T = a.T, tid = threadIdx.x;
+  clear_v(a, blockIdx.x * kPlanThreads + tid, gridDim.x * kPlanThreads);
   const int t = blockIdx.x * kPlanTokPerBlock + (tid >> 2);
   const int q = tid & 3;
   int4 mine = make_int4(0, 0, 0, 0);
@@ -401,28 +441,6 @@ __device__ __forceinline__ void pin_regs(const V& v) {
   for (int i = 0; i < (int)(sizeof(V) / 4); ++i) asm volatile("" ::"v"(w[i]));
 }
 
-// Hand-off of split-K partials between blocks, with no cache-wide fences.
-// Partials and v are written and read with device-coherent 16-byte buffer
-// accesses (cache policy sc1: stores write through to the device-coherent
-// level, loads never return a stale cached copy).  A shrink block waits until its partial
-// stores have completed (s_waitcnt), meets its other waves, and only then bumps
-// the tile's arrival count; an expand block issues its partial loads only after
-// it has seen the count.  Completed device-coherent stores are visible to every
-// later device-coherent load, so the counter orders the data without writing
-// back or invalidating the L2.
-constexpr int kCoherent = 16;                 // buffer cache policy: sc1 (device scope)
-constexpr int kRawBufferWord3 = 0x00020000;   // gfx9 raw buffer resource, dword 3
-
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t coherent_rsrc(const void* base, uint32_t bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, kRawBufferWord3);
-}
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-__device__ __forceinline__ float4 load4_coherent(__amdgpu_buffer_rsrc_t r, uint32_t byte_off) {
-  return __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(r, (int)byte_off, 0, kCoherent));
-}
-__device__ __forceinline__ void store4_coherent(__amdgpu_buffer_rsrc_t r, uint32_t byte_off, float4 v) {
-  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, v), r, (int)byte_off, 0, kCoherent);
-}
 
 // All waves' coherent stores have completed, then one thread adds 1 to
 // `counter`; returns (to every thread) the count after the addition.
@@ -435,36 +453,42 @@ __device__ __forceinline__ uint32_t publish_add(uint32_t* counter, uint32_t* s_w
   return *s_word;
 }
 
-// All waves' coherent stores have completed, then one thread stores `value`.
+// All waves' coherent stores and atomics have completed, then one thread stores `value`.
 __device__ __forceinline__ void publish_store(uint32_t* word, uint32_t value) {
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   if (threadIdx.x == 0) __hip_atomic_store(word, value, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Wait until `word` reaches `target` (wrap-safe), polling with coherent loads.
-// Returns false (and counts an error) if it gives up.
-__device__ __forceinline__ bool await_word(const uint32_t* word, uint32_t target, int32_t* err, int* s_flag) {
-  if (threadIdx.x == 0) {
+// Wait until words[k * kReadyStride], k < n, all reach `target` (wrap-safe,
+// n <= 64): wave 0 polls them with one coherent load per lane.  Returns false
+// (and counts an error) if it gives up.
+__device__ __forceinline__ bool await_words(const uint32_t* words, int n, uint32_t target, int32_t* err,
+                                            int* s_flag) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x;
     uint32_t spins = 0;
     int ok = 1;
-    while ((int32_t)(__hip_atomic_load(const_cast<uint32_t*>(word), __ATOMIC_RELAXED,
-                                       __HIP_MEMORY_SCOPE_AGENT) - target) < 0) {
+    while (true) {
+      const uint32_t w = lane < n ? __hip_atomic_load(const_cast<uint32_t*>(words + lane * kReadyStride), __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT)
+                                  : target;
+      if (__all((int32_t)(w - target) >= 0)) break;
       __builtin_amdgcn_s_sleep(2);
       if (++spins > kSpinMax) {
-        atomicAdd(err, 1);
+        if (lane == 0) atomicAdd(err, 1);
         ok = 0;
         break;
       }
     }
-    *s_flag = ok;
+    if (lane == 0) *s_flag = ok;
   }
   __syncthreads();
   return *s_flag != 0;
 }
 
 // v entries idx .. idx+3 of a tile (row-major [token][R]): the centroid ranks
-// j < r_c are scaled by the token's gamma.
+// j < r_c are scaled by the token's gamma (Sec. 3.3).
 __device__ __forceinline__ float4 scale_centroid(float4 v, int idx, int R, int rc, const int4* s_tile) {
   const int t = idx / R, j = idx - t * R;      // the 4 entries share a row (R % 4 == 0)
   const float g = __int_as_float(s_tile[1 + t].w);
@@ -475,8 +499,10 @@ __device__ __forceinline__ float4 scale_centroid(float4 v, int idx, int R, int r
   return v;
 }
 
-// Shrink block: tile `tau`, K range `s` of the apply.  Writes the tile's
-// split-K partial sums P[s][token][0 : r_c + r_u_max] and counts its arrival.
+// Shrink block: tile `tau`, K range `s` of the apply.  Computes the tile's
+// split-K partial sums P[s][token][0 : r_c + r_u_max]; adds them into v with
+// atomics (default) or stores them for an ordered sum (deterministic mode), and
+// counts its arrival.  With one K range it stores v directly.
 template <typename E, int MB, int RU, int NBM>
 __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s, char* lds) {
   using O = Ops<E>;
@@ -584,6 +610,11 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
   // R is a multiple of 4: rows are whole float4 vectors
   const int nR4 = n * R / 4;
   const __amdgpu_buffer_rsrc_t rv = coherent_rsrc(a.v + (size_t)i0 * R, (uint32_t)(nR4 * 16));
+  if (a.atomic_sum && s == 0) {
+    // the next apply of the plan adds into the other v buffer: clear this tile's rows
+    const __amdgpu_buffer_rsrc_t rz = coherent_rsrc(a.v_clear + (size_t)i0 * R, (uint32_t)(nR4 * 16));
+    for (int i4 = tid; i4 < nR4; i4 += 256) store4_coherent(rz, 16u * i4, make_float4(0.f, 0.f, 0.f, 0.f));
+  }
   if (a.S == 1) {
     // one K range: this block writes v itself
     for (int i4 = tid; i4 < nR4; i4 += 256) {
@@ -593,7 +624,16 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
         const float4 p = *reinterpret_cast<const float4*>(s_part + (size_t)q * M * R + 4 * i4);
         v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
       }
-      store4_coherent(rv, 16u * i4, scale_centroid(v, 4 * i4, R, rc, s_tile));
+      store4_coherent(rv, 16u * i4, v);
+    }
+  } else if (a.atomic_sum) {
+    // add this K range's partial into v (cleared by the previous apply or the build)
+    float* vt = a.v + (size_t)i0 * R;
+    for (int i = tid; i < n * R; i += 256) {
+      float p = 0.f;
+#pragma unroll
+      for (int q = 0; q < KW; ++q) p += s_part[(size_t)q * M * R + i];
+      __hip_atomic_fetch_add(vt + i, p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
   } else {
     const __amdgpu_buffer_rsrc_t rp =
@@ -609,7 +649,7 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
     }
     __shared__ uint32_t s_count;
     if (publish_add(a.arrive + (size_t)tau * kCounterStride, &s_count) != a.target) return;
-    // the last of the tile's S blocks: sum the splits in order, scale by gamma
+    // the last of the tile's S blocks: sum the splits in order
     const size_t split_bytes = (size_t)a.T * R * 4;
     const __amdgpu_buffer_rsrc_t rall = coherent_rsrc(a.partials + (size_t)i0 * R,
                                                       (uint32_t)((a.S - 1) * split_bytes + nR4 * 16));
@@ -639,11 +679,12 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
 #pragma unroll
       for (int q = 0; q < Q; ++q) {
         const int i4 = base + tid + 256 * q;
-        if (i4 < nR4) store4_coherent(rv, 16u * i4, scale_centroid(v[q], 4 * i4, R, rc, s_tile));
+        if (i4 < nR4) store4_coherent(rv, 16u * i4, v[q]);
       }
     }
   }
-  publish_store(a.ready + (size_t)tau * kCounterStride, a.epoch);
+  // atomic sums: this block's own ready word; ordered sums: the tile's one word
+  publish_store(a.ready + (size_t)tau * kReadyPerTile + (a.atomic_sum ? s * kReadyStride : 0), a.epoch);
 }
 
 // Operands of one expand chunk (kNC columns of y for the tile's tokens) that a
@@ -734,13 +775,15 @@ __device__ __forceinline__ void expand_block(const ApplyArgs& a, int tau, int q,
   regs.load(a, s_tile, n, has_c, c, chunk0 * kNC);
   regs.pin();
 
-  // ---- wait for the tile's v ----
-  if (!await_word(a.ready + (size_t)tau * kCounterStride, a.epoch, a.meta + kMetaErr, &s_flag)) return;
+  // ---- wait for the tile's v: the S ready words (atomic sums) or the one word ----
+  const bool ok = await_words(a.ready + (size_t)tau * kReadyPerTile, a.atomic_sum ? a.S : 1, a.epoch,
+                              a.meta + kMetaErr, &s_flag);
+  if (!ok) return;
   {
     const int nR4 = n * R / 4, MR4 = M * R / 4;
     const __amdgpu_buffer_rsrc_t rv = coherent_rsrc(a.v + (size_t)i0 * R, (uint32_t)(nR4 * 16));
-    for (int i4 = tid; i4 < MR4; i4 += 256)
-      reinterpret_cast<float4*>(s_v)[i4] = load4_coherent(rv, 16u * i4);   // past n rows: zeros
+    for (int i4 = tid; i4 < MR4; i4 += 256)   // past n rows: zeros
+      reinterpret_cast<float4*>(s_v)[i4] = scale_centroid(load4_coherent(rv, 16u * i4), 4 * i4, R, rc, s_tile);
   }
   __syncthreads();
   if constexpr (sizeof(E) == 2) {

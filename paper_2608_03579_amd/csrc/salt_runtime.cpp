@@ -125,6 +125,10 @@ void transpose_rank_major(const W* src, W* dst, size_t n, size_t rc, size_t out)
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// Split-K partial sums go through device atomics unless the context asked for
+// bit-reproducible results.
+bool atomic_sums(const salt_ctx* c) { return (c->cfg.flags & SALT_DETERMINISTIC) == 0; }
+
 hipError_t ring_record(EventRing& r, hipStream_t s, int64_t* seq_out) {
   const int64_t seq = r.next;
   const int k = (int)(seq % (int64_t)r.ev.size());
@@ -233,6 +237,7 @@ salt_status salt_create(const salt_config* cfg, salt_ctx** out) {
   if (cfg->n_slots < 1 || cfg->n_slots > (1 << 20) || cfg->r_u_max < 0 || cfg->r_u_max > salt::kMaxRu)
     return SALT_ERR_OUT_OF_RANGE;
   if (cfg->max_tokens < 1 || cfg->max_tokens > (1 << 20)) return SALT_ERR_OUT_OF_RANGE;
+  if (cfg->flags & ~SALT_DETERMINISTIC) return SALT_ERR_INVALID_ARG;
   for (int i = 0; i < cfg->n_tables; ++i) {
     const salt_shape s = cfg->tables[i];
     if (s.in_dim <= 0 || s.out_dim <= 0 || s.in_dim % 8 || s.out_dim % 8 || s.in_dim > (1 << 20) ||
@@ -397,6 +402,7 @@ salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out) {
   PlanBuffers& b = p->dev;
   // split-K partials for up to max(8 T, 64K) (split, token) pairs
   b.partial_cap = std::max<size_t>(8 * T, 65536) * R;
+  b.v_stride = T * R;
   // tiles: at most ceil(T / M) + one partial tile per centroid group (<= 65)
   b.tiles_max = (int32_t)((T + 15) / 16 + 66);
   b.tile_cap = 0;
@@ -413,8 +419,8 @@ salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out) {
             hipMalloc((void**)&b.grp_c, T * 4) == hipSuccess &&
             hipMalloc((void**)&b.tiles, b.tile_cap * sizeof(int4)) == hipSuccess &&
             hipMalloc((void**)&b.arrive, (size_t)b.tiles_max * salt::kCounterStride * 4) == hipSuccess &&
-            hipMalloc((void**)&b.ready, (size_t)b.tiles_max * salt::kCounterStride * 4) == hipSuccess &&
-            hipMalloc((void**)&b.v, T * R * 4) == hipSuccess &&
+            hipMalloc((void**)&b.ready, (size_t)b.tiles_max * salt::kReadyPerTile * 4) == hipSuccess &&
+            hipMalloc((void**)&b.v, 2 * T * R * 4) == hipSuccess &&
             hipMalloc((void**)&b.meta, salt::kMetaWords * 4) == hipSuccess &&
             hipMalloc((void**)&b.counter, 64 * 4) == hipSuccess &&
             hipMalloc((void**)&b.partials, b.partial_cap * 4) == hipSuccess &&
@@ -429,7 +435,7 @@ salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out) {
   if (e == hipSuccess) e = hipMemset(b.counter, 0, 64 * 4);
   if (e == hipSuccess) e = hipMemset(b.meta, 0, salt::kMetaWords * 4);
   if (e == hipSuccess) e = hipMemset(b.arrive, 0, (size_t)b.tiles_max * salt::kCounterStride * 4);
-  if (e == hipSuccess) e = hipMemset(b.ready, 0, (size_t)b.tiles_max * salt::kCounterStride * 4);
+  if (e == hipSuccess) e = hipMemset(b.ready, 0, (size_t)b.tiles_max * salt::kReadyPerTile * 4);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     free_plan_buffers(p);
@@ -529,6 +535,10 @@ salt_status salt_plan_build(salt_ctx* ctx, salt_plan* plan, void* stream) {
   pa.b = plan->dev;
   pa.T = plan->T;
   pa.M = plan->M;
+  // atomic split-K sums: the first apply after the build accumulates into v
+  // buffer 1 (its epoch is 1), which therefore starts at zero
+  pa.v_zero = atomic_sums(ctx) ? plan->dev.v + plan->dev.v_stride : nullptr;
+  pa.R = salt::padded_rank(ctx->cfg.r_c, ctx->cfg.r_u_max);
   SALT_HIP(ctx, salt::launch_plan(pa, (hipStream_t)stream));
   plan->built = true;
   plan->arrivals = 0;
@@ -623,7 +633,6 @@ salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
   a.partials = plan->dev.partials;
   a.arrive = plan->dev.arrive;
   a.ready = plan->dev.ready;
-  a.v = plan->dev.v;
   a.meta = plan->dev.meta;
   a.T = T;
   a.in_dim = sh.in_dim;
@@ -645,7 +654,8 @@ salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
   const int s_traffic = std::max(1, (int)((small ? 0.5 : 0.2) * shrink_bytes / ((double)T * a.R * 8.0)));
   const int gran = 32 * KW;
   // the last block of a tile sums S x M x R partials: keep that within ~64 KiB
-  const int s_reduce = std::max(1, (int)(65536 / ((size_t)M * a.R * 4)));
+  const bool atomic = atomic_sums(ctx);
+  const int s_reduce = atomic ? salt::kMaxSplit : std::max(1, (int)(65536 / ((size_t)M * a.R * 4)));
   int S = std::max(1, std::min({s_bytes, s_traffic, s_reduce, salt::kMaxSplit, (sh.in_dim + gran - 1) / gran}));
   while (S > 1 && (size_t)S * T * a.R > plan->dev.partial_cap) --S;
   const int Kc = ((sh.in_dim + S - 1) / S + gran - 1) / gran * gran;
@@ -656,9 +666,19 @@ salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
   const int chunks = (sh.out_dim + salt::kNC - 1) / salt::kNC;
   a.cpb = std::max(1, std::min(4, (a.n_tiles * chunks) / 1024));
   a.n_col = (chunks + a.cpb - 1) / a.cpb;
-  if (a.S > 1) plan->arrivals += (uint32_t)a.S;
+  if (!atomic && a.S > 1) plan->arrivals += (uint32_t)a.S;
   a.target = plan->arrivals;
   a.epoch = ++plan->epoch;
+  a.atomic_sum = atomic ? 1 : 0;
+  if (atomic) {
+    // v buffers alternate between applies: this apply sums into buffer
+    // (epoch & 1) and clears the other one for the next apply
+    a.v = plan->dev.v + (a.epoch & 1u) * plan->dev.v_stride;
+    a.v_clear = plan->dev.v + ((a.epoch + 1u) & 1u) * plan->dev.v_stride;
+  } else {
+    a.v = plan->dev.v;
+    a.v_clear = nullptr;
+  }
   SALT_HIP(ctx, salt::launch_apply(a, ctx->cfg.dtype == SALT_BF16, M, s));
   int64_t seq;
   SALT_HIP(ctx, ring_record(ctx->readers, s, &seq));

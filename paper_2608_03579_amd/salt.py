@@ -38,7 +38,11 @@ class Shape(C.Structure):
 class Config(C.Structure):
     _fields_ = [("dtype", C.c_int), ("n_tables", C.c_int32), ("tables", C.POINTER(Shape)),
                 ("n_centroids", C.c_int32), ("r_c", C.c_int32), ("n_slots", C.c_int32),
-                ("r_u_max", C.c_int32), ("max_tokens", C.c_int32), ("device", C.c_int32)]
+                ("r_u_max", C.c_int32), ("max_tokens", C.c_int32), ("device", C.c_int32),
+                ("flags", C.c_int32)]
+
+
+DETERMINISTIC = 1   # salt_config.flags: split-K partials summed in a fixed order
 
 
 def _load() -> C.CDLL:
@@ -126,11 +130,12 @@ class Context:
     _N_STAGE = 8
 
     def __init__(self, dtype: str, tables: Sequence[Tuple[int, int]], n_centroids: int, r_c: int,
-                 n_slots: int, r_u_max: int, max_tokens: int, device: int = 0):
+                 n_slots: int, r_u_max: int, max_tokens: int, device: int = 0,
+                 deterministic: bool = False):
         self.dtype = dtype
         self._shapes = (Shape * len(tables))(*[Shape(int(i), int(o)) for i, o in tables])
         cfg = Config(F32 if dtype == "f32" else BF16, len(tables), self._shapes, n_centroids, r_c,
-                     n_slots, r_u_max, max_tokens, device)
+                     n_slots, r_u_max, max_tokens, device, DETERMINISTIC if deterministic else 0)
         h = C.c_void_p()
         st = lib.salt_create(C.byref(cfg), C.byref(h))
         if st != OK:

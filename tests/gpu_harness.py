@@ -38,14 +38,15 @@ def close_enough(got: np.ndarray, ref: np.ndarray, tol: float):
 class Run:
     """One context + one plan for workload ``w``; residual generations per slot."""
 
-    def __init__(self, w: synth.Workload, max_tokens: int = None, pin_tables=None):
+    def __init__(self, w: synth.Workload, max_tokens: int = None, pin_tables=None,
+                 deterministic: bool = False):
         from paper_2608_03579_amd import salt
         self.salt = salt
         self.w = w
         self.gen = {}
         tables = [(i, o) for _, i, o in w.tables]
         self.ctx = salt.Context(w.dtype, tables, w.n_centroids, w.r_c, w.n_slots, w.r_u_max,
-                                max_tokens or max(1, w.T))
+                                max_tokens or max(1, w.T), deterministic=deterministic)
         if w.n_centroids:
             for t in (range(len(tables)) if pin_tables is None else pin_tables):
                 at, b = w.centroids(t)

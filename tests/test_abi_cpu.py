@@ -55,6 +55,7 @@ def test_create_rejects_bad_configs_before_touching_the_gpu():
         dict(max_tokens=0),
         dict(n_slots=0),
     ]
+
     base = dict(dtype="bf16", tables=[(3072, 3072)], n_centroids=4, r_c=32, n_slots=8, r_u_max=2,
                 max_tokens=64)
     for b in bad:
@@ -65,3 +66,10 @@ def test_create_rejects_bad_configs_before_touching_the_gpu():
             assert e.status in (salt.ERR_INVALID_ARG, salt.ERR_OUT_OF_RANGE), e
         else:
             raise AssertionError(f"accepted {b}")
+
+
+def test_create_rejects_unknown_flags():
+    cfg = salt.Config(salt.BF16, 1, (salt.Shape * 1)(salt.Shape(3072, 3072)), 4, 32, 8, 2, 64, 0, 2)
+    h = salt.C.c_void_p()
+    assert salt.lib.salt_create(salt.C.byref(cfg), salt.C.byref(h)) == salt.ERR_INVALID_ARG
+    assert not h.value
