@@ -41,10 +41,9 @@ struct PlanBuffers {
 
 struct PlanArgs {
   PlanBuffers b;
-  float* v_zero;      // [T][R] v buffer to clear, or null
   int32_t T;
-  int32_t M;          // tokens per tile (16, 32 or 64)
-  int32_t R;          // row stride of v
+  int32_t M;            // tokens per tile (16, 32 or 64)
+  int32_t reset_ready;  // 1: zero every ready word (the plan's epochs restart)
 };
 
 // Everything one apply launch needs, passed by value.
@@ -59,7 +58,8 @@ struct ApplyArgs {
   const int4* tiles;
   float* partials;          // [S][T][R] (ordered sums only)
   float* v;                 // [T][R] v of this apply, centroid part not yet scaled by gamma
-  float* v_clear;           // [T][R] v buffer of the next apply, cleared here (atomic sums only)
+  float* v_clear;           // v buffer of the next apply: rows [0, clear_rows) cleared here (atomic sums only)
+  int32_t clear_rows;       // >= T
   uint32_t* arrive;
   uint32_t* ready;
   int32_t* meta;
@@ -70,6 +70,8 @@ struct ApplyArgs {
   int32_t n_col;            // expand blocks per tile
   int32_t cpb;              // kNC-column chunks per expand block
   int32_t atomic_sum;       // 1: split partials are added into v with device atomics
+  int32_t fused_plan;       // 1: this launch also builds the plan (T <= kPlanFusedT)
+  PlanBuffers pb;           // the plan's buffers (fused_plan only)
 };
 
 hipError_t kernels_init(int device);
@@ -78,6 +80,10 @@ hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s);
 
 // Columns of y per expand chunk.
 constexpr int kNC = 128;
+// Batches a single plan block sorts in LDS, and batches an apply launch plans
+// for itself.
+constexpr int kPlanSmallT = 1024;
+constexpr int kPlanFusedT = 256;
 
 // Row stride of the partials and of v: r_c + r_u_max rounded up to whole float4s.
 constexpr int padded_rank(int r_c, int r_u_max) {

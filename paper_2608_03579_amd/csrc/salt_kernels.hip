@@ -28,6 +28,8 @@
 // any expand block waits on it, and shrink blocks never wait: the wait always
 // ends.  It is still bounded; a block that gives up records an error in the
 // plan's meta words and leaves its slice of y untouched.
+#include <algorithm>
+
 #include "salt_internal.h"
 
 namespace salt {
@@ -179,10 +181,9 @@ __device__ __forceinline__ void store4_coherent(__amdgpu_buffer_rsrc_t r, uint32
 // ---------------------------------------------------------------------------
 // plan
 // ---------------------------------------------------------------------------
-constexpr int kPlanSmallT = 1024;     // one 1024-thread block sorts in LDS
-constexpr int kPlanThreads = 256;     // multi-block rank counting
-constexpr int kPlanTokPerBlock = 64;  // four lanes count the rank of one token
-constexpr int kPlanChunk = 2048;      // keys staged in LDS per pass
+constexpr int kPlanThreads = 256;     // threads of every plan block
+constexpr int kPlanTokPerBlock = 64;  // multi-block ranking: four lanes per token
+constexpr int kPlanChunk = 2048;      // keys staged in LDS per pass (multi-block ranking)
 constexpr int kMaxGroups = 72;        // centroid groups: C + 1 <= 65
 
 // Total order key (centroid, slot, token), -1 ids first: each field is shifted by
@@ -190,6 +191,33 @@ constexpr int kMaxGroups = 72;        // centroid groups: C + 1 <= 65
 __device__ __forceinline__ uint64_t plan_key(int c, int u, int t) {
   return (uint64_t(uint32_t(c + 1)) << 42) | (uint64_t(uint32_t(u + 1)) << 21) |
          uint64_t(uint32_t(t));
+}
+constexpr uint64_t kNoKey = ~0ull;    // pads a run; above every real key
+
+// The 64 keys of a wave (one per lane) sorted ascending across the lanes: a
+// bitonic network of compare-exchanges between lanes l and l ^ stride.
+__device__ __forceinline__ uint64_t wave_sort64(uint64_t k) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int size = 2; size <= 64; size <<= 1) {
+#pragma unroll
+    for (int stride = size >> 1; stride > 0; stride >>= 1) {
+      const uint64_t o = __shfl_xor(k, stride);
+      // blocks of `size` lanes alternate ascending / descending; the lower lane
+      // of an ascending pair keeps the minimum
+      const bool keep_min = ((lane & size) == 0) == ((lane & stride) == 0);
+      k = keep_min ? (o < k ? o : k) : (o < k ? k : o);
+    }
+  }
+  return k;
+}
+
+// Entries of the ascending run l[0:64] below k (branch-free binary search).
+__device__ __forceinline__ int count_below64(const uint64_t* l, uint64_t k) {
+  int lo = 0;
+#pragma unroll
+  for (int step = 32; step > 0; step >>= 1) lo += (l[lo + step - 1] < k) ? step : 0;
+  return lo + (l[lo] < k ? 1 : 0);
 }
 
 // Exclusive counts of two predicates over the threads of the block, and their
@@ -228,19 +256,68 @@ __device__ __forceinline__ void block_excl_count2(bool p0, bool p1, int* s_wave,
   __syncthreads();
 }
 
+// Group and tile bookkeeping of one plan, in LDS.
 struct PlanShared {
   int s_wave[72];
-  int g_start[kMaxGroups + 1];
-  int g_c[kMaxGroups];
-  int g_tile[kMaxGroups + 1];
+  int g_start[kMaxGroups + 1];   // first sorted position of each group, then T
+  int g_c[kMaxGroups];           // centroid of each group
+  int g_tile[kMaxGroups + 1];    // first tile of each group, then the tile count
   int n_seg, n_grp, n_tiles;
 };
 
-// Segments, groups and tiles from the sorted order.  Runs in one block;
-// srt / srt_c are read from LDS (small batches) or global memory.
-__device__ void plan_finish(const PlanArgs& a, const int4* srt, const int32_t* srt_c, PlanShared& sh) {
-  const PlanBuffers& b = a.b;
-  const int T = a.T, M = a.M, tid = threadIdx.x, nt = blockDim.x;
+// A batch sorted in LDS by one block: up to CAP tokens.
+template <int CAP>
+struct PlanLds {
+  static_assert(CAP % 64 == 0, "whole runs of 64 keys");
+  uint64_t key[CAP];     // ascending runs of 64 keys
+  int4 maps[CAP];        // staged maps (c, u, r, gamma bits) by token
+  int4 srt[CAP];         // (token, u, r, gamma bits) by sorted position
+  int32_t c[CAP];        // centroid id by sorted position
+  PlanShared sh;
+};
+
+// Sorts maps[0:T] (T <= CAP) by plan key into L.srt / L.c.  Each wave sorts
+// runs of 64 keys across its lanes; a key's rank is its place in its own run
+// plus the number of keys below it in every other run (binary searches).
+template <int CAP>
+__device__ __forceinline__ void plan_sort(const int4* maps, int T, PlanLds<CAP>& L) {
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nrun = (T + 63) >> 6;
+  for (int i = tid; i < T; i += kPlanThreads) L.maps[i] = maps[i];
+  __syncthreads();
+  for (int run = wave; run < nrun; run += kPlanThreads / 64) {
+    const int t = run * 64 + lane;
+    uint64_t k = kNoKey;
+    if (t < T) {
+      const int4 m = L.maps[t];
+      k = plan_key(m.x, m.y, t);
+    }
+    L.key[t] = wave_sort64(k);
+  }
+  __syncthreads();
+  for (int run = wave; run < nrun; run += kPlanThreads / 64) {
+    const uint64_t k = L.key[run * 64 + lane];
+    if (k != kNoKey) {
+      int rank = lane;
+      for (int o = 0; o < nrun; ++o)
+        if (o != run) rank += count_below64(L.key + o * 64, k);
+      const int t = (int)(k & 0x1fffffu);
+      const int4 m = L.maps[t];
+      L.srt[rank] = make_int4(t, m.y, m.z, m.w);
+      L.c[rank] = m.x;
+    }
+  }
+  __syncthreads();
+}
+
+// Segments (equal centroid and slot) and groups (equal centroid) of the sorted
+// batch srt / srt_c (LDS or global memory), and the tiles of M tokens that cut
+// each group.  Writes the segment and group arrays of `out` when `write` is set.
+// (Inlined everywhere: a plan buffer struct whose address escapes would be
+// copied to scratch memory.)
+__device__ __forceinline__ void plan_groups(bool write, const PlanBuffers& out, const int4* srt,
+                                            const int32_t* srt_c, int T, int M, PlanShared& sh) {
+  const int tid = threadIdx.x, nt = blockDim.x;
   int seg_base = 0, grp_base = 0;
   for (int base = 0; base < T; base += nt) {
     const int i = base + tid;
@@ -259,17 +336,19 @@ __device__ void plan_finish(const PlanArgs& a, const int4* srt, const int32_t* s
     }
     int seg_tot, grp_tot, sr, gr;
     block_excl_count2(ns, ng, sh.s_wave, sr, gr, seg_tot, grp_tot);
-    if (ns) {
-      const int s = seg_base + sr;
-      b.seg_off[s] = i;
-      b.seg_c[s] = c;
-      b.seg_u[s] = u;
+    if (ns && write) {
+      const int sg = seg_base + sr;
+      out.seg_off[sg] = i;
+      out.seg_c[sg] = c;
+      out.seg_u[sg] = u;
     }
     if (ng) {
       const int g = grp_base + gr;
-      b.grp_off[g] = seg_base + sr;
-      b.grp_tok[g] = i;
-      b.grp_c[g] = c;
+      if (write) {
+        out.grp_off[g] = seg_base + sr;
+        out.grp_tok[g] = i;
+        out.grp_c[g] = c;
+      }
       if (g < kMaxGroups) {
         sh.g_start[g] = i;
         sh.g_c[g] = c;
@@ -288,93 +367,78 @@ __device__ void plan_finish(const PlanArgs& a, const int4* srt, const int32_t* s
     }
     sh.g_tile[ng] = acc;
     sh.n_seg = seg_base;
-    sh.n_grp = ng;
-    sh.n_tiles = acc;
-    b.seg_off[seg_base] = T;
-    b.grp_off[grp_base] = seg_base;
-    b.grp_tok[grp_base] = T;
+    sh.n_grp = grp_base;
+    sh.n_tiles = grp_base < kMaxGroups ? acc : -1;
+    if (write) {
+      out.seg_off[seg_base] = T;
+      out.grp_off[grp_base] = seg_base;
+      out.grp_tok[grp_base] = T;
+    }
   }
   __syncthreads();
-  const int ng = sh.n_grp, n_tiles = sh.n_tiles;
-  const bool fits = (size_t)n_tiles * (M + 1) <= b.tile_cap && n_tiles <= b.tiles_max && grp_base < kMaxGroups;
-  if (fits) {
-    for (int e = tid; e < n_tiles * (M + 1); e += nt) {
-      const int tau = e / (M + 1), k = e % (M + 1);
-      int lo = 0, hi = ng - 1;  // last group whose first tile <= tau
-      while (lo < hi) {
-        const int mid = (lo + hi + 1) >> 1;
-        if (sh.g_tile[mid] <= tau) lo = mid;
-        else hi = mid - 1;
-      }
-      const int i0 = sh.g_start[lo] + (tau - sh.g_tile[lo]) * M;
-      const int n = min(M, sh.g_start[lo + 1] - i0);
-      int4 rec;
-      if (k == 0) rec = make_int4(i0, n, sh.g_c[lo], 0);
-      else if (k - 1 < n) rec = srt[i0 + k - 1];
-      else rec = make_int4(0, -1, 0, 0);
-      b.tiles[e] = rec;
-    }
-    for (int e = tid; e < n_tiles * kMaxSplit; e += nt) {
-      const size_t t = (size_t)(e / kMaxSplit), j = (size_t)(e % kMaxSplit);
-      if (j == 0) b.arrive[t * kCounterStride] = 0u;
-      b.ready[t * kReadyPerTile + j * kReadyStride] = 0u;
-    }
+}
+
+// First sorted position, token count and centroid of tile tau.
+__device__ __forceinline__ int4 tile_header(const PlanShared& sh, int tau, int M) {
+  int lo = 0, hi = sh.n_grp - 1;    // last group whose first tile <= tau
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (sh.g_tile[mid] <= tau) lo = mid;
+    else hi = mid - 1;
   }
+  const int i0 = sh.g_start[lo] + (tau - sh.g_tile[lo]) * M;
+  return make_int4(i0, min(M, sh.g_start[lo + 1] - i0), sh.g_c[lo], 0);
+}
+
+// Record k of tile tau: k = 0 the header, k = 1 .. M its sorted tokens, padded
+// with (0, -1, 0, 0) past the tile's count.
+__device__ __forceinline__ int4 tile_record(const PlanShared& sh, const int4* srt, int tau, int k, int M) {
+  const int4 h = tile_header(sh, tau, M);
+  if (k == 0) return h;
+  return k - 1 < h.y ? srt[h.x + k - 1] : make_int4(0, -1, 0, 0);
+}
+
+// Tile records and meta words of a plan whose groups are in `sh`; checks that
+// the tiles fit the plan's buffers (else n_tiles = -1 in the meta words).
+__device__ __forceinline__ void plan_write_tiles(const PlanBuffers& b, const int4* srt, int T, int M,
+                                                 const PlanShared& sh) {
+  const int tid = threadIdx.x, nt = blockDim.x;
+  const int n_tiles = sh.n_tiles;
+  const bool fits = n_tiles >= 0 && (size_t)n_tiles * (M + 1) <= b.tile_cap && n_tiles <= b.tiles_max;
+  if (fits)
+    for (int e = tid; e < n_tiles * (M + 1); e += nt) b.tiles[e] = tile_record(sh, srt, e / (M + 1), e % (M + 1), M);
   if (tid == 0) {
     b.meta[kMetaNSeg] = sh.n_seg;
-    b.meta[kMetaNGrp] = grp_base;
+    b.meta[kMetaNGrp] = sh.n_grp;
     b.meta[kMetaT] = T;
     b.meta[kMetaNTiles] = fits ? n_tiles : -1;
-    b.meta[kMetaErr] = 0;
   }
 }
 
-// Zeroes v_zero[0 : T][0 : R] (atomic split-K sums start from it), float4 `i`
-// for i = first, first + step, ...  Device-coherent stores, like every other
-// access to v.
-__device__ __forceinline__ void clear_v(const PlanArgs& a, int first, int step) {
-  if (!a.v_zero) return;
-  const int n4 = a.T * a.R / 4;
-  const __amdgpu_buffer_rsrc_t r = coherent_rsrc(a.v_zero, (uint32_t)n4 * 16u);
-  for (int i = first; i < n4; i += step) store4_coherent(r, 16u * (uint32_t)i, make_float4(0.f, 0.f, 0.f, 0.f));
+// Per-tile words a standalone build resets: the arrival counters (the ordered
+// sums count arrivals from zero after every build) and, when asked, the ready
+// words (epochs restart).
+__device__ __forceinline__ void plan_reset_words(const PlanArgs& a, int first, int step) {
+  const PlanBuffers& b = a.b;
+  for (int t = first; t < b.tiles_max; t += step) b.arrive[(size_t)t * kCounterStride] = 0u;
+  if (a.reset_ready)
+    for (int e = first; e < b.tiles_max * kMaxSplit; e += step)
+      b.ready[(size_t)(e / kMaxSplit) * kReadyPerTile + (size_t)(e % kMaxSplit) * kReadyStride] = 0u;
 }
 
-// Batches of up to kPlanSmallT tokens: one block, everything in LDS.  The
-// block has plan_small_threads(T) threads; each token's rank is counted by
-// blockDim / T lanes (a power of two) and summed with lane shuffles.
-__global__ void __launch_bounds__(kPlanSmallT) k_plan_small(PlanArgs a) {
-  __shared__ uint64_t skey[kPlanSmallT];
-  __shared__ int4 s_maps[kPlanSmallT];
-  __shared__ int4 s_srt[kPlanSmallT];
-  __shared__ int32_t s_c[kPlanSmallT];
-  __shared__ PlanShared sh;
+// Batches of up to kPlanSmallT tokens: one block sorts in LDS.
+__global__ void __launch_bounds__(kPlanThreads) k_plan_small(PlanArgs a) {
+  __shared__ PlanLds<kPlanSmallT> L;
   const int T = a.T, tid = threadIdx.x;
-  if (tid < T) {
-    const int4 m = a.b.maps[tid];
-    s_maps[tid] = m;
-    skey[tid] = plan_key(m.x, m.y, tid);
+  plan_reset_words(a, tid, kPlanThreads);
+  plan_sort(a.b.maps, T, L);
+  for (int i = tid; i < T; i += kPlanThreads) {
+    a.b.perm[i] = L.srt[i].x;
+    a.b.srt[i] = L.srt[i];
+    a.b.srt_c[i] = L.c[i];
   }
-  __syncthreads();
-  int lpt = 1;
-  while (lpt < 16 && lpt * 2 * T <= (int)blockDim.x) lpt *= 2;
-  const int t = tid / lpt, sub = tid % lpt;
-  const uint64_t my = t < T ? skey[t] : ~0ull;
-  int cnt = 0;
-#pragma unroll 8
-  for (int i = sub; i < T; i += lpt) cnt += (skey[i] < my) ? 1 : 0;
-  for (int off = 1; off < lpt; off <<= 1) cnt += __shfl_xor(cnt, off);
-  if (t < T && sub == 0) {
-    const int4 m = s_maps[t];
-    const int4 rec = make_int4(t, m.y, m.z, m.w);
-    s_srt[cnt] = rec;
-    s_c[cnt] = m.x;
-    a.b.perm[cnt] = t;
-    a.b.srt[cnt] = rec;
-    a.b.srt_c[cnt] = m.x;
-  }
-  __syncthreads();
-  plan_finish(a, s_srt, s_c, sh);
-  clear_v(a, tid, blockDim.x);
+  plan_groups(true, a.b, L.srt, L.c, T, a.M, L.sh);
+  plan_write_tiles(a.b, L.srt, T, a.M, L.sh);
 }
 
 // Larger batches: rank by counting smaller keys across blocks; the last block to
@@ -385,11 +449,11 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_large(PlanArgs a) {
   __shared__ int s_last;
   const PlanBuffers& b = a.b;
   const int T = a.T, tid = threadIdx.x;
-  clear_v(a, blockIdx.x * kPlanThreads + tid, gridDim.x * kPlanThreads);
+  plan_reset_words(a, blockIdx.x * kPlanThreads + tid, gridDim.x * kPlanThreads);
   const int t = blockIdx.x * kPlanTokPerBlock + (tid >> 2);
   const int q = tid & 3;
   int4 mine = make_int4(0, 0, 0, 0);
-  uint64_t my = ~0ull;
+  uint64_t my = kNoKey;
   if (t < T) {
     mine = b.maps[t];
     my = plan_key(mine.x, mine.y, t);
@@ -421,7 +485,8 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_large(PlanArgs a) {
   __syncthreads();
   if (!s_last) return;
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-  plan_finish(a, b.srt, b.srt_c, sh);
+  plan_groups(true, b, b.srt, b.srt_c, T, a.M, sh);
+  plan_write_tiles(b, b.srt, T, a.M, sh);
   if (tid == 0) __hip_atomic_store(b.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
@@ -513,9 +578,6 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
   int4* s_tile = reinterpret_cast<int4*>(lds);
   float* s_part = reinterpret_cast<float*>(lds + tile_bytes(M));   // [KW][M][R]
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int4* trec = a.tiles + (size_t)tau * (M + 1);
-  for (int i = tid; i < M + 1; i += 256) s_tile[i] = trec[i];
-  __syncthreads();
   const int i0 = s_tile[0].x, n = s_tile[0].y, c = s_tile[0].z;
   const int R = a.R, in = a.in_dim, rc = a.r_c;
   const bool has_c = c >= 0 && rc > 0;
@@ -610,10 +672,21 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
   // R is a multiple of 4: rows are whole float4 vectors
   const int nR4 = n * R / 4;
   const __amdgpu_buffer_rsrc_t rv = coherent_rsrc(a.v + (size_t)i0 * R, (uint32_t)(nR4 * 16));
-  if (a.atomic_sum && s == 0) {
-    // the next apply of the plan adds into the other v buffer: clear this tile's rows
-    const __amdgpu_buffer_rsrc_t rz = coherent_rsrc(a.v_clear + (size_t)i0 * R, (uint32_t)(nR4 * 16));
-    for (int i4 = tid; i4 < nR4; i4 += 256) store4_coherent(rz, 16u * i4, make_float4(0.f, 0.f, 0.f, 0.f));
+  if (a.atomic_sum) {
+    // the next apply of the plan adds into the other v buffer: split 0 clears
+    // this tile's rows, and all shrink blocks share the rows past the batch
+    // that an earlier, larger batch left behind
+    if (s == 0) {
+      const __amdgpu_buffer_rsrc_t rz = coherent_rsrc(a.v_clear + (size_t)i0 * R, (uint32_t)(nR4 * 16));
+      for (int i4 = tid; i4 < nR4; i4 += 256) store4_coherent(rz, 16u * i4, make_float4(0.f, 0.f, 0.f, 0.f));
+    }
+    if (a.clear_rows > a.T) {
+      const int n4 = (a.clear_rows - a.T) * R / 4;
+      const __amdgpu_buffer_rsrc_t rz = coherent_rsrc(a.v_clear + (size_t)a.T * R, (uint32_t)(n4 * 16));
+      const int nb = a.n_tiles * a.S;
+      for (int i4 = (s * a.n_tiles + tau) * 256 + tid; i4 < n4; i4 += nb * 256)
+        store4_coherent(rz, 16u * i4, make_float4(0.f, 0.f, 0.f, 0.f));
+    }
   }
   if (a.S == 1) {
     // one K range: this block writes v itself
@@ -763,9 +836,6 @@ __device__ __forceinline__ void expand_block(const ApplyArgs& a, int tau, int q,
   uint16_t* s_vl = s_vh + (size_t)M * kVS;
   __shared__ int s_flag;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int4* trec = a.tiles + (size_t)tau * (M + 1);
-  for (int i = tid; i < M + 1; i += 256) s_tile[i] = trec[i];
-  __syncthreads();
   const int i0 = s_tile[0].x, n = s_tile[0].y, c = s_tile[0].z;
   const int R = a.R, out = a.out_dim, rc = a.r_c, in = a.in_dim;
   const bool has_c = c >= 0 && rc > 0;
@@ -882,27 +952,53 @@ __device__ __forceinline__ void expand_block(const ApplyArgs& a, int tau, int q,
 template <typename E, int MB, int RU, int NBM>
 __global__ void __launch_bounds__(256) k_apply(ApplyArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
-  const int b = blockIdx.x;
+  constexpr int M = 16 * MB;
+  const int b = blockIdx.x, tid = threadIdx.x;
   const int n_shrink = a.n_tiles * a.S;
-  if (b < n_shrink) {
-    shrink_block<E, MB, RU, NBM>(a, b % a.n_tiles, b / a.n_tiles, lds);
+  const bool shrink = b < n_shrink;
+  const int tau = (shrink ? b : b - n_shrink) % a.n_tiles;
+  int4* s_tile = reinterpret_cast<int4*>(lds);
+  if (a.fused_plan) {
+    // This launch also builds the plan (small batches): every block sorts the
+    // batch in LDS and cuts its own tile; the last block also writes the plan
+    // out for later applies and plan queries.
+    auto& L = *reinterpret_cast<PlanLds<kPlanFusedT>*>(lds + tile_bytes(M));
+    plan_sort(a.pb.maps, a.T, L);
+    const bool writer = b == (int)gridDim.x - 1;
+    if (writer)
+      for (int i = tid; i < a.T; i += 256) {
+        a.pb.perm[i] = L.srt[i].x;
+        a.pb.srt[i] = L.srt[i];
+        a.pb.srt_c[i] = L.c[i];
+      }
+    plan_groups(writer, a.pb, L.srt, L.c, a.T, M, L.sh);
+    if (writer) plan_write_tiles(a.pb, L.srt, a.T, M, L.sh);
+    if (L.sh.n_tiles != a.n_tiles) {   // cannot happen: the host counts the same tiles
+      if (tid == 0) atomicAdd(a.meta + kMetaErr, 1);
+      return;
+    }
+    for (int k = tid; k < M + 1; k += 256) s_tile[k] = tile_record(L.sh, L.srt, tau, k, M);
   } else {
-    const int e = b - n_shrink;
-    expand_block<E, MB, RU, NBM>(a, e % a.n_tiles, e / a.n_tiles, lds);
+    const int4* trec = a.tiles + (size_t)tau * (M + 1);
+    for (int k = tid; k < M + 1; k += 256) s_tile[k] = trec[k];
   }
+  __syncthreads();
+  if (shrink) shrink_block<E, MB, RU, NBM>(a, tau, b / a.n_tiles, lds);
+  else expand_block<E, MB, RU, NBM>(a, tau, (b - n_shrink) / a.n_tiles, lds);
 }
 
-size_t apply_lds(int M, int R) {
+size_t apply_lds(int M, int R, bool fused_plan) {
   const size_t tb = (size_t)tile_bytes(M);
   const size_t shrink = tb + sizeof(float) * 64 * (size_t)R;           // KW * M == 64
   const size_t expand = tb + sizeof(float) * ((size_t)M * R + (size_t)M * kYS) + 2 * sizeof(uint16_t) * M * kVS;
-  return shrink > expand ? shrink : expand;
+  const size_t plan = fused_plan ? tb + sizeof(PlanLds<kPlanFusedT>) : 0;
+  return std::max({shrink, expand, plan});
 }
 
 template <typename E, int RU, int NBM>
 hipError_t launch_nbm(const ApplyArgs& a, int M, hipStream_t s) {
   const dim3 grid(a.n_tiles * (a.S + a.n_col)), block(256);   // n_col: column blocks of cpb chunks
-  const size_t lds = apply_lds(M, a.R);
+  const size_t lds = apply_lds(M, a.R, a.fused_plan != 0);
   if (M == 16) {
     hipLaunchKernelGGL((k_apply<E, 1, RU, NBM>), grid, block, lds, s, a);
   } else if constexpr (sizeof(E) == 2) {
@@ -934,7 +1030,7 @@ hipError_t kernels_init(int device) {
   int lds_max = 0;
   hipError_t e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, device);
   if (e != hipSuccess) return e;
-  if ((size_t)lds_max < apply_lds(64, kMaxRc + kMaxRu) + 1024) return hipErrorInvalidConfiguration;
+  if ((size_t)lds_max < apply_lds(64, kMaxRc + kMaxRu, true) + 1024) return hipErrorInvalidConfiguration;
   done[device] = true;
   return hipSuccess;
 }
@@ -942,9 +1038,7 @@ hipError_t kernels_init(int device) {
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
   if (a.T <= kPlanSmallT) {
-    // 256 threads up to T = 256 (several lanes per token), else one per token
-    const int threads = a.T <= 256 ? 256 : (a.T + 63) / 64 * 64;
-    hipLaunchKernelGGL(k_plan_small, dim3(1), dim3(threads), 0, s, a);
+    hipLaunchKernelGGL(k_plan_small, dim3(1), dim3(kPlanThreads), 0, s, a);
   } else {
     const int blocks = (a.T + kPlanTokPerBlock - 1) / kPlanTokPerBlock;
     hipLaunchKernelGGL(k_plan_large, dim3(blocks), dim3(kPlanThreads), 0, s, a);

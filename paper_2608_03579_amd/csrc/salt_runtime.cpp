@@ -53,8 +53,15 @@ struct salt_plan {
   int32_t n_tiles = 0;
   int32_t n_groups_c = 0;           // groups with a centroid
   int64_t sum_ru = 0;               // residual rank summed over tokens
-  uint32_t arrivals = 0;            // per-tile arrival count after the last enqueued apply
-  uint32_t epoch = 0;               // applies enqueued since the last build
+  uint32_t arrivals = 0;            // per-tile arrival count after the last enqueued apply (ordered sums)
+  uint32_t epoch = 0;               // applies enqueued since creation or the last epoch reset
+  // A build of a small batch is deferred: the next apply on the same stream
+  // plans the batch itself.  Any other use of the plan first launches the
+  // deferred build on the stream it was requested on.
+  mutable bool build_pending = false;   // running the deferred build changes no visible state
+  hipStream_t build_stream = nullptr;
+  // atomic sums: rows of each v buffer that may be nonzero (all rows below)
+  int32_t v_dirty[2] = {0, 0};
 };
 
 struct salt_ctx {
@@ -128,6 +135,27 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 // Split-K partial sums go through device atomics unless the context asked for
 // bit-reproducible results.
 bool atomic_sums(const salt_ctx* c) { return (c->cfg.flags & SALT_DETERMINISTIC) == 0; }
+
+// Epochs are compared modulo 2^32 by signed difference; restart them well before
+// a ready word could fall 2^31 epochs behind.
+constexpr uint32_t kEpochReset = 1u << 30;
+
+// Launches the plan kernel now.  reset_ready restarts the plan's epochs.
+hipError_t launch_build(const salt_plan* plan, hipStream_t s, bool reset_ready) {
+  salt::PlanArgs pa{};
+  pa.b = plan->dev;
+  pa.T = plan->T;
+  pa.M = plan->M;
+  pa.reset_ready = reset_ready ? 1 : 0;
+  return salt::launch_plan(pa, s);
+}
+
+// Runs a deferred build (see salt_plan) on the stream it was requested on.
+hipError_t flush_build(const salt_plan* plan) {
+  if (!plan->build_pending) return hipSuccess;
+  plan->build_pending = false;
+  return launch_build(plan, plan->build_stream, false);
+}
 
 hipError_t ring_record(EventRing& r, hipStream_t s, int64_t* seq_out) {
   const int64_t seq = r.next;
@@ -436,6 +464,7 @@ salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out) {
   if (e == hipSuccess) e = hipMemset(b.meta, 0, salt::kMetaWords * 4);
   if (e == hipSuccess) e = hipMemset(b.arrive, 0, (size_t)b.tiles_max * salt::kCounterStride * 4);
   if (e == hipSuccess) e = hipMemset(b.ready, 0, (size_t)b.tiles_max * salt::kReadyPerTile * 4);
+  if (e == hipSuccess) e = hipMemset(b.v, 0, 2 * T * R * 4);
   if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     free_plan_buffers(p);
@@ -478,6 +507,7 @@ salt_status salt_plan_set_maps(salt_ctx* ctx, salt_plan* plan, int32_t T, const 
   }
   SALT_HIP(ctx, hipSetDevice(ctx->device));
   hipStream_t s = (hipStream_t)stream;
+  SALT_HIP(ctx, flush_build(plan));
   // the staging buffer may still feed the previous copy
   if (plan->staged_pending) {
     SALT_HIP(ctx, hipEventSynchronize(plan->staged));
@@ -531,18 +561,17 @@ salt_status salt_plan_build(salt_ctx* ctx, salt_plan* plan, void* stream) {
   if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
   if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
   SALT_HIP(ctx, hipSetDevice(ctx->device));
-  salt::PlanArgs pa{};
-  pa.b = plan->dev;
-  pa.T = plan->T;
-  pa.M = plan->M;
-  // atomic split-K sums: the first apply after the build accumulates into v
-  // buffer 1 (its epoch is 1), which therefore starts at zero
-  pa.v_zero = atomic_sums(ctx) ? plan->dev.v + plan->dev.v_stride : nullptr;
-  pa.R = salt::padded_rank(ctx->cfg.r_c, ctx->cfg.r_u_max);
-  SALT_HIP(ctx, salt::launch_plan(pa, (hipStream_t)stream));
+  SALT_HIP(ctx, flush_build(plan));
+  const bool reset = plan->epoch >= kEpochReset;
+  if (reset) plan->epoch &= 1u;   // keeps the parity that picks the v buffer
+  if (!reset && atomic_sums(ctx) && plan->T > 0 && plan->T <= salt::kPlanFusedT) {
+    plan->build_pending = true;
+    plan->build_stream = (hipStream_t)stream;
+  } else {
+    SALT_HIP(ctx, launch_build(plan, (hipStream_t)stream, reset));
+  }
   plan->built = true;
   plan->arrivals = 0;
-  plan->epoch = 0;
   return SALT_OK;
 }
 
@@ -552,7 +581,10 @@ salt_status salt_plan_errors(salt_ctx* ctx, const salt_plan* plan, void* stream,
   *n_errors = 0;
   if (!plan->built || plan->T == 0) return SALT_OK;
   SALT_HIP(ctx, hipSetDevice(ctx->device));
+  SALT_HIP(ctx, flush_build(plan));
   SALT_HIP(ctx, hipStreamSynchronize((hipStream_t)stream));
+  if (plan->build_stream && plan->build_stream != (hipStream_t)stream)
+    SALT_HIP(ctx, hipStreamSynchronize(plan->build_stream));
   int32_t meta[salt::kMetaWords];
   SALT_HIP(ctx, hipMemcpy(meta, plan->dev.meta, sizeof meta, hipMemcpyDeviceToHost));
   if (meta[salt::kMetaNTiles] != plan->n_tiles) {
@@ -561,6 +593,10 @@ salt_status salt_plan_errors(salt_ctx* ctx, const salt_plan* plan, void* stream,
                 meta[salt::kMetaNTiles], plan->n_tiles);
   }
   *n_errors = meta[salt::kMetaErr];
+  if (meta[salt::kMetaErr] != 0) {
+    const int32_t zero = 0;
+    SALT_HIP(ctx, hipMemcpy(plan->dev.meta + salt::kMetaErr, &zero, 4, hipMemcpyHostToDevice));
+  }
   return SALT_OK;
 }
 
@@ -572,7 +608,9 @@ salt_status salt_plan_download(salt_ctx* ctx, const salt_plan* plan, void* strea
   if (!plan->built) return fail(ctx, SALT_ERR_BAD_STATE, "plan was not built");
   SALT_HIP(ctx, hipSetDevice(ctx->device));
   hipStream_t s = (hipStream_t)stream;
+  SALT_HIP(ctx, flush_build(plan));
   SALT_HIP(ctx, hipStreamSynchronize(s));
+  if (plan->build_stream && plan->build_stream != s) SALT_HIP(ctx, hipStreamSynchronize(plan->build_stream));
   const int T = plan->T;
   int32_t meta[3] = {0, 0, 0};
   if (T > 0) SALT_HIP(ctx, hipMemcpy(meta, plan->dev.meta, sizeof meta, hipMemcpyDeviceToHost));
@@ -618,6 +656,9 @@ salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
   }
   SALT_HIP(ctx, hipSetDevice(ctx->device));
   hipStream_t s = (hipStream_t)stream;
+  // a deferred build runs inside this launch when it was requested on this stream
+  const bool fused_plan = plan->build_pending && plan->build_stream == s;
+  if (!fused_plan) SALT_HIP(ctx, flush_build(plan));
   SALT_HIP(ctx, ring_wait(ctx->loaders, s, need_load));
 
   const salt_shape sh = ctx->tables[table];
@@ -670,14 +711,25 @@ salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
   a.target = plan->arrivals;
   a.epoch = ++plan->epoch;
   a.atomic_sum = atomic ? 1 : 0;
+  a.clear_rows = T;
   if (atomic) {
     // v buffers alternate between applies: this apply sums into buffer
-    // (epoch & 1) and clears the other one for the next apply
-    a.v = plan->dev.v + (a.epoch & 1u) * plan->dev.v_stride;
-    a.v_clear = plan->dev.v + ((a.epoch + 1u) & 1u) * plan->dev.v_stride;
+    // p = epoch & 1 (all zero: the previous apply cleared it) and clears the
+    // other one, including rows an earlier larger batch used
+    const int p = (int)(a.epoch & 1u), q = p ^ 1;
+    a.v = plan->dev.v + (size_t)p * plan->dev.v_stride;
+    a.v_clear = plan->dev.v + (size_t)q * plan->dev.v_stride;
+    a.clear_rows = std::max(T, plan->v_dirty[q]);
+    plan->v_dirty[q] = 0;
+    plan->v_dirty[p] = T;
   } else {
     a.v = plan->dev.v;
     a.v_clear = nullptr;
+  }
+  a.fused_plan = fused_plan ? 1 : 0;
+  if (fused_plan) {
+    a.pb = plan->dev;
+    plan->build_pending = false;
   }
   SALT_HIP(ctx, salt::launch_apply(a, ctx->cfg.dtype == SALT_BF16, M, s));
   int64_t seq;

@@ -1,6 +1,9 @@
 """GPU parity: libsalt (through the C ABI) against the fp64 CPU oracle.
 
-Plans must match the oracle bit for bit.  Outputs must satisfy
+Plans must match the oracle bit for bit.  A build of a batch of at most 256
+tokens is deferred into the next apply on its stream, so a case that applies
+before it downloads the plan checks the plan that apply wrote, and one that
+downloads first checks the standalone plan kernel.  Outputs must satisfy
 |y - ref| <= 1e-2 * (1 + |ref|) element-wise for bf16 (fp32 accumulation), and
 1e-5 * (1 + |ref|) for the fp32 Tiny workload; the integer-valued variants must be
 bit-exact.  Every case prints its name before the GPU work starts.
@@ -51,8 +54,8 @@ def test_tiny_fp32(seed, y0):
     run = Run(synth.make(1, seed, y0=y0))
     try:
         run.set_and_build()
+        _check_table(run, 0)     # the apply builds the plan
         _check_plan(run)
-        _check_table(run, 0)
     finally:
         run.close()
 
@@ -63,8 +66,12 @@ def test_llama32_qproj_decode(seed):
     run = Run(synth.make(2, seed, y0="normal" if seed == 1 else "zero"))
     try:
         run.set_and_build()
-        _check_plan(run)
-        _check_table(run, 0)
+        if seed == 2:
+            _check_plan(run)     # standalone plan kernel, then the apply reads its tiles
+            _check_table(run, 0)
+        else:
+            _check_table(run, 0)
+            _check_plan(run)
     finally:
         run.close()
 
@@ -102,9 +109,9 @@ def test_llama31_decode_with_swaps():
         for s in w.meta["swap_slots"]:
             run.load(int(s), 1)
         run.set_and_build()
-        _check_plan(run)
         for t in range(len(w.tables)):
             _check_table(run, t)
+        _check_plan(run)
     finally:
         run.close()
 
