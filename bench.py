@@ -227,13 +227,15 @@ def run_gpu(w, dw, args, hip, salt):
     t0 = time.perf_counter()
     for k in range(args.steps):
         step(k)
+    enqueue = time.perf_counter() - t0
     e1.record(stream)
     e1.synchronize()
     wall = time.perf_counter() - t0
     hip.synchronize()
     ms_total = e0.elapsed_ms(e1)
     ms_step = ms_total / args.steps
-    log(f"timed {args.steps} steps: {ms_total:.3f} ms GPU ({wall * 1e3:.1f} ms wall), {ms_step * 1e3:.2f} us/step")
+    log(f"timed {args.steps} steps: {ms_total:.3f} ms GPU ({wall * 1e3:.1f} ms wall, host enqueue "
+        f"{enqueue * 1e3:.1f} ms), {ms_step * 1e3:.2f} us/step")
 
     # roofline: the apply kernel's own duration, from a second timed region of
     # back-to-back applies (plans already built), events on the kernel's stream

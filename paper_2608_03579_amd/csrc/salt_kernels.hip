@@ -298,9 +298,11 @@ __device__ __forceinline__ void plan_sort(const int4* maps, int T, PlanLds<CAP>&
   for (int run = wave; run < nrun; run += kPlanThreads / 64) {
     const uint64_t k = L.key[run * 64 + lane];
     if (k != kNoKey) {
+      // the searches in different runs are independent: unrolled, they overlap
       int rank = lane;
-      for (int o = 0; o < nrun; ++o)
-        if (o != run) rank += count_below64(L.key + o * 64, k);
+#pragma unroll
+      for (int o = 0; o < CAP / 64; ++o)
+        if (o < nrun && o != run) rank += count_below64(L.key + o * 64, k);
       const int t = (int)(k & 0x1fffffu);
       const int4 m = L.maps[t];
       L.srt[rank] = make_int4(t, m.y, m.z, m.w);
@@ -488,6 +490,85 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_large(PlanArgs a) {
   plan_groups(true, b, b.srt, b.srt_c, T, a.M, sh);
   plan_write_tiles(b, b.srt, T, a.M, sh);
   if (tid == 0) __hip_atomic_store(b.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// One tile of a batch of T <= kPlanFusedT tokens, cut straight from the maps by
+// an apply block that plans for itself.  Groups are the centroid ids in order
+// (-1 first), so a per-id token count and its prefix sums give every group's
+// first sorted position and first tile; only the tokens of the block's own
+// group are then ranked, by counting the smaller keys of that group.
+struct TileLds {
+  uint64_t key[kPlanFusedT];   // plan key by token
+  int cnt[80];                 // tokens per centroid id + 1 (0 .. 64)
+  int4 hdr;                    // (i0, n, c, c + 1) of the block's tile
+  int chunk;                   // the tile is chunk `chunk` of its group
+  int n_tiles;
+};
+
+// Writes the header and the M token records of tile tau to s_tile; returns
+// false (for the whole block) if the batch does not cut into n_tiles tiles.
+__device__ __forceinline__ bool tile_from_maps(const int4* maps, int T, int M, int tau, int n_tiles, TileLds& L,
+                                               int4* s_tile) {
+  const int tid = threadIdx.x, lane = tid & 63;
+  int4 m = make_int4(0, 0, 0, 0);
+  if (tid < T) m = maps[tid];
+  if (tid < 80) L.cnt[tid] = 0;
+  // every record starts as padding, so none is ever left unset
+  if (tid < M) s_tile[1 + tid] = make_int4(0, -1, 0, 0);
+  __syncthreads();
+  uint64_t key = kNoKey;
+  if (tid < T) {
+    key = plan_key(m.x, m.y, tid);
+    L.key[tid] = key;
+    atomicAdd(&L.cnt[m.x + 1], 1);
+  }
+  __syncthreads();
+  if (tid < 64) {
+    // lane l: centroid id l; id 64 (c = 63) follows lane 63
+    const int cnt_l = L.cnt[lane], tiles_l = (cnt_l + M - 1) / M;
+    int inc_c = cnt_l, inc_t = tiles_l;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int ac = __shfl_up(inc_c, off), at = __shfl_up(inc_t, off);
+      if (lane >= off) {
+        inc_c += ac;
+        inc_t += at;
+      }
+    }
+    const int start_l = inc_c - cnt_l, tbase_l = inc_t - tiles_l;
+    const int cnt64 = L.cnt[64], start64 = __shfl(inc_c, 63), tbase64 = __shfl(inc_t, 63);
+    const int tiles64 = (cnt64 + M - 1) / M;
+    if (tau >= tbase_l && tau < tbase_l + tiles_l) {
+      const int k = tau - tbase_l;
+      L.hdr = make_int4(start_l + k * M, min(M, cnt_l - k * M), lane - 1, lane);
+      L.chunk = k;
+    }
+    if (lane == 0) {
+      L.n_tiles = tbase64 + tiles64;
+      if (tau >= tbase64 && tau < tbase64 + tiles64) {
+        const int k = tau - tbase64;
+        L.hdr = make_int4(start64 + k * M, min(M, cnt64 - k * M), 63, 64);
+        L.chunk = k;
+      }
+    }
+  }
+  __syncthreads();
+  if (L.n_tiles != n_tiles) return false;
+  const int4 h = L.hdr;
+  if (tid < T && m.x + 1 == h.w) {
+    const uint64_t lo = uint64_t(uint32_t(h.w)) << 42;
+    int r = 0;
+#pragma unroll 8
+    for (int i = 0; i < T; ++i) {
+      const uint64_t o = L.key[i];
+      r += (o >= lo && o < key) ? 1 : 0;
+    }
+    r -= L.chunk * M;
+    if (r >= 0 && r < h.y) s_tile[1 + r] = make_int4(tid, m.y, m.z, m.w);
+  }
+  if (tid == 0) s_tile[0] = make_int4(h.x, h.y, h.z, 0);
+  __syncthreads();
+  return true;
 }
 
 // ---------------------------------------------------------------------------
@@ -949,6 +1030,19 @@ __device__ __forceinline__ void expand_block(const ApplyArgs& a, int tau, int q,
   }
 }
 
+// The plan a launch builds for itself, written out by its first block.
+template <int CAP>
+__device__ __forceinline__ void write_plan(const ApplyArgs& a, int M, PlanLds<CAP>& L) {
+  plan_sort(a.pb.maps, a.T, L);
+  for (int i = threadIdx.x; i < a.T; i += 256) {
+    a.pb.perm[i] = L.srt[i].x;
+    a.pb.srt[i] = L.srt[i];
+    a.pb.srt_c[i] = L.c[i];
+  }
+  plan_groups(true, a.pb, L.srt, L.c, a.T, M, L.sh);
+  plan_write_tiles(a.pb, L.srt, a.T, M, L.sh);
+}
+
 template <typename E, int MB, int RU, int NBM>
 __global__ void __launch_bounds__(256) k_apply(ApplyArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
@@ -959,46 +1053,43 @@ __global__ void __launch_bounds__(256) k_apply(ApplyArgs a) {
   const int tau = (shrink ? b : b - n_shrink) % a.n_tiles;
   int4* s_tile = reinterpret_cast<int4*>(lds);
   if (a.fused_plan) {
-    // This launch also builds the plan (small batches): every block sorts the
-    // batch in LDS and cuts its own tile; the last block also writes the plan
-    // out for later applies and plan queries.
-    auto& L = *reinterpret_cast<PlanLds<kPlanFusedT>*>(lds + tile_bytes(M));
-    plan_sort(a.pb.maps, a.T, L);
-    const bool writer = b == (int)gridDim.x - 1;
-    if (writer)
-      for (int i = tid; i < a.T; i += 256) {
-        a.pb.perm[i] = L.srt[i].x;
-        a.pb.srt[i] = L.srt[i];
-        a.pb.srt_c[i] = L.c[i];
-      }
-    plan_groups(writer, a.pb, L.srt, L.c, a.T, M, L.sh);
-    if (writer) plan_write_tiles(a.pb, L.srt, a.T, M, L.sh);
-    if (L.sh.n_tiles != a.n_tiles) {   // cannot happen: the host counts the same tiles
-      if (tid == 0) atomicAdd(a.meta + kMetaErr, 1);
+    // This launch also builds the plan (batches of up to kPlanFusedT tokens).
+    // One extra block, the last, sorts the whole batch and writes the plan out
+    // for later applies and plan queries; every other block cuts its own tile
+    // from the maps.
+    if (b == (int)gridDim.x - 1) {
+      write_plan(a, M, *reinterpret_cast<PlanLds<kPlanFusedT>*>(lds));
       return;
     }
-    for (int k = tid; k < M + 1; k += 256) s_tile[k] = tile_record(L.sh, L.srt, tau, k, M);
+    auto& L = *reinterpret_cast<TileLds*>(lds + tile_bytes(M));
+    if (!tile_from_maps(a.pb.maps, a.T, M, tau, a.n_tiles, L, s_tile)) {
+      if (tid == 0) atomicAdd(a.meta + kMetaErr, 1);   // cannot happen: the host counts the same tiles
+      return;
+    }
   } else {
     const int4* trec = a.tiles + (size_t)tau * (M + 1);
     for (int k = tid; k < M + 1; k += 256) s_tile[k] = trec[k];
+    __syncthreads();
   }
-  __syncthreads();
   if (shrink) shrink_block<E, MB, RU, NBM>(a, tau, b / a.n_tiles, lds);
   else expand_block<E, MB, RU, NBM>(a, tau, (b - n_shrink) / a.n_tiles, lds);
 }
 
-size_t apply_lds(int M, int R, bool fused_plan) {
+// fused_T: batch size of a launch that builds its plan, else 0
+size_t apply_lds(int M, int R, int fused_T) {
   const size_t tb = (size_t)tile_bytes(M);
   const size_t shrink = tb + sizeof(float) * 64 * (size_t)R;           // KW * M == 64
   const size_t expand = tb + sizeof(float) * ((size_t)M * R + (size_t)M * kYS) + 2 * sizeof(uint16_t) * M * kVS;
-  const size_t plan = fused_plan ? tb + sizeof(PlanLds<kPlanFusedT>) : 0;
+  const size_t plan = fused_T > 0 ? std::max(sizeof(PlanLds<kPlanFusedT>), tb + sizeof(TileLds)) : 0;
   return std::max({shrink, expand, plan});
 }
 
 template <typename E, int RU, int NBM>
 hipError_t launch_nbm(const ApplyArgs& a, int M, hipStream_t s) {
-  const dim3 grid(a.n_tiles * (a.S + a.n_col)), block(256);   // n_col: column blocks of cpb chunks
-  const size_t lds = apply_lds(M, a.R, a.fused_plan != 0);
+  // n_col: column blocks of cpb chunks; one more block, the last, writes a plan
+  // built in this launch
+  const dim3 grid(a.n_tiles * (a.S + a.n_col) + a.fused_plan), block(256);
+  const size_t lds = apply_lds(M, a.R, a.fused_plan ? a.T : 0);
   if (M == 16) {
     hipLaunchKernelGGL((k_apply<E, 1, RU, NBM>), grid, block, lds, s, a);
   } else if constexpr (sizeof(E) == 2) {
@@ -1030,7 +1121,7 @@ hipError_t kernels_init(int device) {
   int lds_max = 0;
   hipError_t e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, device);
   if (e != hipSuccess) return e;
-  if ((size_t)lds_max < apply_lds(64, kMaxRc + kMaxRu, true) + 1024) return hipErrorInvalidConfiguration;
+  if ((size_t)lds_max < apply_lds(64, kMaxRc + kMaxRu, kPlanFusedT) + 1024) return hipErrorInvalidConfiguration;
   done[device] = true;
   return hipSuccess;
 }

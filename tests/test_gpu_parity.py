@@ -123,9 +123,12 @@ def test_zipf_multitenant(baseline):
     run = Run(w)
     try:
         run.set_and_build()
-        _check_plan(run)
+        if baseline:
+            _check_plan(run)
         for t in range(len(w.tables)):
             _check_table(run, t)
+        if not baseline:
+            _check_plan(run)     # written by the first apply, which built it
     finally:
         run.close()
 
