@@ -237,13 +237,18 @@ def run_gpu(w, dw, args, hip, salt):
     log(f"timed {args.steps} steps: {ms_total:.3f} ms GPU ({wall * 1e3:.1f} ms wall, host enqueue "
         f"{enqueue * 1e3:.1f} ms), {ms_step * 1e3:.2f} us/step")
 
-    # roofline: the apply kernel's own duration, from a second timed region of
-    # back-to-back applies (plans already built), events on the kernel's stream
+    # roofline: the apply kernel's own duration.  A second timed region runs
+    # applies of one table on plans already built, back to back (launch-to-launch
+    # period, HIP events around the run); a third launches the same applies
+    # through salt_apply_timed, whose HIP events record each kernel's own start
+    # and end (the duration the rocprofv3 kernel trace reports).
     maps = (w.tok_c, w.tok_u)
     bytes_tab = np.array([apply_bytes(w, maps, t) for t in range(n_tab)], dtype=np.float64)
     flops_tab = np.array([apply_flops(w, maps, t) for t in range(n_tab)], dtype=np.float64)
     n_meas = max(1, min(args.steps, 4000) // n_tab)
     per_tab = np.zeros(n_tab)
+    period_tab = np.zeros(n_tab)
+    ev = [hip.Event() for _ in range(2 * n_meas)]
     for t in range(n_tab):
         a, b = hip.Event(), hip.Event()
         a.record(stream)
@@ -253,7 +258,17 @@ def run_gpu(w, dw, args, hip, salt):
             ctx.apply(tab, plans[slot], xs[tab].ptr, ys[tab].ptr, stream.h)
         b.record(stream)
         b.synchronize()
-        per_tab[t] = a.elapsed_ms(b) / n_meas
+        period_tab[t] = a.elapsed_ms(b) / n_meas
+        a.destroy()
+        b.destroy()
+        for k in range(n_meas):
+            slot = k % rot
+            tab = slot * n_tab + t
+            ctx.apply_timed(tab, plans[slot], xs[tab].ptr, ys[tab].ptr, stream.h, ev[2 * k].h, ev[2 * k + 1].h)
+        stream.synchronize()
+        per_tab[t] = float(np.mean([ev[2 * k].elapsed_ms(ev[2 * k + 1]) for k in range(n_meas)]))
+    for e in ev:
+        e.destroy()
     errors = sum(p.errors(stream.h) for p in plans)
     if errors:
         raise RuntimeError(f"{errors} apply blocks gave up waiting; results invalid")
@@ -261,6 +276,7 @@ def run_gpu(w, dw, args, hip, salt):
     achieved = bytes_tab[dom] / (per_tab[dom] * 1e-3) / 1e9
     step_bytes = float(bytes_tab.sum())
     log(f"apply durations (us): " + ", ".join(f"{w.tables[t][0]} {per_tab[t] * 1e3:.2f}" for t in range(n_tab)))
+    log(f"apply launch periods (us): " + ", ".join(f"{w.tables[t][0]} {period_tab[t] * 1e3:.2f}" for t in range(n_tab)))
 
     swap = swap_timing(w, hip, salt) if args.swap else None
     if args.copy_mb:
@@ -286,7 +302,10 @@ def run_gpu(w, dw, args, hip, salt):
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
                      "kernel": f"k_apply (salt_apply, one launch) on {w.tables[dom][0]}",
                      "bytes_per_launch": int(bytes_tab[dom]), "avg_us": per_tab[dom] * 1e3,
-                     "timing": f"HIP events around {n_meas} back-to-back applies on the kernel's stream"},
+                     "period_us": period_tab[dom] * 1e3,
+                     "timing": f"avg_us: mean kernel duration over {n_meas} applies, from HIP events that "
+                               "record each apply kernel's own start and end (salt_apply_timed) on its stream; "
+                               "period_us: launch-to-launch period of back-to-back applies, with the dispatch gap"},
         "swap": swap,
     }
 

@@ -190,6 +190,13 @@ SALT_API salt_status salt_plan_download(salt_ctx* ctx, const salt_plan* plan, vo
 SALT_API salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y,
                        void* stream);
 
+/* salt_apply for measurement: the same apply, and the HIP events `start_event`
+ * and `stop_event` (hipEvent_t, created with timing enabled) record the apply
+ * kernel's own start and end, so hipEventElapsedTime gives its duration without
+ * the dispatch gap.  Errors as salt_apply; SALT_ERR_INVALID_ARG for a null event. */
+SALT_API salt_status salt_apply_timed(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y,
+                                      void* stream, void* start_event, void* stop_event);
+
 /* Synchronise `stream`, then report in *n_errors the number of apply blocks of
  * this plan that gave up waiting for their tile since the last salt_plan_build
  * (their slice of y was left unchanged; 0 in normal operation).  Also checks

@@ -76,7 +76,8 @@ struct ApplyArgs {
 
 hipError_t kernels_init(int device);
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
-hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s);
+// e0 / e1: if set, HIP events that record the apply kernel's own start and end.
+hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 
 // Columns of y per expand chunk.
 constexpr int kNC = 128;

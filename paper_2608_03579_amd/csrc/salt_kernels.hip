@@ -28,6 +28,8 @@
 // any expand block waits on it, and shrink blocks never wait: the wait always
 // ends.  It is still bounded; a block that gives up records an error in the
 // plan's meta words and leaves its slice of y untouched.
+#include <hip/hip_ext.h>
+
 #include <algorithm>
 
 #include "salt_internal.h"
@@ -1084,17 +1086,25 @@ size_t apply_lds(int M, int R, int fused_T) {
   return std::max({shrink, expand, plan});
 }
 
+// A launch; with events, they record the kernel's own start and end.
+template <typename K>
+void launch_k(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, const ApplyArgs& a, hipEvent_t e0,
+              hipEvent_t e1) {
+  if (e0 || e1) hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, s, e0, e1, 0u, a);
+  else hipLaunchKernelGGL(kernel, grid, block, lds, s, a);
+}
+
 template <typename E, int RU, int NBM>
-hipError_t launch_nbm(const ApplyArgs& a, int M, hipStream_t s) {
+hipError_t launch_nbm(const ApplyArgs& a, int M, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   // n_col: column blocks of cpb chunks; one more block, the last, writes a plan
   // built in this launch
   const dim3 grid(a.n_tiles * (a.S + a.n_col) + a.fused_plan), block(256);
   const size_t lds = apply_lds(M, a.R, a.fused_plan ? a.T : 0);
   if (M == 16) {
-    hipLaunchKernelGGL((k_apply<E, 1, RU, NBM>), grid, block, lds, s, a);
+    launch_k(k_apply<E, 1, RU, NBM>, grid, block, lds, s, a, e0, e1);
   } else if constexpr (sizeof(E) == 2) {
-    if (M == 32) hipLaunchKernelGGL((k_apply<E, 2, RU, NBM>), grid, block, lds, s, a);
-    else if (M == 64) hipLaunchKernelGGL((k_apply<E, 4, RU, NBM>), grid, block, lds, s, a);
+    if (M == 32) launch_k(k_apply<E, 2, RU, NBM>, grid, block, lds, s, a, e0, e1);
+    else if (M == 64) launch_k(k_apply<E, 4, RU, NBM>, grid, block, lds, s, a, e0, e1);
     else return hipErrorInvalidValue;
   } else {
     return hipErrorInvalidValue;
@@ -1104,10 +1114,10 @@ hipError_t launch_nbm(const ApplyArgs& a, int M, hipStream_t s) {
 
 // NBM: 16-rank blocks of the centroid held per lane (r_c <= 16 * NBM)
 template <typename E, int RU>
-hipError_t launch_typed(const ApplyArgs& a, int M, hipStream_t s) {
-  if (a.r_c <= 32) return launch_nbm<E, RU, 2>(a, M, s);
-  if (a.r_c <= 64) return launch_nbm<E, RU, 4>(a, M, s);
-  return launch_nbm<E, RU, 8>(a, M, s);
+hipError_t launch_typed(const ApplyArgs& a, int M, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (a.r_c <= 32) return launch_nbm<E, RU, 2>(a, M, s, e0, e1);
+  if (a.r_c <= 64) return launch_nbm<E, RU, 4>(a, M, s, e0, e1);
+  return launch_nbm<E, RU, 8>(a, M, s, e0, e1);
 }
 
 }  // namespace
@@ -1139,17 +1149,17 @@ hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
 
 // RU: residual ranks held per lane (1, 2 or kMaxRu).  fp32 plans use 16-token
 // tiles only.
-hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s) {
+hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (a.T <= 0 || a.n_tiles <= 0) return hipSuccess;
   if (!bf16) {
     if (M != 16) return hipErrorInvalidValue;
-    if (a.r_u_max <= 1) return launch_typed<float, 1>(a, M, s);
-    if (a.r_u_max <= 2) return launch_typed<float, 2>(a, M, s);
-    return launch_typed<float, kMaxRu>(a, M, s);
+    if (a.r_u_max <= 1) return launch_typed<float, 1>(a, M, s, e0, e1);
+    if (a.r_u_max <= 2) return launch_typed<float, 2>(a, M, s, e0, e1);
+    return launch_typed<float, kMaxRu>(a, M, s, e0, e1);
   }
-  if (a.r_u_max <= 1) return launch_typed<uint16_t, 1>(a, M, s);
-  if (a.r_u_max <= 2) return launch_typed<uint16_t, 2>(a, M, s);
-  return launch_typed<uint16_t, kMaxRu>(a, M, s);
+  if (a.r_u_max <= 1) return launch_typed<uint16_t, 1>(a, M, s, e0, e1);
+  if (a.r_u_max <= 2) return launch_typed<uint16_t, 2>(a, M, s, e0, e1);
+  return launch_typed<uint16_t, kMaxRu>(a, M, s, e0, e1);
 }
 
 }  // namespace salt

@@ -630,8 +630,27 @@ salt_status salt_plan_download(salt_ctx* ctx, const salt_plan* plan, void* strea
   return SALT_OK;
 }
 
+namespace {
+salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y, void* stream,
+                       hipEvent_t e0, hipEvent_t e1);
+}  // namespace
+
 salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y,
                        void* stream) {
+  return apply_impl(ctx, table, plan, x, y, stream, nullptr, nullptr);
+}
+
+salt_status salt_apply_timed(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y,
+                             void* stream, void* start_event, void* stop_event) {
+  if (!start_event || !stop_event) return fail(ctx, SALT_ERR_INVALID_ARG, "null event");
+  return apply_impl(ctx, table, plan, x, y, stream, (hipEvent_t)start_event, (hipEvent_t)stop_event);
+}
+
+}  // extern "C"
+
+namespace {
+salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y, void* stream,
+                       hipEvent_t e0, hipEvent_t e1) {
   if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
   if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
   if (table < 0 || table >= ctx->cfg.n_tables)
@@ -731,11 +750,11 @@ salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
     a.pb = plan->dev;
     plan->build_pending = false;
   }
-  SALT_HIP(ctx, salt::launch_apply(a, ctx->cfg.dtype == SALT_BF16, M, s));
+  SALT_HIP(ctx, salt::launch_apply(a, ctx->cfg.dtype == SALT_BF16, M, s, e0, e1));
   int64_t seq;
   SALT_HIP(ctx, ring_record(ctx->readers, s, &seq));
   for (int slot : plan->slots) ctx->slot_reader[slot] = seq;
   return SALT_OK;
 }
 
-}  // extern "C"
+}  // namespace

@@ -26,7 +26,8 @@ EXPORTS = (
     "salt_create", "salt_destroy", "salt_pin_centroids", "salt_residual_bytes",
     "salt_residual_bytes_for", "salt_load_residual", "salt_wait_loads", "salt_host_alloc",
     "salt_host_free", "salt_plan_create", "salt_plan_destroy", "salt_plan_set_maps",
-    "salt_plan_build", "salt_plan_download", "salt_plan_errors", "salt_apply", "salt_status_str",
+    "salt_plan_build", "salt_plan_download", "salt_plan_errors", "salt_apply", "salt_apply_timed",
+    "salt_status_str",
     "salt_last_error", "salt_version",
 )
 
@@ -68,6 +69,7 @@ def _load() -> C.CDLL:
         "salt_plan_download": (C.c_int, [P, P, VP, IP, IP, IP, IP, IP, IP, IP]),
         "salt_plan_errors": (C.c_int, [P, P, VP, IP]),
         "salt_apply": (C.c_int, [P, I32, P, VP, VP, VP]),
+        "salt_apply_timed": (C.c_int, [P, I32, P, VP, VP, VP, VP, VP]),
         "salt_status_str": (C.c_char_p, [C.c_int]),
         "salt_last_error": (C.c_char_p, [P]),
         "salt_version": (I32, []),
@@ -214,6 +216,12 @@ class Context:
 
     def apply_status(self, table: int, plan: "Plan", x_ptr: int, y_ptr: int, stream: int = 0) -> int:
         return lib.salt_apply(self.h, table, plan.h, x_ptr, y_ptr, stream)
+
+    def apply_timed(self, table: int, plan: "Plan", x_ptr: int, y_ptr: int, stream: int, start_event: int,
+                    stop_event: int):
+        """``apply`` whose two HIP events record the kernel's own start and end."""
+        self._check(lib.salt_apply_timed(self.h, table, plan.h, x_ptr, y_ptr, stream, start_event, stop_event),
+                    "salt_apply_timed")
 
 
 class Plan:

@@ -242,3 +242,31 @@ def test_prefill_full_size_sampled():
             _check(run, t, rows=rows)
     finally:
         run.close()
+
+
+def test_timed_apply_matches_apply_and_times_the_kernel():
+    """salt_apply_timed runs the same apply (bit-identical in the deterministic
+    mode); its events bracket the kernel."""
+    _announce("salt_apply_timed on q_proj decode")
+    from paper_2608_03579_amd import hip
+    from tests.gpu_harness import to_dev
+    w = synth.make(2, 11, y0="normal")
+    run = Run(w, deterministic=True)
+    try:
+        run.set_and_build()
+        want = run.apply(0)
+        xd, yd = to_dev(w.x(0)), to_dev(w.y0(0))
+        e0, e1 = hip.Event(), hip.Event()
+        run.ctx.apply_timed(0, run.plan, xd.ptr, yd.ptr, run.stream, e0.h, e1.h)
+        run._stream.synchronize()
+        assert np.array_equal(yd.to_host(), want)
+        ms = e0.elapsed_ms(e1)
+        assert 0.0 < ms < 100.0, ms
+        assert run.plan.errors(run.stream) == 0
+        from paper_2608_03579_amd import salt
+        assert salt.lib.salt_apply_timed(run.ctx.h, 0, run.plan.h, xd.ptr, yd.ptr, run.stream, None, e1.h) \
+            == salt.ERR_INVALID_ARG
+        e0.destroy()
+        e1.destroy()
+    finally:
+        run.close()
