@@ -34,6 +34,7 @@ struct PlanBuffers {
   int32_t* meta;      // [kMetaWords]
   uint32_t* counter;  // [64] arrival counter of the multi-block plan build
   float* partials;    // [partial_cap] split-K partial sums of the shrink
+  char* sink;         // [kSinkBytes] target of the y stores of lanes with nothing to write (never read)
   size_t partial_cap; // floats
   size_t tile_cap;    // int4 entries
   int32_t tiles_max;  // entries of arrive
@@ -46,8 +47,23 @@ struct PlanArgs {
   int32_t reset_ready;  // 1: zero every ready word (the plan's epochs restart)
 };
 
-// Everything one apply launch needs, passed by value.
-struct ApplyArgs {
+// Everything one apply launch needs, passed by value.  The first 64 bytes hold
+// what every block reads before its first data load (its role, its tile and
+// where the tile's tokens come from), so that they arrive in one scalar
+// cache line.
+struct alignas(64) ApplyArgs {
+  int32_t n_tiles, S;       // tiles; K ranges of the shrink (split-K)
+  int32_t n_col;            // expand blocks per tile
+  int32_t fused_plan;       // 1: this launch also builds the plan (T <= kPlanFusedT)
+  int32_t writer;           // block that writes the plan (fused_plan), else -1
+  int32_t T;
+  const int4* tiles;        // tile records of a built plan
+  const int4* maps;         // staged maps (c, u, r, gamma bits) by token (fused_plan)
+  int32_t Kc;               // K range length of one shrink block
+  int32_t cpb;              // kNC-column chunks per expand block
+  int32_t atomic_sum;       // 1: split partials are added into v with device atomics
+  int32_t two_pass;         // 1: a shrink launch stores split partials, an expand launch sums them
+  int32_t in_dim, out_dim, r_c, r_u_max, R;
   const void* x;            // [T][in]
   void* y;                  // [T][out]
   const void* cent_at;      // [C][r_c][in]  centroid A, transposed
@@ -55,32 +71,41 @@ struct ApplyArgs {
   const char* pool;         // residual slot pool
   size_t slot_stride;       // bytes between slots
   int64_t tab_prefix;       // sum of (in + out) over earlier tables (elements per rank)
-  const int4* tiles;
   float* partials;          // [S][T][R] (ordered sums only)
   float* v;                 // [T][R] v of this apply, centroid part not yet scaled by gamma
   float* v_clear;           // v buffer of the next apply: rows [0, clear_rows) cleared here (atomic sums only)
   int32_t clear_rows;       // >= T
+  uint32_t target;          // arrival count of every tile once this apply's shrink is done
+  uint32_t epoch;           // 1, 2, ... per apply of the plan since its build
   uint32_t* arrive;
   uint32_t* ready;
   int32_t* meta;
-  uint32_t target;          // arrival count of every tile once this apply's shrink is done
-  uint32_t epoch;           // 1, 2, ... per apply of the plan since its build
-  int32_t T, in_dim, out_dim, r_c, r_u_max, R;
-  int32_t n_tiles, S, Kc;
-  int32_t n_col;            // expand blocks per tile
-  int32_t cpb;              // kNC-column chunks per expand block
-  int32_t atomic_sum;       // 1: split partials are added into v with device atomics
-  int32_t fused_plan;       // 1: this launch also builds the plan (T <= kPlanFusedT)
+  char* sink;               // kSinkBytes that absorb the y stores of lanes with nothing to write
   PlanBuffers pb;           // the plan's buffers (fused_plan only)
 };
+static_assert(offsetof(ApplyArgs, maps) + sizeof(void*) <= 64, "the fields a block reads first share one 64-byte line");
 
 hipError_t kernels_init(int device);
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 // e0 / e1: if set, HIP events that record the apply kernel's own start and end.
 hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+// Blocks of the two-launch apply's shrink and expand kernels one compute unit
+// holds at once (bf16, r_u_max <= 2).
+hipError_t two_pass_occupancy(int r_c, int r_u_max, int R, int* shrink_per_cu, int* expand_per_cu);
 
 // Columns of y per expand chunk.
 constexpr int kNC = 128;
+// Sink for the y stores of lanes past the tile or past out_dim: one 32-byte
+// slot per thread of a block.  An expand issues the same stores on every path,
+// so its waits on outstanding memory operations count them exactly.
+constexpr int kSinkBytes = 256 * 32;
+// Tokens per tile of the two-launch apply (large batches).
+constexpr int kTwoPassM = 64;
+// 16-rank blocks of the centroid a lane holds for rank r_c: r_c <= 16 * nbm.
+constexpr int centroid_blocks(int r_c) { return r_c <= 32 ? 2 : (r_c <= 64 ? 4 : 8); }
+// Row stride (bf16 elements) of the expand's bf16 copies of v's centroid part:
+// 32-rank MFMA steps plus 8 elements of padding.
+constexpr int expand_vs(int nbm) { return (nbm + 1) / 2 * 32 + 8; }
 // Batches a single plan block sorts in LDS, and batches an apply launch plans
 // for itself.
 constexpr int kPlanSmallT = 1024;
@@ -101,9 +126,10 @@ constexpr int kReadyStride = 16;
 constexpr int kReadyPerTile = kMaxSplit * kReadyStride;
 
 // 32-wide K steps whose loads a shrink wave issues together: about 96 VGPRs of
-// operands (x, nbm A_c rows, ru A_u rows per step, vec_regs registers each).
-constexpr int shrink_batch(int vec_regs, int nbm, int ru) {
-  const int u = 96 / (vec_regs * (1 + nbm + ru));
+// operands (per step: x and ru A_u rows for each of its mbw M-blocks, nbm A_c
+// rows; vec_regs registers each).
+constexpr int shrink_batch(int vec_regs, int mbw, int nbm, int ru) {
+  const int u = 96 / (vec_regs * (mbw + nbm + mbw * ru));
   return u < 1 ? 1 : (u > 4 ? 4 : u);
 }
 // Largest supported ranks.

@@ -43,7 +43,6 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 constexpr uint32_t kSpinMax = 1u << 24;   // ~0.5 s of polling before giving up
 constexpr int kYS = kNC + 4;              // LDS row stride of the expand's y tile (floats)
-constexpr int kVS = kMaxRc + 8;           // LDS row stride of the bf16 v operands (elements)
 
 // ---------------------------------------------------------------------------
 // element types: bf16 (uint16 storage) and fp32, 8 elements per vector
@@ -51,12 +50,13 @@ constexpr int kVS = kMaxRc + 8;           // LDS row stride of the bf16 v operan
 __device__ __forceinline__ float bf_lo(uint32_t w) { return __uint_as_float(w << 16); }
 __device__ __forceinline__ float bf_hi(uint32_t w) { return __uint_as_float(w & 0xffff0000u); }
 
-// fp32 -> bf16 bits, round to nearest even (NaN stays a quiet NaN).
-__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (u >> 16) | 0x40u;
-  return (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+// fp32 -> bf16, round to nearest even: gfx950's packed conversion
+// (v_cvt_pk_bf16_f32), two values per instruction; `lo` lands in the low half.
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2){lo, hi}, bf16x2));
 }
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) { return pack_bf16x2(f, 0.f) & 0xffffu; }
 
 template <typename E>
 struct Ops;
@@ -74,10 +74,10 @@ struct Ops<uint16_t> {
   }
   static __device__ __forceinline__ void store(uint16_t* p, const float* f) {
     uint4 w;
-    w.x = f32_to_bf16_rne(f[0]) | (f32_to_bf16_rne(f[1]) << 16);
-    w.y = f32_to_bf16_rne(f[2]) | (f32_to_bf16_rne(f[3]) << 16);
-    w.z = f32_to_bf16_rne(f[4]) | (f32_to_bf16_rne(f[5]) << 16);
-    w.w = f32_to_bf16_rne(f[6]) | (f32_to_bf16_rne(f[7]) << 16);
+    w.x = pack_bf16x2(f[0], f[1]);
+    w.y = pack_bf16x2(f[2], f[3]);
+    w.z = pack_bf16x2(f[4], f[5]);
+    w.w = pack_bf16x2(f[6], f[7]);
     *reinterpret_cast<uint4*>(p) = w;
   }
   // acc + sum_e a[e] * b[e], products exact in fp32
@@ -494,14 +494,17 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_large(PlanArgs a) {
   if (tid == 0) __hip_atomic_store(b.counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// One tile of a batch of T <= kPlanFusedT tokens, cut straight from the maps by
-// an apply block that plans for itself.  Groups are the centroid ids in order
-// (-1 first), so a per-id token count and its prefix sums give every group's
-// first sorted position and first tile; only the tokens of the block's own
-// group are then ranked, by counting the smaller keys of that group.
+// One tile of a batch of T <= kPlanFusedT tokens (one token per thread), cut
+// straight from the maps by an apply block that plans for itself.  Groups are the
+// centroid ids in order (-1 first), so a per-id token count and its prefix sums
+// give every group's first position and first tile.  Inside its group a token's
+// place is its rank in batch order (ballots): the apply needs each tile to hold
+// tokens of one centroid, not the canonical slot order within the group, which the
+// plan written by the launch's last block keeps.
+static_assert(kPlanFusedT <= kPlanThreads, "one token per thread of an apply block");
 struct TileLds {
-  uint64_t key[kPlanFusedT];   // plan key by token
   int cnt[80];                 // tokens per centroid id + 1 (0 .. 64)
+  int wcnt[kPlanThreads / 64]; // tokens of the block's group in each wave
   int4 hdr;                    // (i0, n, c, c + 1) of the block's tile
   int chunk;                   // the tile is chunk `chunk` of its group
   int n_tiles;
@@ -511,19 +514,14 @@ struct TileLds {
 // false (for the whole block) if the batch does not cut into n_tiles tiles.
 __device__ __forceinline__ bool tile_from_maps(const int4* maps, int T, int M, int tau, int n_tiles, TileLds& L,
                                                int4* s_tile) {
-  const int tid = threadIdx.x, lane = tid & 63;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   int4 m = make_int4(0, 0, 0, 0);
   if (tid < T) m = maps[tid];
   if (tid < 80) L.cnt[tid] = 0;
   // every record starts as padding, so none is ever left unset
   if (tid < M) s_tile[1 + tid] = make_int4(0, -1, 0, 0);
   __syncthreads();
-  uint64_t key = kNoKey;
-  if (tid < T) {
-    key = plan_key(m.x, m.y, tid);
-    L.key[tid] = key;
-    atomicAdd(&L.cnt[m.x + 1], 1);
-  }
+  if (tid < T) atomicAdd(&L.cnt[m.x + 1], 1);
   __syncthreads();
   if (tid < 64) {
     // lane l: centroid id l; id 64 (c = 63) follows lane 63
@@ -557,14 +555,13 @@ __device__ __forceinline__ bool tile_from_maps(const int4* maps, int T, int M, i
   __syncthreads();
   if (L.n_tiles != n_tiles) return false;
   const int4 h = L.hdr;
-  if (tid < T && m.x + 1 == h.w) {
-    const uint64_t lo = uint64_t(uint32_t(h.w)) << 42;
-    int r = 0;
-#pragma unroll 8
-    for (int i = 0; i < T; ++i) {
-      const uint64_t o = L.key[i];
-      r += (o >= lo && o < key) ? 1 : 0;
-    }
+  const bool mine = tid < T && m.x + 1 == h.w;
+  const uint64_t bal = __ballot(mine);
+  if (lane == 0) L.wcnt[wave] = __popcll(bal);
+  __syncthreads();
+  if (mine) {
+    int r = (int)__builtin_amdgcn_mbcnt_hi((uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+    for (int w = 0; w < wave; ++w) r += L.wcnt[w];
     r -= L.chunk * M;
     if (r >= 0 && r < h.y) s_tile[1 + r] = make_int4(tid, m.y, m.z, m.w);
   }
@@ -648,112 +645,223 @@ __device__ __forceinline__ float4 scale_centroid(float4 v, int idx, int R, int r
 }
 
 // Shrink block: tile `tau`, K range `s` of the apply.  Computes the tile's
-// split-K partial sums P[s][token][0 : r_c + r_u_max]; adds them into v with
-// atomics (default) or stores them for an ordered sum (deterministic mode), and
-// counts its arrival.  With one K range it stores v directly.
-template <typename E, int MB, int RU, int NBM>
+// split-K partial sums P[s][token][0 : r_c + r_u_max].  In the single-launch
+// apply it adds them into v with atomics (default) or stores them for an
+// ordered sum (deterministic mode), and counts its arrival; with one K range it
+// stores v directly.  In the two-launch apply it stores them for the expand
+// launch, which sums the K ranges in order.
+// Wave layout: each wave covers MBW of the tile's MB 16-token M-blocks and
+// 1/KW of the K range (KW = 4 * MBW / MB waves along K).  With MBW = MB every
+// wave holds all of the tile's tokens, so the centroid rows it loads serve
+// 16 * MB tokens.
+template <typename E, int MB, int MBW, int RU, int NBM>
 __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s, char* lds) {
   using O = Ops<E>;
   using Vec = typename O::Vec;
-  constexpr int M = 16 * MB, KW = 4 / MB;
-  constexpr int U0 = shrink_batch((int)(sizeof(Vec) / 4), NBM, RU) / 2;
+  static_assert(MB % MBW == 0 && 4 % (MB / MBW) == 0, "waves tile the M-blocks");
+  constexpr int M = 16 * MB, MG = MB / MBW, KW = 4 / MG;
+  constexpr int U0 = shrink_batch((int)(sizeof(Vec) / 4), MBW, NBM, RU) / 2;
   constexpr int U = U0 < 1 ? 1 : U0;            // steps per register buffer
+  constexpr int kStepRegs = (int)(sizeof(Vec) / 4) * (MBW + NBM + MBW * RU);   // VGPRs of one step's operands
   int4* s_tile = reinterpret_cast<int4*>(lds);
   float* s_part = reinterpret_cast<float*>(lds + tile_bytes(M));   // [KW][M][R]
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int i0 = s_tile[0].x, n = s_tile[0].y, c = s_tile[0].z;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int i0 = __builtin_amdgcn_readfirstlane(s_tile[0].x), n = __builtin_amdgcn_readfirstlane(s_tile[0].y),
+            c = __builtin_amdgcn_readfirstlane(s_tile[0].z);   // tile header: uniform
   const int R = a.R, in = a.in_dim, rc = a.r_c;
   const bool has_c = c >= 0 && rc > 0;
-  const int mb = wave % MB, kq = wave / MB;
-  const int tl = mb * 16 + (lane & 15);        // token of this lane within the tile
+  const int mg = wave % MG, kq = wave / MG;
   const int kseg = (lane >> 4) * 8;             // k offset of this lane inside a 32-wide step
-  const int4 tk = s_tile[1 + tl];
-  const bool tok_ok = tl < n;
-  const int ru = (tok_ok && tk.y >= 0) ? tk.z : 0;
-  const E* xrow = reinterpret_cast<const E*>(a.x) + (size_t)(tok_ok ? tk.x : 0) * in;
-  const E* au = ru ? reinterpret_cast<const E*>(a.pool + (size_t)tk.y * a.slot_stride) + (int64_t)ru * a.tab_prefix
-                   : xrow;
+  int tl[MBW], ru[MBW];                         // lane's token (within the tile) per M-block
+  bool tok_ok[MBW];
+  const E* xrow[MBW];
+  const E* au[MBW];
+#pragma unroll
+  for (int m = 0; m < MBW; ++m) {
+    tl[m] = (mg * MBW + m) * 16 + (lane & 15);
+    const int4 tk = s_tile[1 + tl[m]];
+    tok_ok[m] = tl[m] < n;
+    ru[m] = (tok_ok[m] && tk.y >= 0) ? tk.z : 0;
+    xrow[m] = reinterpret_cast<const E*>(a.x) + (size_t)(tok_ok[m] ? tk.x : 0) * in;
+    // rank-0 tokens read x's first row instead (a base the compiler cannot
+    // merge with the x load, which would make the x load wait)
+    const E* slot_a = reinterpret_cast<const E*>(a.pool + (size_t)(tk.y > 0 ? tk.y : 0) * a.slot_stride) +
+                      (int64_t)ru[m] * a.tab_prefix;
+    au[m] = ru[m] ? slot_a : reinterpret_cast<const E*>(a.x);
+  }
   const E* arow[NBM];                           // A_c^T row of this lane per 16-rank block
   bool aok[NBM];
 #pragma unroll
   for (int nb = 0; nb < NBM; ++nb) {
     const int j = nb * 16 + (lane & 15);
     aok[nb] = has_c && j < rc;
-    arow[nb] = reinterpret_cast<const E*>(a.cent_at) + ((size_t)(has_c ? c : 0) * rc + (aok[nb] ? j : 0)) * in;
+    // without a centroid term the (never multiplied) loads read the x row
+    arow[nb] = has_c ? reinterpret_cast<const E*>(a.cent_at) + ((size_t)c * rc + (aok[nb] ? j : 0)) * in : xrow[0];
   }
 
-  const int kw_len = a.Kc / KW;                 // a multiple of 32
-  const int kbeg = s * a.Kc + kq * kw_len;
-  const int kend = min(in, kbeg + kw_len);
+  // The block's K range is [kblk, kend), in 32-wide steps; the KW waves along K
+  // take its steps in turn (wave kq: steps kq, kq + KW, ...), so that at any
+  // time they read neighbouring pieces of the same x rows.
+  const int kblk = s * a.Kc;
+  const int kend = min(in, kblk + a.Kc);
+  const int nstep_blk = kend > kblk ? (kend - kblk) / 32 : 0;   // whole steps of the block
 
-  f32x4 acc[NBM];
+  f32x4 acc[MBW][NBM];
 #pragma unroll
-  for (int nb = 0; nb < NBM; ++nb) acc[nb] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float accu[RU];
+  for (int m = 0; m < MBW; ++m)
 #pragma unroll
-  for (int j = 0; j < RU; ++j) accu[j] = 0.f;
+    for (int nb = 0; nb < NBM; ++nb) acc[m][nb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float accu[MBW][RU];
+#pragma unroll
+  for (int m = 0; m < MBW; ++m)
+#pragma unroll
+    for (int j = 0; j < RU; ++j) accu[m][j] = 0.f;
 
-  // two register buffers of U steps each: the loads of batch b + 1 are in
-  // flight while batch b is multiplied
-  Vec xv[2][U], av[2][U][NBM], uv[2][U][RU];
-  auto load_batch = [&](Vec (&x_)[U], Vec (&a_)[U][NBM], Vec (&u_)[U][RU], int k0) {
+  // A_u row of rank j for this lane's token: a rank past the token's own reads
+  // its rank-0 row (or its x row) instead, so that every load of a whole step
+  // is unconditional; those sums are dropped when the partial is written.  In
+  // the same way rows past the tile's tokens read row 0 of x and ranks past
+  // r_c read rank 0 of the centroid: they only feed MFMA outputs that are
+  // never written.
+  const E* aurow[MBW][RU];
+#pragma unroll
+  for (int m = 0; m < MBW; ++m)
+#pragma unroll
+    for (int j = 0; j < RU; ++j) aurow[m][j] = au[m] + (size_t)(j < ru[m] ? j : 0) * in;
+
+  // two register buffers of up to U steps each: the loads of batch b + 1 are
+  // in flight while batch b is multiplied.  Every batch issues the same loads
+  // (a step past the wave's last, in a short last batch or a batch past the
+  // end, re-reads that last step and is not multiplied), so the wait before
+  // each multiply counts the loads exactly and never waits for the batch
+  // behind it.
+  Vec xv[2][U][MBW], av[2][U][NBM], uv[2][U][MBW][RU];
+  const int nfull = nstep_blk > kq ? (nstep_blk - kq + KW - 1) / KW : 0;   // this wave's whole steps
+  auto load_steps = [&](Vec (&x_)[U][MBW], Vec (&a_)[U][NBM], Vec (&u_)[U][MBW][RU], int step0) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int kk = k0 + 32 * u + kseg;
-      const bool kin = kk < kend;
-      x_[u] = (tok_ok && kin) ? O::load(xrow + kk) : O::zero();
+      const int kk = kblk + 32 * (kq + KW * (step0 + u < nfull ? step0 + u : nfull - 1)) + kseg;
 #pragma unroll
-      for (int nb = 0; nb < NBM; ++nb) a_[u][nb] = (aok[nb] && kin) ? O::load(arow[nb] + kk) : O::zero();
+      for (int m = 0; m < MBW; ++m) x_[u][m] = O::load(xrow[m] + kk);
 #pragma unroll
-      for (int j = 0; j < RU; ++j) u_[u][j] = (j < ru && kin) ? O::load(au + (size_t)j * in + kk) : O::zero();
+      for (int nb = 0; nb < NBM; ++nb) a_[u][nb] = O::load(arow[nb] + kk);
+#pragma unroll
+      for (int m = 0; m < MBW; ++m)
+#pragma unroll
+        for (int j = 0; j < RU; ++j) u_[u][m][j] = O::load(aurow[m][j] + kk);
     }
   };
-  auto mul_batch = [&](const Vec (&x_)[U], const Vec (&a_)[U][NBM], const Vec (&u_)[U][RU]) {
+  auto mul_steps = [&](const Vec (&x_)[U][MBW], const Vec (&a_)[U][NBM], const Vec (&u_)[U][MBW][RU], int ns) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      if (has_c) {
+      if (u < ns) {
+        if (has_c) {
 #pragma unroll
-        for (int nb = 0; nb < NBM; ++nb) acc[nb] = O::mma(x_[u], a_[u][nb], acc[nb]);
+          for (int m = 0; m < MBW; ++m)
+#pragma unroll
+            for (int nb = 0; nb < NBM; ++nb) acc[m][nb] = O::mma(x_[u][m], a_[u][nb], acc[m][nb]);
+        }
+#pragma unroll
+        for (int m = 0; m < MBW; ++m)
+#pragma unroll
+          for (int j = 0; j < RU; ++j) accu[m][j] = O::dot(x_[u][m], u_[u][m][j], accu[m][j]);
       }
-#pragma unroll
-      for (int j = 0; j < RU; ++j) accu[j] = O::dot(x_[u], u_[u][j], accu[j]);
     }
   };
-  const int nbat = (kend - kbeg + 32 * U - 1) / (32 * U);
-  if (nbat > 0) load_batch(xv[0], av[0], uv[0], kbeg);
-  for (int b = 0; b < nbat; b += 2) {
-    if (b + 1 < nbat) load_batch(xv[1], av[1], uv[1], kbeg + (b + 1) * 32 * U);
-    mul_batch(xv[0], av[0], uv[0]);
-    if (b + 1 < nbat) {
-      if (b + 2 < nbat) load_batch(xv[0], av[0], uv[0], kbeg + (b + 2) * 32 * U);
-      mul_batch(xv[1], av[1], uv[1]);
+  const int nbat = (nfull + U - 1) / U;
+  auto steps_of = [&](int b) { return min(U, nfull - b * U); };
+  if (nbat == 1) {
+    // one batch (short K ranges of small batches): nothing to overlap
+    load_steps(xv[0], av[0], uv[0], 0);
+    mul_steps(xv[0], av[0], uv[0], steps_of(0));
+  } else if (kStepRegs <= 128 && nbat == 2) {
+    // two batches: both in flight at once
+    load_steps(xv[0], av[0], uv[0], 0);
+    load_steps(xv[1], av[1], uv[1], U);
+    mul_steps(xv[0], av[0], uv[0], steps_of(0));
+    mul_steps(xv[1], av[1], uv[1], steps_of(1));
+  } else if constexpr (kStepRegs <= 128) {
+    if (nbat > 1) {
+      // (a peeled last pair would need a second set of accumulators)
+      load_steps(xv[0], av[0], uv[0], 0);
+      for (int b = 0; b < nbat; b += 2) {
+        load_steps(xv[1], av[1], uv[1], (b + 1) * U);
+        mul_steps(xv[0], av[0], uv[0], steps_of(b));
+        load_steps(xv[0], av[0], uv[0], (b + 2) * U);
+        if (b + 1 < nbat) mul_steps(xv[1], av[1], uv[1], steps_of(b + 1));
+      }
     }
+  } else {
+    // one step's operands alone fill most of the register file (fp32 with
+    // wide centroid and residual ranks): no second buffer
+    for (int b = 0; b < nbat; ++b) {
+      load_steps(xv[0], av[0], uv[0], b * U);
+      mul_steps(xv[0], av[0], uv[0], steps_of(b));
+    }
+  }
+  if (kend > kblk + 32 * nstep_blk && nstep_blk % KW == kq) {
+    // ragged end of the K range (in_dim not a multiple of 32), taken by the wave
+    // whose turn it is: k >= kend reads zero
+    const int kk = kblk + 32 * nstep_blk + kseg;
+    const bool kin = kk < kend;
+#pragma unroll
+    for (int m = 0; m < MBW; ++m) xv[0][0][m] = kin ? O::load(xrow[m] + kk) : O::zero();
+    if (has_c) {
+#pragma unroll
+      for (int nb = 0; nb < NBM; ++nb) av[0][0][nb] = kin ? O::load(arow[nb] + kk) : O::zero();
+    }
+#pragma unroll
+    for (int m = 0; m < MBW; ++m)
+#pragma unroll
+      for (int j = 0; j < RU; ++j) uv[0][0][m][j] = kin ? O::load(aurow[m][j] + kk) : O::zero();
+    mul_steps(xv[0], av[0], uv[0], 1);
   }
   // residual: lanes l, l^16, l^32, l^48 hold the four k offsets of one token
 #pragma unroll
-  for (int j = 0; j < RU; ++j) {
-    accu[j] += __shfl_xor(accu[j], 16);
-    accu[j] += __shfl_xor(accu[j], 32);
-  }
+  for (int m = 0; m < MBW; ++m)
+#pragma unroll
+    for (int j = 0; j < RU; ++j) {
+      accu[m][j] += __shfl_xor(accu[m][j], 16);
+      accu[m][j] += __shfl_xor(accu[m][j], 32);
+    }
   // this wave's partial -> LDS [kq][token][j]
   float* P = s_part + (size_t)kq * M * R;
 #pragma unroll
-  for (int nb = 0; nb < NBM; ++nb) {
-    const int j = nb * 16 + (lane & 15);
-    if (j < rc) {
+  for (int m = 0; m < MBW; ++m)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) P[(mb * 16 + 4 * (lane >> 4) + e) * R + j] = acc[nb][e];
+    for (int nb = 0; nb < NBM; ++nb) {
+      const int j = nb * 16 + (lane & 15);
+      if (j < rc) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) P[((mg * MBW + m) * 16 + 4 * (lane >> 4) + e) * R + j] = acc[m][nb][e];
+      }
     }
-  }
   if (lane < 16) {
 #pragma unroll
-    for (int j = 0; j < RU; ++j)
-      if (j < a.r_u_max) P[tl * R + rc + j] = accu[j];
-    for (int j = rc + a.r_u_max; j < R; ++j) P[tl * R + j] = 0.f;   // row padding
+    for (int m = 0; m < MBW; ++m) {
+#pragma unroll
+      for (int j = 0; j < RU; ++j)
+        if (j < a.r_u_max) P[tl[m] * R + rc + j] = j < ru[m] ? accu[m][j] : 0.f;
+      for (int j = rc + a.r_u_max; j < R; ++j) P[tl[m] * R + j] = 0.f;   // row padding
+    }
   }
   __syncthreads();
   // R is a multiple of 4: rows are whole float4 vectors
   const int nR4 = n * R / 4;
+  if (a.two_pass && !a.atomic_sum) {
+    // two-launch apply, ordered sums: this K range's partial for the expand launch
+    float4* dst = reinterpret_cast<float4*>(a.partials + ((size_t)s * a.T + i0) * R);
+    for (int i4 = tid; i4 < nR4; i4 += 256) {
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int q = 0; q < KW; ++q) {
+        const float4 p = *reinterpret_cast<const float4*>(s_part + (size_t)q * M * R + 4 * i4);
+        v.x += p.x; v.y += p.y; v.z += p.z; v.w += p.w;
+      }
+      dst[i4] = v;
+    }
+    return;
+  }
   const __amdgpu_buffer_rsrc_t rv = coherent_rsrc(a.v + (size_t)i0 * R, (uint32_t)(nR4 * 16));
   if (a.atomic_sum) {
     // the next apply of the plan adds into the other v buffer: split 0 clears
@@ -839,6 +947,8 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
       }
     }
   }
+  // the two-launch apply hands v over at the kernel boundary
+  if (a.two_pass) return;
   // atomic sums: this block's own ready word; ordered sums: the tile's one word
   publish_store(a.ready + (size_t)tau * kReadyPerTile + (a.atomic_sum ? s * kReadyStride : 0), a.epoch);
 }
@@ -859,31 +969,44 @@ struct ExpandRegs {
   Vec bu[ITEMS][RP > 0 ? RP : 1];
   Vec bct[NBW][KS];
 
+  // Unconditional loads: a row past the tile's tokens reads the tile's first
+  // token, a column past out_dim reads column 0 and a residual rank past the
+  // token's rank reads that token's y; none of those values is ever stored or
+  // added.  Centroid ranks past r_c are zeroed: they meet zero v entries in the
+  // MFMA, which must not see a non-finite table value.
   __device__ __forceinline__ void load(const ApplyArgs& a, const int4* s_tile, int n, bool has_c, int c, int n0) {
     using O = Ops<E>;
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int out = a.out_dim, rc = a.r_c;
+    const int tok0 = s_tile[1].x;
 #pragma unroll
     for (int it = 0; it < ITEMS; ++it) {
       const int idx = tid + 256 * it, t = idx / CG, col = n0 + (idx % CG) * 8;
       const int4 tk = s_tile[1 + t];
-      const bool ok = t < n && col < out;
+      const bool ok = t < n;
+      const int colc = col < out ? col : 0;
       const int ru = (ok && tk.y >= 0) ? tk.z : 0;
-      yold[it] = ok ? O::load(reinterpret_cast<const E*>(a.y) + (size_t)tk.x * out + col) : O::zero();
-      const E* bup = ru ? reinterpret_cast<const E*>(a.pool + (size_t)tk.y * a.slot_stride) +
-                              (int64_t)ru * (a.tab_prefix + a.in_dim)
-                        : nullptr;
+      const E* yp = reinterpret_cast<const E*>(a.y) + (size_t)(ok ? tk.x : tok0) * out + colc;
+      yold[it] = O::load(yp);
+      // rank-0 tokens read the first token's y row (a base the compiler cannot
+      // merge with yp, which would make the y load wait)
+      const E* slot_b = reinterpret_cast<const E*>(a.pool + (size_t)(tk.y > 0 ? tk.y : 0) * a.slot_stride) +
+                        (int64_t)ru * (a.tab_prefix + a.in_dim) + colc;
+      const E* bup = ru ? slot_b : reinterpret_cast<const E*>(a.y) + (size_t)tok0 * out + colc;
 #pragma unroll
-      for (int j = 0; j < RP; ++j) bu[it][j] = (j < ru) ? O::load(bup + (size_t)j * out + col) : O::zero();
+      for (int j = 0; j < RP; ++j) bu[it][j] = O::load(bup + (size_t)(j < ru ? j : 0) * out);
     }
-    const E* bt = reinterpret_cast<const E*>(a.cent_bt) + (size_t)(has_c ? c : 0) * out * rc;
+    // without a centroid term the (zeroed) operands read the first token's y
+    const E* bt = has_c ? reinterpret_cast<const E*>(a.cent_bt) + (size_t)c * out * rc : nullptr;
+    const E* safe = reinterpret_cast<const E*>(a.y) + (size_t)tok0 * out;
 #pragma unroll
     for (int w = 0; w < NBW; ++w) {
       const int col = n0 + (wave + 4 * w) * 16 + (lane & 15);
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) {
         const int j = ks * 32 + (lane >> 4) * 8;
-        bct[w][ks] = (has_c && col < out && j < rc) ? O::load(bt + (size_t)col * rc + j) : O::zero();
+        const Vec b = O::load(has_c ? bt + (size_t)(col < out ? col : 0) * rc + (j < rc ? j : 0) : safe);
+        bct[w][ks] = (has_c && j < rc) ? b : O::zero();
       }
     }
   }
@@ -902,38 +1025,166 @@ struct ExpandRegs {
   }
 };
 
-// Expand block: tile `tau`, column chunks [q * cpb, q * cpb + cpb) of kNC
-// columns each.  The first chunk's operands are loaded before the wait.
+// One chunk of an expand block: kNC columns of y for the tile's tokens, with
+// the operands already in `regs`.  Leaves s_y free for the next chunk.
 template <typename E, int MB, int RU, int NBM>
-__device__ __forceinline__ void expand_block(const ApplyArgs& a, int tau, int q, char* lds) {
+__device__ __forceinline__ void expand_chunk(const ApplyArgs& a, const ExpandRegs<E, MB, RU, NBM>& regs,
+                                             const int4* s_tile, const float* s_v, float* s_y,
+                                             const uint16_t* s_vh, const uint16_t* s_vl, int n, bool has_c,
+                                             int n0) {
   using O = Ops<E>;
   using Vec = typename O::Vec;
   using Regs = ExpandRegs<E, MB, RU, NBM>;
-  constexpr int M = Regs::M, CG = Regs::CG, ITEMS = Regs::ITEMS, RP = Regs::RP;
-  constexpr int NBW = Regs::NBW, KS = Regs::KS;
+  constexpr int CG = Regs::CG, ITEMS = Regs::ITEMS, RP = Regs::RP, NBW = Regs::NBW, KS = Regs::KS;
+  constexpr int VS = expand_vs(NBM);
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int R = a.R, out = a.out_dim, rc = a.r_c, in = a.in_dim;
+  // ---- centroid part on MFMA: y^T block [16 cols x 16 tokens] = B_c^T . v_c^T ----
+  if (has_c) {
+#pragma unroll
+    for (int w = 0; w < NBW; ++w) {
+      const int cb = (wave + 4 * w) * 16;       // first column of the block, local
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+        const int t = mb * 16 + (lane & 15);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const int j = ks * 32 + (lane >> 4) * 8;
+          if constexpr (sizeof(E) == 2) {
+            const uint4 hi = *reinterpret_cast<const uint4*>(s_vh + t * VS + j);
+            const uint4 lo = *reinterpret_cast<const uint4*>(s_vl + t * VS + j);
+            acc = O::mma(regs.bct[w][ks], hi, acc);
+            acc = O::mma(regs.bct[w][ks], lo, acc);
+          } else {
+            float vv[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) vv[e] = (j + e < rc) ? s_v[t * R + j + e] : 0.f;
+            acc = O::mma_f32rhs(regs.bct[w][ks], vv, acc);
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < 4; ++e) s_y[t * kYS + cb + 4 * (lane >> 4) + e] = acc[e];
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- residual part, add, round, store (lanes with nothing to write store
+  // to the sink, so that every path issues the same stores) ----
+#pragma unroll
+  for (int it = 0; it < ITEMS; ++it) {
+    const int idx = tid + 256 * it, t = idx / CG, cl = (idx % CG) * 8, col = n0 + cl;
+    const bool ok = t < n && col < out;
+    const int4 tk = s_tile[1 + t];
+    const int ru = tk.y >= 0 ? tk.z : 0;
+    float accv[8], yv[8];
+    if (has_c) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) accv[e] = s_y[t * kYS + cl + e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) accv[e] = 0.f;
+    }
+    const float* vt = s_v + t * R + rc;
+#pragma unroll
+    for (int j = 0; j < RU; ++j) {
+      if (j < ru) {
+        Vec bv;
+        if (j < RP) {
+          bv = regs.bu[it][j < RP ? j : 0];
+        } else {
+          const E* bup = reinterpret_cast<const E*>(a.pool + (size_t)tk.y * a.slot_stride) +
+                         (int64_t)ru * (a.tab_prefix + in);
+          bv = O::load(bup + (size_t)j * out + col);
+        }
+        float b8[8];
+        O::to_f32(bv, b8);
+        const float vj = vt[j];
+#pragma unroll
+        for (int e = 0; e < 8; ++e) accv[e] = fmaf(vj, b8[e], accv[e]);
+      }
+    }
+    O::to_f32(regs.yold[it], yv);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) yv[e] += accv[e];
+    E* dst = ok ? reinterpret_cast<E*>(a.y) + (size_t)tk.x * out + col : reinterpret_cast<E*>(a.sink + tid * 32);
+    O::store(dst, yv);
+  }
+  __syncthreads();                              // s_y consumed
+}
+
+// Expand block: tile `tau`, column chunks [q * cpb, q * cpb + cpb) of kNC
+// columns each.  Two register sets alternate between chunks: the first two
+// chunks' operands are loaded before the wait for v, and chunk k + 2 loads
+// while chunk k + 1 is computed.
+template <typename E, int MB, int RU, int NBM>
+__device__ __forceinline__ void expand_block(const ApplyArgs& a, int tau, int q, char* lds) {
+  using Regs = ExpandRegs<E, MB, RU, NBM>;
+  constexpr int M = Regs::M, KS = Regs::KS, VS = expand_vs(NBM);
   int4* s_tile = reinterpret_cast<int4*>(lds);
   float* s_v = reinterpret_cast<float*>(lds + tile_bytes(M));     // [M][R]
   float* s_y = s_v + (size_t)M * a.R;                             // [M][kYS]
-  // bf16: hi and lo halves of the centroid part of v, [M][kVS] each, built once
+  // bf16: hi and lo halves of the centroid part of v, [M][VS] each, built once
   uint16_t* s_vh = reinterpret_cast<uint16_t*>(s_y + (size_t)M * kYS);
-  uint16_t* s_vl = s_vh + (size_t)M * kVS;
+  uint16_t* s_vl = s_vh + (size_t)M * VS;
   __shared__ int s_flag;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int i0 = s_tile[0].x, n = s_tile[0].y, c = s_tile[0].z;
-  const int R = a.R, out = a.out_dim, rc = a.r_c, in = a.in_dim;
+  const int tid = threadIdx.x;
+  const int i0 = __builtin_amdgcn_readfirstlane(s_tile[0].x), n = __builtin_amdgcn_readfirstlane(s_tile[0].y),
+            c = __builtin_amdgcn_readfirstlane(s_tile[0].z);   // tile header: uniform
+  const int R = a.R, out = a.out_dim, rc = a.r_c;
   const bool has_c = c >= 0 && rc > 0;
   const int chunk0 = q * a.cpb;
+  const int nch = min(a.cpb, (out + kNC - 1) / kNC - chunk0);   // chunks of this block, >= 1
+  // operands of chunk k; a prefetch past the block's last chunk re-reads it
+  auto n0_of = [&](int k) { return (chunk0 + (k < nch ? k : nch - 1)) * kNC; };
 
-  Regs regs;
-  regs.load(a, s_tile, n, has_c, c, chunk0 * kNC);
-  regs.pin();
-
-  // ---- wait for the tile's v: the S ready words (atomic sums) or the one word ----
-  const bool ok = await_words(a.ready + (size_t)tau * kReadyPerTile, a.atomic_sum ? a.S : 1, a.epoch,
-                              a.meta + kMetaErr, &s_flag);
-  if (!ok) return;
-  {
-    const int nR4 = n * R / 4, MR4 = M * R / 4;
+  Regs ra, rb;
+  const int nR4 = n * R / 4, MR4 = M * R / 4;
+  if (a.two_pass) {
+    // two-launch apply: v is complete (kernel boundary).  Its loads go out
+    // first and the first two chunks' operands right behind them, so that
+    // filling s_v waits only for v.
+    constexpr int VQ = (M * padded_rank(16 * NBM, 2) / 4 + 255) / 256;   // float4s of v per thread
+    float4 vv[VQ];
+    if (a.atomic_sum) {
+      const float4* pv = reinterpret_cast<const float4*>(a.v + (size_t)i0 * R);
+#pragma unroll
+      for (int k = 0; k < VQ; ++k) {
+        const int i4 = tid + 256 * k;
+        vv[k] = i4 < nR4 ? pv[i4] : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    } else {
+      // ordered sums: the shrink launch's K-range partials, added in K order
+      const size_t split = (size_t)a.T * R / 4;   // float4s between K ranges
+      const float4* p = reinterpret_cast<const float4*>(a.partials + (size_t)i0 * R);
+#pragma unroll
+      for (int k = 0; k < VQ; ++k) {
+        const int i4 = tid + 256 * k;
+        vv[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (i4 < nR4)
+          for (int q = 0; q < a.S; ++q) {
+            const float4 t4 = p[(size_t)q * split + i4];
+            vv[k].x += t4.x; vv[k].y += t4.y; vv[k].z += t4.z; vv[k].w += t4.w;
+          }
+      }
+    }
+    ra.load(a, s_tile, n, has_c, c, n0_of(0));
+    if (nch > 1) rb.load(a, s_tile, n, has_c, c, n0_of(1));
+#pragma unroll
+    for (int k = 0; k < VQ; ++k) {
+      const int i4 = tid + 256 * k;
+      if (i4 < MR4) reinterpret_cast<float4*>(s_v)[i4] = scale_centroid(vv[k], 4 * i4, R, rc, s_tile);
+    }
+  } else {
+    ra.load(a, s_tile, n, has_c, c, n0_of(0));
+    if (nch > 1) rb.load(a, s_tile, n, has_c, c, n0_of(1));
+    ra.pin();
+    if (nch > 1) rb.pin();
+    // ---- wait for the tile's v: the S ready words (atomic sums) or the one word ----
+    const bool ok = await_words(a.ready + (size_t)tau * kReadyPerTile, a.atomic_sum ? a.S : 1, a.epoch,
+                                a.meta + kMetaErr, &s_flag);
+    if (!ok) return;
     const __amdgpu_buffer_rsrc_t rv = coherent_rsrc(a.v + (size_t)i0 * R, (uint32_t)(nR4 * 16));
     for (int i4 = tid; i4 < MR4; i4 += 256)   // past n rows: zeros
       reinterpret_cast<float4*>(s_v)[i4] = scale_centroid(load4_coherent(rv, 16u * i4), 4 * i4, R, rc, s_tile);
@@ -946,90 +1197,27 @@ __device__ __forceinline__ void expand_block(const ApplyArgs& a, int tau, int q,
       const int t = i / (KS * 32), j = i - t * (KS * 32);
       const float v = j < rc ? s_v[t * R + j] : 0.f;
       const uint32_t h = f32_to_bf16_rne(v);
-      s_vh[t * kVS + j] = (uint16_t)h;
-      s_vl[t * kVS + j] = (uint16_t)f32_to_bf16_rne(v - __uint_as_float(h << 16));
+      s_vh[t * VS + j] = (uint16_t)h;
+      s_vl[t * VS + j] = (uint16_t)f32_to_bf16_rne(v - __uint_as_float(h << 16));
     }
     __syncthreads();
   }
 
-  for (int cc = 0; cc < a.cpb; ++cc) {
-    const int n0 = (chunk0 + cc) * kNC;
-    if (n0 >= out) break;
-    if (cc > 0) {
-      regs.load(a, s_tile, n, has_c, c, n0);
-      __syncthreads();                          // s_y of the previous chunk fully consumed
-    }
-    // ---- centroid part on MFMA: y^T block [16 cols x 16 tokens] = B_c^T . v_c^T ----
-    if (has_c) {
-#pragma unroll
-      for (int w = 0; w < NBW; ++w) {
-        const int cb = (wave + 4 * w) * 16;     // first column of the block, local
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb) {
-          f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
-          const int t = mb * 16 + (lane & 15);
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks) {
-            const int j = ks * 32 + (lane >> 4) * 8;
-            if constexpr (sizeof(E) == 2) {
-              const uint4 hi = *reinterpret_cast<const uint4*>(s_vh + t * kVS + j);
-              const uint4 lo = *reinterpret_cast<const uint4*>(s_vl + t * kVS + j);
-              acc = O::mma(regs.bct[w][ks], hi, acc);
-              acc = O::mma(regs.bct[w][ks], lo, acc);
-            } else {
-              float vv[8];
-#pragma unroll
-              for (int e = 0; e < 8; ++e) vv[e] = (j + e < rc) ? s_v[t * R + j + e] : 0.f;
-              acc = O::mma_f32rhs(regs.bct[w][ks], vv, acc);
-            }
-          }
-#pragma unroll
-          for (int e = 0; e < 4; ++e) s_y[t * kYS + cb + 4 * (lane >> 4) + e] = acc[e];
-        }
-      }
-    }
-    __syncthreads();
-
-    // ---- residual part, add, round, store ----
-#pragma unroll
-    for (int it = 0; it < ITEMS; ++it) {
-      const int idx = tid + 256 * it, t = idx / CG, cl = (idx % CG) * 8, col = n0 + cl;
-      if (t >= n || col >= out) continue;
-      const int4 tk = s_tile[1 + t];
-      const int ru = tk.y >= 0 ? tk.z : 0;
-      float accv[8], yv[8];
-      if (has_c) {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) accv[e] = s_y[t * kYS + cl + e];
-      } else {
-#pragma unroll
-        for (int e = 0; e < 8; ++e) accv[e] = 0.f;
-      }
-      const float* vt = s_v + t * R + rc;
-#pragma unroll
-      for (int j = 0; j < RU; ++j) {
-        if (j < ru) {
-          Vec bv;
-          if (j < RP) {
-            bv = regs.bu[it][j < RP ? j : 0];
-          } else {
-            const E* bup = reinterpret_cast<const E*>(a.pool + (size_t)tk.y * a.slot_stride) +
-                           (int64_t)ru * (a.tab_prefix + in);
-            bv = O::load(bup + (size_t)j * out + col);
-          }
-          float b8[8];
-          O::to_f32(bv, b8);
-          const float vj = vt[j];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) accv[e] = fmaf(vj, b8[e], accv[e]);
-        }
-      }
-      O::to_f32(regs.yold[it], yv);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) yv[e] += accv[e];
-      O::store(reinterpret_cast<E*>(a.y) + (size_t)tk.x * out + col, yv);
-    }
+  // pairs of chunks while the next two exist (no conditional memory operation
+  // inside the loop), then the last one to three chunks (ra holds chunk cc,
+  // rb chunk cc + 1)
+  int cc = 0;
+  for (; cc + 3 < nch; cc += 2) {
+    expand_chunk(a, ra, s_tile, s_v, s_y, s_vh, s_vl, n, has_c, (chunk0 + cc) * kNC);
+    ra.load(a, s_tile, n, has_c, c, n0_of(cc + 2));
+    expand_chunk(a, rb, s_tile, s_v, s_y, s_vh, s_vl, n, has_c, (chunk0 + cc + 1) * kNC);
+    rb.load(a, s_tile, n, has_c, c, n0_of(cc + 3));
   }
+  const int rem = nch - cc;
+  expand_chunk(a, ra, s_tile, s_v, s_y, s_vh, s_vl, n, has_c, (chunk0 + cc) * kNC);
+  if (rem == 3) ra.load(a, s_tile, n, has_c, c, n0_of(cc + 2));
+  if (rem >= 2) expand_chunk(a, rb, s_tile, s_v, s_y, s_vh, s_vl, n, has_c, (chunk0 + cc + 1) * kNC);
+  if (rem == 3) expand_chunk(a, ra, s_tile, s_v, s_y, s_vh, s_vl, n, has_c, (chunk0 + cc + 2) * kNC);
 }
 
 // The plan a launch builds for itself, written out by its first block.
@@ -1059,12 +1247,12 @@ __global__ void __launch_bounds__(256) k_apply(ApplyArgs a) {
     // One extra block, the last, sorts the whole batch and writes the plan out
     // for later applies and plan queries; every other block cuts its own tile
     // from the maps.
-    if (b == (int)gridDim.x - 1) {
+    if (b == a.writer) {
       write_plan(a, M, *reinterpret_cast<PlanLds<kPlanFusedT>*>(lds));
       return;
     }
     auto& L = *reinterpret_cast<TileLds*>(lds + tile_bytes(M));
-    if (!tile_from_maps(a.pb.maps, a.T, M, tau, a.n_tiles, L, s_tile)) {
+    if (!tile_from_maps(a.maps, a.T, M, tau, a.n_tiles, L, s_tile)) {
       if (tid == 0) atomicAdd(a.meta + kMetaErr, 1);   // cannot happen: the host counts the same tiles
       return;
     }
@@ -1073,17 +1261,53 @@ __global__ void __launch_bounds__(256) k_apply(ApplyArgs a) {
     for (int k = tid; k < M + 1; k += 256) s_tile[k] = trec[k];
     __syncthreads();
   }
-  if (shrink) shrink_block<E, MB, RU, NBM>(a, tau, b / a.n_tiles, lds);
+  if (shrink) shrink_block<E, MB, 1, RU, NBM>(a, tau, b / a.n_tiles, lds);
   else expand_block<E, MB, RU, NBM>(a, tau, (b - n_shrink) / a.n_tiles, lds);
 }
 
-// fused_T: batch size of a launch that builds its plan, else 0
-size_t apply_lds(int M, int R, int fused_T) {
-  const size_t tb = (size_t)tile_bytes(M);
-  const size_t shrink = tb + sizeof(float) * 64 * (size_t)R;           // KW * M == 64
-  const size_t expand = tb + sizeof(float) * ((size_t)M * R + (size_t)M * kYS) + 2 * sizeof(uint16_t) * M * kVS;
-  const size_t plan = fused_T > 0 ? std::max(sizeof(PlanLds<kPlanFusedT>), tb + sizeof(TileLds)) : 0;
-  return std::max({shrink, expand, plan});
+// The two-launch apply of large batches (tiles of kTwoPassM tokens).  The
+// shrink launch: one block per (tile, K range); every wave covers all of the
+// tile's tokens.  Block ids run over tiles first.
+template <typename E, int MB, int RU, int NBM>
+__global__ void __launch_bounds__(256) k_shrink(ApplyArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  constexpr int M = 16 * MB;
+  const int b = blockIdx.x, tau = b % a.n_tiles;
+  int4* s_tile = reinterpret_cast<int4*>(lds);
+  const int4* trec = a.tiles + (size_t)tau * (M + 1);
+  for (int k = threadIdx.x; k < M + 1; k += 256) s_tile[k] = trec[k];
+  __syncthreads();
+  shrink_block<E, MB, MB, RU, NBM>(a, tau, b / a.n_tiles, lds);
+}
+
+// The expand launch: one block per (tile, range of cpb column chunks).
+template <typename E, int MB, int RU, int NBM>
+__global__ void __launch_bounds__(256) k_expand(ApplyArgs a) {
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  constexpr int M = 16 * MB;
+  const int b = blockIdx.x, tau = b % a.n_tiles;
+  int4* s_tile = reinterpret_cast<int4*>(lds);
+  const int4* trec = a.tiles + (size_t)tau * (M + 1);
+  for (int k = threadIdx.x; k < M + 1; k += 256) s_tile[k] = trec[k];
+  __syncthreads();
+  expand_block<E, MB, RU, NBM>(a, tau, b / a.n_tiles, lds);
+}
+
+// LDS of the block roles.  Shrink: tile records + the per-wave partials
+// [KW][M][R] (KW * M = 64 in the single launch, 4 * M in the two-launch one).
+size_t lds_shrink(int M, int R, int kw_m) {
+  return (size_t)tile_bytes(M) + sizeof(float) * (size_t)kw_m * R;
+}
+// Expand: tile records, v [M][R], the MFMA output [M][kYS] and the bf16 hi/lo
+// copies of v's centroid part [2][M][VS].
+size_t lds_expand(int M, int R, int nbm) {
+  return (size_t)tile_bytes(M) + sizeof(float) * ((size_t)M * R + (size_t)M * kYS) +
+         2 * sizeof(uint16_t) * (size_t)M * expand_vs(nbm);
+}
+// Single launch; fused_T: batch size of a launch that builds its plan, else 0.
+size_t apply_lds(int M, int R, int nbm, int fused_T) {
+  const size_t plan = fused_T > 0 ? std::max(sizeof(PlanLds<kPlanFusedT>), tile_bytes(M) + sizeof(TileLds)) : 0;
+  return std::max({lds_shrink(M, R, 64), lds_expand(M, R, nbm), plan});
 }
 
 // A launch; with events, they record the kernel's own start and end.
@@ -1096,15 +1320,28 @@ void launch_k(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, const 
 
 template <typename E, int RU, int NBM>
 hipError_t launch_nbm(const ApplyArgs& a, int M, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (a.two_pass) {
+    // shrink launch, then expand launch; the events bracket both
+    if constexpr (sizeof(E) == 2 && RU <= 2) {
+      if (M != kTwoPassM) return hipErrorInvalidValue;
+      constexpr int MB = kTwoPassM / 16;
+      launch_k(k_shrink<E, MB, RU, NBM>, dim3(a.n_tiles * a.S), dim3(256), lds_shrink(M, a.R, 4 * M), s, a, e0,
+               nullptr);
+      launch_k(k_expand<E, MB, RU, NBM>, dim3(a.n_tiles * a.n_col), dim3(256), lds_expand(M, a.R, NBM), s, a,
+               nullptr, e1);
+      return hipGetLastError();
+    } else {
+      return hipErrorInvalidValue;
+    }
+  }
   // n_col: column blocks of cpb chunks; one more block, the last, writes a plan
   // built in this launch
   const dim3 grid(a.n_tiles * (a.S + a.n_col) + a.fused_plan), block(256);
-  const size_t lds = apply_lds(M, a.R, a.fused_plan ? a.T : 0);
+  const size_t lds = apply_lds(M, a.R, NBM, a.fused_plan ? a.T : 0);
   if (M == 16) {
     launch_k(k_apply<E, 1, RU, NBM>, grid, block, lds, s, a, e0, e1);
   } else if constexpr (sizeof(E) == 2) {
     if (M == 32) launch_k(k_apply<E, 2, RU, NBM>, grid, block, lds, s, a, e0, e1);
-    else if (M == 64) launch_k(k_apply<E, 4, RU, NBM>, grid, block, lds, s, a, e0, e1);
     else return hipErrorInvalidValue;
   } else {
     return hipErrorInvalidValue;
@@ -1115,12 +1352,39 @@ hipError_t launch_nbm(const ApplyArgs& a, int M, hipStream_t s, hipEvent_t e0, h
 // NBM: 16-rank blocks of the centroid held per lane (r_c <= 16 * NBM)
 template <typename E, int RU>
 hipError_t launch_typed(const ApplyArgs& a, int M, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
-  if (a.r_c <= 32) return launch_nbm<E, RU, 2>(a, M, s, e0, e1);
-  if (a.r_c <= 64) return launch_nbm<E, RU, 4>(a, M, s, e0, e1);
-  return launch_nbm<E, RU, 8>(a, M, s, e0, e1);
+  switch (centroid_blocks(a.r_c)) {
+    case 2: return launch_nbm<E, RU, 2>(a, M, s, e0, e1);
+    case 4: return launch_nbm<E, RU, 4>(a, M, s, e0, e1);
+    default: return launch_nbm<E, RU, 8>(a, M, s, e0, e1);
+  }
+}
+
+template <int RU, int NBM>
+hipError_t two_pass_occ(int R, int* shrink_per_cu, int* expand_per_cu) {
+  constexpr int MB = kTwoPassM / 16;
+  hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+      shrink_per_cu, reinterpret_cast<const void*>(k_shrink<uint16_t, MB, RU, NBM>), 256,
+      lds_shrink(kTwoPassM, R, 4 * kTwoPassM));
+  if (e != hipSuccess) return e;
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(
+      expand_per_cu, reinterpret_cast<const void*>(k_expand<uint16_t, MB, RU, NBM>), 256,
+      lds_expand(kTwoPassM, R, NBM));
 }
 
 }  // namespace
+
+// Blocks of the two-launch apply's kernels that one compute unit holds at once.
+hipError_t two_pass_occupancy(int r_c, int r_u_max, int R, int* shrink_per_cu, int* expand_per_cu) {
+  const int nbm = centroid_blocks(r_c);
+  if (r_u_max <= 1) {
+    if (nbm == 2) return two_pass_occ<1, 2>(R, shrink_per_cu, expand_per_cu);
+    if (nbm == 4) return two_pass_occ<1, 4>(R, shrink_per_cu, expand_per_cu);
+    return two_pass_occ<1, 8>(R, shrink_per_cu, expand_per_cu);
+  }
+  if (nbm == 2) return two_pass_occ<2, 2>(R, shrink_per_cu, expand_per_cu);
+  if (nbm == 4) return two_pass_occ<2, 4>(R, shrink_per_cu, expand_per_cu);
+  return two_pass_occ<2, 8>(R, shrink_per_cu, expand_per_cu);
+}
 
 // Per-device set-up: checks that the device has the LDS the apply kernels may
 // ask for (gfx950: 160 KiB per workgroup; dynamic LDS needs no opt-in on AMD).
@@ -1131,7 +1395,10 @@ hipError_t kernels_init(int device) {
   int lds_max = 0;
   hipError_t e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, device);
   if (e != hipSuccess) return e;
-  if ((size_t)lds_max < apply_lds(64, kMaxRc + kMaxRu, kPlanFusedT) + 1024) return hipErrorInvalidConfiguration;
+  const size_t need = std::max({apply_lds(32, padded_rank(kMaxRc, kMaxRu), 8, kPlanFusedT),
+                                lds_shrink(kTwoPassM, padded_rank(kMaxRc, 2), 4 * kTwoPassM),
+                                lds_expand(kTwoPassM, padded_rank(kMaxRc, 2), 8)});
+  if ((size_t)lds_max < need + 1024) return hipErrorInvalidConfiguration;
   done[device] = true;
   return hipSuccess;
 }

@@ -71,6 +71,8 @@ struct salt_ctx {
   int64_t sum_io = 0;
   size_t esize = 2;
   int device = 0;
+  int n_cu = 256;                        // compute units of the device
+  int occ_shrink = 0, occ_expand = 0;    // blocks per compute unit of the two-launch kernels (0: not asked yet)
   // device memory
   std::vector<char*> cent_at, cent_b;    // per table
   std::vector<uint8_t> cent_pinned;      // per table x centroid
@@ -181,7 +183,8 @@ hipError_t ring_wait(EventRing& r, hipStream_t s, int64_t seq) {
 void free_plan_buffers(salt_plan* p) {
   PlanBuffers& b = p->dev;
   void* ptrs[] = {b.maps, b.perm, b.srt, b.srt_c, b.seg_off, b.seg_c, b.seg_u, b.grp_off,
-                  b.grp_tok, b.grp_c, b.tiles, b.arrive, b.ready, b.meta, b.counter, b.partials, b.v};
+                  b.grp_tok, b.grp_c, b.tiles, b.arrive, b.ready, b.meta, b.counter, b.partials, b.v,
+                  b.sink};
   for (void* q : ptrs)
     if (q) (void)hipFree(q);
   if (p->staging) (void)hipHostFree(p->staging);
@@ -298,6 +301,8 @@ salt_status salt_create(const salt_config* cfg, salt_ctx** out) {
   if (e != hipSuccess) return bail(SALT_ERR_HIP, e, "hipSetDevice");
   e = salt::kernels_init(cfg->device);
   if (e != hipSuccess) return bail(SALT_ERR_HIP, e, "kernels_init");
+  e = hipDeviceGetAttribute(&c->n_cu, hipDeviceAttributeMultiprocessorCount, cfg->device);
+  if (e != hipSuccess) return bail(SALT_ERR_HIP, e, "hipDeviceGetAttribute");
   const size_t C = (size_t)cfg->n_centroids, rc = (size_t)cfg->r_c;
   c->cent_at.assign(cfg->n_tables, nullptr);
   c->cent_b.assign(cfg->n_tables, nullptr);
@@ -452,6 +457,7 @@ salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out) {
             hipMalloc((void**)&b.meta, salt::kMetaWords * 4) == hipSuccess &&
             hipMalloc((void**)&b.counter, 64 * 4) == hipSuccess &&
             hipMalloc((void**)&b.partials, b.partial_cap * 4) == hipSuccess &&
+            hipMalloc((void**)&b.sink, salt::kSinkBytes) == hipSuccess &&
             hipHostMalloc((void**)&p->staging, T * sizeof(int4), hipHostMallocDefault) == hipSuccess;
   if (!ok) {
     (void)hipGetLastError();
@@ -541,6 +547,10 @@ salt_status salt_plan_set_maps(salt_ctx* ctx, salt_plan* plan, int32_t T, const 
     }
   const double mean = n_groups ? (double)T / n_groups : 0.0;
   plan->M = (ctx->cfg.dtype == SALT_F32 || mean <= 24.0) ? 16 : 32;
+  // large bf16 batches with long centroid groups and residual rank <= 2: the
+  // two-launch apply with 64-token tiles (bandwidth bound; no in-launch hand-off)
+  if (ctx->cfg.dtype == SALT_BF16 && T > salt::kPlanFusedT && ctx->cfg.r_u_max <= 2 && mean >= 96.0)
+    plan->M = salt::kTwoPassM;
   int n_tiles = 0;
   for (int g = 0; g <= C; ++g) n_tiles += (per_c[g] + plan->M - 1) / plan->M;
   plan->n_tiles = n_tiles;
@@ -694,6 +704,7 @@ salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
   a.arrive = plan->dev.arrive;
   a.ready = plan->dev.ready;
   a.meta = plan->dev.meta;
+  a.sink = plan->dev.sink;
   a.T = T;
   a.in_dim = sh.in_dim;
   a.out_dim = sh.out_dim;
@@ -701,6 +712,54 @@ salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
   a.r_u_max = ctx->cfg.r_u_max;
   a.R = salt::padded_rank(a.r_c, a.r_u_max);
   a.n_tiles = plan->n_tiles;
+  if (plan->M == salt::kTwoPassM) {
+    // Two launches, each sized to what the device holds at once (one round of
+    // blocks).  Shrink: (tile, K range) blocks, K ranges a multiple of 4 waves x
+    // 32.  Expand: (tile, column range) blocks, each streaming its chunks two
+    // at a time.
+    if (!ctx->occ_shrink) {
+      SALT_HIP(ctx, salt::two_pass_occupancy(a.r_c, a.r_u_max, a.R, &ctx->occ_shrink, &ctx->occ_expand));
+      ctx->occ_shrink = std::max(1, ctx->occ_shrink);
+      ctx->occ_expand = std::max(1, ctx->occ_expand);
+    }
+    const bool atomic = atomic_sums(ctx);
+    const int gran = 128;
+    int S = (int)std::max<int64_t>(1, (int64_t)ctx->occ_shrink * ctx->n_cu / a.n_tiles);
+    S = std::min({S, 8, (sh.in_dim + gran - 1) / gran});
+    while (!atomic && S > 1 && (size_t)S * T * a.R > plan->dev.partial_cap) --S;
+    a.Kc = ((sh.in_dim + S - 1) / S + gran - 1) / gran * gran;
+    a.S = (sh.in_dim + a.Kc - 1) / a.Kc;
+    const int chunks = (sh.out_dim + salt::kNC - 1) / salt::kNC;
+    const int n_col = (int)std::min<int64_t>(
+        chunks, std::max<int64_t>(1, (int64_t)ctx->occ_expand * ctx->n_cu / a.n_tiles));
+    a.cpb = (chunks + n_col - 1) / n_col;
+    a.n_col = (chunks + a.cpb - 1) / a.cpb;
+    a.two_pass = 1;
+    a.fused_plan = 0;
+    a.writer = -1;
+    a.maps = plan->dev.maps;
+    a.partials = plan->dev.partials;
+    a.atomic_sum = atomic ? 1 : 0;
+    a.epoch = ++plan->epoch;
+    a.clear_rows = T;
+    if (atomic) {
+      // the same alternating v buffers as the single-launch atomic sums
+      const int p = (int)(a.epoch & 1u), q = p ^ 1;
+      a.v = plan->dev.v + (size_t)p * plan->dev.v_stride;
+      a.v_clear = plan->dev.v + (size_t)q * plan->dev.v_stride;
+      a.clear_rows = std::max(T, plan->v_dirty[q]);
+      plan->v_dirty[q] = 0;
+      plan->v_dirty[p] = T;
+    } else {
+      a.v = plan->dev.v;
+      a.v_clear = nullptr;
+    }
+    SALT_HIP(ctx, salt::launch_apply(a, 1, salt::kTwoPassM, s, e0, e1));
+    int64_t seq;
+    SALT_HIP(ctx, ring_record(ctx->readers, s, &seq));
+    for (int slot : plan->slots) ctx->slot_reader[slot] = seq;
+    return SALT_OK;
+  }
   // K split.  Small (decode) batches are latency bound: spread the shrink input
   // over many blocks (~16 KiB each) so no CU streams much more than its share,
   // and let partial traffic reach half of the input.  Large (prefill) batches
@@ -717,14 +776,26 @@ salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
   const bool atomic = atomic_sums(ctx);
   const int s_reduce = atomic ? salt::kMaxSplit : std::max(1, (int)(65536 / ((size_t)M * a.R * 4)));
   int S = std::max(1, std::min({s_bytes, s_traffic, s_reduce, salt::kMaxSplit, (sh.in_dim + gran - 1) / gran}));
+  if (small) {
+    // at most two register batches of U steps per wave (U as the kernel picks
+    // it), so that the shrink loop runs straight through with every load in flight
+    const int ru_t = a.r_u_max <= 1 ? 1 : (a.r_u_max <= 2 ? 2 : salt::kMaxRu);
+    const int U = std::max(1, salt::shrink_batch(ctx->esize == 2 ? 4 : 8, 1, salt::centroid_blocks(a.r_c), ru_t) / 2);
+    const int s_steps = (sh.in_dim + 2 * U * gran - 1) / (2 * U * gran);
+    S = std::max(S, std::min({s_steps, salt::kMaxSplit, (sh.in_dim + gran - 1) / gran}));
+  }
   while (S > 1 && (size_t)S * T * a.R > plan->dev.partial_cap) --S;
   const int Kc = ((sh.in_dim + S - 1) / S + gran - 1) / gran * gran;
   a.Kc = Kc;
   a.S = (sh.in_dim + Kc - 1) / Kc;   // <= S
-  // expand: several kNC-column chunks per block when there are blocks to spare,
-  // so one block reads the tile's v once for more columns
+  // expand: one kNC-column chunk per block while the launch fits the device
+  // at about four blocks per compute unit; past that, each block streams several
+  // chunks (two in flight), so that the expand blocks left beside the shrink
+  // blocks are all resident and load their first chunks before v is ready
   const int chunks = (sh.out_dim + salt::kNC - 1) / salt::kNC;
-  a.cpb = std::max(1, std::min(4, (a.n_tiles * chunks) / 1024));
+  const int64_t n_exp = std::max<int64_t>({(int64_t)a.n_tiles, 4 * (int64_t)ctx->n_cu - (int64_t)a.n_tiles * a.S,
+                                           2 * (int64_t)ctx->n_cu});
+  a.cpb = (int)std::max<int64_t>(1, ((int64_t)a.n_tiles * chunks + n_exp - 1) / n_exp);
   a.n_col = (chunks + a.cpb - 1) / a.cpb;
   if (!atomic && a.S > 1) plan->arrivals += (uint32_t)a.S;
   a.target = plan->arrivals;
@@ -746,8 +817,11 @@ salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
     a.v_clear = nullptr;
   }
   a.fused_plan = fused_plan ? 1 : 0;
+  a.writer = -1;
+  a.maps = plan->dev.maps;
   if (fused_plan) {
     a.pb = plan->dev;
+    a.writer = a.n_tiles * (a.S + a.n_col);   // one block past the apply's own
     plan->build_pending = false;
   }
   SALT_HIP(ctx, salt::launch_apply(a, ctx->cfg.dtype == SALT_BF16, M, s, e0, e1));

@@ -1,0 +1,137 @@
+"""GPU parity of the two-launch apply (large bf16 batches, 64-token tiles).
+
+libsalt serves a bf16 batch of more than 256 tokens whose centroid groups hold
+96 tokens or more on average, with residual rank <= 2, in two launches: a shrink
+launch whose split-K partial sums are added into v with fp32 atomics (or, with
+SALT_DETERMINISTIC, stored and summed in K order by the expand launch) and an
+expand launch that reads v and updates y.  These batches are built to take that
+path and to reach its corners: centroid ranks 32 / 64 / 128 (2, 4 and 8 blocks of 16 ranks), residual ranks
+0 / 1 / 2 mixed, tokens without a centroid or without a residual, ragged K and
+output widths (not multiples of the 128-wide K ranges or column chunks),
+ragged last tiles of every group, gamma bins, y0 ~ N(0, 1), and an integer
+variant that must be bit-exact.  Expected values come from the CPU oracle on the
+same seeded inputs.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_03579_amd import synth
+from tests.gpu_harness import TOL_NORTH_STAR, Run, close_enough
+
+pytestmark = pytest.mark.gpu
+
+
+def _announce(name):
+    print(f"\n[gpu case] {name}", flush=True)
+
+
+def _batch(seed, T, C, r_c, r_u_max, tables, gamma=False, y0="normal", exact=False):
+    """Prefill-shaped batch: contiguous user segments of 1..64 tokens; each user
+    has a centroid (or none, 1 in 8 users) and a residual slot of rank
+    0..r_u_max (no residual for 1 in 8 users)."""
+    rng = np.random.default_rng(np.random.SeedSequence([2608, 3579, 99, seed]))
+    lens = []
+    while sum(lens) < T:
+        lens.append(int(rng.integers(1, 65)))
+    lens[-1] -= sum(lens) - T
+    n_users = len(lens)
+    c_of_user = rng.integers(0, C, size=n_users).astype(np.int32)
+    c_of_user[rng.random(n_users) < 0.125] = -1
+    u_of_user = np.arange(n_users, dtype=np.int32)
+    u_of_user[rng.random(n_users) < 0.125] = -1
+    tok_user = np.repeat(np.arange(n_users), lens)
+    tok_c = c_of_user[tok_user].astype(np.int32)
+    tok_u = u_of_user[tok_user].astype(np.int32)
+    slot_rank = rng.integers(0, r_u_max + 1, size=n_users).astype(np.int32)
+    g = None
+    if gamma:
+        g = np.asarray(synth.GAMMA_BINS, np.float32)[rng.integers(0, 3, size=n_users)][tok_user]
+    return synth.Workload(cfg=3, seed=1000 + seed, name=f"two-launch batch {seed}", dtype="bf16",
+                          tables=tables, n_centroids=C, r_c=r_c, n_slots=n_users, r_u_max=r_u_max,
+                          slot_rank=slot_rank, tok_c=tok_c, tok_u=tok_u, gamma=g,
+                          y0_kind=("int" if exact else y0), exact=exact)
+
+
+def _check_all(run, exact=False):
+    p = run.plan.download(run.stream)
+    want = oracle.plan(run.maps[0], run.maps[1])
+    for k in want:
+        assert np.array_equal(p[k], want[k]), k
+    for t in range(len(run.w.tables)):
+        got = oracle.decode(run.apply(t), "bf16")
+        assert run.plan.errors(run.stream) == 0
+        ref = run.oracle_table(t)
+        if exact:
+            assert np.array_equal(got, ref), f"table {t}: {np.sum(got != ref)} exact mismatches"
+        else:
+            ok, worst, nbad = close_enough(got, ref, TOL_NORTH_STAR)
+            assert ok, f"table {t}: {nbad} elements out of tolerance, worst {worst:.3f}x the bound"
+
+
+CASES = [
+    # seed, T, C, r_c, r_u_max, gamma
+    (0, 1000, 4, 32, 2, False),
+    (1, 2048, 8, 64, 1, True),
+    (2, 1536, 6, 128, 2, False),
+]
+
+
+@pytest.mark.parametrize("seed,T,C,r_c,r_u_max,gamma", CASES)
+def test_two_launch_parity(seed, T, C, r_c, r_u_max, gamma):
+    _announce(f"two-launch T={T} C={C} r_c={r_c} r_u<={r_u_max} gamma={gamma}")
+    tables = [("a", 520, 776), ("b", 1024, 384), ("c", 3072, 1024)]
+    w = _batch(seed, T, C, r_c, r_u_max, tables, gamma=gamma)
+    run = Run(w)
+    try:
+        run.set_and_build()
+        _check_all(run)
+    finally:
+        run.close()
+
+
+def test_two_launch_integer_inputs_bit_exact():
+    _announce("two-launch integer inputs, bit-exact")
+    w = _batch(7, 1280, 5, 64, 2, [("a", 776, 520), ("b", 2048, 1024)], exact=True)
+    run = Run(w)
+    try:
+        run.set_and_build()
+        _check_all(run, exact=True)
+    finally:
+        run.close()
+
+
+def test_two_launch_deterministic_parity_and_repeats():
+    """SALT_DETERMINISTIC: the expand launch sums the K-range partials in a fixed
+    order, so the result matches the oracle and repeated applies of one plan give
+    bit-identical y."""
+    _announce("two-launch deterministic sums")
+    w = _batch(3, 1024, 4, 64, 2, [("a", 3072, 1024), ("b", 1024, 776)])
+    run = Run(w, deterministic=True)
+    try:
+        run.set_and_build()
+        _check_all(run)
+        first = run.apply(0)
+        for _ in range(3):
+            assert np.array_equal(run.apply(0), first)
+        assert run.plan.errors(run.stream) == 0
+    finally:
+        run.close()
+
+
+def test_two_launch_atomic_applies_alternate_buffers():
+    """Default mode: consecutive applies of one plan sum into alternating v
+    buffers, each cleared by the apply before; every apply must match."""
+    _announce("two-launch atomic sums, consecutive applies")
+    w = _batch(4, 1536, 6, 64, 2, [("a", 3072, 1024), ("b", 1024, 3072)])
+    run = Run(w)
+    try:
+        run.set_and_build()
+        for rep in range(3):
+            for t in range(len(w.tables)):
+                got = oracle.decode(run.apply(t), "bf16")
+                ok, worst, nbad = close_enough(got, run.oracle_table(t), TOL_NORTH_STAR)
+                assert ok, f"rep {rep} table {t}: {nbad} out of tolerance, worst {worst:.3f}x"
+        assert run.plan.errors(run.stream) == 0
+    finally:
+        run.close()
