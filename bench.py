@@ -209,6 +209,8 @@ def run_gpu(w, dw, args, hip, salt):
         p.set_maps(w.tok_c, w.tok_u, w.gamma, stream.h)
         plans.append(p)
     stream.synchronize()
+    tile_m, n_tiles, launches = plans[0].tiling()
+    log(f"tiles of {tile_m} tokens: {n_tiles}; kernel launches per apply: {launches}")
 
     def step(k):
         slot = k % rot
@@ -300,12 +302,15 @@ def run_gpu(w, dw, args, hip, salt):
         "apply_flops": {w.tables[t][0]: int(flops_tab[t]) for t in range(n_tab)},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
-                     "kernel": f"k_apply (salt_apply, one launch) on {w.tables[dom][0]}",
+                     "kernel": (f"k_apply (salt_apply, one launch) on {w.tables[dom][0]}" if launches == 1 else
+                                f"k_shrink + k_expand (salt_apply, two launches) on {w.tables[dom][0]}"),
+                     "tiling": {"tile_tokens": tile_m, "tiles": n_tiles, "launches_per_apply": launches},
                      "bytes_per_launch": int(bytes_tab[dom]), "avg_us": per_tab[dom] * 1e3,
                      "period_us": period_tab[dom] * 1e3,
-                     "timing": f"avg_us: mean kernel duration over {n_meas} applies, from HIP events that "
-                               "record each apply kernel's own start and end (salt_apply_timed) on its stream; "
-                               "period_us: launch-to-launch period of back-to-back applies, with the dispatch gap"},
+                     "timing": f"avg_us: mean apply duration over {n_meas} applies, from HIP events that "
+                               "record the start of each apply's first kernel and the end of its last "
+                               "(salt_apply_timed) on its stream; period_us: launch-to-launch period of "
+                               "back-to-back applies, with the dispatch gap"},
         "swap": swap,
     }
 

@@ -181,19 +181,20 @@ SALT_API salt_status salt_plan_download(salt_ctx* ctx, const salt_plan* plan, vo
  *      (round-to-nearest-even) from fp32 y + fp32 delta.
  * Accumulation is fp32: the centroid contractions run on bf16 MFMA with fp32
  * accumulation (the expand splits the fp32 v into two bf16 terms), the residual
- * contractions on fp32 vector ALUs.  One kernel launch; the plan's scratch
- * (split-K partials, v, per-tile flags) is reused, so applies of one plan must be
- * ordered on one stream.  Enqueued on `stream` after the swaps of every slot the
- * plan references.  Errors: SALT_ERR_OUT_OF_RANGE (table), SALT_ERR_BAD_STATE
+ * contractions on fp32 vector ALUs.  One kernel launch, or two for large bf16
+ * batches with long centroid groups (salt_plan_tiling tells which); the plan's
+ * scratch (split-K partials, v, per-tile flags) is reused, so applies of one plan
+ * must be ordered on one stream.  Enqueued on `stream` after the swaps of every
+ * slot the plan references.  Errors: SALT_ERR_OUT_OF_RANGE (table), SALT_ERR_BAD_STATE
  * (centroids of the table not pinned; a referenced slot was reloaded with a
  * different rank after salt_plan_set_maps). */
 SALT_API salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y,
                        void* stream);
 
 /* salt_apply for measurement: the same apply, and the HIP events `start_event`
- * and `stop_event` (hipEvent_t, created with timing enabled) record the apply
- * kernel's own start and end, so hipEventElapsedTime gives its duration without
- * the dispatch gap.  Errors as salt_apply; SALT_ERR_INVALID_ARG for a null event. */
+ * and `stop_event` (hipEvent_t, created with timing enabled) record the start of
+ * the apply's first kernel and the end of its last, so hipEventElapsedTime gives
+ * its duration without the dispatch gap before it.  Errors as salt_apply; SALT_ERR_INVALID_ARG for a null event. */
 SALT_API salt_status salt_apply_timed(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y,
                                       void* stream, void* start_event, void* stop_event);
 
@@ -203,6 +204,18 @@ SALT_API salt_status salt_apply_timed(salt_ctx* ctx, int32_t table, salt_plan* p
  * that the device-built tiling matches the host's (SALT_ERR_BAD_STATE if not). */
 SALT_API salt_status salt_plan_errors(salt_ctx* ctx, const salt_plan* plan, void* stream,
                                       int32_t* n_errors);
+
+/* How the applies of a plan whose maps are set run (host-only; no HIP call):
+ *   *tile_tokens: tokens per tile (16, 32 or 64; the tiles of a centroid group
+ *                 cut its tokens into runs of at most this many),
+ *   *n_tiles:     tiles of the batch,
+ *   *launches:    kernel launches per salt_apply: 1 (shrink and expand blocks in
+ *                 one launch, v handed over inside it), or 2 (large bf16
+ *                 batches with long centroid groups and residual rank <= 2: a
+ *                 shrink launch, then an expand launch).
+ * Any pointer may be NULL.  SALT_ERR_BAD_STATE if no maps were set. */
+SALT_API salt_status salt_plan_tiling(salt_ctx* ctx, const salt_plan* plan, int32_t* tile_tokens,
+                                      int32_t* n_tiles, int32_t* launches);
 
 /* ---- diagnostics -------------------------------------------------------------------- */
 SALT_API const char* salt_status_str(salt_status s);

@@ -585,6 +585,16 @@ salt_status salt_plan_build(salt_ctx* ctx, salt_plan* plan, void* stream) {
   return SALT_OK;
 }
 
+salt_status salt_plan_tiling(salt_ctx* ctx, const salt_plan* plan, int32_t* tile_tokens, int32_t* n_tiles,
+                             int32_t* launches) {
+  if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
+  if (plan->T < 0 || plan->M <= 0) return fail(ctx, SALT_ERR_BAD_STATE, "no maps were set on the plan");
+  if (tile_tokens) *tile_tokens = plan->M;
+  if (n_tiles) *n_tiles = plan->n_tiles;
+  if (launches) *launches = plan->M == salt::kTwoPassM ? 2 : 1;
+  return SALT_OK;
+}
+
 salt_status salt_plan_errors(salt_ctx* ctx, const salt_plan* plan, void* stream, int32_t* n_errors) {
   if (!ctx || !plan || !n_errors) return SALT_ERR_INVALID_ARG;
   if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());

@@ -26,7 +26,8 @@ EXPORTS = (
     "salt_create", "salt_destroy", "salt_pin_centroids", "salt_residual_bytes",
     "salt_residual_bytes_for", "salt_load_residual", "salt_wait_loads", "salt_host_alloc",
     "salt_host_free", "salt_plan_create", "salt_plan_destroy", "salt_plan_set_maps",
-    "salt_plan_build", "salt_plan_download", "salt_plan_errors", "salt_apply", "salt_apply_timed",
+    "salt_plan_build", "salt_plan_download", "salt_plan_errors", "salt_plan_tiling", "salt_apply",
+    "salt_apply_timed",
     "salt_status_str",
     "salt_last_error", "salt_version",
 )
@@ -68,6 +69,7 @@ def _load() -> C.CDLL:
         "salt_plan_build": (C.c_int, [P, P, VP]),
         "salt_plan_download": (C.c_int, [P, P, VP, IP, IP, IP, IP, IP, IP, IP]),
         "salt_plan_errors": (C.c_int, [P, P, VP, IP]),
+        "salt_plan_tiling": (C.c_int, [P, P, IP, IP, IP]),
         "salt_apply": (C.c_int, [P, I32, P, VP, VP, VP]),
         "salt_apply_timed": (C.c_int, [P, I32, P, VP, VP, VP, VP, VP]),
         "salt_status_str": (C.c_char_p, [C.c_int]),
@@ -262,6 +264,13 @@ class Plan:
         n = C.c_int32()
         self.ctx._check(lib.salt_plan_errors(self.ctx.h, self.h, stream, C.byref(n)), "salt_plan_errors")
         return int(n.value)
+
+    def tiling(self) -> Tuple[int, int, int]:
+        """(tokens per tile, tiles, kernel launches per apply) of the staged maps."""
+        m, n, l = C.c_int32(), C.c_int32(), C.c_int32()
+        self.ctx._check(lib.salt_plan_tiling(self.ctx.h, self.h, C.byref(m), C.byref(n), C.byref(l)),
+                        "salt_plan_tiling")
+        return int(m.value), int(n.value), int(l.value)
 
     def download(self, stream: int = 0) -> Dict[str, np.ndarray]:
         T = self.T

@@ -270,3 +270,21 @@ def test_timed_apply_matches_apply_and_times_the_kernel():
         e1.destroy()
     finally:
         run.close()
+
+
+def test_plan_tiling_reports_the_launch_structure():
+    """salt_plan_tiling: decode batches run in one launch with 16- or 32-token
+    tiles, fp32 in one launch with 16-token tiles, the 8192-token prefill in two
+    launches with 64-token tiles; the tile count matches the centroid groups."""
+    _announce("salt_plan_tiling")
+    for cfg, kw, want in ((2, {}, (16, 1)), (1, {}, (16, 1)), (5, {}, (32, 1)), (3, {"layers": 1}, (64, 2))):
+        w = synth.make(cfg, 0, **kw)
+        run = Run(w, pin_tables=[])
+        try:
+            run.plan.set_maps(w.tok_c, w.tok_u, w.gamma, run.stream)
+            m, n_tiles, launches = run.plan.tiling()
+            assert (m, launches) == want, (cfg, m, launches)
+            counts = np.bincount(w.tok_c + 1)
+            assert n_tiles == int(sum((c + m - 1) // m for c in counts if c)), (cfg, n_tiles)
+        finally:
+            run.close()

@@ -54,6 +54,7 @@ def _batch(seed, T, C, r_c, r_u_max, tables, gamma=False, y0="normal", exact=Fal
 
 
 def _check_all(run, exact=False):
+    assert run.plan.tiling()[2] == 2, "the batch must take the two-launch apply"
     p = run.plan.download(run.stream)
     want = oracle.plan(run.maps[0], run.maps[1])
     for k in want:
@@ -127,6 +128,7 @@ def test_two_launch_atomic_applies_alternate_buffers():
     run = Run(w)
     try:
         run.set_and_build()
+        assert run.plan.tiling()[2] == 2
         for rep in range(3):
             for t in range(len(w.tables)):
                 got = oracle.decode(run.apply(t), "bf16")
