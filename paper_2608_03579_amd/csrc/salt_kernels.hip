@@ -644,6 +644,113 @@ __device__ __forceinline__ float4 scale_centroid(float4 v, int idx, int R, int r
   return v;
 }
 
+// Staged shrink of a 64-token tile (bf16): wave w computes M-block w (16
+// tokens) over 64-wide K units [kblk, kblk + 64 * nunit).  An MFMA operand
+// fragment is 64 bytes of each of 16 rows, so register loads in that layout
+// fetch half lines; from L2 (the centroid rows, shared by every tile of the
+// group) that halves what a compute unit can pull.  Here x rows and A_c rows
+// are instead loaded as whole 128-byte lines (8 lanes per row) and written to
+// LDS, from where each lane reads its fragment.  A 16-byte chunk ch of row r
+// sits in slot ch ^ ((r >> 1) & 7) of the row's 8 slots, so that both the
+// line-wise writes and the fragment reads hit every LDS bank once per 16
+// lanes.  The per-token A_u rows stay register loads in fragment layout
+// (lanes of one segment read the same row).  Units rotate through kStageD
+// register sets (loads of unit u + kStageD are issued while unit u computes)
+// and two LDS stages (one barrier per unit).
+constexpr int kStageD = 4;
+template <int NBM>
+__host__ __device__ constexpr int stage_bytes() { return 4 * 2048 + NBM * 2048; }
+
+template <int NBM, int RU>
+__device__ __forceinline__ void shrink_staged_units(const ApplyArgs& a, char* stg, const int4* s_tile, int wave,
+                                                    int lane, int n, int c, bool has_c, int kblk, int nunit,
+                                                    const uint16_t* const (&aurow)[RU], f32x4 (&acc)[NBM],
+                                                    float (&accu)[RU]) {
+  using O = Ops<uint16_t>;
+  using Vec = O::Vec;
+  constexpr int NA = NBM / 2;                   // line loads of A_c per lane and unit (NBM * 16 rows / 8 / 4 waves)
+  constexpr int SB = stage_bytes<NBM>();
+  if (nunit <= 0) return;
+  const int in = a.in_dim, rc = a.r_c;
+  const uint16_t* x = reinterpret_cast<const uint16_t*>(a.x);
+  // line-load sources: row r8 = lane >> 3 of each 8-row group, slot lane & 7
+  const uint16_t* xsrc[2];
+#pragma unroll
+  for (int q = 0; q < 2; ++q) {
+    const int r = 8 * q + (lane >> 3);          // row within this wave's M-block
+    const int t = wave * 16 + r;
+    const int ch = (lane & 7) ^ ((r >> 1) & 7);
+    xsrc[q] = x + (size_t)s_tile[1 + (t < n ? t : 0)].x * in + kblk + 8 * ch;
+  }
+  const uint16_t* asrc[NA];
+#pragma unroll
+  for (int q = 0; q < NA; ++q) {
+    const int J = 8 * (wave * NA + q) + (lane >> 3);   // rank row of the block's A_c stage
+    const int ch = (lane & 7) ^ ((J >> 1) & 7);
+    // without a centroid term (or past r_c) the loads read x's first row / rank 0
+    asrc[q] = has_c ? reinterpret_cast<const uint16_t*>(a.cent_at) + ((size_t)c * rc + (J < rc ? J : 0)) * in + kblk + 8 * ch
+                    : x + kblk + 8 * ch;
+  }
+  const int kfrag = 8 * (lane >> 4);            // element offset of this lane's fragment in a 32-wide half
+  struct Set {
+    Vec xl[2], al[NA], ul[2][RU];
+  } set[kStageD];
+  auto load = [&](Set& L, int u) {
+    const int off = 64 * (u < nunit ? u : nunit - 1);
+#pragma unroll
+    for (int q = 0; q < 2; ++q) L.xl[q] = O::load(xsrc[q] + off);
+#pragma unroll
+    for (int q = 0; q < NA; ++q) L.al[q] = O::load(asrc[q] + off);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int j = 0; j < RU; ++j) L.ul[h][j] = O::load(aurow[j] + kblk + off + 32 * h + kfrag);
+  };
+  // issued in set order (the waits below count on it)
+#pragma unroll
+  for (int d = 0; d < kStageD; ++d) {
+    load(set[d], d);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  // fragment read offsets (bytes inside a stage): row r = lane & 15, chunk 4h + g
+  const int r = lane & 15, g = lane >> 4, sw = (r >> 1) & 7;
+  const int xoff = wave * 2048 + r * 128, aoff = 4 * 2048 + r * 128;
+  const int nround = (nunit + kStageD - 1) / kStageD;
+  for (int rr = 0; rr < nround; ++rr) {
+#pragma unroll
+    for (int d = 0; d < kStageD; ++d) {
+      const int u = rr * kStageD + d;
+      char* st = stg + (u & 1) * SB;
+      // this unit's lines into the stage, in lane order
+#pragma unroll
+      for (int q = 0; q < 2; ++q) *reinterpret_cast<Vec*>(st + wave * 2048 + (64 * q + lane) * 16) = set[d].xl[q];
+#pragma unroll
+      for (int q = 0; q < NA; ++q) *reinterpret_cast<Vec*>(st + 4 * 2048 + (64 * (wave * NA + q) + lane) * 16) = set[d].al[q];
+      Vec ul[2][RU];
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int j = 0; j < RU; ++j) ul[h][j] = set[d].ul[h][j];
+      __syncthreads();
+      load(set[d], u + kStageD);
+      if (u < nunit) {
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          const int slot = ((4 * h + g) ^ sw) * 16;
+          const Vec xf = *reinterpret_cast<const Vec*>(st + xoff + slot);
+          if (has_c) {
+#pragma unroll
+            for (int nb = 0; nb < NBM; ++nb)
+              acc[nb] = O::mma(xf, *reinterpret_cast<const Vec*>(st + aoff + nb * 2048 + slot), acc[nb]);
+          }
+#pragma unroll
+          for (int j = 0; j < RU; ++j) accu[j] = O::dot(xf, ul[h][j], accu[j]);
+        }
+      }
+    }
+  }
+}
+
 // Shrink block: tile `tau`, K range `s` of the apply.  Computes the tile's
 // split-K partial sums P[s][token][0 : r_c + r_u_max].  In the single-launch
 // apply it adds them into v with atomics (default) or stores them for an
@@ -654,7 +761,9 @@ __device__ __forceinline__ float4 scale_centroid(float4 v, int idx, int R, int r
 // 1/KW of the K range (KW = 4 * MBW / MB waves along K).  With MBW = MB every
 // wave holds all of the tile's tokens, so the centroid rows it loads serve
 // 16 * MB tokens.
-template <typename E, int MB, int MBW, int RU, int NBM>
+// STG (bf16, 64-token tiles, one M-block per wave): x and A_c pass through LDS
+// (see shrink_staged_units).
+template <typename E, int MB, int MBW, int RU, int NBM, bool STG = false>
 __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s, char* lds) {
   using O = Ops<E>;
   using Vec = typename O::Vec;
@@ -736,21 +845,6 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
   // each multiply counts the loads exactly and never waits for the batch
   // behind it.
   Vec xv[2][U][MBW], av[2][U][NBM], uv[2][U][MBW][RU];
-  const int nfull = nstep_blk > kq ? (nstep_blk - kq + KW - 1) / KW : 0;   // this wave's whole steps
-  auto load_steps = [&](Vec (&x_)[U][MBW], Vec (&a_)[U][NBM], Vec (&u_)[U][MBW][RU], int step0) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int kk = kblk + 32 * (kq + KW * (step0 + u < nfull ? step0 + u : nfull - 1)) + kseg;
-#pragma unroll
-      for (int m = 0; m < MBW; ++m) x_[u][m] = O::load(xrow[m] + kk);
-#pragma unroll
-      for (int nb = 0; nb < NBM; ++nb) a_[u][nb] = O::load(arow[nb] + kk);
-#pragma unroll
-      for (int m = 0; m < MBW; ++m)
-#pragma unroll
-        for (int j = 0; j < RU; ++j) u_[u][m][j] = O::load(aurow[m][j] + kk);
-    }
-  };
   auto mul_steps = [&](const Vec (&x_)[U][MBW], const Vec (&a_)[U][NBM], const Vec (&u_)[U][MBW][RU], int ns) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
@@ -768,35 +862,73 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
       }
     }
   };
-  const int nbat = (nfull + U - 1) / U;
-  auto steps_of = [&](int b) { return min(U, nfull - b * U); };
-  if (nbat == 1) {
-    // one batch (short K ranges of small batches): nothing to overlap
-    load_steps(xv[0], av[0], uv[0], 0);
-    mul_steps(xv[0], av[0], uv[0], steps_of(0));
-  } else if (kStepRegs <= 128 && nbat == 2) {
-    // two batches: both in flight at once
-    load_steps(xv[0], av[0], uv[0], 0);
-    load_steps(xv[1], av[1], uv[1], U);
-    mul_steps(xv[0], av[0], uv[0], steps_of(0));
-    mul_steps(xv[1], av[1], uv[1], steps_of(1));
-  } else if constexpr (kStepRegs <= 128) {
-    if (nbat > 1) {
-      // (a peeled last pair would need a second set of accumulators)
-      load_steps(xv[0], av[0], uv[0], 0);
-      for (int b = 0; b < nbat; b += 2) {
-        load_steps(xv[1], av[1], uv[1], (b + 1) * U);
-        mul_steps(xv[0], av[0], uv[0], steps_of(b));
-        load_steps(xv[0], av[0], uv[0], (b + 2) * U);
-        if (b + 1 < nbat) mul_steps(xv[1], av[1], uv[1], steps_of(b + 1));
+  if constexpr (STG) {
+    static_assert(sizeof(E) == 2 && MB == 4 && MBW == 1, "staged shrink: bf16, 64-token tiles, one M-block per wave");
+    // whole 64-wide units through LDS, then an odd last 32-wide step from
+    // registers (the ragged end below takes whatever is left)
+    const int nunit = (kend - kblk) / 64;
+    shrink_staged_units<NBM, RU>(a, lds + tile_bytes(M) + sizeof(float) * (size_t)M * R, s_tile, wave, lane, n,
+                                 c, has_c, kblk, nunit, aurow[0], acc[0], accu[0]);
+    if (nstep_blk > 2 * nunit) {
+      const int kk = kblk + 64 * nunit + kseg;
+      xv[0][0][0] = O::load(xrow[0] + kk);
+#pragma unroll
+      for (int nb = 0; nb < NBM; ++nb) av[0][0][nb] = O::load(arow[nb] + kk);
+#pragma unroll
+      for (int j = 0; j < RU; ++j) uv[0][0][0][j] = O::load(aurow[0][j] + kk);
+      if (has_c) {
+#pragma unroll
+        for (int nb = 0; nb < NBM; ++nb) acc[0][nb] = O::mma(xv[0][0][0], av[0][0][nb], acc[0][nb]);
       }
+#pragma unroll
+      for (int j = 0; j < RU; ++j) accu[0][j] = O::dot(xv[0][0][0], uv[0][0][0][j], accu[0][j]);
     }
   } else {
-    // one step's operands alone fill most of the register file (fp32 with
-    // wide centroid and residual ranks): no second buffer
-    for (int b = 0; b < nbat; ++b) {
-      load_steps(xv[0], av[0], uv[0], b * U);
-      mul_steps(xv[0], av[0], uv[0], steps_of(b));
+    const int nfull = nstep_blk > kq ? (nstep_blk - kq + KW - 1) / KW : 0;   // this wave's whole steps
+    auto load_steps = [&](Vec (&x_)[U][MBW], Vec (&a_)[U][NBM], Vec (&u_)[U][MBW][RU], int step0) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int kk = kblk + 32 * (kq + KW * (step0 + u < nfull ? step0 + u : nfull - 1)) + kseg;
+#pragma unroll
+        for (int m = 0; m < MBW; ++m) x_[u][m] = O::load(xrow[m] + kk);
+#pragma unroll
+        for (int nb = 0; nb < NBM; ++nb) a_[u][nb] = O::load(arow[nb] + kk);
+#pragma unroll
+        for (int m = 0; m < MBW; ++m)
+#pragma unroll
+          for (int j = 0; j < RU; ++j) u_[u][m][j] = O::load(aurow[m][j] + kk);
+      }
+    };
+    const int nbat = (nfull + U - 1) / U;
+    auto steps_of = [&](int b) { return min(U, nfull - b * U); };
+    if (nbat == 1) {
+      // one batch (short K ranges of small batches): nothing to overlap
+      load_steps(xv[0], av[0], uv[0], 0);
+      mul_steps(xv[0], av[0], uv[0], steps_of(0));
+    } else if (kStepRegs <= 128 && nbat == 2) {
+      // two batches: both in flight at once
+      load_steps(xv[0], av[0], uv[0], 0);
+      load_steps(xv[1], av[1], uv[1], U);
+      mul_steps(xv[0], av[0], uv[0], steps_of(0));
+      mul_steps(xv[1], av[1], uv[1], steps_of(1));
+    } else if constexpr (kStepRegs <= 128) {
+      if (nbat > 1) {
+        // (a peeled last pair would need a second set of accumulators)
+        load_steps(xv[0], av[0], uv[0], 0);
+        for (int b = 0; b < nbat; b += 2) {
+          load_steps(xv[1], av[1], uv[1], (b + 1) * U);
+          mul_steps(xv[0], av[0], uv[0], steps_of(b));
+          load_steps(xv[0], av[0], uv[0], (b + 2) * U);
+          if (b + 1 < nbat) mul_steps(xv[1], av[1], uv[1], steps_of(b + 1));
+        }
+      }
+    } else {
+      // one step's operands alone fill most of the register file (fp32 with
+      // wide centroid and residual ranks): no second buffer
+      for (int b = 0; b < nbat; ++b) {
+        load_steps(xv[0], av[0], uv[0], b * U);
+        mul_steps(xv[0], av[0], uv[0], steps_of(b));
+      }
     }
   }
   if (kend > kblk + 32 * nstep_blk && nstep_blk % KW == kq) {
@@ -1266,8 +1398,9 @@ __global__ void __launch_bounds__(256) k_apply(ApplyArgs a) {
 }
 
 // The two-launch apply of large batches (tiles of kTwoPassM tokens).  The
-// shrink launch: one block per (tile, K range); every wave covers all of the
-// tile's tokens.  Block ids run over tiles first.
+// shrink launch: one block per (tile, K range); wave w covers M-block w over
+// the whole K range, x and A_c staged through LDS.  Block ids run over tiles
+// first.
 template <typename E, int MB, int RU, int NBM>
 __global__ void __launch_bounds__(256) k_shrink(ApplyArgs a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
@@ -1277,7 +1410,7 @@ __global__ void __launch_bounds__(256) k_shrink(ApplyArgs a) {
   const int4* trec = a.tiles + (size_t)tau * (M + 1);
   for (int k = threadIdx.x; k < M + 1; k += 256) s_tile[k] = trec[k];
   __syncthreads();
-  shrink_block<E, MB, MB, RU, NBM>(a, tau, b / a.n_tiles, lds);
+  shrink_block<E, MB, 1, RU, NBM, true>(a, tau, b / a.n_tiles, lds);
 }
 
 // The expand launch: one block per (tile, range of cpb column chunks).
@@ -1297,6 +1430,11 @@ __global__ void __launch_bounds__(256) k_expand(ApplyArgs a) {
 // [KW][M][R] (KW * M = 64 in the single launch, 4 * M in the two-launch one).
 size_t lds_shrink(int M, int R, int kw_m) {
   return (size_t)tile_bytes(M) + sizeof(float) * (size_t)kw_m * R;
+}
+// Two-launch shrink: tile records, partials [M][R], two staging buffers.
+template <int NBM>
+size_t lds_shrink_staged(int R) {
+  return lds_shrink(kTwoPassM, R, kTwoPassM) + 2 * (size_t)stage_bytes<NBM>();
 }
 // Expand: tile records, v [M][R], the MFMA output [M][kYS] and the bf16 hi/lo
 // copies of v's centroid part [2][M][VS].
@@ -1325,7 +1463,7 @@ hipError_t launch_nbm(const ApplyArgs& a, int M, hipStream_t s, hipEvent_t e0, h
     if constexpr (sizeof(E) == 2 && RU <= 2) {
       if (M != kTwoPassM) return hipErrorInvalidValue;
       constexpr int MB = kTwoPassM / 16;
-      launch_k(k_shrink<E, MB, RU, NBM>, dim3(a.n_tiles * a.S), dim3(256), lds_shrink(M, a.R, 4 * M), s, a, e0,
+      launch_k(k_shrink<E, MB, RU, NBM>, dim3(a.n_tiles * a.S), dim3(256), lds_shrink_staged<NBM>(a.R), s, a, e0,
                nullptr);
       launch_k(k_expand<E, MB, RU, NBM>, dim3(a.n_tiles * a.n_col), dim3(256), lds_expand(M, a.R, NBM), s, a,
                nullptr, e1);
@@ -1364,7 +1502,7 @@ hipError_t two_pass_occ(int R, int* shrink_per_cu, int* expand_per_cu) {
   constexpr int MB = kTwoPassM / 16;
   hipError_t e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
       shrink_per_cu, reinterpret_cast<const void*>(k_shrink<uint16_t, MB, RU, NBM>), 256,
-      lds_shrink(kTwoPassM, R, 4 * kTwoPassM));
+      lds_shrink_staged<NBM>(R));
   if (e != hipSuccess) return e;
   return hipOccupancyMaxActiveBlocksPerMultiprocessor(
       expand_per_cu, reinterpret_cast<const void*>(k_expand<uint16_t, MB, RU, NBM>), 256,
@@ -1396,7 +1534,7 @@ hipError_t kernels_init(int device) {
   hipError_t e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, device);
   if (e != hipSuccess) return e;
   const size_t need = std::max({apply_lds(32, padded_rank(kMaxRc, kMaxRu), 8, kPlanFusedT),
-                                lds_shrink(kTwoPassM, padded_rank(kMaxRc, 2), 4 * kTwoPassM),
+                                lds_shrink_staged<8>(padded_rank(kMaxRc, 2)),
                                 lds_expand(kTwoPassM, padded_rank(kMaxRc, 2), 8)});
   if ((size_t)lds_max < need + 1024) return hipErrorInvalidConfiguration;
   done[device] = true;
