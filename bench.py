@@ -347,7 +347,106 @@ WORKLOADS = {
     "decode8b": dict(cfg=4, rot=4, steps=500, warmup=50),
     "zipf": dict(cfg=5, rot=4, steps=500, warmup=50),
     "zipf-baseline": dict(cfg=5, rot=4, baseline=True, steps=200, warmup=20),
+    # Sec. 3.3: a centroid fused into the base weights of one Llama-3.2-3B layer
+    "fuse": dict(cfg=5, rot=2, steps=20, warmup=3, fuse=True),
 }
+
+
+def fuse_bytes(n_in, n_out, r_c, esize=2):
+    """Algorithmic bytes of one salt_fuse_centroid: W read and written once, the
+    centroid's A and B read once."""
+    return esize * (2 * n_in * n_out + r_c * (n_in + n_out))
+
+
+def run_fuse(w, args, hip, salt):
+    """One step = centroid 0 of every table folded into that table's base weight
+    (gamma alternating +0.8 / -0.8 between steps so the weights stay put); the
+    weights rotate over `rot` copies."""
+    tables = [(i, o) for _, i, o in w.tables]
+    n_tab = len(tables)
+    ctx = salt.Context(w.dtype, tables, w.n_centroids, w.r_c, 1, 0, 1)
+    for t in range(n_tab):
+        at, b = w.centroids(t)
+        ctx.pin_centroids(t, at, b)
+    stream = hip.Stream()
+    ws = []
+    for k in range(args.rot):
+        for t in range(n_tab):
+            ws.append(hip.DeviceArray.from_host(w.base_weight(t)))
+    hip.synchronize()
+    bytes_tab = np.array([fuse_bytes(i, o, w.r_c) for i, o in tables], dtype=np.float64)
+
+    def step(k):
+        g = 0.8 if k % 2 == 0 else -0.8
+        base = (k % args.rot) * n_tab
+        for t in range(n_tab):
+            ctx.fuse_centroid(t, 0, g, ws[base + t].ptr, tables[t][1], stream.h)
+
+    for k in range(args.warmup):
+        step(k)
+    stream.synchronize()
+    e0, e1 = hip.Event(), hip.Event()
+    e0.record(stream)
+    for k in range(args.steps):
+        step(k)
+    e1.record(stream)
+    stream.synchronize()
+    ms_step = e0.elapsed_ms(e1) / args.steps
+    n_meas = 20
+    ev = [hip.Event() for _ in range(2 * n_meas)]
+    per_tab = np.zeros(n_tab)
+    for t in range(n_tab):
+        for k in range(n_meas):
+            ctx.fuse_centroid_timed(t, 0, 0.8 if k % 2 == 0 else -0.8, ws[(k % args.rot) * n_tab + t].ptr,
+                                    tables[t][1], stream.h, ev[2 * k].h, ev[2 * k + 1].h)
+        stream.synchronize()
+        per_tab[t] = float(np.mean([ev[2 * k].elapsed_ms(ev[2 * k + 1]) for k in range(n_meas)]))
+    for e in ev + [e0, e1]:
+        e.destroy()
+    for d in ws:
+        d.free()
+    ctx.close()
+    dom = int(np.argmax(per_tab))
+    achieved = bytes_tab[dom] / (per_tab[dom] * 1e-3) / 1e9
+    log(f"fuse durations (us): " + ", ".join(f"{w.tables[t][0]} {per_tab[t] * 1e3:.2f}" for t in range(n_tab)))
+    return {"ms_per_step": ms_step, "step_GBps": bytes_tab.sum() / (ms_step * 1e-3) / 1e9,
+            "fuse_us": {w.tables[t][0]: round(per_tab[t] * 1e3, 3) for t in range(n_tab)},
+            "fuse_bytes": {w.tables[t][0]: int(bytes_tab[t]) for t in range(n_tab)},
+            "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                         "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                         "kernel": f"k_fuse (salt_fuse_centroid) on {w.tables[dom][0]}",
+                         "bytes_per_launch": int(bytes_tab[dom]), "avg_us": per_tab[dom] * 1e3,
+                         "timing": f"avg_us: mean kernel duration over {n_meas} calls from HIP events that record "
+                                   "the kernel's own start and end (salt_fuse_centroid_timed)"}}
+
+
+def cpu_fuse_baseline(w, budget_s=12.0):
+    """GB/s of the oracle's fuse (float64 numpy, BLAS limited to one thread) over
+    the same tables, counted with the same algorithmic bytes."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=1)
+    except Exception:   # pragma: no cover
+        limiter = None
+    d = w.dtype
+    data = []
+    for t in range(len(w.tables)):
+        at, b = w.centroids(t)
+        data.append((oracle.decode(w.base_weight(t), d), oracle.decode(at[0], d), oracle.decode(b[0], d)))
+    done, nbytes = 0, 0.0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < budget_s:
+        W, A, B = data[done % len(data)]
+        oracle.fuse_centroid(W, A, B, 0.8)
+        nbytes += fuse_bytes(W.shape[0], W.shape[1], A.shape[0])
+        done += 1
+    dt = time.perf_counter() - t0
+    if limiter is not None and hasattr(limiter, "unregister"):
+        limiter.unregister()
+    return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} table fuses (one layer's 7 tables in turn) in {dt:.1f} s; fp64 numpy, BLAS "
+                      f"limited to 1 thread; host has {os.cpu_count()} logical cpus"}
 
 
 def main():
@@ -387,6 +486,21 @@ def main():
         print("no HIP device visible", file=sys.stderr)
         sys.exit(1)
     hip.set_device(0)
+    if spec.get("fuse"):
+        res = run_fuse(w, args, hip, salt)
+        cpu = None if args.no_cpu else cpu_fuse_baseline(w)
+        print(json.dumps({
+            "metric": "Centroid fused into the base weights (Sec. 3.3 node start-up): achieved HBM GB/s, "
+                      "Llama-3.2-3B",
+            "value": res["step_GBps"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": res["ms_per_step"], "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": "llama3.2-3b one layer, centroid fused into the base weights",
+                       "tables": tables_summary(w), "centroid_rank": w.r_c, "rotation": args.rot,
+                       "step": "salt_fuse_centroid per table (W read + written once, A_c and B_c read once)"},
+            "fuse_us": res["fuse_us"], "fuse_bytes": res["fuse_bytes"], "roofline": res["roofline"],
+            "cpu_baseline": cpu}), flush=True)
+        return
     res = run_gpu(w, dw, args, hip, salt)
     res["roofline"]["traffic"] = measured_traffic(args.workload)
 

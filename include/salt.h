@@ -217,6 +217,30 @@ SALT_API salt_status salt_plan_errors(salt_ctx* ctx, const salt_plan* plan, void
 SALT_API salt_status salt_plan_tiling(salt_ctx* ctx, const salt_plan* plan, int32_t* tile_tokens,
                                       int32_t* n_tiles, int32_t* launches);
 
+/* ---- a centroid fused into the base weight -------------------------------------------
+ * Sec. 3.3: for a high-frequency domain the provider folds the scaled centroid
+ * into the base weight at node start-up; such a node then serves its tokens with
+ * the residual alone (maps with c = -1).  For one pinned centroid c of `table`:
+ *
+ *     W[i][o] <- rne(W[i][o] + gamma * sum_r A_c[i][r] B_c[r][o])
+ *
+ *   W: device, the table's base weight in the context dtype, row-major
+ *      [in_dim][ldw] (ldw elements between rows, a multiple of 8, >= out_dim;
+ *      columns past out_dim are not touched), 16-byte aligned, owned by the
+ *      caller.  Each element is read and written once; the rank-r_c product is
+ *      accumulated in fp32 (bf16 MFMA for bf16 contexts) and added with one
+ *      rounding (round-to-nearest-even).
+ * Enqueued on `stream`.  The same call with -gamma takes the centroid out again
+ * up to one rounding per call (not bit-exact in bf16).  Errors:
+ * SALT_ERR_OUT_OF_RANGE (table, c), SALT_ERR_BAD_STATE (centroid never pinned),
+ * SALT_ERR_INVALID_ARG (null or misaligned W, bad ldw, non-finite gamma). */
+SALT_API salt_status salt_fuse_centroid(salt_ctx* ctx, int32_t table, int32_t c, float gamma, void* w,
+                                        int64_t ldw, void* stream);
+/* salt_fuse_centroid for measurement: the HIP events `start_event` and
+ * `stop_event` record the start and end of its kernel (as salt_apply_timed). */
+SALT_API salt_status salt_fuse_centroid_timed(salt_ctx* ctx, int32_t table, int32_t c, float gamma, void* w,
+                                              int64_t ldw, void* stream, void* start_event, void* stop_event);
+
 /* ---- diagnostics -------------------------------------------------------------------- */
 SALT_API const char* salt_status_str(salt_status s);
 SALT_API const char* salt_last_error(const salt_ctx* ctx);

@@ -25,6 +25,10 @@ delta for token t with centroid c_t and residual slot u_t is
 the storage layout of the boundary: A transposed, ``At[r][in]``, and ``B[r][out]``.
 Everything here is float64 numpy, one token at a time; ``y`` is left unrounded.
 
+Sec. 3.3 also lets a node fold one scaled centroid into its base weight at
+start-up (``fuse_centroid``: ``W_base + gamma * A_c B_c``) and then add only the
+residual per request.
+
 Readings where the paper is silent are listed in the design doc (orientation of A/B,
 gamma scaling only the centroid, the canonical segment order, -1 meaning "term
 absent").
@@ -146,6 +150,24 @@ def apply(x: np.ndarray, y0: np.ndarray,
     if not out:
         return np.zeros((0, y0.shape[1]), dtype=np.float64)
     return np.stack(out)
+
+
+# --------------------------------------------------------------------------
+# O3: a centroid fused into the base weight (Sec. 3.3, high-frequency domains)
+# --------------------------------------------------------------------------
+def fuse_centroid(w: np.ndarray, at: np.ndarray, b: np.ndarray, gamma: float) -> np.ndarray:
+    """Base weight with the scaled centroid folded in, float64, unrounded.
+
+    w      [in][out]   base weight (float64), row-vector convention y = x @ w
+    at     [r][in]     the centroid's A, transposed (float64)
+    b      [r][out]    the centroid's B (float64)
+    gamma  the centroid scale of the node's domain
+
+    Sec. 3.3 serves W_base + gamma * Wbar + delta_i; a node that fuses Wbar keeps
+    W_base + gamma * Wbar as its weight and adds only delta_i per request.  With
+    Wbar = A B (Sec. 1, A in x r, B r x out) the fused weight is
+    ``w + gamma * (A @ B)``."""
+    return w + float(gamma) * (at.T @ b)
 
 
 # --------------------------------------------------------------------------

@@ -85,10 +85,22 @@ struct alignas(64) ApplyArgs {
 };
 static_assert(offsetof(ApplyArgs, maps) + sizeof(void*) <= 64, "the fields a block reads first share one 64-byte line");
 
+// One centroid fused into a base weight: W <- rne(W + gamma * A_c B_c).
+struct FuseArgs {
+  const void* at;           // [r_c][in] A_c^T of the centroid
+  const void* bt;           // [out][r_c] B_c^T of the centroid (internal layout)
+  void* w;                  // [in][ldw] base weight, row-major
+  int64_t ldw;              // elements between rows of w (multiple of 8, >= out)
+  int32_t in_dim, out_dim, r_c;
+  float gamma;
+};
+
 hipError_t kernels_init(int device);
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 // e0 / e1: if set, HIP events that record the apply kernel's own start and end.
 hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+// e0 / e1 as for launch_apply.
+hipError_t launch_fuse(const FuseArgs& f, int bf16, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 // Blocks of the two-launch apply's shrink and expand kernels one compute unit
 // holds at once (bf16, r_u_max <= 2).
 hipError_t two_pass_occupancy(int r_c, int r_u_max, int R, int* shrink_per_cu, int* expand_per_cu);

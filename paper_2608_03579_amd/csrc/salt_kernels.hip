@@ -1449,8 +1449,8 @@ size_t apply_lds(int M, int R, int nbm, int fused_T) {
 }
 
 // A launch; with events, they record the kernel's own start and end.
-template <typename K>
-void launch_k(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, const ApplyArgs& a, hipEvent_t e0,
+template <typename K, typename Args>
+void launch_k(K kernel, dim3 grid, dim3 block, size_t lds, hipStream_t s, const Args& a, hipEvent_t e0,
               hipEvent_t e1) {
   if (e0 || e1) hipExtLaunchKernelGGL(kernel, grid, block, (uint32_t)lds, s, e0, e1, 0u, a);
   else hipLaunchKernelGGL(kernel, grid, block, lds, s, a);
@@ -1509,6 +1509,122 @@ hipError_t two_pass_occ(int R, int* shrink_per_cu, int* expand_per_cu) {
       lds_expand(kTwoPassM, R, NBM));
 }
 
+
+// ---------------------------------------------------------------------------
+// centroid fused into a base weight
+// ---------------------------------------------------------------------------
+// Raw elements of an operand vector (8 per lane).
+__device__ __forceinline__ void vec_elems(const uint4& v, uint16_t (&e)[8]) {
+  const uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int k = 0; k < 8; ++k) e[k] = (uint16_t)(w[k >> 1] >> (16 * (k & 1)));
+}
+__device__ __forceinline__ void vec_elems(const Ops<float>::Vec& v, float (&e)[8]) {
+  e[0] = v.lo.x; e[1] = v.lo.y; e[2] = v.lo.z; e[3] = v.lo.w;
+  e[4] = v.hi.x; e[5] = v.hi.y; e[6] = v.hi.z; e[7] = v.hi.w;
+}
+
+constexpr int kFuseTI = 64, kFuseTO = 128, kFuseDS = kFuseTO + 4;
+// Row stride (elements) of the transposed A_c tile: 32 * KS ranks + 8 of padding.
+__host__ __device__ constexpr int fuse_rp(int ks) { return 32 * ks + 8; }
+size_t fuse_lds(int ks, int esize) {
+  return std::max((size_t)kFuseTI * fuse_rp(ks) * esize, sizeof(float) * kFuseTI * kFuseDS);
+}
+
+// W[i][o] <- rne(W[i][o] + gamma * sum_r A_c[i][r] B_c[r][o]) over a 64 x 128
+// tile of W (in rows i, out columns o).  The rank-r_c product is an MFMA
+// contraction over the ranks: D[o][i] = sum_r Bt_c[o][r] At_c[r][i], with the
+// rows of Bt_c (8 consecutive ranks per lane) read straight from the pinned
+// transposed B and At_c's columns taken from an LDS copy of the tile transposed
+// to [i][r].  The fp32 delta goes through LDS so that W is read and written in
+// whole rows, once, with one rounding.
+template <typename E, int KS>
+__global__ void __launch_bounds__(256) k_fuse(FuseArgs f) {
+  using O = Ops<E>;
+  using Vec = typename O::Vec;
+  constexpr int TI = kFuseTI, TO = kFuseTO, DS = kFuseDS, RP = fuse_rp(KS);
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  E* s_a = reinterpret_cast<E*>(lds);            // [TI][RP]: A_c[i][r], ranks past r_c zero
+  float* s_d = reinterpret_cast<float*>(lds);    // [TI][DS] delta, after s_a is consumed
+  const int i0 = blockIdx.x * TI, o0 = blockIdx.y * TO;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, g = lane >> 4;
+  const int in = f.in_dim, out = f.out_dim, rc = f.r_c;
+  const E* at = reinterpret_cast<const E*>(f.at);   // [r_c][in] of the centroid
+  const E* bt = reinterpret_cast<const E*>(f.bt);   // [out][r_c]
+
+  for (int k = tid; k < 32 * KS * (TI / 8); k += 256) {
+    const int r = k / (TI / 8), i8 = (k % (TI / 8)) * 8;
+    E e[8];
+    if (r < rc && i0 + i8 < in) {
+      vec_elems(O::load(at + (size_t)r * in + i0 + i8), e);
+    } else {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) e[q] = E(0);
+    }
+#pragma unroll
+    for (int q = 0; q < 8; ++q) s_a[(i8 + q) * RP + r] = e[q];
+  }
+  __syncthreads();
+
+  f32x4 acc[2][4];
+#pragma unroll
+  for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+    for (int ib = 0; ib < 4; ++ib) acc[ob][ib] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    const int r8 = 32 * ks + 8 * g;               // this lane's 8 ranks (r_c is a multiple of 8)
+    Vec bfr[2];
+#pragma unroll
+    for (int ob = 0; ob < 2; ++ob) {
+      const int o = o0 + 32 * wave + 16 * ob + (lane & 15);
+      bfr[ob] = (o < out && r8 < rc) ? O::load(bt + (size_t)o * rc + r8) : O::zero();
+    }
+#pragma unroll
+    for (int ib = 0; ib < 4; ++ib) {
+      const Vec afr = *reinterpret_cast<const Vec*>(s_a + (16 * ib + (lane & 15)) * RP + r8);
+#pragma unroll
+      for (int ob = 0; ob < 2; ++ob) acc[ob][ib] = O::mma(bfr[ob], afr, acc[ob][ib]);
+    }
+  }
+  __syncthreads();                                // s_a consumed; s_d reuses it
+  // D[o][i]: lane holds o = 4g + e (of its 16-row block), i = lane & 15
+#pragma unroll
+  for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+    for (int ib = 0; ib < 4; ++ib)
+      *reinterpret_cast<float4*>(s_d + (16 * ib + (lane & 15)) * DS + 32 * wave + 16 * ob + 4 * g) =
+          make_float4(acc[ob][ib][0], acc[ob][ib][1], acc[ob][ib][2], acc[ob][ib][3]);
+  __syncthreads();
+
+  for (int k = tid; k < TI * (TO / 8); k += 256) {
+    const int i = k / (TO / 8), o8 = (k % (TO / 8)) * 8;
+    if (i0 + i >= in || o0 + o8 >= out) continue;
+    E* w = reinterpret_cast<E*>(f.w) + (size_t)(i0 + i) * f.ldw + o0 + o8;
+    float v[8];
+    O::to_f32(O::load(w), v);
+    const float4 d0 = *reinterpret_cast<const float4*>(s_d + i * DS + o8);
+    const float4 d1 = *reinterpret_cast<const float4*>(s_d + i * DS + o8 + 4);
+    v[0] += f.gamma * d0.x; v[1] += f.gamma * d0.y; v[2] += f.gamma * d0.z; v[3] += f.gamma * d0.w;
+    v[4] += f.gamma * d1.x; v[5] += f.gamma * d1.y; v[6] += f.gamma * d1.z; v[7] += f.gamma * d1.w;
+    O::store(w, v);
+  }
+}
+
+template <typename E>
+hipError_t launch_fuse_t(const FuseArgs& f, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  const dim3 grid((f.in_dim + kFuseTI - 1) / kFuseTI, (f.out_dim + kFuseTO - 1) / kFuseTO), block(256);
+  const int ks = (f.r_c + 31) / 32;
+  const size_t lds = fuse_lds(ks, (int)sizeof(E));
+  switch (ks) {
+    case 1: launch_k(k_fuse<E, 1>, grid, block, lds, s, f, e0, e1); break;
+    case 2: launch_k(k_fuse<E, 2>, grid, block, lds, s, f, e0, e1); break;
+    case 3: launch_k(k_fuse<E, 3>, grid, block, lds, s, f, e0, e1); break;
+    case 4: launch_k(k_fuse<E, 4>, grid, block, lds, s, f, e0, e1); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
 }  // namespace
 
 // Blocks of the two-launch apply's kernels that one compute unit holds at once.
@@ -1565,6 +1681,11 @@ hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s, hipE
   if (a.r_u_max <= 1) return launch_typed<uint16_t, 1>(a, M, s, e0, e1);
   if (a.r_u_max <= 2) return launch_typed<uint16_t, 2>(a, M, s, e0, e1);
   return launch_typed<uint16_t, kMaxRu>(a, M, s, e0, e1);
+}
+
+hipError_t launch_fuse(const FuseArgs& f, int bf16, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
+  if (f.r_c < 8 || f.r_c > kMaxRc || f.r_c % 8 || f.in_dim <= 0 || f.out_dim <= 0) return hipErrorInvalidValue;
+  return bf16 ? launch_fuse_t<uint16_t>(f, s, e0, e1) : launch_fuse_t<float>(f, s, e0, e1);
 }
 
 }  // namespace salt

@@ -653,6 +653,8 @@ salt_status salt_plan_download(salt_ctx* ctx, const salt_plan* plan, void* strea
 namespace {
 salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y, void* stream,
                        hipEvent_t e0, hipEvent_t e1);
+salt_status fuse_impl(salt_ctx* ctx, int32_t table, int32_t c, float gamma, void* w, int64_t ldw, void* stream,
+                      hipEvent_t e0, hipEvent_t e1);
 }  // namespace
 
 salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y,
@@ -666,9 +668,51 @@ salt_status salt_apply_timed(salt_ctx* ctx, int32_t table, salt_plan* plan, cons
   return apply_impl(ctx, table, plan, x, y, stream, (hipEvent_t)start_event, (hipEvent_t)stop_event);
 }
 
+salt_status salt_fuse_centroid(salt_ctx* ctx, int32_t table, int32_t c, float gamma, void* w, int64_t ldw,
+                               void* stream) {
+  return fuse_impl(ctx, table, c, gamma, w, ldw, stream, nullptr, nullptr);
+}
+
+salt_status salt_fuse_centroid_timed(salt_ctx* ctx, int32_t table, int32_t c, float gamma, void* w, int64_t ldw,
+                                     void* stream, void* start_event, void* stop_event) {
+  if (!start_event || !stop_event) return fail(ctx, SALT_ERR_INVALID_ARG, "null event");
+  return fuse_impl(ctx, table, c, gamma, w, ldw, stream, (hipEvent_t)start_event, (hipEvent_t)stop_event);
+}
+
 }  // extern "C"
 
 namespace {
+salt_status fuse_impl(salt_ctx* ctx, int32_t table, int32_t c, float gamma, void* w, int64_t ldw, void* stream,
+                      hipEvent_t e0, hipEvent_t e1) {
+  if (!ctx) return SALT_ERR_INVALID_ARG;
+  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  if (table < 0 || table >= ctx->cfg.n_tables)
+    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "table %d not in [0, %d)", table, ctx->cfg.n_tables);
+  const int C = ctx->cfg.n_centroids;
+  if (c < 0 || c >= C) return fail(ctx, SALT_ERR_OUT_OF_RANGE, "centroid %d not in [0, %d)", c, C);
+  if (!ctx->cent_pinned[(size_t)table * C + c])
+    return fail(ctx, SALT_ERR_BAD_STATE, "centroid %d of table %d was never pinned", c, table);
+  const salt_shape sh = ctx->tables[table];
+  if (!w || !aligned16(w)) return fail(ctx, SALT_ERR_INVALID_ARG, "null or misaligned weight");
+  if (ldw < sh.out_dim || ldw % 8 != 0)
+    return fail(ctx, SALT_ERR_INVALID_ARG, "ldw %lld: need a multiple of 8 and >= out_dim %d", (long long)ldw,
+                sh.out_dim);
+  if (!std::isfinite(gamma)) return fail(ctx, SALT_ERR_INVALID_ARG, "gamma is not finite");
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  const size_t rc = ctx->cfg.r_c, es = ctx->esize;
+  salt::FuseArgs f{};
+  f.at = ctx->cent_at[table] + (size_t)c * rc * sh.in_dim * es;
+  f.bt = ctx->cent_b[table] + (size_t)c * rc * sh.out_dim * es;
+  f.w = w;
+  f.ldw = ldw;
+  f.in_dim = sh.in_dim;
+  f.out_dim = sh.out_dim;
+  f.r_c = (int32_t)rc;
+  f.gamma = gamma;
+  SALT_HIP(ctx, salt::launch_fuse(f, ctx->cfg.dtype == SALT_BF16, (hipStream_t)stream, e0, e1));
+  return SALT_OK;
+}
+
 salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y, void* stream,
                        hipEvent_t e0, hipEvent_t e1) {
   if (!ctx || !plan) return SALT_ERR_INVALID_ARG;

@@ -27,7 +27,7 @@ EXPORTS = (
     "salt_residual_bytes_for", "salt_load_residual", "salt_wait_loads", "salt_host_alloc",
     "salt_host_free", "salt_plan_create", "salt_plan_destroy", "salt_plan_set_maps",
     "salt_plan_build", "salt_plan_download", "salt_plan_errors", "salt_plan_tiling", "salt_apply",
-    "salt_apply_timed",
+    "salt_apply_timed", "salt_fuse_centroid", "salt_fuse_centroid_timed",
     "salt_status_str",
     "salt_last_error", "salt_version",
 )
@@ -72,6 +72,8 @@ def _load() -> C.CDLL:
         "salt_plan_tiling": (C.c_int, [P, P, IP, IP, IP]),
         "salt_apply": (C.c_int, [P, I32, P, VP, VP, VP]),
         "salt_apply_timed": (C.c_int, [P, I32, P, VP, VP, VP, VP, VP]),
+        "salt_fuse_centroid": (C.c_int, [P, I32, I32, C.c_float, VP, C.c_int64, VP]),
+        "salt_fuse_centroid_timed": (C.c_int, [P, I32, I32, C.c_float, VP, C.c_int64, VP, VP, VP]),
         "salt_status_str": (C.c_char_p, [C.c_int]),
         "salt_last_error": (C.c_char_p, [P]),
         "salt_version": (I32, []),
@@ -224,6 +226,19 @@ class Context:
         """``apply`` whose two HIP events record the kernel's own start and end."""
         self._check(lib.salt_apply_timed(self.h, table, plan.h, x_ptr, y_ptr, stream, start_event, stop_event),
                     "salt_apply_timed")
+
+    def fuse_centroid(self, table: int, c: int, gamma: float, w_ptr: int, ldw: int, stream: int = 0):
+        """Fold gamma * centroid c of `table` into the base weight at w_ptr ([in][ldw], device)."""
+        self._check(lib.salt_fuse_centroid(self.h, table, c, gamma, w_ptr, ldw, stream), "salt_fuse_centroid")
+
+    def fuse_centroid_status(self, table: int, c: int, gamma: float, w_ptr: int, ldw: int, stream: int = 0) -> int:
+        return lib.salt_fuse_centroid(self.h, table, c, gamma, w_ptr, ldw, stream)
+
+    def fuse_centroid_timed(self, table: int, c: int, gamma: float, w_ptr: int, ldw: int, stream: int,
+                            start_event: int, stop_event: int):
+        """``fuse_centroid`` whose two HIP events record the kernel's own start and end."""
+        self._check(lib.salt_fuse_centroid_timed(self.h, table, c, gamma, w_ptr, ldw, stream, start_event,
+                                                 stop_event), "salt_fuse_centroid_timed")
 
 
 class Plan:

@@ -43,9 +43,10 @@ import numpy as np
 SEED_ROOT = (2608, 3579)
 
 # stream kinds (part of the SeedSequence entropy)
-_K_MAP, _K_CENT, _K_RES, _K_X, _K_Y0, _K_GAMMA, _K_SEGLEN = range(7)
+_K_MAP, _K_CENT, _K_RES, _K_X, _K_Y0, _K_GAMMA, _K_SEGLEN, _K_W = range(8)
 
 ADAPTER_STD = 0.02   # A, B ~ N(0, 0.02^2)
+BASE_STD = 0.02      # base weight entries ~ N(0, 0.02^2) (a centroid is folded into it)
 GAMMA_BINS = (0.6, 0.8, 1.0)   # discrete centroid scales, Sec. 3.3
 
 # Decoder-layer projection shapes (in -> out). "All linear layers" are the LoRA
@@ -238,6 +239,19 @@ class Workload:
             a = rng.standard_normal(size=(self.T, n_in), dtype=np.float32)
         if rows is not None:
             a = a[np.asarray(rows)]
+        return self._encode(a)
+
+    def base_weight(self, table: int, ldw: Optional[int] = None) -> np.ndarray:
+        """Base weight of one table, [in][ldw] storage form (ldw >= out; the
+        columns past out are drawn too and must come back unchanged from a fuse).
+        Exact variant: integers in [-8, 8]."""
+        _, n_in, n_out = self.tables[table]
+        ldw = n_out if ldw is None else int(ldw)
+        rng = _rng(self.cfg, self.seed, _K_W, table)
+        if self.exact:
+            a = rng.integers(-8, 9, size=(n_in, ldw)).astype(np.float32)
+        else:
+            a = _normal(rng, (n_in, ldw), BASE_STD)
         return self._encode(a)
 
     def y0(self, table: int, rows: Optional[Sequence[int]] = None) -> np.ndarray:

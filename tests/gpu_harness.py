@@ -35,6 +35,18 @@ def close_enough(got: np.ndarray, ref: np.ndarray, tol: float):
     return bool(np.all(err <= bound)), float(ratio.max(initial=0.0)), int(np.sum(err > bound))
 
 
+def fuse_within_bound(got: np.ndarray, ref: np.ndarray, w0: np.ndarray, a: np.ndarray, b: np.ndarray,
+                      gamma: float, dtype: str):
+    """Bound of a fused weight (rne of W + gamma * A B with an fp32 contraction):
+    one rounding of the result, 2^-8 |ref| for bf16 (2^-22 for fp32), plus the
+    fp32 accumulation error, 2^-16 (|W| + |gamma| sum_r |A_ir B_ro|).  Returns
+    (ok, worst ratio, n_bad)."""
+    rel = 2.0 ** -8 if dtype == "bf16" else 2.0 ** -22
+    bound = rel * np.abs(ref) + 2.0 ** -16 * (np.abs(w0) + abs(gamma) * (np.abs(a).T @ np.abs(b)))
+    err = np.abs(got - ref)
+    return bool(np.all(err <= bound)), float(np.max(err / bound, initial=0.0)), int(np.sum(err > bound))
+
+
 class Run:
     """One context + one plan for workload ``w``; residual generations per slot."""
 

@@ -58,3 +58,27 @@ def test_gate_rejects_planted_mistakes(cfg, kw):
     for name, m in mutants.items():
         passed, worst, nbad = close_enough(to_bf16_values(m), ref, TOL_NORTH_STAR)
         assert not passed, f"cfg {cfg}: the gate accepts '{name}' (worst {worst:.2f}x)"
+
+
+# ---------------------------------------------------------------------------
+# the fused-weight bound (salt_fuse_centroid parity) against planted mistakes
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("kind", ["dropped", "negated", "gamma_ignored", "other_centroid", "b_rank_reversed"])
+def test_fuse_bound_rejects_planted_mistakes(kind):
+    from tests.gpu_harness import fuse_within_bound
+    tables = [("a", 264, 200)]
+    one = np.zeros(1, np.int32)
+    w = synth.Workload(cfg=6, seed=0, name="fuse", dtype="bf16", tables=tables, n_centroids=2, r_c=32,
+                       n_slots=1, r_u_max=0, slot_rank=one, tok_c=one - 1, tok_u=one - 1, gamma=None)
+    at, b = (oracle.decode(a, "bf16") for a in w.centroids(0))
+    W0 = oracle.decode(w.base_weight(0), "bf16")
+    gamma = 0.6
+    ref = oracle.fuse_centroid(W0, at[0], b[0], gamma)
+    good = to_bf16_values(ref)
+    assert fuse_within_bound(good, ref, W0, at[0], b[0], gamma, "bf16")[0]
+    bad = {"dropped": W0,
+           "negated": oracle.fuse_centroid(W0, at[0], b[0], -gamma),
+           "gamma_ignored": oracle.fuse_centroid(W0, at[0], b[0], 1.0),
+           "other_centroid": oracle.fuse_centroid(W0, at[1], b[1], gamma),
+           "b_rank_reversed": oracle.fuse_centroid(W0, at[0], b[0][::-1], gamma)}[kind]
+    assert not fuse_within_bound(to_bf16_values(bad), ref, W0, at[0], b[0], gamma, "bf16")[0], kind

@@ -28,7 +28,7 @@ def test_no_kernel_uses_scratch():
         assert res.returncode == 0, res.stderr[-2000:]
         meta = open(out).read()
     kernels = re.findall(r"\.name:\s+(\S+)\n(.*?)(?=\n  - \.|\Z)", meta, re.S)
-    kernels = [(n, b) for n, b in kernels if any(k in n for k in ("k_apply", "k_shrink", "k_expand", "k_plan"))]
+    kernels = [(n, b) for n, b in kernels if any(k in n for k in ("k_apply", "k_shrink", "k_expand", "k_plan", "k_fuse"))]
     assert kernels, "no kernel metadata found"
     for name, body in kernels:
         priv = int(re.search(r"\.private_segment_fixed_size:\s+(\d+)", body).group(1))

@@ -303,3 +303,77 @@ def test_pins_catch_planted_mistakes(kind):
         got = bad(*case[:5], case[5], case[6], case[7])
         caught.append(not np.allclose(got, want, rtol=1e-9, atol=1e-9))
     assert any(caught), kind
+
+
+# ---------------------------------------------------------------------------
+# O3: a centroid fused into the base weight (Sec. 3.3)
+# ---------------------------------------------------------------------------
+def _fuse_case(seed, n_in=8, n_out=6, C=3, rc=4, S=3, T=7):
+    rng = np.random.default_rng(100 + seed)
+    w = rng.standard_normal((n_in, n_out))
+    x = rng.standard_normal((T, n_in))
+    cat = rng.standard_normal((C, rc, n_in))
+    cb = rng.standard_normal((C, rc, n_out))
+    res = {s: (rng.standard_normal((2, n_in)), rng.standard_normal((2, n_out))) for s in range(S)}
+    tok_u = rng.integers(-1, S, size=T).astype(np.int32)
+    return w, x, cat, cb, res, tok_u
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+@pytest.mark.parametrize("gamma", [1.0, 0.6, -0.8])
+def test_fused_node_serves_the_same_outputs(seed, gamma):
+    """Sec. 3.3: a node whose weight holds W_base + gamma * Wbar and adds only the
+    residual (c = -1) serves what a node with the plain base weight serves when
+    it adds gamma * centroid + residual (the apply, pinned on its own above)."""
+    w, x, cat, cb, res, tok_u = _fuse_case(seed)
+    T = x.shape[0]
+    for c in range(cat.shape[0]):
+        g = np.full(T, gamma)
+        unfused = oracle.apply(x, x @ w, cat, cb, res, np.full(T, c, np.int32), tok_u, g)
+        fused_w = oracle.fuse_centroid(w, cat[c], cb[c], gamma)
+        fused = oracle.apply(x, x @ fused_w, cat, cb, res, np.full(T, -1, np.int32), tok_u)
+        np.testing.assert_allclose(fused, unfused, rtol=1e-12, atol=1e-12)
+
+
+def test_fuse_rank_one_unit_factors_touch_one_entry():
+    """With A = e_i (one rank, column i) and B = e_o, Wbar has a single nonzero
+    entry, 1 at (i, o): only W[i][o] moves, by gamma."""
+    rng = np.random.default_rng(7)
+    w = rng.standard_normal((5, 4))
+    for i in range(5):
+        for o in range(4):
+            at = np.zeros((1, 5)); at[0, i] = 1.0
+            b = np.zeros((1, 4)); b[0, o] = 1.0
+            got = oracle.fuse_centroid(w, at, b, 0.6)
+            want = w.copy(); want[i, o] += 0.6
+            assert np.array_equal(got, want)
+
+
+def test_fuse_gamma_zero_and_round_trip():
+    w, _, cat, cb, _, _ = _fuse_case(3)
+    assert np.array_equal(oracle.fuse_centroid(w, cat[0], cb[0], 0.0), w)
+    back = oracle.fuse_centroid(oracle.fuse_centroid(w, cat[1], cb[1], 0.8), cat[1], cb[1], -0.8)
+    np.testing.assert_allclose(back, w, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("kind", ["transposed", "gamma_ignored", "sign", "rank_reversed_b"])
+def test_fuse_pins_catch_planted_mistakes(kind):
+    """Plausible mistakes in a copy of the fuse formula fail the served-output pin."""
+    def bad(w, at, b, gamma):
+        if kind == "transposed":
+            m = (at.T @ b)
+            return w + gamma * (m if m.shape != m.T.shape else m.T)
+        if kind == "gamma_ignored":
+            return w + at.T @ b
+        if kind == "sign":
+            return w - gamma * (at.T @ b)
+        return w + gamma * (at.T @ b[::-1])
+    caught = False
+    for seed in range(3):
+        w, x, cat, cb, res, tok_u = _fuse_case(seed, n_in=6, n_out=6)
+        T = x.shape[0]
+        g = np.full(T, 0.6)
+        unfused = oracle.apply(x, x @ w, cat, cb, res, np.zeros(T, np.int32), tok_u, g)
+        fused = oracle.apply(x, x @ bad(w, cat[0], cb[0], 0.6), cat, cb, res, np.full(T, -1, np.int32), tok_u)
+        caught |= not np.allclose(fused, unfused, rtol=1e-9, atol=1e-9)
+    assert caught, kind
