@@ -349,7 +349,76 @@ WORKLOADS = {
     "zipf-baseline": dict(cfg=5, rot=4, baseline=True, steps=200, warmup=20),
     # Sec. 3.3: a centroid fused into the base weights of one Llama-3.2-3B layer
     "fuse": dict(cfg=5, rot=2, steps=20, warmup=3, fuse=True),
+    # Sec. 3.1 Eq. 2 / Sec. 4.5: layer-wise cosine of two rank-16 adapters over the
+    # 196 tables of the 28-layer Llama-3.2-3B
+    "gram": dict(cfg=3, rot=1, steps=10, warmup=2, gram=True),
 }
+
+
+def gram_workload(rank=16):
+    """Two rank-`rank` adapters over the 196 tables of the 28-layer Llama-3.2-3B, in
+    residual-blob layout (slots 0 and 1 of a seeded workload)."""
+    from paper_2608_03579_amd import synth
+    tables = synth.make(3, 0).tables
+    z = np.zeros(1, np.int32)
+    return synth.Workload(cfg=7, seed=1, name="gram", dtype="bf16", tables=tables, n_centroids=0, r_c=0,
+                          n_slots=2, r_u_max=rank, slot_rank=np.array([rank, rank], np.int32), tok_c=z - 1,
+                          tok_u=z - 1, gamma=None)
+
+
+def run_gram(args, hip, salt, rank=16):
+    w = gram_workload(rank)
+    tables = [(i, o) for _, i, o in w.tables]
+    ctx = salt.Context("bf16", tables, 0, 0, 1, 0, 1)
+    d1 = hip.DeviceArray.from_host(w.residual_blob(0))
+    d2 = hip.DeviceArray.from_host(w.residual_blob(1))
+    stream = hip.Stream()
+    nbytes = 2 * rank * sum(i + o for i, o in tables) * 2
+    for _ in range(args.warmup):
+        ctx.adapter_gram(d1.ptr, rank, d2.ptr, rank, stream.h)
+    e0, e1 = hip.Event(), hip.Event()
+    times, walls = [], []
+    for _ in range(args.steps):
+        t0 = time.perf_counter()
+        e0.record(stream)
+        terms = ctx.adapter_gram(d1.ptr, rank, d2.ptr, rank, stream.h)
+        e1.record(stream)
+        stream.synchronize()
+        walls.append(time.perf_counter() - t0)
+        times.append(e0.elapsed_ms(e1))
+    cos = terms[:, 0] / (np.sqrt(terms[:, 1] * terms[:, 2]) + 1e-8)
+    ms = float(np.median(times))
+    log(f"gram: {len(tables)} tables, {nbytes / 1e6:.1f} MB of factors; stream time {ms * 1e3:.1f} us "
+        f"(median of {args.steps}), call wall {np.median(walls) * 1e6:.1f} us; |cos| max {np.abs(cos).max():.4f}")
+    e0.destroy(); e1.destroy()
+    d1.free(); d2.free()
+    ctx.close()
+    return w, {"ms": ms, "wall_ms": float(np.median(walls)) * 1e3, "bytes": nbytes}
+
+
+def cpu_gram_baseline(w, rank=16, budget_s=12.0):
+    """GB/s of the oracle (dense updates formed in float64, one BLAS thread) on the
+    same tables, counted with the same bytes of factors."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_limits
+        limiter = threadpool_limits(limits=1)
+    except Exception:   # pragma: no cover
+        limiter = None
+    done, nbytes = 0, 0.0
+    t0 = time.perf_counter()
+    while time.perf_counter() - t0 < budget_s and done < len(w.tables):
+        at1, b1 = (oracle.decode(a, "bf16") for a in w.residual(0, done))
+        at2, b2 = (oracle.decode(a, "bf16") for a in w.residual(1, done))
+        oracle.update_terms(at1, b1, at2, b2)
+        nbytes += 2 * rank * (at1.shape[1] + b1.shape[1]) * 2
+        done += 1
+    dt = time.perf_counter() - t0
+    if limiter is not None and hasattr(limiter, "unregister"):
+        limiter.unregister()
+    return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
+            "sample": f"{done} of {len(w.tables)} tables (dense updates in fp64) in {dt:.1f} s; BLAS limited to "
+                      f"1 thread; host has {os.cpu_count()} logical cpus"}
 
 
 def fuse_bytes(n_in, n_out, r_c, esize=2):
@@ -486,6 +555,26 @@ def main():
         print("no HIP device visible", file=sys.stderr)
         sys.exit(1)
     hip.set_device(0)
+    if spec.get("gram"):
+        w, res = run_gram(args, hip, salt)
+        cpu = None if args.no_cpu else cpu_gram_baseline(w)
+        achieved = res["bytes"] / (res["ms"] * 1e-3) / 1e9
+        print(json.dumps({
+            "metric": "Adapter cosine in factor space (Sec. 3.1 Eq. 2, Sec. 4.5): achieved HBM GB/s, Llama-3.2-3B",
+            "value": achieved, "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": res["ms"], "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+            "dtype": "bf16", "data": "synthetic",
+            "config": {"workload": "two rank-16 adapters, 196 tables of the 28-layer Llama-3.2-3B",
+                       "step": "salt_adapter_gram (Grams over in and out, fp32; products in fp64)"},
+            "call_wall_ms": res["wall_ms"],
+            "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                         "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
+                         "kernel": "k_gram + k_gram_finish (salt_adapter_gram)",
+                         "bytes_per_launch": res["bytes"], "avg_us": res["ms"] * 1e3,
+                         "timing": "avg_us: median stream time of the whole call (descriptor upload, Gram "
+                                   "buffer clear, both kernels, result copy) between HIP events"},
+            "cpu_baseline": cpu}), flush=True)
+        return
     if spec.get("fuse"):
         res = run_fuse(w, args, hip, salt)
         cpu = None if args.no_cpu else cpu_fuse_baseline(w)

@@ -241,6 +241,25 @@ SALT_API salt_status salt_fuse_centroid(salt_ctx* ctx, int32_t table, int32_t c,
 SALT_API salt_status salt_fuse_centroid_timed(salt_ctx* ctx, int32_t table, int32_t c, float gamma, void* w,
                                               int64_t ldw, void* stream, void* start_event, void* stop_event);
 
+/* ---- adapter similarity in factor space -------------------------------------------------
+ * Sec. 3.1, Eq. 2: the alignment penalty between two low-rank updates is one
+ * minus their matrix cosine, L_align(dW1, dW2) = 1 - Tr(dW1^T dW2) /
+ * (||dW1||_F ||dW2||_F + 1e-8); Sec. 4.5 compares adapters and the centroid layer
+ * by layer with the same cosine.  With dW = A B (A in x r, B r x out) the three
+ * terms are sums over r x r Gram products, so the in x out updates are never
+ * formed:  Tr(dW1^T dW2) = sum_ab (A1^T A2)_ab (B1 B2^T)_ab and
+ * ||dW||_F^2 = sum_ab (A^T A)_ab (B B^T)_ab.
+ *   blob1, blob2: device, 16-byte aligned, laid out like residual blobs of the
+ *       context (for each table, At[r][in] then B[r][out], context dtype), ranks
+ *       r1, r2 in [1, 256]; a centroid is passed the same way.
+ *   out: host, [n_tables][3] doubles: Tr(dW1^T dW2), ||dW1||_F^2, ||dW2||_F^2 per table.
+ * The Grams accumulate in fp32 (MFMA over in and over out), their elementwise
+ * products in fp64.  Allocates temporary device memory, enqueues on `stream`
+ * and synchronises it before returning.  Errors: SALT_ERR_OUT_OF_RANGE (rank),
+ * SALT_ERR_INVALID_ARG (null or misaligned pointer), SALT_ERR_OUT_OF_MEMORY. */
+SALT_API salt_status salt_adapter_gram(salt_ctx* ctx, const void* blob1, int32_t r1, const void* blob2,
+                                       int32_t r2, double* out, void* stream);
+
 /* ---- diagnostics -------------------------------------------------------------------- */
 SALT_API const char* salt_status_str(salt_status s);
 SALT_API const char* salt_last_error(const salt_ctx* ctx);

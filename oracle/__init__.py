@@ -3,4 +3,4 @@
 Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s ``cpu_baseline``
 leg may import this package.  The product path never imports or calls it.
 """
-from .ref import adapter_bytes, apply, decode, fuse_centroid, plan  # noqa: F401
+from .ref import adapter_bytes, align_loss, apply, decode, fuse_centroid, plan, update_terms  # noqa: F401

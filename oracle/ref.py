@@ -171,6 +171,25 @@ def fuse_centroid(w: np.ndarray, at: np.ndarray, b: np.ndarray, gamma: float) ->
 
 
 # --------------------------------------------------------------------------
+# O4: the alignment penalty / matrix cosine of two updates (Sec. 3.1, Eq. 2)
+# --------------------------------------------------------------------------
+def update_terms(at1: np.ndarray, b1: np.ndarray, at2: np.ndarray, b2: np.ndarray) -> Tuple[float, float, float]:
+    """(Tr(dW1^T dW2), ||dW1||_F^2, ||dW2||_F^2), float64, from the dense updates.
+
+    dW_k = A_k B_k is formed explicitly (in x out) from the storage factors
+    At_k [r_k][in] and B_k [r_k][out]; Tr(X^T Y) is the sum of the elementwise
+    product of X and Y."""
+    dw1 = at1.T @ b1
+    dw2 = at2.T @ b2
+    return float(np.sum(dw1 * dw2)), float(np.sum(dw1 * dw1)), float(np.sum(dw2 * dw2))
+
+
+def align_loss(inner: float, norm1_sq: float, norm2_sq: float, eps: float = 1e-8) -> float:
+    """Eq. 2: 1 - Tr(dW1^T dW2) / (||dW1||_F ||dW2||_F + eps), eps = 1e-8 (Sec. 3.1)."""
+    return 1.0 - inner / (np.sqrt(norm1_sq) * np.sqrt(norm2_sq) + eps)
+
+
+# --------------------------------------------------------------------------
 # swap footprint (Table 1 and the appendix tables, Memory (MB) columns)
 # --------------------------------------------------------------------------
 def adapter_bytes(rank: int, shapes: Sequence[Tuple[int, int]], n_layers: int = 1,

@@ -95,12 +95,34 @@ struct FuseArgs {
   float gamma;
 };
 
+// Gram products of two low-rank updates dW_k = A_k B_k per table (factor form):
+// g holds, per table and factor side (At: over in, B: over out), the Grams
+// X1 X2^T [nb1*16][nb2*16], X1 X1^T [nb1*16][nb1*16], X2 X2^T [nb2*16][nb2*16]
+// (ranks padded to 16); out[3 t + 0..2] = Tr(dW1^T dW2), ||dW1||^2, ||dW2||^2.
+struct GramTable {
+  const void* at1;          // [r1][in]
+  const void* b1;           // [r1][out]
+  const void* at2;          // [r2][in]
+  const void* b2;           // [r2][out]
+  int32_t in_dim, out_dim;
+};
+struct GramArgs {
+  const GramTable* tabs;    // [n_tables], device
+  int32_t n_tables, r1, r2;
+  float* g;                 // zeroed by the caller
+  size_t g_table, g_side;   // floats per table, per factor side
+  int32_t g_12, g_11, g_22; // floats of each Gram
+  double* out;              // [n_tables][3], device
+};
+
 hipError_t kernels_init(int device);
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s);
 // e0 / e1: if set, HIP events that record the apply kernel's own start and end.
 hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 // e0 / e1 as for launch_apply.
 hipError_t launch_fuse(const FuseArgs& f, int bf16, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
+// k_gram then k_gram_finish on s; max_in / max_out: largest in / out over the tables.
+hipError_t launch_gram(const GramArgs& a, int max_in, int max_out, int bf16, hipStream_t s);
 // Blocks of the two-launch apply's shrink and expand kernels one compute unit
 // holds at once (bf16, r_u_max <= 2).
 hipError_t two_pass_occupancy(int r_c, int r_u_max, int R, int* shrink_per_cu, int* expand_per_cu);

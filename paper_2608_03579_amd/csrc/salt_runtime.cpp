@@ -132,6 +132,7 @@ void transpose_rank_major(const W* src, W* dst, size_t n, size_t rc, size_t out)
   }
 }
 
+constexpr int kMaxGramRank = 256;   // largest adapter rank of salt_adapter_gram
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // Split-K partial sums go through device atomics unless the context asked for
@@ -677,6 +678,72 @@ salt_status salt_fuse_centroid_timed(salt_ctx* ctx, int32_t table, int32_t c, fl
                                      void* stream, void* start_event, void* stop_event) {
   if (!start_event || !stop_event) return fail(ctx, SALT_ERR_INVALID_ARG, "null event");
   return fuse_impl(ctx, table, c, gamma, w, ldw, stream, (hipEvent_t)start_event, (hipEvent_t)stop_event);
+}
+
+salt_status salt_adapter_gram(salt_ctx* ctx, const void* blob1, int32_t r1, const void* blob2, int32_t r2,
+                              double* out, void* stream) {
+  if (!ctx || !out) return SALT_ERR_INVALID_ARG;
+  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  if (r1 < 1 || r1 > kMaxGramRank || r2 < 1 || r2 > kMaxGramRank)
+    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "adapter ranks %d, %d not in [1, %d]", r1, r2, kMaxGramRank);
+  if (!blob1 || !blob2 || !aligned16(blob1) || !aligned16(blob2))
+    return fail(ctx, SALT_ERR_INVALID_ARG, "null or misaligned adapter");
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  hipStream_t s = (hipStream_t)stream;
+  const int nt = ctx->cfg.n_tables;
+  const size_t es = ctx->esize;
+  std::vector<salt::GramTable> tabs(nt);
+  size_t prefix = 0;
+  int max_in = 0, max_out = 0;
+  for (int t = 0; t < nt; ++t) {
+    const salt_shape sh = ctx->tables[t];
+    salt::GramTable& g = tabs[t];
+    g.at1 = static_cast<const char*>(blob1) + (size_t)r1 * prefix * es;
+    g.b1 = static_cast<const char*>(g.at1) + (size_t)r1 * sh.in_dim * es;
+    g.at2 = static_cast<const char*>(blob2) + (size_t)r2 * prefix * es;
+    g.b2 = static_cast<const char*>(g.at2) + (size_t)r2 * sh.in_dim * es;
+    g.in_dim = sh.in_dim;
+    g.out_dim = sh.out_dim;
+    prefix += (size_t)sh.in_dim + sh.out_dim;
+    max_in = std::max(max_in, sh.in_dim);
+    max_out = std::max(max_out, sh.out_dim);
+  }
+  const int p1 = (r1 + 15) / 16 * 16, p2 = (r2 + 15) / 16 * 16;
+  salt::GramArgs a{};
+  a.n_tables = nt;
+  a.r1 = r1;
+  a.r2 = r2;
+  a.g_12 = p1 * p2;
+  a.g_11 = p1 * p1;
+  a.g_22 = p2 * p2;
+  a.g_side = (size_t)a.g_12 + a.g_11 + a.g_22;
+  a.g_table = 2 * a.g_side;
+  const size_t g_bytes = sizeof(float) * a.g_table * nt;
+  void* tabs_d = nullptr;
+  void* g_d = nullptr;
+  void* out_d = nullptr;
+  auto release = [&]() {
+    if (tabs_d) (void)hipFree(tabs_d);
+    if (g_d) (void)hipFree(g_d);
+    if (out_d) (void)hipFree(out_d);
+  };
+  if (hipMalloc(&tabs_d, sizeof(salt::GramTable) * nt) != hipSuccess || hipMalloc(&g_d, g_bytes) != hipSuccess ||
+      hipMalloc(&out_d, sizeof(double) * 3 * nt) != hipSuccess) {
+    (void)hipGetLastError();
+    release();
+    return fail(ctx, SALT_ERR_OUT_OF_MEMORY, "adapter Gram scratch (%zu bytes)", g_bytes);
+  }
+  a.tabs = static_cast<const salt::GramTable*>(tabs_d);
+  a.g = static_cast<float*>(g_d);
+  a.out = static_cast<double*>(out_d);
+  hipError_t e = hipMemcpyAsync(tabs_d, tabs.data(), sizeof(salt::GramTable) * nt, hipMemcpyHostToDevice, s);
+  if (e == hipSuccess) e = hipMemsetAsync(g_d, 0, g_bytes, s);
+  if (e == hipSuccess) e = salt::launch_gram(a, max_in, max_out, ctx->cfg.dtype == SALT_BF16, s);
+  if (e == hipSuccess) e = hipMemcpyAsync(out, out_d, sizeof(double) * 3 * nt, hipMemcpyDeviceToHost, s);
+  if (e == hipSuccess) e = hipStreamSynchronize(s);
+  release();
+  SALT_HIP(ctx, e);
+  return SALT_OK;
 }
 
 }  // extern "C"

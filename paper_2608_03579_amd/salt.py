@@ -27,7 +27,7 @@ EXPORTS = (
     "salt_residual_bytes_for", "salt_load_residual", "salt_wait_loads", "salt_host_alloc",
     "salt_host_free", "salt_plan_create", "salt_plan_destroy", "salt_plan_set_maps",
     "salt_plan_build", "salt_plan_download", "salt_plan_errors", "salt_plan_tiling", "salt_apply",
-    "salt_apply_timed", "salt_fuse_centroid", "salt_fuse_centroid_timed",
+    "salt_apply_timed", "salt_fuse_centroid", "salt_fuse_centroid_timed", "salt_adapter_gram",
     "salt_status_str",
     "salt_last_error", "salt_version",
 )
@@ -74,6 +74,7 @@ def _load() -> C.CDLL:
         "salt_apply_timed": (C.c_int, [P, I32, P, VP, VP, VP, VP, VP]),
         "salt_fuse_centroid": (C.c_int, [P, I32, I32, C.c_float, VP, C.c_int64, VP]),
         "salt_fuse_centroid_timed": (C.c_int, [P, I32, I32, C.c_float, VP, C.c_int64, VP, VP, VP]),
+        "salt_adapter_gram": (C.c_int, [P, VP, I32, VP, I32, C.POINTER(C.c_double), VP]),
         "salt_status_str": (C.c_char_p, [C.c_int]),
         "salt_last_error": (C.c_char_p, [P]),
         "salt_version": (I32, []),
@@ -233,6 +234,18 @@ class Context:
 
     def fuse_centroid_status(self, table: int, c: int, gamma: float, w_ptr: int, ldw: int, stream: int = 0) -> int:
         return lib.salt_fuse_centroid(self.h, table, c, gamma, w_ptr, ldw, stream)
+
+    def adapter_gram(self, blob1_ptr: int, r1: int, blob2_ptr: int, r2: int, stream: int = 0) -> np.ndarray:
+        """Per table (Tr(dW1^T dW2), ||dW1||^2, ||dW2||^2) of two adapter blobs in device memory."""
+        out = np.zeros((len(self.tables), 3), dtype=np.float64)
+        self._check(lib.salt_adapter_gram(self.h, blob1_ptr, r1, blob2_ptr, r2,
+                                          out.ctypes.data_as(C.POINTER(C.c_double)), stream), "salt_adapter_gram")
+        return out
+
+    def adapter_gram_status(self, blob1_ptr: int, r1: int, blob2_ptr: int, r2: int, stream: int = 0) -> int:
+        out = np.zeros((len(self.tables), 3), dtype=np.float64)
+        return lib.salt_adapter_gram(self.h, blob1_ptr, r1, blob2_ptr, r2,
+                                     out.ctypes.data_as(C.POINTER(C.c_double)), stream)
 
     def fuse_centroid_timed(self, table: int, c: int, gamma: float, w_ptr: int, ldw: int, stream: int,
                             start_event: int, stop_event: int):

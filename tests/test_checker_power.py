@@ -82,3 +82,35 @@ def test_fuse_bound_rejects_planted_mistakes(kind):
            "other_centroid": oracle.fuse_centroid(W0, at[1], b[1], gamma),
            "b_rank_reversed": oracle.fuse_centroid(W0, at[0], b[0][::-1], gamma)}[kind]
     assert not fuse_within_bound(to_bf16_values(bad), ref, W0, at[0], b[0], gamma, "bf16")[0], kind
+
+
+# ---------------------------------------------------------------------------
+# the adapter-Gram bound (salt_adapter_gram parity) against planted mistakes
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("kind", ["b_gram_transposed", "second_adapter_truncated", "norm_not_squared",
+                                  "cross_with_own_b", "sign"])
+def test_gram_bound_rejects_planted_mistakes(kind):
+    rng = np.random.default_rng(5)
+    r, rx, n_in, n_out = 8, 2, 520, 776
+    to = lambda a: oracle.decode(synth.f32_to_bf16_bits((a * 0.02).astype(np.float32)), "bf16")
+    A1, B1 = to(rng.standard_normal((r, n_in))), to(rng.standard_normal((r, n_out)))
+    Ax, Bx = to(rng.standard_normal((rx, n_in))), to(rng.standard_normal((rx, n_out)))
+    A2, B2 = np.concatenate([A1[::-1], Ax]), np.concatenate([B1[::-1], Bx])   # dW2 = dW1 + dWx
+    ref = np.array(oracle.update_terms(A1, B1, A2, B2))
+    t_abs = np.array([oracle.update_terms(np.abs(A1), np.abs(B1), np.abs(A2), np.abs(B2))[0],
+                      oracle.update_terms(np.abs(A1), np.abs(B1), np.abs(A1), np.abs(B1))[0],
+                      oracle.update_terms(np.abs(A2), np.abs(B2), np.abs(A2), np.abs(B2))[0]])
+    ga = A1 @ A2.T                                    # Gram of the At rows (r x (r + rx))
+    gb = B1 @ B2.T
+    bad = ref.copy()
+    if kind == "b_gram_transposed":
+        bad[0] = np.sum(ga[:, :r] * gb[:, :r].T) + np.sum(ga[:, r:] * gb[:, r:])   # r x r block transposed
+    elif kind == "second_adapter_truncated":
+        bad[0] = oracle.update_terms(A1, B1, A2[:r], B2[:r])[0]                    # extra rows of adapter 2 lost
+    elif kind == "norm_not_squared":
+        bad[1] = np.sqrt(ref[1])
+    elif kind == "cross_with_own_b":
+        bad[0] = np.sum(ga[:, :r] * (B1 @ B1.T)[:, ::-1])                          # B side of the cross term from adapter 1
+    else:
+        bad[0] = -ref[0]
+    assert not np.all(np.abs(bad - ref) <= 2.0 ** -16 * t_abs), kind

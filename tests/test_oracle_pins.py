@@ -377,3 +377,63 @@ def test_fuse_pins_catch_planted_mistakes(kind):
         fused = oracle.apply(x, x @ bad(w, cat[0], cb[0], 0.6), cat, cb, res, np.full(T, -1, np.int32), tok_u)
         caught |= not np.allclose(fused, unfused, rtol=1e-9, atol=1e-9)
     assert caught, kind
+
+
+# ---------------------------------------------------------------------------
+# O4: the alignment penalty of Eq. 2 (matrix cosine of two updates)
+# ---------------------------------------------------------------------------
+def _factors(rng, r, n_in=7, n_out=5):
+    return rng.standard_normal((r, n_in)), rng.standard_normal((r, n_out))
+
+
+def test_update_terms_match_pure_python_loops():
+    """Brute force: Tr(dW1^T dW2) and the Frobenius norms entry by entry, with the
+    updates built from the factors by explicit sums (no matrix products)."""
+    rng = np.random.default_rng(11)
+    at1, b1 = _factors(rng, 3)
+    at2, b2 = _factors(rng, 2)
+    n_in, n_out = at1.shape[1], b1.shape[1]
+    def dw(at, b):
+        return [[sum(at[r][i] * b[r][o] for r in range(at.shape[0])) for o in range(n_out)] for i in range(n_in)]
+    d1, d2 = dw(at1, b1), dw(at2, b2)
+    inner = sum(d1[i][o] * d2[i][o] for i in range(n_in) for o in range(n_out))
+    n1 = sum(d1[i][o] ** 2 for i in range(n_in) for o in range(n_out))
+    n2 = sum(d2[i][o] ** 2 for i in range(n_in) for o in range(n_out))
+    got = oracle.update_terms(at1, b1, at2, b2)
+    np.testing.assert_allclose(got, (inner, n1, n2), rtol=1e-12)
+
+
+def test_align_loss_special_cases():
+    """Eq. 2 on cases with a known cosine: an update against itself or a positive
+    multiple of itself (cosine 1), against its negative (cosine -1), against an update
+    on disjoint input coordinates (Tr = 0 exactly, loss 1), and the zero update
+    (eps keeps it finite: loss 1)."""
+    rng = np.random.default_rng(12)
+    at, b = _factors(rng, 2, n_in=8)
+    eps = 1e-8
+    n = oracle.update_terms(at, b, at, b)[1]
+    # cosine +1 / -1: the loss is eps / (s n + eps) or 2 - eps / (n + eps) with s the scale
+    t = oracle.update_terms(at, b, at, b)
+    assert abs(oracle.align_loss(*t) - eps / (n + eps)) < 1e-14
+    t = oracle.update_terms(at, b, 3.0 * at, b)
+    assert abs(oracle.align_loss(*t) - eps / (3.0 * n + eps)) < 1e-14
+    t = oracle.update_terms(at, b, -at, b)
+    assert abs(oracle.align_loss(*t) - (2.0 - eps / (n + eps))) < 1e-14
+    at1 = at.copy(); at1[:, 4:] = 0.0
+    at2 = at.copy(); at2[:, :4] = 0.0
+    t = oracle.update_terms(at1, b, at2, b)
+    assert t[0] == 0.0 and oracle.align_loss(*t) == 1.0
+    t = oracle.update_terms(np.zeros_like(at), b, at, b)
+    assert oracle.align_loss(*t) == 1.0
+
+
+def test_update_terms_invariant_to_factor_rotation():
+    """dW = A B is unchanged by A -> A R, B -> R^T B for an orthogonal r x r R, so
+    the terms are too (a check that the oracle uses the product, not the factors)."""
+    rng = np.random.default_rng(13)
+    at1, b1 = _factors(rng, 4)
+    at2, b2 = _factors(rng, 3)
+    q, _ = np.linalg.qr(rng.standard_normal((4, 4)))
+    base = oracle.update_terms(at1, b1, at2, b2)
+    rot = oracle.update_terms(q.T @ at1, q.T @ b1, at2, b2)   # A R = (R^T At)^T, R^T B
+    np.testing.assert_allclose(rot, base, rtol=1e-10, atol=1e-12)
