@@ -127,6 +127,11 @@ SALT_API size_t salt_residual_bytes_for(salt_dtype dtype, int32_t n_tables, cons
  * in-flight apply still sees the slot's previous residual.  Every later
  * salt_apply whose plan references the slot waits for this copy.  The blob must
  * stay valid and unmodified until the copy completes (salt_wait_loads).
+ * The event that orders the copy behind those applies is recorded on their
+ * stream when it is needed (here, at the plan's next salt_plan_set_maps, or when
+ * the plan moves to another stream), not after every apply, so it also covers
+ * work enqueued on that stream since; the stream of a plan's latest applies must
+ * therefore stay valid until one of those calls or salt_plan_destroy.
  * Errors: SALT_ERR_OUT_OF_RANGE (slot, r_u > r_u_max), SALT_ERR_INVALID_ARG
  * (bytes mismatch), SALT_ERR_NOT_PINNED (pageable blob; no synchronous fallback). */
 SALT_API salt_status salt_load_residual(salt_ctx* ctx, int32_t slot, int32_t r_u, const void* blob,

@@ -62,6 +62,11 @@ struct salt_plan {
   hipStream_t build_stream = nullptr;
   // atomic sums: rows of each v buffer that may be nonzero (all rows below)
   int32_t v_dirty[2] = {0, 0};
+  // Applies of this plan enqueued on reader_stream since its last reader event:
+  // the event that covers them (a swap of one of the plan's slots waits for
+  // it) is recorded only when something needs it, not after every apply.
+  bool readers_open = false;
+  hipStream_t reader_stream = nullptr;
 };
 
 struct salt_ctx {
@@ -179,6 +184,29 @@ hipError_t ring_record(EventRing& r, hipStream_t s, int64_t* seq_out) {
 hipError_t ring_wait(EventRing& r, hipStream_t s, int64_t seq) {
   if (seq < 0 || seq <= r.done) return hipSuccess;
   return hipStreamWaitEvent(s, r.ev[(int)(seq % (int64_t)r.ev.size())], 0);
+}
+
+// Record the reader event that covers the plan's open applies and hand its
+// sequence to every slot the plan references.
+hipError_t close_readers(salt_ctx* ctx, salt_plan* plan) {
+  if (!plan->readers_open) return hipSuccess;
+  int64_t seq;
+  hipError_t e = ring_record(ctx->readers, plan->reader_stream, &seq);
+  if (e != hipSuccess) return e;
+  for (int slot : plan->slots) ctx->slot_reader[slot] = std::max(ctx->slot_reader[slot], seq);
+  plan->readers_open = false;
+  return hipSuccess;
+}
+
+// After an apply of `plan` on `s`: its reads of the plan's slots are open.
+hipError_t open_readers(salt_ctx* ctx, salt_plan* plan, hipStream_t s) {
+  if (plan->readers_open && plan->reader_stream != s) {
+    hipError_t e = close_readers(ctx, plan);
+    if (e != hipSuccess) return e;
+  }
+  plan->readers_open = true;
+  plan->reader_stream = s;
+  return hipSuccess;
 }
 
 void free_plan_buffers(salt_plan* p) {
@@ -404,6 +432,9 @@ salt_status salt_load_residual(salt_ctx* ctx, int32_t slot, int32_t r_u, const v
   }
   SALT_HIP(ctx, hipSetDevice(ctx->device));
   // the swap may not overwrite what an enqueued apply still reads
+  for (salt_plan* p : ctx->plans)
+    if (p->readers_open && std::binary_search(p->slots.begin(), p->slots.end(), slot))
+      SALT_HIP(ctx, close_readers(ctx, p));
   SALT_HIP(ctx, ring_wait(ctx->readers, ctx->side, ctx->slot_reader[slot]));
   if (want > 0)
     SALT_HIP(ctx, hipMemcpyAsync(ctx->pool + (size_t)slot * ctx->slot_stride, blob, want,
@@ -536,6 +567,8 @@ salt_status salt_plan_set_maps(salt_ctx* ctx, salt_plan* plan, int32_t T, const 
   }
   std::sort(slots.begin(), slots.end());
   slots.erase(std::unique(slots.begin(), slots.end()), slots.end());
+  // the previous batch's applies still read the old slots
+  SALT_HIP(ctx, close_readers(ctx, plan));
   plan->slots = slots;
   plan->slot_rank.resize(slots.size());
   for (size_t i = 0; i < slots.size(); ++i) plan->slot_rank[i] = ctx->slot_rank[slots[i]];
@@ -876,9 +909,7 @@ salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
       a.v_clear = nullptr;
     }
     SALT_HIP(ctx, salt::launch_apply(a, 1, salt::kTwoPassM, s, e0, e1));
-    int64_t seq;
-    SALT_HIP(ctx, ring_record(ctx->readers, s, &seq));
-    for (int slot : plan->slots) ctx->slot_reader[slot] = seq;
+    SALT_HIP(ctx, open_readers(ctx, plan, s));
     return SALT_OK;
   }
   // K split.  Small (decode) batches are latency bound: spread the shrink input
@@ -946,9 +977,7 @@ salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
     plan->build_pending = false;
   }
   SALT_HIP(ctx, salt::launch_apply(a, ctx->cfg.dtype == SALT_BF16, M, s, e0, e1));
-  int64_t seq;
-  SALT_HIP(ctx, ring_record(ctx->readers, s, &seq));
-  for (int slot : plan->slots) ctx->slot_reader[slot] = seq;
+  SALT_HIP(ctx, open_readers(ctx, plan, s));
   return SALT_OK;
 }
 

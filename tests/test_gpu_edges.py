@@ -225,6 +225,62 @@ def test_swap_is_ordered_after_inflight_apply():
         run.close()
 
 
+def test_swap_waits_for_applies_of_replaced_maps_and_other_streams():
+    """The reader event of a plan's applies is recorded lazily: when the plan's
+    maps are replaced, when the plan moves to another stream, or when a slot it
+    references is swapped.  Each of those must still order a later swap behind
+    the applies that read the slot."""
+    _announce("swap ordering: replaced maps, second stream")
+    from paper_2608_03579_amd import hip
+    from tests.gpu_harness import to_dev
+    w = synth.make(4, 3)
+    run = Run(w)
+    try:
+        run.set_and_build()
+        t = 4
+        swapped = [int(s) for s in w.meta["swap_slots"]]
+        xd = to_dev(w.x(t))
+        # (1) apply, then new maps without the swapped slots, then the swap
+        y1 = to_dev(w.y0(t))
+        run.ctx.apply(t, run.plan, xd.ptr, y1.ptr, run.stream)
+        keep = ~np.isin(w.tok_u, swapped)
+        tok_u2 = np.where(keep, w.tok_u, -1).astype(np.int32)
+        run.plan.set_maps(w.tok_c, tok_u2, w.gamma, run.stream)
+        for s in swapped:
+            run.load(s, 1)
+        run._stream.synchronize()
+        run.ctx.wait_loads()
+        got1 = oracle.decode(y1.to_host(), w.dtype)
+        for s in swapped:
+            run.gen[s] = 0
+        ref1 = run.oracle_table(t)
+        assert close_enough(got1, ref1, TOL_NORTH_STAR)[0], "swap overtook an apply of the replaced maps"
+        # (2) the plan applied on a second stream, then the swap back to generation 0
+        run.plan.set_maps(w.tok_c, w.tok_u, w.gamma, run.stream)
+        run.plan.build(run.stream)
+        for s in swapped:
+            run.gen[s] = 1
+        other = hip.Stream()
+        run._stream.synchronize()
+        y2, y3 = to_dev(w.y0(t)), to_dev(w.y0(t))
+        run.ctx.apply(t, run.plan, xd.ptr, y2.ptr, run.stream)
+        run._stream.synchronize()                    # applies of one plan are ordered
+        run.ctx.apply(t, run.plan, xd.ptr, y3.ptr, other.h)
+        for s in swapped:
+            run.load(s, 0)
+        run._stream.synchronize()
+        other.synchronize()
+        run.ctx.wait_loads()
+        for s in swapped:
+            run.gen[s] = 1                           # what both applies read (run.load set 0)
+        ref_gen1 = run.oracle_table(t)
+        assert close_enough(oracle.decode(y2.to_host(), w.dtype), ref_gen1, TOL_NORTH_STAR)[0]
+        assert close_enough(oracle.decode(y3.to_host(), w.dtype), ref_gen1, TOL_NORTH_STAR)[0]
+        other.destroy()
+    finally:
+        run.close()
+
+
 def test_prefill_full_size_sampled():
     """28-layer Llama-3.2-3B prefill at full size (196 tables, T = 8192), the
     shapes and launch configuration bench.py times; sampled tables and rows."""
