@@ -183,7 +183,8 @@ __device__ __forceinline__ void store4_coherent(__amdgpu_buffer_rsrc_t r, uint32
 // ---------------------------------------------------------------------------
 // plan
 // ---------------------------------------------------------------------------
-constexpr int kPlanThreads = 256;     // threads of every plan block
+constexpr int kPlanThreads = 256;     // threads of a plan block (the large-batch ranking, an apply's writer)
+constexpr int kPlanSmallThreads = 1024;   // threads of the one-block plan: one wave per run of 64 keys
 constexpr int kPlanTokPerBlock = 64;  // multi-block ranking: four lanes per token
 constexpr int kPlanChunk = 2048;      // keys staged in LDS per pass (multi-block ranking)
 constexpr int kMaxGroups = 72;        // centroid groups: C + 1 <= 65
@@ -281,13 +282,13 @@ struct PlanLds {
 // Sorts maps[0:T] (T <= CAP) by plan key into L.srt / L.c.  Each wave sorts
 // runs of 64 keys across its lanes; a key's rank is its place in its own run
 // plus the number of keys below it in every other run (binary searches).
-template <int CAP>
+template <int CAP, int NT = kPlanThreads>
 __device__ __forceinline__ void plan_sort(const int4* maps, int T, PlanLds<CAP>& L) {
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nrun = (T + 63) >> 6;
-  for (int i = tid; i < T; i += kPlanThreads) L.maps[i] = maps[i];
+  for (int i = tid; i < T; i += NT) L.maps[i] = maps[i];
   __syncthreads();
-  for (int run = wave; run < nrun; run += kPlanThreads / 64) {
+  for (int run = wave; run < nrun; run += NT / 64) {
     const int t = run * 64 + lane;
     uint64_t k = kNoKey;
     if (t < T) {
@@ -297,7 +298,7 @@ __device__ __forceinline__ void plan_sort(const int4* maps, int T, PlanLds<CAP>&
     L.key[t] = wave_sort64(k);
   }
   __syncthreads();
-  for (int run = wave; run < nrun; run += kPlanThreads / 64) {
+  for (int run = wave; run < nrun; run += NT / 64) {
     const uint64_t k = L.key[run * 64 + lane];
     if (k != kNoKey) {
       // the searches in different runs are independent: unrolled, they overlap
@@ -430,13 +431,15 @@ __device__ __forceinline__ void plan_reset_words(const PlanArgs& a, int first, i
       b.ready[(size_t)(e / kMaxSplit) * kReadyPerTile + (size_t)(e % kMaxSplit) * kReadyStride] = 0u;
 }
 
-// Batches of up to kPlanSmallT tokens: one block sorts in LDS.
-__global__ void __launch_bounds__(kPlanThreads) k_plan_small(PlanArgs a) {
+// Batches of up to kPlanSmallT tokens: one block of 16 waves sorts in LDS
+// (each wave one run of 64 keys).
+__global__ void __launch_bounds__(kPlanSmallThreads) k_plan_small(PlanArgs a) {
+  static_assert(kPlanSmallT <= 64 * (kPlanSmallThreads / 64), "one run of 64 keys per wave");
   __shared__ PlanLds<kPlanSmallT> L;
   const int T = a.T, tid = threadIdx.x;
-  plan_reset_words(a, tid, kPlanThreads);
-  plan_sort(a.b.maps, T, L);
-  for (int i = tid; i < T; i += kPlanThreads) {
+  plan_reset_words(a, tid, kPlanSmallThreads);
+  plan_sort<kPlanSmallT, kPlanSmallThreads>(a.b.maps, T, L);
+  for (int i = tid; i < T; i += kPlanSmallThreads) {
     a.b.perm[i] = L.srt[i].x;
     a.b.srt[i] = L.srt[i];
     a.b.srt_c[i] = L.c[i];
@@ -1813,7 +1816,7 @@ hipError_t kernels_init(int device) {
 hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
   if (a.T <= kPlanSmallT) {
-    hipLaunchKernelGGL(k_plan_small, dim3(1), dim3(kPlanThreads), 0, s, a);
+    hipLaunchKernelGGL(k_plan_small, dim3(1), dim3(kPlanSmallThreads), 0, s, a);
   } else {
     const int blocks = (a.T + kPlanTokPerBlock - 1) / kPlanTokPerBlock;
     hipLaunchKernelGGL(k_plan_large, dim3(blocks), dim3(kPlanThreads), 0, s, a);
