@@ -265,6 +265,31 @@ SALT_API salt_status salt_fuse_centroid_timed(salt_ctx* ctx, int32_t table, int3
 SALT_API salt_status salt_adapter_gram(salt_ctx* ctx, const void* blob1, int32_t r1, const void* blob2,
                                        int32_t r2, double* out, void* stream);
 
+/* ---- centroid routing (host only) ------------------------------------------------------
+ * Sec. 3.2: a user's dataset is routed to a centroid of the library, or to the
+ * standard-LoRA fallback, from the token-normalised displacement norms N_k its
+ * profiling subset induces under each of the K centroids and the per-centroid
+ * statistics calibrated at the end of Phase 1:
+ *   stage 1 (out-of-distribution): Z_N,k = |N_k - mu_N,k| / sigma_N,k; the data is
+ *       rejected when min_k Z_N,k > tau_N;
+ *   stage 2 (expert routing): R_k = N_k / (mean of N_j over j != k),
+ *       Z_R,k = |R_k - mu_R,k| / sigma_R,k, k* = argmin_k Z_R,k (lowest k on ties);
+ *       the data is sent to the fallback as blended when Z_R,k* > tau_R.
+ * Inputs are host arrays of K >= 2 finite values (N_k >= 0, sigma > 0, the other
+ * norms of every k not all zero); z_n / z_r (may be NULL) receive Z_N,k / Z_R,k
+ * (Z_R only when stage 1 passes).  No GPU work; no context needed.
+ * Errors: SALT_ERR_INVALID_ARG. */
+typedef struct {
+  int32_t k_star;      /* routed centroid, or -1 for the fallback               */
+  int32_t ood;         /* 1: rejected by stage 1                                  */
+  int32_t blended;     /* 1: passed stage 1, rejected by stage 2's threshold      */
+  double z_n_min;      /* min_k Z_N,k                                             */
+  double z_r_min;      /* min_k Z_R,k (0 when stage 1 rejected)                   */
+} salt_route_result;
+SALT_API salt_status salt_route(int32_t K, const double* n_k, const double* mu_n, const double* sigma_n,
+                                const double* mu_r, const double* sigma_r, double tau_n, double tau_r,
+                                double* z_n, double* z_r, salt_route_result* out);
+
 /* ---- diagnostics -------------------------------------------------------------------- */
 SALT_API const char* salt_status_str(salt_status s);
 SALT_API const char* salt_last_error(const salt_ctx* ctx);

@@ -190,6 +190,41 @@ def align_loss(inner: float, norm1_sq: float, norm2_sq: float, eps: float = 1e-8
 
 
 # --------------------------------------------------------------------------
+# O5: centroid routing (Sec. 3.2, the two-stage activation profiling filter)
+# --------------------------------------------------------------------------
+def route_decide(z_n_min: float, z_r: Sequence[float], tau_n: float, tau_r: float) -> Tuple[int, bool, bool]:
+    """(k*, out_of_distribution, blended) from the two stages' deviations.
+
+    Stage 1 rejects the data when the smallest norm deviation exceeds tau_N.
+    Stage 2 picks the centroid with the smallest ratio deviation; if even that
+    one exceeds tau_R the task is treated as blended and also falls back.
+    k* = -1 means the fallback (standard LoRA)."""
+    if z_n_min > tau_n:
+        return -1, True, False
+    best = min(range(len(z_r)), key=lambda k: (z_r[k], k))
+    if z_r[best] > tau_r:
+        return -1, False, True
+    return best, False, False
+
+
+def route(n: Sequence[float], mu_n: Sequence[float], sigma_n: Sequence[float],
+          mu_r: Sequence[float], sigma_r: Sequence[float], tau_n: float = 2.0,
+          tau_r: float = 2.0) -> Dict[str, object]:
+    """Sec. 3.2 on per-centroid displacement norms N_k and their Phase 1
+    calibration (mu, sigma): Z_N,k = |N_k - mu_N,k| / sigma_N,k; the dominance
+    ratio R_k = N_k / ((1 / (K - 1)) sum_{j != k} N_j); Z_R,k = |R_k - mu_R,k| /
+    sigma_R,k; then ``route_decide``.  Plain Python floats."""
+    K = len(n)
+    z_n = [abs(n[k] - mu_n[k]) / sigma_n[k] for k in range(K)]
+    z_r = []
+    for k in range(K):
+        others = sum(n[j] for j in range(K) if j != k) / (K - 1)
+        z_r.append(abs(n[k] / others - mu_r[k]) / sigma_r[k])
+    k_star, ood, blended = route_decide(min(z_n), z_r, tau_n, tau_r)
+    return {"k_star": k_star, "ood": ood, "blended": blended, "z_n": z_n, "z_r": z_r}
+
+
+# --------------------------------------------------------------------------
 # swap footprint (Table 1 and the appendix tables, Memory (MB) columns)
 # --------------------------------------------------------------------------
 def adapter_bytes(rank: int, shapes: Sequence[Tuple[int, int]], n_layers: int = 1,

@@ -713,6 +713,54 @@ salt_status salt_fuse_centroid_timed(salt_ctx* ctx, int32_t table, int32_t c, fl
   return fuse_impl(ctx, table, c, gamma, w, ldw, stream, (hipEvent_t)start_event, (hipEvent_t)stop_event);
 }
 
+salt_status salt_route(int32_t K, const double* n_k, const double* mu_n, const double* sigma_n,
+                       const double* mu_r, const double* sigma_r, double tau_n, double tau_r, double* z_n,
+                       double* z_r, salt_route_result* out) {
+  if (K < 2 || !n_k || !mu_n || !sigma_n || !mu_r || !sigma_r || !out) return SALT_ERR_INVALID_ARG;
+  if (!std::isfinite(tau_n) || !std::isfinite(tau_r)) return SALT_ERR_INVALID_ARG;
+  double total = 0.0;
+  for (int k = 0; k < K; ++k) {
+    if (!std::isfinite(n_k[k]) || n_k[k] < 0.0 || !std::isfinite(mu_n[k]) || !std::isfinite(mu_r[k]) ||
+        !(sigma_n[k] > 0.0) || !(sigma_r[k] > 0.0) || !std::isfinite(sigma_n[k]) || !std::isfinite(sigma_r[k]))
+      return SALT_ERR_INVALID_ARG;
+    total += n_k[k];
+  }
+  for (int k = 0; k < K; ++k)
+    if (!(total - n_k[k] > 0.0)) return SALT_ERR_INVALID_ARG;   // mean of the others must be positive
+  salt_route_result r{};
+  r.k_star = -1;
+  // stage 1: distance of each norm from its centroid's calibrated range
+  double zn_min = 0.0;
+  for (int k = 0; k < K; ++k) {
+    const double z = std::fabs(n_k[k] - mu_n[k]) / sigma_n[k];
+    if (z_n) z_n[k] = z;
+    if (k == 0 || z < zn_min) zn_min = z;
+  }
+  r.z_n_min = zn_min;
+  if (zn_min > tau_n) {
+    r.ood = 1;
+    *out = r;
+    return SALT_OK;
+  }
+  // stage 2: dominance ratio against the mean of the other centroids
+  int best = 0;
+  double zr_min = 0.0;
+  for (int k = 0; k < K; ++k) {
+    const double others = (total - n_k[k]) / (double)(K - 1);
+    const double z = std::fabs(n_k[k] / others - mu_r[k]) / sigma_r[k];
+    if (z_r) z_r[k] = z;
+    if (k == 0 || z < zr_min) {
+      zr_min = z;
+      best = k;
+    }
+  }
+  r.z_r_min = zr_min;
+  if (zr_min > tau_r) r.blended = 1;
+  else r.k_star = best;
+  *out = r;
+  return SALT_OK;
+}
+
 salt_status salt_adapter_gram(salt_ctx* ctx, const void* blob1, int32_t r1, const void* blob2, int32_t r2,
                               double* out, void* stream) {
   if (!ctx || !out) return SALT_ERR_INVALID_ARG;

@@ -27,7 +27,7 @@ EXPORTS = (
     "salt_residual_bytes_for", "salt_load_residual", "salt_wait_loads", "salt_host_alloc",
     "salt_host_free", "salt_plan_create", "salt_plan_destroy", "salt_plan_set_maps",
     "salt_plan_build", "salt_plan_download", "salt_plan_errors", "salt_plan_tiling", "salt_apply",
-    "salt_apply_timed", "salt_fuse_centroid", "salt_fuse_centroid_timed", "salt_adapter_gram",
+    "salt_apply_timed", "salt_fuse_centroid", "salt_fuse_centroid_timed", "salt_adapter_gram", "salt_route",
     "salt_status_str",
     "salt_last_error", "salt_version",
 )
@@ -45,6 +45,11 @@ class Config(C.Structure):
 
 
 DETERMINISTIC = 1   # salt_config.flags: split-K partials summed in a fixed order
+
+
+class RouteResult(C.Structure):
+    _fields_ = [("k_star", C.c_int32), ("ood", C.c_int32), ("blended", C.c_int32), ("z_n_min", C.c_double),
+                ("z_r_min", C.c_double)]
 
 
 def _load() -> C.CDLL:
@@ -75,6 +80,8 @@ def _load() -> C.CDLL:
         "salt_fuse_centroid": (C.c_int, [P, I32, I32, C.c_float, VP, C.c_int64, VP]),
         "salt_fuse_centroid_timed": (C.c_int, [P, I32, I32, C.c_float, VP, C.c_int64, VP, VP, VP]),
         "salt_adapter_gram": (C.c_int, [P, VP, I32, VP, I32, C.POINTER(C.c_double), VP]),
+        "salt_route": (C.c_int, [I32] + [C.POINTER(C.c_double)] * 5 + [C.c_double, C.c_double] +
+                       [C.POINTER(C.c_double)] * 2 + [C.POINTER(RouteResult)]),
         "salt_status_str": (C.c_char_p, [C.c_int]),
         "salt_last_error": (C.c_char_p, [P]),
         "salt_version": (I32, []),
@@ -87,6 +94,20 @@ def _load() -> C.CDLL:
 
 
 lib = _load()
+
+
+def route(n, mu_n, sigma_n, mu_r, sigma_r, tau_n: float = 2.0, tau_r: float = 2.0):
+    """salt_route (Sec. 3.2, host only): returns (status, result dict)."""
+    K = len(n)
+    arrs = [np.ascontiguousarray(a, dtype=np.float64) for a in (n, mu_n, sigma_n, mu_r, sigma_r)]
+    z_n = np.zeros(K, np.float64)
+    z_r = np.zeros(K, np.float64)
+    res = RouteResult()
+    dp = C.POINTER(C.c_double)
+    st = lib.salt_route(K, *[a.ctypes.data_as(dp) for a in arrs], tau_n, tau_r, z_n.ctypes.data_as(dp),
+                        z_r.ctypes.data_as(dp), C.byref(res))
+    return st, {"k_star": res.k_star, "ood": bool(res.ood), "blended": bool(res.blended), "z_n_min": res.z_n_min,
+                "z_r_min": res.z_r_min, "z_n": z_n, "z_r": z_r}
 
 
 class SaltError(RuntimeError):

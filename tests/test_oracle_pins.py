@@ -437,3 +437,43 @@ def test_update_terms_invariant_to_factor_rotation():
     base = oracle.update_terms(at1, b1, at2, b2)
     rot = oracle.update_terms(q.T @ at1, q.T @ b1, at2, b2)   # A R = (R^T At)^T, R^T B
     np.testing.assert_allclose(rot, base, rtol=1e-10, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------
+# O5: centroid routing (Sec. 3.2)
+# ---------------------------------------------------------------------------
+def test_route_decide_reproduces_the_paper_routing_table():
+    """tests/golden/paper_routing_table.json: the printed Z_N and Z_R of six
+    held-out tasks and where each was routed (Sec. 4.6, tau_N = tau_R = 2.0)."""
+    g = json.load(open(os.path.join(GOLDEN, "paper_routing_table.json")))
+    for row in g["rows"]:
+        k, ood, blended = oracle.route_decide(row["z_n_min"], row["z_r"], g["tau_n"], g["tau_r"])
+        got = "OOD" if ood else ("blended" if blended else g["centroids"][k])
+        assert got == row["routed"], row
+
+
+def test_route_statistics_exact_small_case():
+    """K = 3 with rational inputs, the statistics worked out by hand in exact
+    arithmetic: N = (2, 4, 6), mu_N = (1, 4, 9), sigma_N = (1/2, 1, 3):
+    Z_N = (2, 0, 1); R = (2/5, 4/4, 6/3) = (0.4, 1, 2); mu_R = (1/2, 1, 3/2),
+    sigma_R = (1/10, 1/4, 1/4): Z_R = (1, 0, 2); k* = 1."""
+    n = [2.0, 4.0, 6.0]
+    res = oracle.route(n, [1.0, 4.0, 9.0], [0.5, 1.0, 3.0], [0.5, 1.0, 1.5], [0.1, 0.25, 0.25], 2.0, 2.0)
+    np.testing.assert_allclose(res["z_n"], [2.0, 0.0, 1.0], rtol=0, atol=1e-15)
+    np.testing.assert_allclose(res["z_r"], [1.0, 0.0, 2.0], rtol=0, atol=1e-14)
+    assert (res["k_star"], res["ood"], res["blended"]) == (1, False, False)
+    # tau_N below the smallest norm deviation (0): rejected as out of distribution
+    assert oracle.route(n, [1.0, 4.5, 9.0], [0.5, 1.0, 3.0], [0.5, 1.0, 1.5], [0.1, 0.25, 0.25], 0.4, 2.0)["ood"]
+    # every ratio deviation above tau_R: blended, fallback
+    blended = oracle.route(n, [1.0, 4.0, 9.0], [0.5, 1.0, 3.0], [0.9, 1.6, 2.6], [0.1, 0.25, 0.25], 2.0, 2.0)
+    assert blended["blended"] and blended["k_star"] == -1
+
+
+def test_route_ratio_is_scale_free():
+    """Sec. 3.2 uses the dominance ratio because absolute norms move with prompt
+    structure: scaling every N_k by the same factor leaves Z_R unchanged."""
+    rng = np.random.default_rng(21)
+    n = rng.uniform(0.5, 3.0, size=4).tolist()
+    base = oracle.route(n, [1.0] * 4, [1.0] * 4, [1.0] * 4, [0.3] * 4, 10.0, 10.0)
+    scaled = oracle.route([3.7 * v for v in n], [1.0] * 4, [1.0] * 4, [1.0] * 4, [0.3] * 4, 10.0, 10.0)
+    np.testing.assert_allclose(scaled["z_r"], base["z_r"], rtol=1e-13)
