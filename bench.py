@@ -90,6 +90,7 @@ def cpu_baseline(w, budget_s=12.0):
         cat, cb = (oracle.decode(a, d) for a in w.centroids(t)) if w.n_centroids else (None, None)
         res = {int(s): tuple(oracle.decode(a, d) for a in w.residual(int(s), t)) for s in w.referenced_slots()}
         data.append((x, y0, cat, cb, res))
+        log(f"cpu baseline: table {t + 1} of {n_tab} staged")
     pairs = 0            # (token, table) pairs computed
     t0 = time.perf_counter()
     start = 0
@@ -347,6 +348,9 @@ WORKLOADS = {
     "decode8b": dict(cfg=4, rot=4, steps=500, warmup=50),
     "zipf": dict(cfg=5, rot=4, steps=500, warmup=50),
     "zipf-baseline": dict(cfg=5, rot=4, baseline=True, steps=200, warmup=20),
+    # Sec. 3.3's long tail: the Zipf batch with the users of slots >= 100 served by
+    # concatenated rank-65/66 adapters (no centroid), the head by centroid + residual
+    "longtail": dict(cfg=5, rot=4, tail=100, steps=300, warmup=30),
     # Sec. 3.3: a centroid fused into the base weights of one Llama-3.2-3B layer
     "fuse": dict(cfg=5, rot=2, steps=20, warmup=3, fuse=True),
     # Sec. 3.1 Eq. 2 / Sec. 4.5: layer-wise cosine of two rank-16 adapters over the
@@ -546,6 +550,8 @@ def main():
 
     from paper_2608_03579_amd import synth
     w = synth.make(spec["cfg"], 0, baseline=spec.get("baseline", False))
+    if spec.get("tail"):
+        w = synth.long_tail(w, spec["tail"])
     # the 28-layer prefill draws adapter and activation values for one layer and
     # repeats them over the layers (distinct memory per table)
     dw = synth.make(3, 0, layers=1) if spec["cfg"] == 3 else w

@@ -72,7 +72,10 @@ typedef struct {
   int32_t n_centroids;       /* C in [0, 64]: centroid library size (Sec. 3.2)     */
   int32_t r_c;               /* centroid rank in [0, 128], a multiple of 8 (0 iff C == 0) */
   int32_t n_slots;           /* residual slot-pool size, >= 1                      */
-  int32_t r_u_max;           /* largest residual rank a slot holds, in [0, 16]     */
+  int32_t r_u_max;           /* largest residual rank a slot holds, in [0, 72]: ranks
+                                up to 2 are the SALT residuals, larger ones serve
+                                long-tail adapters that concatenate a centroid and a
+                                residual (Sec. 3.3, e.g. r = 17 / 33 / 65)           */
   int32_t max_tokens;        /* largest batch a plan accepts, in [1, 1 << 20]      */
   int32_t device;            /* HIP device ordinal                                  */
   int32_t flags;             /* 0 or SALT_DETERMINISTIC                             */

@@ -52,7 +52,8 @@ struct PlanArgs {
 // where the tile's tokens come from), so that they arrive in one scalar
 // cache line.
 struct alignas(64) ApplyArgs {
-  int32_t n_tiles, S;       // tiles; K ranges of the shrink (split-K)
+  int32_t n_tiles, S;       // tiles; shrink blocks per tile (K ranges x residual rank chunks)
+  int32_t sk;               // K ranges per tile (S = sk x rank chunks)
   int32_t n_col;            // expand blocks per tile
   int32_t fused_plan;       // 1: this launch also builds the plan (T <= kPlanFusedT)
   int32_t writer;           // block that writes the plan (fused_plan), else -1
@@ -153,7 +154,7 @@ constexpr int padded_rank(int r_c, int r_u_max) {
 // Per-tile arrival counters sit 256 bytes apart (no two share a cache line).
 constexpr int kCounterStride = 64;
 // Largest K split of one apply.
-constexpr int kMaxSplit = 32;
+constexpr int kMaxSplit = 64;
 // Ready words: kMaxSplit per tile, 64 bytes apart, so that the S blocks of a
 // tile that raise them concurrently never write the same 64-byte sector.
 constexpr int kReadyStride = 16;
@@ -166,8 +167,11 @@ constexpr int shrink_batch(int vec_regs, int mbw, int nbm, int ru) {
   const int u = 96 / (vec_regs * (mbw + nbm + mbw * ru));
   return u < 1 ? 1 : (u > 4 ? 4 : u);
 }
-// Largest supported ranks.
+// Largest supported ranks.  Residual ranks above 16 (long-tail adapters that
+// concatenate a centroid and a residual, e.g. r = 17 / 33 / 65) run in chunks
+// of kRankChunk ranks, one shrink block per (K range, chunk).
 constexpr int kMaxRc = 128;
-constexpr int kMaxRu = 16;
+constexpr int kMaxRu = 72;
+constexpr int kRankChunk = 16;
 
 }  // namespace salt

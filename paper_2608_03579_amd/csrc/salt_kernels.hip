@@ -781,7 +781,15 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
   const int i0 = __builtin_amdgcn_readfirstlane(s_tile[0].x), n = __builtin_amdgcn_readfirstlane(s_tile[0].y),
             c = __builtin_amdgcn_readfirstlane(s_tile[0].z);   // tile header: uniform
   const int R = a.R, in = a.in_dim, rc = a.r_c;
-  const bool has_c = c >= 0 && rc > 0;
+  // shrink block s of the tile: K range s % sk and, for residual ranks above
+  // kRankChunk, rank chunk s / sk (ranks r0 .. r0 + RU - 1); the centroid
+  // term belongs to chunk 0
+  int sk = s, r0 = 0;
+  if constexpr (RU == kRankChunk) {
+    sk = s % a.sk;
+    r0 = (s / a.sk) * RU;
+  }
+  const bool has_c = c >= 0 && rc > 0 && r0 == 0;
   const int mg = wave % MG, kq = wave / MG;
   const int kseg = (lane >> 4) * 8;             // k offset of this lane inside a 32-wide step
   int tl[MBW], ru[MBW];                         // lane's token (within the tile) per M-block
@@ -814,7 +822,7 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
   // The block's K range is [kblk, kend), in 32-wide steps; the KW waves along K
   // take its steps in turn (wave kq: steps kq, kq + KW, ...), so that at any
   // time they read neighbouring pieces of the same x rows.
-  const int kblk = s * a.Kc;
+  const int kblk = sk * a.Kc;
   const int kend = min(in, kblk + a.Kc);
   const int nstep_blk = kend > kblk ? (kend - kblk) / 32 : 0;   // whole steps of the block
 
@@ -839,7 +847,7 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
 #pragma unroll
   for (int m = 0; m < MBW; ++m)
 #pragma unroll
-    for (int j = 0; j < RU; ++j) aurow[m][j] = au[m] + (size_t)(j < ru[m] ? j : 0) * in;
+    for (int j = 0; j < RU; ++j) aurow[m][j] = au[m] + (size_t)(r0 + j < ru[m] ? r0 + j : 0) * in;
 
   // two register buffers of up to U steps each: the loads of batch b + 1 are
   // in flight while batch b is multiplied.  Every batch issues the same loads
@@ -976,7 +984,10 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
     for (int m = 0; m < MBW; ++m) {
 #pragma unroll
       for (int j = 0; j < RU; ++j)
-        if (j < a.r_u_max) P[tl[m] * R + rc + j] = j < ru[m] ? accu[m][j] : 0.f;
+        if (r0 + j < a.r_u_max) P[tl[m] * R + rc + r0 + j] = r0 + j < ru[m] ? accu[m][j] : 0.f;
+      if (RU == kRankChunk && a.S > a.sk)               // the other chunks' residual columns
+        for (int j = 0; j < a.r_u_max; ++j)
+          if (j < r0 || j >= r0 + RU) P[tl[m] * R + rc + j] = 0.f;
       for (int j = rc + a.r_u_max; j < R; ++j) P[tl[m] * R + j] = 0.f;   // row padding
     }
   }
@@ -1222,22 +1233,37 @@ __device__ __forceinline__ void expand_chunk(const ApplyArgs& a, const ExpandReg
       for (int e = 0; e < 8; ++e) accv[e] = 0.f;
     }
     const float* vt = s_v + t * R + rc;
+    // the first RP ranks come from the registers loaded ahead, the rest (any
+    // rank up to r_u_max) straight from the slot
 #pragma unroll
-    for (int j = 0; j < RU; ++j) {
+    for (int j = 0; j < RP; ++j) {
       if (j < ru) {
-        Vec bv;
-        if (j < RP) {
-          bv = regs.bu[it][j < RP ? j : 0];
-        } else {
-          const E* bup = reinterpret_cast<const E*>(a.pool + (size_t)tk.y * a.slot_stride) +
-                         (int64_t)ru * (a.tab_prefix + in);
-          bv = O::load(bup + (size_t)j * out + col);
-        }
         float b8[8];
-        O::to_f32(bv, b8);
+        O::to_f32(regs.bu[it][j], b8);
         const float vj = vt[j];
 #pragma unroll
         for (int e = 0; e < 8; ++e) accv[e] = fmaf(vj, b8[e], accv[e]);
+      }
+    }
+    if constexpr (RU > RP) {
+      // eight rows in flight at a time (a row past the token's rank re-reads its
+      // last row and is not added)
+      const E* bup = reinterpret_cast<const E*>(a.pool + (size_t)(tk.y > 0 ? tk.y : 0) * a.slot_stride) +
+                     (int64_t)ru * (a.tab_prefix + in);
+      for (int j0 = RP; j0 < ru; j0 += 8) {
+        Vec bv[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) bv[q] = O::load(bup + (size_t)(j0 + q < ru ? j0 + q : ru - 1) * out + col);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          if (j0 + q < ru) {
+            float b8[8];
+            O::to_f32(bv[q], b8);
+            const float vj = vt[j0 + q];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) accv[e] = fmaf(vj, b8[e], accv[e]);
+          }
+        }
       }
     }
     O::to_f32(regs.yold[it], yv);
@@ -1824,7 +1850,7 @@ hipError_t launch_plan(const PlanArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-// RU: residual ranks held per lane (1, 2 or kMaxRu).  fp32 plans use 16-token
+// RU: residual ranks held per lane (1, 2 or kRankChunk; larger ranks in chunks).  fp32 plans use 16-token
 // tiles only.
 hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {
   if (a.T <= 0 || a.n_tiles <= 0) return hipSuccess;
@@ -1832,11 +1858,11 @@ hipError_t launch_apply(const ApplyArgs& a, int bf16, int M, hipStream_t s, hipE
     if (M != 16) return hipErrorInvalidValue;
     if (a.r_u_max <= 1) return launch_typed<float, 1>(a, M, s, e0, e1);
     if (a.r_u_max <= 2) return launch_typed<float, 2>(a, M, s, e0, e1);
-    return launch_typed<float, kMaxRu>(a, M, s, e0, e1);
+    return launch_typed<float, kRankChunk>(a, M, s, e0, e1);
   }
   if (a.r_u_max <= 1) return launch_typed<uint16_t, 1>(a, M, s, e0, e1);
   if (a.r_u_max <= 2) return launch_typed<uint16_t, 2>(a, M, s, e0, e1);
-  return launch_typed<uint16_t, kMaxRu>(a, M, s, e0, e1);
+  return launch_typed<uint16_t, kRankChunk>(a, M, s, e0, e1);
 }
 
 hipError_t launch_fuse(const FuseArgs& f, int bf16, hipStream_t s, hipEvent_t e0, hipEvent_t e1) {

@@ -931,6 +931,7 @@ salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
     while (!atomic && S > 1 && (size_t)S * T * a.R > plan->dev.partial_cap) --S;
     a.Kc = ((sh.in_dim + S - 1) / S + gran - 1) / gran * gran;
     a.S = (sh.in_dim + a.Kc - 1) / a.Kc;
+    a.sk = a.S;
     const int chunks = (sh.out_dim + salt::kNC - 1) / salt::kNC;
     const int n_col = (int)std::min<int64_t>(
         chunks, std::max<int64_t>(1, (int64_t)ctx->occ_expand * ctx->n_cu / a.n_tiles));
@@ -979,15 +980,19 @@ salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
   if (small) {
     // at most two register batches of U steps per wave (U as the kernel picks
     // it), so that the shrink loop runs straight through with every load in flight
-    const int ru_t = a.r_u_max <= 1 ? 1 : (a.r_u_max <= 2 ? 2 : salt::kMaxRu);
+    const int ru_t = a.r_u_max <= 1 ? 1 : (a.r_u_max <= 2 ? 2 : salt::kRankChunk);
     const int U = std::max(1, salt::shrink_batch(ctx->esize == 2 ? 4 : 8, 1, salt::centroid_blocks(a.r_c), ru_t) / 2);
     const int s_steps = (sh.in_dim + 2 * U * gran - 1) / (2 * U * gran);
     S = std::max(S, std::min({s_steps, salt::kMaxSplit, (sh.in_dim + gran - 1) / gran}));
   }
-  while (S > 1 && (size_t)S * T * a.R > plan->dev.partial_cap) --S;
+  // residual ranks above kRankChunk: one shrink block per (K range, chunk)
+  const int nq = a.r_u_max > salt::kRankChunk ? (a.r_u_max + salt::kRankChunk - 1) / salt::kRankChunk : 1;
+  S = std::max(1, std::min(S, salt::kMaxSplit / nq));
+  while (S > 1 && (size_t)S * nq * T * a.R > plan->dev.partial_cap) --S;
   const int Kc = ((sh.in_dim + S - 1) / S + gran - 1) / gran * gran;
   a.Kc = Kc;
-  a.S = (sh.in_dim + Kc - 1) / Kc;   // <= S
+  a.sk = (sh.in_dim + Kc - 1) / Kc;   // <= S
+  a.S = a.sk * nq;
   // expand: one kNC-column chunk per block while the launch fits the device
   // at about four blocks per compute unit; past that, each block streams several
   // chunks (two in flight), so that the expand blocks left beside the shrink

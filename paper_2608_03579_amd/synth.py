@@ -269,6 +269,47 @@ class Workload:
         return self._encode(a)
 
 
+class ConcatTail(Workload):
+    """A workload whose slots in ``concat`` (slot -> (centroid c, base slot)) hold
+    long-tail concatenated adapters: per table, the rows of centroid c followed
+    by the rows of the residual drawn for the base slot (At stacked over At, B
+    over B; rank r_c + rank of the base slot).  Array stacking only."""
+
+    def residual_blob(self, slot: int, gen: int = 0) -> np.ndarray:
+        cat_map = getattr(self, "concat", {})
+        if slot not in cat_map:
+            return super().residual_blob(slot, gen)
+        c, base = cat_map[slot]
+        parts = []
+        for t in range(len(self.tables)):
+            cat, cb = self.centroids(t)
+            at_u, b_u = self.residual(base, t, gen)
+            parts.append(np.concatenate([cat[c], at_u]).reshape(-1))
+            parts.append(np.concatenate([cb[c], b_u]).reshape(-1))
+        return np.ascontiguousarray(np.concatenate(parts))
+
+
+def long_tail(w: Workload, tail_from: int) -> "ConcatTail":
+    """The batch of ``w`` with the users of slots >= tail_from (the rare end of a
+    Zipf draw) served by concatenated adapters: each such user gets a new slot
+    (n_slots + its slot) of rank r_c + r_u and its tokens no centroid (c = -1).
+    Sec. 3.3's long tail next to the centroid + residual head."""
+    tail = w.tok_u >= tail_from
+    tok_c = np.where(tail, -1, w.tok_c).astype(np.int32)
+    tok_u = np.where(tail, w.n_slots + w.tok_u, w.tok_u).astype(np.int32)
+    slot_rank = np.concatenate([w.slot_rank, w.r_c + w.slot_rank]).astype(np.int32)
+    concat = {}
+    for t in np.nonzero(tail)[0]:
+        concat[int(tok_u[t])] = (int(w.tok_c[t]), int(w.tok_u[t]))
+    out = ConcatTail(cfg=w.cfg, seed=w.seed, name=w.name + " (long tail concatenated)", dtype=w.dtype,
+                     tables=w.tables, n_centroids=w.n_centroids, r_c=w.r_c, n_slots=2 * w.n_slots,
+                     r_u_max=int(slot_rank[np.unique(tok_u[tok_u >= 0])].max()), slot_rank=slot_rank,
+                     tok_c=tok_c, tok_u=tok_u, gamma=None if w.gamma is None else w.gamma.copy(),
+                     y0_kind=w.y0_kind, exact=w.exact, meta=dict(w.meta, tail_from=tail_from))
+    out.concat = concat
+    return out
+
+
 def _gamma_per_user(cfg: int, seed: int, n_users: int) -> np.ndarray:
     rng = _rng(cfg, seed, _K_GAMMA)
     return np.asarray(GAMMA_BINS, dtype=np.float32)[rng.integers(0, len(GAMMA_BINS), size=n_users)]

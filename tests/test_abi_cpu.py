@@ -51,7 +51,7 @@ def test_create_rejects_bad_configs_before_touching_the_gpu():
         dict(tables=[(3072, 3071)]),                # out_dim not a multiple of 8
         dict(n_centroids=65),                       # C > 64
         dict(n_centroids=0, r_c=8),                 # rank without centroids
-        dict(r_u_max=17),
+        dict(r_u_max=73),                           # above the largest residual rank (72)
         dict(max_tokens=0),
         dict(n_slots=0),
     ]
