@@ -873,91 +873,102 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
       }
     }
   };
-  if constexpr (STG) {
-    static_assert(sizeof(E) == 2 && MB == 4 && MBW == 1, "staged shrink: bf16, 64-token tiles, one M-block per wave");
-    // whole 64-wide units through LDS, then an odd last 32-wide step from
-    // registers (the ragged end below takes whatever is left)
-    const int nunit = (kend - kblk) / 64;
-    shrink_staged_units<NBM, RU>(a, lds + tile_bytes(M) + sizeof(float) * (size_t)M * R, s_tile, wave, lane, n,
-                                 c, has_c, kblk, nunit, aurow[0], acc[0], accu[0]);
-    if (nstep_blk > 2 * nunit) {
-      const int kk = kblk + 64 * nunit + kseg;
-      xv[0][0][0] = O::load(xrow[0] + kk);
+  // a residual rank chunk past every rank of this wave's tokens has nothing to
+  // add: its loads and products are skipped (its partial stays zero)
+  bool idle = false;
+  if constexpr (RU == kRankChunk && !STG) {      // (the staged loop has block barriers)
+    bool busy = false;
 #pragma unroll
-      for (int nb = 0; nb < NBM; ++nb) av[0][0][nb] = O::load(arow[nb] + kk);
+    for (int m = 0; m < MBW; ++m) busy |= ru[m] > r0;
+    idle = r0 > 0 && __ballot(busy) == 0ull;
+  }
+  if (!idle) {
+    if constexpr (STG) {
+      static_assert(sizeof(E) == 2 && MB == 4 && MBW == 1, "staged shrink: bf16, 64-token tiles, one M-block per wave");
+      // whole 64-wide units through LDS, then an odd last 32-wide step from
+      // registers (the ragged end below takes whatever is left)
+      const int nunit = (kend - kblk) / 64;
+      shrink_staged_units<NBM, RU>(a, lds + tile_bytes(M) + sizeof(float) * (size_t)M * R, s_tile, wave, lane, n,
+                                   c, has_c, kblk, nunit, aurow[0], acc[0], accu[0]);
+      if (nstep_blk > 2 * nunit) {
+        const int kk = kblk + 64 * nunit + kseg;
+        xv[0][0][0] = O::load(xrow[0] + kk);
 #pragma unroll
-      for (int j = 0; j < RU; ++j) uv[0][0][0][j] = O::load(aurow[0][j] + kk);
-      if (has_c) {
+        for (int nb = 0; nb < NBM; ++nb) av[0][0][nb] = O::load(arow[nb] + kk);
 #pragma unroll
-        for (int nb = 0; nb < NBM; ++nb) acc[0][nb] = O::mma(xv[0][0][0], av[0][0][nb], acc[0][nb]);
-      }
+        for (int j = 0; j < RU; ++j) uv[0][0][0][j] = O::load(aurow[0][j] + kk);
+        if (has_c) {
 #pragma unroll
-      for (int j = 0; j < RU; ++j) accu[0][j] = O::dot(xv[0][0][0], uv[0][0][0][j], accu[0][j]);
-    }
-  } else {
-    const int nfull = nstep_blk > kq ? (nstep_blk - kq + KW - 1) / KW : 0;   // this wave's whole steps
-    auto load_steps = [&](Vec (&x_)[U][MBW], Vec (&a_)[U][NBM], Vec (&u_)[U][MBW][RU], int step0) {
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int kk = kblk + 32 * (kq + KW * (step0 + u < nfull ? step0 + u : nfull - 1)) + kseg;
-#pragma unroll
-        for (int m = 0; m < MBW; ++m) x_[u][m] = O::load(xrow[m] + kk);
-#pragma unroll
-        for (int nb = 0; nb < NBM; ++nb) a_[u][nb] = O::load(arow[nb] + kk);
-#pragma unroll
-        for (int m = 0; m < MBW; ++m)
-#pragma unroll
-          for (int j = 0; j < RU; ++j) u_[u][m][j] = O::load(aurow[m][j] + kk);
-      }
-    };
-    const int nbat = (nfull + U - 1) / U;
-    auto steps_of = [&](int b) { return min(U, nfull - b * U); };
-    if (nbat == 1) {
-      // one batch (short K ranges of small batches): nothing to overlap
-      load_steps(xv[0], av[0], uv[0], 0);
-      mul_steps(xv[0], av[0], uv[0], steps_of(0));
-    } else if (kStepRegs <= 128 && nbat == 2) {
-      // two batches: both in flight at once
-      load_steps(xv[0], av[0], uv[0], 0);
-      load_steps(xv[1], av[1], uv[1], U);
-      mul_steps(xv[0], av[0], uv[0], steps_of(0));
-      mul_steps(xv[1], av[1], uv[1], steps_of(1));
-    } else if constexpr (kStepRegs <= 128) {
-      if (nbat > 1) {
-        // (a peeled last pair would need a second set of accumulators)
-        load_steps(xv[0], av[0], uv[0], 0);
-        for (int b = 0; b < nbat; b += 2) {
-          load_steps(xv[1], av[1], uv[1], (b + 1) * U);
-          mul_steps(xv[0], av[0], uv[0], steps_of(b));
-          load_steps(xv[0], av[0], uv[0], (b + 2) * U);
-          if (b + 1 < nbat) mul_steps(xv[1], av[1], uv[1], steps_of(b + 1));
+          for (int nb = 0; nb < NBM; ++nb) acc[0][nb] = O::mma(xv[0][0][0], av[0][0][nb], acc[0][nb]);
         }
+#pragma unroll
+        for (int j = 0; j < RU; ++j) accu[0][j] = O::dot(xv[0][0][0], uv[0][0][0][j], accu[0][j]);
       }
     } else {
-      // one step's operands alone fill most of the register file (fp32 with
-      // wide centroid and residual ranks): no second buffer
-      for (int b = 0; b < nbat; ++b) {
-        load_steps(xv[0], av[0], uv[0], b * U);
-        mul_steps(xv[0], av[0], uv[0], steps_of(b));
+      const int nfull = nstep_blk > kq ? (nstep_blk - kq + KW - 1) / KW : 0;   // this wave's whole steps
+      auto load_steps = [&](Vec (&x_)[U][MBW], Vec (&a_)[U][NBM], Vec (&u_)[U][MBW][RU], int step0) {
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+          const int kk = kblk + 32 * (kq + KW * (step0 + u < nfull ? step0 + u : nfull - 1)) + kseg;
+#pragma unroll
+          for (int m = 0; m < MBW; ++m) x_[u][m] = O::load(xrow[m] + kk);
+#pragma unroll
+          for (int nb = 0; nb < NBM; ++nb) a_[u][nb] = O::load(arow[nb] + kk);
+#pragma unroll
+          for (int m = 0; m < MBW; ++m)
+#pragma unroll
+            for (int j = 0; j < RU; ++j) u_[u][m][j] = O::load(aurow[m][j] + kk);
+        }
+      };
+      const int nbat = (nfull + U - 1) / U;
+      auto steps_of = [&](int b) { return min(U, nfull - b * U); };
+      if (nbat == 1) {
+        // one batch (short K ranges of small batches): nothing to overlap
+        load_steps(xv[0], av[0], uv[0], 0);
+        mul_steps(xv[0], av[0], uv[0], steps_of(0));
+      } else if (kStepRegs <= 128 && nbat == 2) {
+        // two batches: both in flight at once
+        load_steps(xv[0], av[0], uv[0], 0);
+        load_steps(xv[1], av[1], uv[1], U);
+        mul_steps(xv[0], av[0], uv[0], steps_of(0));
+        mul_steps(xv[1], av[1], uv[1], steps_of(1));
+      } else if constexpr (kStepRegs <= 128) {
+        if (nbat > 1) {
+          // (a peeled last pair would need a second set of accumulators)
+          load_steps(xv[0], av[0], uv[0], 0);
+          for (int b = 0; b < nbat; b += 2) {
+            load_steps(xv[1], av[1], uv[1], (b + 1) * U);
+            mul_steps(xv[0], av[0], uv[0], steps_of(b));
+            load_steps(xv[0], av[0], uv[0], (b + 2) * U);
+            if (b + 1 < nbat) mul_steps(xv[1], av[1], uv[1], steps_of(b + 1));
+          }
+        }
+      } else {
+        // one step's operands alone fill most of the register file (fp32 with
+        // wide centroid and residual ranks): no second buffer
+        for (int b = 0; b < nbat; ++b) {
+          load_steps(xv[0], av[0], uv[0], b * U);
+          mul_steps(xv[0], av[0], uv[0], steps_of(b));
+        }
       }
     }
-  }
-  if (kend > kblk + 32 * nstep_blk && nstep_blk % KW == kq) {
-    // ragged end of the K range (in_dim not a multiple of 32), taken by the wave
-    // whose turn it is: k >= kend reads zero
-    const int kk = kblk + 32 * nstep_blk + kseg;
-    const bool kin = kk < kend;
+    if (kend > kblk + 32 * nstep_blk && nstep_blk % KW == kq) {
+      // ragged end of the K range (in_dim not a multiple of 32), taken by the wave
+      // whose turn it is: k >= kend reads zero
+      const int kk = kblk + 32 * nstep_blk + kseg;
+      const bool kin = kk < kend;
 #pragma unroll
-    for (int m = 0; m < MBW; ++m) xv[0][0][m] = kin ? O::load(xrow[m] + kk) : O::zero();
-    if (has_c) {
+      for (int m = 0; m < MBW; ++m) xv[0][0][m] = kin ? O::load(xrow[m] + kk) : O::zero();
+      if (has_c) {
 #pragma unroll
-      for (int nb = 0; nb < NBM; ++nb) av[0][0][nb] = kin ? O::load(arow[nb] + kk) : O::zero();
+        for (int nb = 0; nb < NBM; ++nb) av[0][0][nb] = kin ? O::load(arow[nb] + kk) : O::zero();
+      }
+#pragma unroll
+      for (int m = 0; m < MBW; ++m)
+#pragma unroll
+        for (int j = 0; j < RU; ++j) uv[0][0][m][j] = kin ? O::load(aurow[m][j] + kk) : O::zero();
+      mul_steps(xv[0], av[0], uv[0], 1);
     }
-#pragma unroll
-    for (int m = 0; m < MBW; ++m)
-#pragma unroll
-      for (int j = 0; j < RU; ++j) uv[0][0][m][j] = kin ? O::load(aurow[m][j] + kk) : O::zero();
-    mul_steps(xv[0], av[0], uv[0], 1);
   }
   // residual: lanes l, l^16, l^32, l^48 hold the four k offsets of one token
 #pragma unroll
