@@ -996,7 +996,7 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
 #pragma unroll
       for (int j = 0; j < RU; ++j)
         if (r0 + j < a.r_u_max) P[tl[m] * R + rc + r0 + j] = r0 + j < ru[m] ? accu[m][j] : 0.f;
-      if (RU == kRankChunk && a.S > a.sk)               // the other chunks' residual columns
+      if (RU == kRankChunk && a.S > a.sk && !a.atomic_sum)   // the other chunks' residual columns
         for (int j = 0; j < a.r_u_max; ++j)
           if (j < r0 || j >= r0 + RU) P[tl[m] * R + rc + j] = 0.f;
       for (int j = rc + a.r_u_max; j < R; ++j) P[tl[m] * R + j] = 0.f;   // row padding
@@ -1050,11 +1050,36 @@ __device__ __forceinline__ void shrink_block(const ApplyArgs& a, int tau, int s,
   } else if (a.atomic_sum) {
     // add this K range's partial into v (cleared by the previous apply or the build)
     float* vt = a.v + (size_t)i0 * R;
-    for (int i = tid; i < n * R; i += 256) {
-      float p = 0.f;
+    if (RU == kRankChunk && a.S > a.sk && r0 > 0) {
+      // a rank chunk past the first adds only its own ranks of the tokens that
+      // have them (every other entry of its partial is zero)
+      for (int i = tid; i < n * RU; i += 256) {
+        const int t = i / RU, j = r0 + i % RU;
+        const int4 tk = s_tile[1 + t];
+        if (tk.y >= 0 && j < tk.z) {
+          float p = 0.f;
 #pragma unroll
-      for (int q = 0; q < KW; ++q) p += s_part[(size_t)q * M * R + i];
-      __hip_atomic_fetch_add(vt + i, p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          for (int q = 0; q < KW; ++q) p += s_part[(size_t)q * M * R + t * R + rc + j];
+          __hip_atomic_fetch_add(vt + t * R + rc + j, p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      }
+    } else if (RU == kRankChunk && a.S > a.sk) {
+      // the first rank chunk: the centroid ranks and residual ranks 0 .. RU - 1
+      const int w = rc + RU;
+      for (int i = tid; i < n * w; i += 256) {
+        const int t = i / w, j = i % w;
+        float p = 0.f;
+#pragma unroll
+        for (int q = 0; q < KW; ++q) p += s_part[(size_t)q * M * R + t * R + j];
+        __hip_atomic_fetch_add(vt + t * R + j, p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    } else {
+      for (int i = tid; i < n * R; i += 256) {
+        float p = 0.f;
+#pragma unroll
+        for (int q = 0; q < KW; ++q) p += s_part[(size_t)q * M * R + i];
+        __hip_atomic_fetch_add(vt + i, p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
     }
   } else {
     const __amdgpu_buffer_rsrc_t rp =
@@ -1229,59 +1254,123 @@ __device__ __forceinline__ void expand_chunk(const ApplyArgs& a, const ExpandReg
 
   // ---- residual part, add, round, store (lanes with nothing to write store
   // to the sink, so that every path issues the same stores) ----
+  if constexpr (RU <= RP) {
 #pragma unroll
-  for (int it = 0; it < ITEMS; ++it) {
-    const int idx = tid + 256 * it, t = idx / CG, cl = (idx % CG) * 8, col = n0 + cl;
-    const bool ok = t < n && col < out;
-    const int4 tk = s_tile[1 + t];
-    const int ru = tk.y >= 0 ? tk.z : 0;
-    float accv[8], yv[8];
-    if (has_c) {
+    for (int it = 0; it < ITEMS; ++it) {
+      const int idx = tid + 256 * it, t = idx / CG, cl = (idx % CG) * 8, col = n0 + cl;
+      const bool ok = t < n && col < out;
+      const int4 tk = s_tile[1 + t];
+      const int ru = tk.y >= 0 ? tk.z : 0;
+      float accv[8], yv[8];
+      if (has_c) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) accv[e] = s_y[t * kYS + cl + e];
-    } else {
+        for (int e = 0; e < 8; ++e) accv[e] = s_y[t * kYS + cl + e];
+      } else {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) accv[e] = 0.f;
+        for (int e = 0; e < 8; ++e) accv[e] = 0.f;
+      }
+      const float* vt = s_v + t * R + rc;
+      // the ranks come from the registers loaded ahead
+#pragma unroll
+      for (int j = 0; j < RP; ++j) {
+        if (j < ru) {
+          float b8[8];
+          O::to_f32(regs.bu[it][j], b8);
+          const float vj = vt[j];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) accv[e] = fmaf(vj, b8[e], accv[e]);
+        }
+      }
+      O::to_f32(regs.yold[it], yv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) yv[e] += accv[e];
+      E* dst = ok ? reinterpret_cast<E*>(a.y) + (size_t)tk.x * out + col : reinterpret_cast<E*>(a.sink + tid * 32);
+      O::store(dst, yv);
     }
-    const float* vt = s_v + t * R + rc;
-    // the first RP ranks come from the registers loaded ahead, the rest (any
-    // rank up to r_u_max) straight from the slot
+  } else {
+    float accv[ITEMS][8];
+    int ruv[ITEMS];
 #pragma unroll
-    for (int j = 0; j < RP; ++j) {
-      if (j < ru) {
-        float b8[8];
-        O::to_f32(regs.bu[it][j], b8);
-        const float vj = vt[j];
+    for (int it = 0; it < ITEMS; ++it) {
+      const int idx = tid + 256 * it, t = idx / CG, cl = (idx % CG) * 8;
+      const int4 tk = s_tile[1 + t];
+      const int ru = tk.y >= 0 ? tk.z : 0;
+      ruv[it] = ru;
+      if (has_c) {
 #pragma unroll
-        for (int e = 0; e < 8; ++e) accv[e] = fmaf(vj, b8[e], accv[e]);
+        for (int e = 0; e < 8; ++e) accv[it][e] = s_y[t * kYS + cl + e];
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) accv[it][e] = 0.f;
+      }
+      const float* vt = s_v + t * R + rc;
+      // the first RP ranks come from the registers loaded ahead
+#pragma unroll
+      for (int j = 0; j < RP; ++j) {
+        if (j < ru) {
+          float b8[8];
+          O::to_f32(regs.bu[it][j], b8);
+          const float vj = vt[j];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) accv[it][e] = fmaf(vj, b8[e], accv[it][e]);
+        }
       }
     }
-    if constexpr (RU > RP) {
-      // eight rows in flight at a time (a row past the token's rank re-reads its
-      // last row and is not added)
-      const E* bup = reinterpret_cast<const E*>(a.pool + (size_t)(tk.y > 0 ? tk.y : 0) * a.slot_stride) +
-                     (int64_t)ru * (a.tab_prefix + in);
-      for (int j0 = RP; j0 < ru; j0 += 8) {
-        Vec bv[8];
+    // the rest (any rank up to r_u_max) straight from the slots: QN rows of
+    // every item of the thread in flight at a time.  A row past a token's rank
+    // re-reads its last row and is not added; a token without ranks past RP
+    // reads its first row of B (any rank >= 1) or the tile's first y row, and a
+    // column past out_dim reads column 0.
+    constexpr int QN = ITEMS >= 2 ? 8 : 16;
+    const E* bup[ITEMS];
+    int rmax = 0;
 #pragma unroll
-        for (int q = 0; q < 8; ++q) bv[q] = O::load(bup + (size_t)(j0 + q < ru ? j0 + q : ru - 1) * out + col);
+    for (int it = 0; it < ITEMS; ++it) {
+      const int idx = tid + 256 * it, t = idx / CG, col = n0 + (idx % CG) * 8;
+      const int4 tk = s_tile[1 + t];
+      const int ru = ruv[it], colc = col < out ? col : 0;
+      bup[it] = ru ? reinterpret_cast<const E*>(a.pool + (size_t)(tk.y > 0 ? tk.y : 0) * a.slot_stride) +
+                         (int64_t)ru * (a.tab_prefix + in) + colc
+                   : reinterpret_cast<const E*>(a.y) + (size_t)s_tile[1].x * out + colc;
+      rmax = max(rmax, ru);
+    }
+    for (int j0 = RP; j0 < rmax; j0 += QN) {
+      Vec bv[ITEMS][QN];
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-          if (j0 + q < ru) {
+      for (int it = 0; it < ITEMS; ++it) {
+        const int last = ruv[it] > 0 ? ruv[it] - 1 : 0;
+#pragma unroll
+        for (int q = 0; q < QN; ++q) bv[it][q] = O::load(bup[it] + (size_t)(j0 + q < last ? j0 + q : last) * out);
+      }
+#pragma unroll
+      for (int it = 0; it < ITEMS; ++it) {
+        const int idx = tid + 256 * it, t = idx / CG;
+        const float* vt = s_v + t * R + rc;
+#pragma unroll
+        for (int q = 0; q < QN; ++q) {
+          if (j0 + q < ruv[it]) {
             float b8[8];
-            O::to_f32(bv[q], b8);
+            O::to_f32(bv[it][q], b8);
             const float vj = vt[j0 + q];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) accv[e] = fmaf(vj, b8[e], accv[e]);
+            for (int e = 0; e < 8; ++e) accv[it][e] = fmaf(vj, b8[e], accv[it][e]);
           }
         }
       }
     }
-    O::to_f32(regs.yold[it], yv);
+
 #pragma unroll
-    for (int e = 0; e < 8; ++e) yv[e] += accv[e];
-    E* dst = ok ? reinterpret_cast<E*>(a.y) + (size_t)tk.x * out + col : reinterpret_cast<E*>(a.sink + tid * 32);
-    O::store(dst, yv);
+    for (int it = 0; it < ITEMS; ++it) {
+      const int idx = tid + 256 * it, t = idx / CG, col = n0 + (idx % CG) * 8;
+      const bool ok = t < n && col < out;
+      float yv[8];
+      O::to_f32(regs.yold[it], yv);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) yv[e] += accv[it][e];
+      E* dst = ok ? reinterpret_cast<E*>(a.y) + (size_t)s_tile[1 + t].x * out + col
+                  : reinterpret_cast<E*>(a.sink + tid * 32);
+      O::store(dst, yv);
+    }
   }
   __syncthreads();                              // s_y consumed
 }
