@@ -76,18 +76,16 @@ typedef struct {
                                 up to 2 are the SALT residuals, larger ones serve
                                 long-tail adapters that concatenate a centroid and a
                                 residual (Sec. 3.3, e.g. r = 17 / 33 / 65)           */
-  int32_t max_tokens;        /* largest batch a plan accepts, in [1, 1 << 20]      */
+  int32_t max_tokens;        /* largest batch a plan accepts, in [1, 65536]         */
   int32_t device;            /* HIP device ordinal                                  */
-  int32_t flags;             /* 0 or SALT_DETERMINISTIC                             */
+  int32_t flags;             /* reserved, must be 0                                 */
 } salt_config;
 
-/* salt_config.flags.  By default an apply that splits the shrink contraction
- * over several blocks sums their fp32 partial results with device atomics, in
- * arrival order: y is correct to fp32 rounding, but two runs may differ in its
- * last bits.  SALT_DETERMINISTIC sums the partials in a fixed order instead, so
- * equal inputs give bit-identical y, at the cost of one more round trip through
- * memory per apply. */
-#define SALT_DETERMINISTIC 1
+/* Results are reproducible: the split-K partial sums of the shrink are added
+ * in a fixed order, so the same call on equal inputs gives bit-identical y on
+ * every run.  The K split depends on the tables that share a launch, so one
+ * table applied alone and inside a salt_apply_batch may differ in the last
+ * bits (both within fp32 accumulation error). */
 
 typedef struct salt_ctx salt_ctx;
 typedef struct salt_plan salt_plan;
@@ -140,6 +138,15 @@ SALT_API size_t salt_residual_bytes_for(salt_dtype dtype, int32_t n_tables, cons
 SALT_API salt_status salt_load_residual(salt_ctx* ctx, int32_t slot, int32_t r_u, const void* blob,
                                size_t bytes);
 
+/* A batch of swaps (Sec. 4.4: the per-step H2D traffic of the users that come
+ * in): slots[i] <- blobs[i] of rank ranks[i] and bytes[i] bytes, for i < n, as
+ * salt_load_residual would do them one by one, but validated as a whole first
+ * (an invalid entry fails the call and changes no state) and ordered with one
+ * event for the whole batch.  Blobs inside memory from salt_host_alloc need no
+ * pointer query.  A slot listed twice receives its last blob. */
+SALT_API salt_status salt_load_residuals(salt_ctx* ctx, int32_t n, const int32_t* slots, const int32_t* ranks,
+                                         const void* const* blobs, const size_t* bytes);
+
 /* Block the host until every residual swap enqueued so far has completed. */
 SALT_API salt_status salt_wait_loads(salt_ctx* ctx);
 
@@ -151,9 +158,16 @@ SALT_API void salt_host_free(void* p);
  * A plan is the canonical grouping of one batch (Sec. 3.3: the frontend groups
  * requests by their centroid): tokens ordered by (centroid id, residual slot,
  * token index) ascending, -1 first.  Built once per batch on the device, then
- * reused by every table's salt_apply.  A plan owns device buffers sized for
- * max_tokens, including the apply's scratch, so applies that share a plan must
- * be ordered on one stream; use one plan per concurrently running stream. */
+ * reused by every table's apply.  A plan owns device buffers sized for
+ * max_tokens, including the apply's scratch (split-K partials): the work of one
+ * plan is ordered by the library, also across streams (a call on a stream other
+ * than the one of the plan's last work first waits for that work), so several
+ * streams that run concurrently need one plan each.
+ * Why four calls (create / set_maps / build / destroy) instead of one build
+ * that allocates: a serving loop keeps one plan per stream and reuses its
+ * buffers batch after batch, so no call on the hot path allocates; the maps
+ * are staged (host validation, one H2D copy) separately from the device build
+ * so that the copy can be issued early.  salt_apply_map is the one-shot form. */
 SALT_API salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out);
 SALT_API void salt_plan_destroy(salt_ctx* ctx, salt_plan* plan);
 
@@ -171,7 +185,11 @@ SALT_API salt_status salt_plan_set_maps(salt_ctx* ctx, salt_plan* plan, int32_t 
 
 /* Build the plan on the device from the staged maps (enqueued on `stream`):
  * the sorted order, the segments of equal (centroid, slot) and the groups of
- * equal centroid.  Integer work; the result is bit-exact and unique. */
+ * equal centroid.  Integer work; the result is bit-exact and unique.  One
+ * kernel for batches of up to 4096 tokens, three above.  The tiles the apply
+ * kernels walk (runs of at most 16 / 32 / 64 tokens of one centroid group) are
+ * cut on the host by salt_plan_set_maps from its per-centroid token counts; the
+ * build checks them against the sorted order (salt_plan_errors). */
 SALT_API salt_status salt_plan_build(salt_ctx* ctx, salt_plan* plan, void* stream);
 
 /* Copy a built plan to host arrays (synchronises `stream`).  Sizes: perm[T],
@@ -187,40 +205,63 @@ SALT_API salt_status salt_plan_download(salt_ctx* ctx, const salt_plan* plan, vo
  *   x: device [T][in_dim], y: device [T][out_dim], context dtype, row-major,
  *      16-byte aligned; y is read and written once per element, rounded once
  *      (round-to-nearest-even) from fp32 y + fp32 delta.
- * Accumulation is fp32: the centroid contractions run on bf16 MFMA with fp32
- * accumulation (the expand splits the fp32 v into two bf16 terms), the residual
- * contractions on fp32 vector ALUs.  One kernel launch, or two for large bf16
- * batches with long centroid groups (salt_plan_tiling tells which); the plan's
- * scratch (split-K partials, v, per-tile flags) is reused, so applies of one plan
- * must be ordered on one stream.  Enqueued on `stream` after the swaps of every
- * slot the plan references.  Errors: SALT_ERR_OUT_OF_RANGE (table), SALT_ERR_BAD_STATE
- * (centroids of the table not pinned; a referenced slot was reloaded with a
- * different rank after salt_plan_set_maps). */
+ * Accumulation is fp32: the centroid contractions run on MFMA with fp32
+ * accumulation (bf16 contexts: the expand splits the fp32 v into two bf16
+ * terms), the residual contractions on fp32 vector ALUs.  Two kernel launches
+ * on `stream` (the shrink, then the expand), enqueued after the swaps of every
+ * slot the plan references; no block of either waits for another block.
+ * Errors: SALT_ERR_OUT_OF_RANGE (table), SALT_ERR_BAD_STATE (plan not built;
+ * centroids of the table not all pinned; a referenced slot was reloaded with a
+ * different rank after salt_plan_set_maps), SALT_ERR_INVALID_ARG (null or
+ * misaligned x / y).  T == 0 is a no-op. */
 SALT_API salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y,
                        void* stream);
 
-/* salt_apply for measurement: the same apply, and the HIP events `start_event`
- * and `stop_event` (hipEvent_t, created with timing enabled) record the start of
- * the apply's first kernel and the end of its last, so hipEventElapsedTime gives
- * its duration without the dispatch gap before it.  Errors as salt_apply; SALT_ERR_INVALID_ARG for a null event. */
-SALT_API salt_status salt_apply_timed(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y,
-                                      void* stream, void* start_event, void* stop_event);
+/* The apply of n tables on one plan (a decoder layer's projections, Sec. 3.3:
+ * every table of a batch shares its grouping): tables[i] with xs[i] -> ys[i]
+ * for i < n, the same result as n calls of salt_apply, in launches of up to 16
+ * tables (each launch two kernels, whatever n).  Tables may repeat and x
+ * pointers may be shared (q / k / v read one x); y buffers must not overlap.
+ * Errors as salt_apply, for any entry; nothing is enqueued then. */
+SALT_API salt_status salt_apply_batch(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_plan* plan,
+                                      const void* const* xs, void* const* ys, void* stream);
 
-/* Synchronise `stream`, then report in *n_errors the number of apply blocks of
- * this plan that gave up waiting for their tile since the last salt_plan_build
- * (their slice of y was left unchanged; 0 in normal operation).  Also checks
- * that the device-built tiling matches the host's (SALT_ERR_BAD_STATE if not). */
+/* salt_apply_batch for measurement (n <= 16: one launch): events[0] and
+ * events[1] (hipEvent_t, timing enabled) record the start and end of the
+ * shrink kernel, events[2] and events[3] those of the expand kernel
+ * (hipExtLaunchKernel), so hipEventElapsedTime gives each kernel's own
+ * duration without the dispatch gaps.  SALT_ERR_INVALID_ARG for a null
+ * event; SALT_ERR_OUT_OF_RANGE for n > 16. */
+SALT_API salt_status salt_apply_batch_timed(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_plan* plan,
+                                            const void* const* xs, void* const* ys, void* stream,
+                                            void* const* events);
+
+/* One-shot apply on host maps (the frontend call of Sec. 3.3: group the
+ * incoming requests, then serve them): salt_plan_set_maps + salt_plan_build +
+ * salt_apply on a plan the context owns and reuses (created on the first call;
+ * no allocation after that), all on `stream`.  Maps as salt_plan_set_maps, x /
+ * y as salt_apply; the host arrays are read before the call returns.  Calls
+ * that share the context's plan are ordered by the library. */
+SALT_API salt_status salt_apply_map(salt_ctx* ctx, int32_t table, int32_t T, const int32_t* tok_c,
+                                    const int32_t* tok_u, const float* tok_gamma, const void* x, void* y,
+                                    void* stream);
+
+/* Synchronise `stream`, then report in *n_errors how many tile records the
+ * device build found inconsistent with the sorted order (a tile holding a
+ * token of another centroid, or a malformed tile); 0 in normal operation.
+ * SALT_ERR_BAD_STATE (and *n_errors >= 1) if the device plan's token or tile
+ * count differs from what the host staged.  The apply kernels clamp every
+ * index they read from a plan, so an inconsistent plan cannot make them access
+ * memory outside their buffers; it would make y wrong, which this call reports. */
 SALT_API salt_status salt_plan_errors(salt_ctx* ctx, const salt_plan* plan, void* stream,
                                       int32_t* n_errors);
 
 /* How the applies of a plan whose maps are set run (host-only; no HIP call):
  *   *tile_tokens: tokens per tile (16, 32 or 64; the tiles of a centroid group
- *                 cut its tokens into runs of at most this many),
+ *                 cut its tokens into near-equal runs of at most this many),
  *   *n_tiles:     tiles of the batch,
- *   *launches:    kernel launches per salt_apply: 1 (shrink and expand blocks in
- *                 one launch, v handed over inside it), or 2 (large bf16
- *                 batches with long centroid groups and residual rank <= 2: a
- *                 shrink launch, then an expand launch).
+ *   *launches:    kernel launches per apply of up to 16 tables: 2 (shrink,
+ *                 then expand), 0 for an empty batch.
  * Any pointer may be NULL.  SALT_ERR_BAD_STATE if no maps were set. */
 SALT_API salt_status salt_plan_tiling(salt_ctx* ctx, const salt_plan* plan, int32_t* tile_tokens,
                                       int32_t* n_tiles, int32_t* launches);

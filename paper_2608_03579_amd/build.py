@@ -14,15 +14,16 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsalt.so")
-SOURCES = [os.path.join(CSRC, "salt_kernels.hip"), os.path.join(CSRC, "salt_runtime.cpp")]
+SOURCES = [os.path.join(CSRC, f) for f in ("salt_plan.hip", "salt_apply.hip", "salt_fuse_gram.hip", "salt_runtime.cpp")]
 ARCH = "gfx950"
+
+BUILD_DIR = os.path.join(HERE, "_build")
 
 HIPCC_FLAGS = [
     f"--offload-arch={ARCH}",
     "-O3",
     "-std=c++17",
     "-fPIC",
-    "-shared",
     "-Wall",
     "-fvisibility=hidden",
     "-fvisibility-inlines-hidden",
@@ -37,40 +38,40 @@ def hipcc() -> str:
     return os.path.join(rocm, "bin", "hipcc")
 
 
+def _filtered(stderr: str):
+    return [l for l in (stderr or "").splitlines() if "packed-fp32-ops" not in l and l.strip()]
+
+
 def build(verbose: bool = False) -> str:
-    """Compile every source into ``libsalt.so``; always recompiles."""
+    """Compile every source into ``libsalt.so``; always recompiles (one hipcc
+    process per source, in parallel, then one link)."""
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    objs, procs = [], []
+    for src in SOURCES:
+        obj = os.path.join(BUILD_DIR, os.path.basename(src) + ".o")
+        cmd = [hipcc(), *HIPCC_FLAGS, "-c", src, "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        procs.append((src, subprocess.Popen(cmd, stdout=subprocess.PIPE, stderr=subprocess.PIPE, text=True)))
+        objs.append(obj)
+    failed = []
+    for src, p in procs:
+        _, err = p.communicate()
+        errs = _filtered(err)
+        if p.returncode != 0:
+            failed.append(f"{os.path.basename(src)}:\n" + "\n".join(errs))
+        elif verbose and errs:
+            print("\n".join(errs), file=sys.stderr)
+    if failed:
+        raise RuntimeError("hipcc failed:\n" + "\n".join(failed))
     tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, *SOURCES, "-o", tmp]
-    if verbose:
-        print(" ".join(cmd), flush=True)
+    cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
-    errs = [l for l in (res.stderr or "").splitlines()
-            if "packed-fp32-ops" not in l and l.strip()]
     if res.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + "\n".join(errs))
-    if verbose and errs:
-        print("\n".join(errs), file=sys.stderr)
+        raise RuntimeError("hipcc link failed:\n" + "\n".join(_filtered(res.stderr)))
     os.replace(tmp, LIB)
     return LIB
 
 
-PROBE_SRC = os.path.join(CSRC, "hbm_probe.hip")
-PROBE = os.path.join(HERE, "hbm_probe")
-
-
-def build_probe(verbose: bool = False) -> str:
-    """Compile the HBM streaming probe (a stand-alone executable)."""
-    cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-Xclang", "-target-feature", "-Xclang",
-           "-packed-fp32-ops", PROBE_SRC, "-o", PROBE + ".tmp"]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        raise RuntimeError("hipcc failed:\n" + res.stderr[-4000:])
-    os.replace(PROBE + ".tmp", PROBE)
-    return PROBE
-
-
 if __name__ == "__main__":
     print(build(verbose=True))
-    print(build_probe(verbose=True))

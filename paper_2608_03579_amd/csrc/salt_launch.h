@@ -1,0 +1,129 @@
+// Host-side choices of an apply: tokens per tile, the tiles of a batch, the K
+// split of the shrink and the column blocks of the expand.  Header-only and free
+// of HIP calls, so that the runtime and the host-side address checks use the
+// same code.
+#pragma once
+
+#include <stdint.h>
+
+#include <algorithm>
+#include <cmath>
+#include <vector>
+
+#include "salt_layout.h"
+
+namespace salt {
+
+// Tokens per tile, from the mean size of the batch's centroid groups: short
+// groups (decode batches) take 16-token tiles, long ones (prefill) 64.  fp32
+// contexts always use 16.
+inline int choose_tile_tokens(int esize, int T, int n_groups) {
+  if (esize == 4 || n_groups <= 0) return 16;
+  const double mean = (double)T / n_groups;
+  if (mean <= 24.0) return 16;
+  if (mean <= 48.0) return 32;
+  return 64;
+}
+
+// Tiles of a batch from the token counts of its centroid groups, per_c[c + 1]
+// for c = -1 .. C - 1 (the sorted order puts c = -1 first).  A group of n tokens
+// becomes ceil(n / M) tiles of near-equal size, the first n mod k of them one
+// token longer.  Tiles are contiguous in sorted order and cover [0, T).
+inline void cut_tiles(const std::vector<int>& per_c, int M, std::vector<int4>& tiles) {
+  tiles.clear();
+  int start = 0;
+  for (size_t g = 0; g < per_c.size(); ++g) {
+    const int n = per_c[g];
+    if (n <= 0) continue;
+    const int k = cdiv(n, M), base = n / k, extra = n % k;
+    int p = start;
+    for (int i = 0; i < k; ++i) {
+      const int len = base + (i < extra ? 1 : 0);
+      int4 t;
+      t.x = p;
+      t.y = len;
+      t.z = (int)g - 1;
+      t.w = 0;
+      tiles.push_back(t);
+      p += len;
+    }
+    start += n;
+  }
+}
+
+// Largest number of tiles a batch of T tokens over C centroids can cut into.
+inline int max_tiles(int T, int C) { return cdiv(T, 16) + C + 1; }
+
+// K ranges, column blocks and block offsets of launch `a`, whose jobs (in,
+// out, prefix, pointers) and batch fields (T, M, n_tiles, C, r_c, r_u, nq, R,
+// esize, partial_cap) are set.  n_groups_c: centroids the batch references;
+// sum_rank: residual ranks summed over the slots it references (both for the
+// byte counts that bound the partial traffic).  Returns false if the partials
+// of a one-range shrink do not fit.
+inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t sum_rank) {
+  const int TB = a.M / 16, KW = kWaves / TB, CW = kWaves / TB;
+  const int target = 4 * std::max(1, n_cu);
+  const double es = (double)a.esize;
+  int64_t sum_in = 0, sum_out = 0;
+  for (int j = 0; j < a.n_jobs; ++j) {
+    sum_in += a.jobs[j].in;
+    sum_out += a.jobs[j].out;
+  }
+  const double pairs = (double)a.n_tiles * a.nq;
+  const double part_row = 8.0 * a.T * a.R;        // bytes of one K range's partials, written and read
+  std::vector<int> S(a.n_jobs);
+  for (int j = 0; j < a.n_jobs; ++j) {
+    const Job& jb = a.jobs[j];
+    const double adapters = (double)n_groups_c * a.r_c + (double)sum_rank;
+    const double bytes = es * ((double)a.T * (jb.in + 2.0 * jb.out) + adapters * (jb.in + jb.out));
+    const int s_blocks = (int)std::ceil((double)target * jb.in / ((double)sum_in * pairs));
+    const int s_traffic = std::max(1, (int)(0.1 * bytes / part_row));
+    const int s_max = cdiv(jb.in, kStepK * KW);
+    S[j] = std::max(1, std::min({s_blocks, s_traffic, s_max}));
+  }
+  // partials must fit: shrink the largest split until they do
+  auto total = [&]() {
+    int64_t t = 0;
+    for (int j = 0; j < a.n_jobs; ++j) t += (int64_t)S[j] * a.T * a.R;
+    return t;
+  };
+  while (total() > a.partial_cap) {
+    int jm = 0;
+    for (int j = 1; j < a.n_jobs; ++j)
+      if (S[j] > S[jm]) jm = j;
+    if (S[jm] == 1) return false;
+    S[jm] = (S[jm] + 1) / 2;
+  }
+  int64_t poff = 0;
+  int sb = 0, eb = 0;
+  const int e_target = 4 * std::max(1, n_cu);
+  for (int j = 0; j < a.n_jobs; ++j) {
+    Job& jb = a.jobs[j];
+    const int gran = kStepK * KW;
+    jb.Kc = cdiv(cdiv(jb.in, S[j]), gran) * gran;
+    jb.S = cdiv(jb.in, jb.Kc);
+    jb.poff = poff;
+    poff += (int64_t)jb.S * a.T * a.R;
+    // column blocks: about e_target over the launch, no more than keep the
+    // tile's partial re-reads within a quarter of the expand's own bytes
+    const double adapters = (double)n_groups_c * a.r_c + (double)sum_rank;
+    const double e_bytes = es * (2.0 * a.T * jb.out + adapters * jb.out);
+    const double reread = 4.0 * jb.S * a.T * a.R;
+    const int n_blocks = (int)std::lround((double)e_target * jb.out / ((double)sum_out * a.n_tiles));
+    const int n_traffic = std::max(1, (int)(0.25 * e_bytes / reread));
+    const int n_max = cdiv(jb.out, kChunkCols * CW);
+    int n_col = std::max(1, std::min({n_blocks, n_traffic, n_max}));
+    const int cgran = kChunkCols * CW;
+    jb.cpb = cdiv(cdiv(jb.out, n_col), cgran) * cgran;
+    jb.n_col = cdiv(jb.out, jb.cpb);
+    jb.shrink_base = sb;
+    jb.expand_base = eb;
+    sb += a.n_tiles * jb.S * a.nq;
+    eb += a.n_tiles * jb.n_col;
+  }
+  a.shrink_blocks = sb;
+  a.expand_blocks = eb;
+  return true;
+}
+
+}  // namespace salt

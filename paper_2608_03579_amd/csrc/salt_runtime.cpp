@@ -11,15 +11,14 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <string>
 #include <vector>
 
 #include "../../include/salt.h"
 #include "salt_internal.h"
-
-using salt::ApplyArgs;
-using salt::PlanBuffers;
+#include "salt_launch.h"
 
 namespace {
 
@@ -38,35 +37,77 @@ struct EventRing {
   int64_t done = -1;  // all sequences <= done have completed
 };
 
+// Page-locked ranges handed out by salt_host_alloc: a blob inside one of them
+// needs no pointer query before its swap.
+struct HostRanges {
+  std::mutex mu;
+  std::vector<std::pair<uintptr_t, size_t>> r;   // sorted by start
+  bool contains(const void* p, size_t n) {
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+    std::lock_guard<std::mutex> g(mu);
+    auto it = std::upper_bound(r.begin(), r.end(), std::make_pair(a, ~(size_t)0));
+    if (it == r.begin()) return false;
+    --it;
+    return a >= it->first && a - it->first <= it->second && n <= it->second - (a - it->first);
+  }
+  void add(void* p, size_t n) {
+    std::lock_guard<std::mutex> g(mu);
+    auto v = std::make_pair(reinterpret_cast<uintptr_t>(p), n);
+    r.insert(std::upper_bound(r.begin(), r.end(), v), v);
+  }
+  void remove(void* p) {
+    std::lock_guard<std::mutex> g(mu);
+    const uintptr_t a = reinterpret_cast<uintptr_t>(p);
+    for (auto it = r.begin(); it != r.end(); ++it)
+      if (it->first == a) {
+        r.erase(it);
+        return;
+      }
+  }
+};
+HostRanges g_host_ranges;
+
 }  // namespace
 
 struct salt_plan {
-  PlanBuffers dev{};
-  int4* staging = nullptr;          // pinned host copy of the maps
-  hipEvent_t staged = nullptr;      // recorded after the H2D copy of the maps
+  // device buffers, sized for max_tokens
+  int4* staged_dev = nullptr;       // [max_T + tile_cap]: the batch's maps [T], then its tiles
+  uint64_t* keys = nullptr;         // [2][max_T]
+  int4* srt = nullptr;              // [max_T]
+  int32_t* ints = nullptr;          // perm [max_T], seg_off / grp_off [max_T + 1], seg_c / seg_u [max_T]
+  int32_t* meta = nullptr;          // [kMetaWords]
+  float* partials = nullptr;
+  size_t partial_cap = 0;           // floats
+  int4* staging = nullptr;          // pinned host copy of maps + tiles
+  hipEvent_t staged = nullptr;      // recorded after the H2D copy of the staging buffer
   bool staged_pending = false;
-  int32_t T = 0;
+  hipEvent_t hop = nullptr;         // orders the plan's work across streams
+  int32_t max_T = 0, tile_cap = 0;
+  // the batch
+  int32_t T = -1;                   // -1: no maps set
   bool built = false;
-  std::vector<int32_t> slots;       // distinct referenced slots
-  std::vector<int32_t> slot_rank;   // rank of each at set_maps time
   int32_t M = 16;                   // tokens per tile
   int32_t n_tiles = 0;
-  int32_t n_groups_c = 0;           // groups with a centroid
-  int64_t sum_ru = 0;               // residual rank summed over tokens
-  uint32_t arrivals = 0;            // per-tile arrival count after the last enqueued apply (ordered sums)
-  uint32_t epoch = 0;               // applies enqueued since creation or the last epoch reset
-  // A build of a small batch is deferred: the next apply on the same stream
-  // plans the batch itself.  Any other use of the plan first launches the
-  // deferred build on the stream it was requested on.
-  mutable bool build_pending = false;   // running the deferred build changes no visible state
-  hipStream_t build_stream = nullptr;
-  // atomic sums: rows of each v buffer that may be nonzero (all rows below)
-  int32_t v_dirty[2] = {0, 0};
+  int32_t n_groups_c = 0;           // centroids referenced
+  int32_t ru_max = 0;               // largest residual rank referenced
+  int64_t sum_rank = 0;             // ranks summed over the distinct referenced slots
+  std::vector<int32_t> slots;       // distinct referenced slots
+  std::vector<int32_t> slot_rank;   // rank of each at set_maps time
+  // the stream of the last operation that touched the plan's device buffers
+  bool used = false;
+  hipStream_t last_stream = nullptr;
   // Applies of this plan enqueued on reader_stream since its last reader event:
   // the event that covers them (a swap of one of the plan's slots waits for
   // it) is recorded only when something needs it, not after every apply.
   bool readers_open = false;
   hipStream_t reader_stream = nullptr;
+
+  int32_t* perm() const { return ints; }
+  int32_t* seg_off() const { return ints + max_T; }
+  int32_t* grp_off() const { return ints + 2 * max_T + 1; }
+  int32_t* seg_c() const { return ints + 3 * max_T + 2; }
+  int32_t* seg_u() const { return ints + 4 * max_T + 2; }
+  static size_t n_ints(size_t T) { return 5 * T + 2; }
 };
 
 struct salt_ctx {
@@ -77,19 +118,20 @@ struct salt_ctx {
   size_t esize = 2;
   int device = 0;
   int n_cu = 256;                        // compute units of the device
-  int occ_shrink = 0, occ_expand = 0;    // blocks per compute unit of the two-launch kernels (0: not asked yet)
   // device memory
   std::vector<char*> cent_at, cent_b;    // per table
   std::vector<uint8_t> cent_pinned;      // per table x centroid
+  std::vector<uint8_t> table_ready;      // per table: every centroid pinned
   char* pool = nullptr;
   size_t slot_stride = 0;
   hipStream_t side = nullptr;
   // bookkeeping
   std::vector<int32_t> slot_rank;        // -1 = never loaded
-  std::vector<int64_t> slot_reader;      // apply sequence of the last reader
+  std::vector<int64_t> slot_reader;      // reader sequence of the last apply that read the slot
   std::vector<int64_t> slot_loader;      // load sequence of the last swap
   EventRing readers, loaders;
   std::vector<salt_plan*> plans;
+  salt_plan* map_plan = nullptr;         // the plan salt_apply_map builds and applies
   bool poisoned = false;
   std::string err;
 };
@@ -125,6 +167,12 @@ salt_status hip_fail(salt_ctx* c, hipError_t e, const char* what) {
     if (e_ != hipSuccess) return hip_fail((ctx), e_, #call);  \
   } while (0)
 
+#define SALT_LIVE(ctx)                                                                          \
+  do {                                                                                          \
+    if (!(ctx)) return SALT_ERR_INVALID_ARG;                                                    \
+    if ((ctx)->poisoned) return fail((ctx), SALT_ERR_BAD_STATE, "context is poisoned: %s", (ctx)->err.c_str()); \
+  } while (0)
+
 // dst[i][o][j] = src[i][j][o] for n matrices of rc x out elements.
 template <typename W>
 void transpose_rank_major(const W* src, W* dst, size_t n, size_t rc, size_t out) {
@@ -139,31 +187,6 @@ void transpose_rank_major(const W* src, W* dst, size_t n, size_t rc, size_t out)
 
 constexpr int kMaxGramRank = 256;   // largest adapter rank of salt_adapter_gram
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
-
-// Split-K partial sums go through device atomics unless the context asked for
-// bit-reproducible results.
-bool atomic_sums(const salt_ctx* c) { return (c->cfg.flags & SALT_DETERMINISTIC) == 0; }
-
-// Epochs are compared modulo 2^32 by signed difference; restart them well before
-// a ready word could fall 2^31 epochs behind.
-constexpr uint32_t kEpochReset = 1u << 30;
-
-// Launches the plan kernel now.  reset_ready restarts the plan's epochs.
-hipError_t launch_build(const salt_plan* plan, hipStream_t s, bool reset_ready) {
-  salt::PlanArgs pa{};
-  pa.b = plan->dev;
-  pa.T = plan->T;
-  pa.M = plan->M;
-  pa.reset_ready = reset_ready ? 1 : 0;
-  return salt::launch_plan(pa, s);
-}
-
-// Runs a deferred build (see salt_plan) on the stream it was requested on.
-hipError_t flush_build(const salt_plan* plan) {
-  if (!plan->build_pending) return hipSuccess;
-  plan->build_pending = false;
-  return launch_build(plan, plan->build_stream, false);
-}
 
 hipError_t ring_record(EventRing& r, hipStream_t s, int64_t* seq_out) {
   const int64_t seq = r.next;
@@ -209,15 +232,31 @@ hipError_t open_readers(salt_ctx* ctx, salt_plan* plan, hipStream_t s) {
   return hipSuccess;
 }
 
-void free_plan_buffers(salt_plan* p) {
-  PlanBuffers& b = p->dev;
-  void* ptrs[] = {b.maps, b.perm, b.srt, b.srt_c, b.seg_off, b.seg_c, b.seg_u, b.grp_off,
-                  b.grp_tok, b.grp_c, b.tiles, b.arrive, b.ready, b.meta, b.counter, b.partials, b.v,
-                  b.sink};
-  for (void* q : ptrs)
+// Work on the plan's device buffers is about to be enqueued on `s`: if the
+// plan's last work went to another stream, `s` first waits for it.  Work on a
+// single stream needs no event.
+hipError_t use_stream(salt_ctx* ctx, salt_plan* plan, hipStream_t s) {
+  if (plan->used && plan->last_stream != s) {
+    hipError_t e = close_readers(ctx, plan);
+    if (e != hipSuccess) return e;
+    e = hipEventRecord(plan->hop, plan->last_stream);
+    if (e != hipSuccess) return e;
+    e = hipStreamWaitEvent(s, plan->hop, 0);
+    if (e != hipSuccess) return e;
+  }
+  plan->used = true;
+  plan->last_stream = s;
+  return hipSuccess;
+}
+
+void free_plan(salt_plan* p) {
+  void* dev[] = {p->staged_dev, p->keys, p->srt, p->ints, p->meta, p->partials};
+  for (void* q : dev)
     if (q) (void)hipFree(q);
   if (p->staging) (void)hipHostFree(p->staging);
   if (p->staged) (void)hipEventDestroy(p->staged);
+  if (p->hop) (void)hipEventDestroy(p->hop);
+  delete p;
 }
 
 void destroy_ctx_memory(salt_ctx* c) {
@@ -231,6 +270,307 @@ void destroy_ctx_memory(salt_ctx* c) {
   for (hipEvent_t e : c->loaders.ev)
     if (e) (void)hipEventDestroy(e);
   if (c->side) (void)hipStreamDestroy(c->side);
+}
+
+// Partial capacity of a plan: two K ranges per token row for a full launch of
+// kMaxJobs tables, or one if that would pass 256 MiB.
+size_t plan_partial_cap(size_t T, size_t R) {
+  const size_t two = 2 * (size_t)salt::kMaxJobs * T * R;
+  return two * 4 <= ((size_t)256 << 20) ? two : (size_t)salt::kMaxJobs * T * R;
+}
+
+salt_status plan_create(salt_ctx* ctx, salt_plan** out) {
+  salt_plan* p = new (std::nothrow) salt_plan();
+  if (!p) return fail(ctx, SALT_ERR_OUT_OF_MEMORY, "plan");
+  const size_t T = (size_t)ctx->cfg.max_tokens;
+  const size_t R = salt::padded_rank(ctx->cfg.r_c, ctx->cfg.r_u_max);
+  p->max_T = (int32_t)T;
+  p->tile_cap = salt::max_tiles((int)T, ctx->cfg.n_centroids);
+  p->partial_cap = plan_partial_cap(T, R);
+  const size_t staged = T + (size_t)p->tile_cap;
+  bool ok = hipMalloc((void**)&p->staged_dev, staged * sizeof(int4)) == hipSuccess &&
+            hipMalloc((void**)&p->keys, 2 * T * sizeof(uint64_t)) == hipSuccess &&
+            hipMalloc((void**)&p->srt, T * sizeof(int4)) == hipSuccess &&
+            hipMalloc((void**)&p->ints, salt_plan::n_ints(T) * 4) == hipSuccess &&
+            hipMalloc((void**)&p->meta, salt::kMetaWords * 4) == hipSuccess &&
+            hipMalloc((void**)&p->partials, p->partial_cap * 4) == hipSuccess &&
+            hipHostMalloc((void**)&p->staging, staged * sizeof(int4), hipHostMallocDefault) == hipSuccess;
+  if (!ok) {
+    (void)hipGetLastError();
+    free_plan(p);
+    return fail(ctx, SALT_ERR_OUT_OF_MEMORY, "plan buffers for %zu tokens do not fit", T);
+  }
+  hipError_t e = hipEventCreateWithFlags(&p->staged, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&p->hop, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipMemset(p->meta, 0, salt::kMetaWords * 4);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) {
+    free_plan(p);
+    return hip_fail(ctx, e, "plan init");
+  }
+  ctx->plans.push_back(p);
+  *out = p;
+  return SALT_OK;
+}
+
+salt_status set_maps_impl(salt_ctx* ctx, salt_plan* plan, int32_t T, const int32_t* tok_c, const int32_t* tok_u,
+                          const float* tok_gamma, hipStream_t s) {
+  if (T < 0 || T > plan->max_T)
+    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "T = %d not in [0, %d]", T, plan->max_T);
+  if (T > 0 && (!tok_c || !tok_u)) return fail(ctx, SALT_ERR_INVALID_ARG, "null map");
+  const int C = ctx->cfg.n_centroids, S = ctx->cfg.n_slots;
+  for (int t = 0; t < T; ++t) {
+    if (tok_c[t] < -1 || tok_c[t] >= C)
+      return fail(ctx, SALT_ERR_OUT_OF_RANGE, "tok_c[%d] = %d not in [-1, %d)", t, tok_c[t], C);
+    if (tok_u[t] < -1 || tok_u[t] >= S)
+      return fail(ctx, SALT_ERR_OUT_OF_RANGE, "tok_u[%d] = %d not in [-1, %d)", t, tok_u[t], S);
+    if (tok_u[t] >= 0 && ctx->slot_rank[tok_u[t]] < 0)
+      return fail(ctx, SALT_ERR_SLOT_EMPTY, "tok_u[%d] = %d: slot never loaded", t, tok_u[t]);
+    if (tok_gamma && !std::isfinite(tok_gamma[t]))
+      return fail(ctx, SALT_ERR_INVALID_ARG, "tok_gamma[%d] is not finite", t);
+  }
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  // the staging buffer may still feed the previous copy
+  if (plan->staged_pending) {
+    SALT_HIP(ctx, hipEventSynchronize(plan->staged));
+    plan->staged_pending = false;
+  }
+  // the previous batch's applies still read the old slots
+  SALT_HIP(ctx, close_readers(ctx, plan));
+  std::vector<int32_t> slots;
+  std::vector<int> per_c((size_t)C + 1, 0);   // tokens per centroid id (+1 for c = -1)
+  int ru_max = 0;
+  for (int t = 0; t < T; ++t) {
+    const int u = tok_u[t];
+    const int r = u >= 0 ? ctx->slot_rank[u] : 0;
+    const float g = tok_gamma ? tok_gamma[t] : 1.0f;
+    int32_t gbits;
+    std::memcpy(&gbits, &g, 4);
+    plan->staging[t] = make_int4(tok_c[t], u, r, gbits);
+    if (u >= 0) slots.push_back(u);
+    per_c[(size_t)tok_c[t] + 1]++;
+    ru_max = std::max(ru_max, r);
+  }
+  std::sort(slots.begin(), slots.end());
+  slots.erase(std::unique(slots.begin(), slots.end()), slots.end());
+  plan->slots = slots;
+  plan->slot_rank.resize(slots.size());
+  int64_t sum_rank = 0;
+  for (size_t i = 0; i < slots.size(); ++i) {
+    plan->slot_rank[i] = ctx->slot_rank[slots[i]];
+    sum_rank += plan->slot_rank[i];
+  }
+  int n_groups = 0, n_groups_c = 0;
+  for (int g = 0; g <= C; ++g)
+    if (per_c[g]) {
+      ++n_groups;
+      n_groups_c += (g > 0);
+    }
+  plan->M = salt::choose_tile_tokens((int)ctx->esize, T, n_groups);
+  std::vector<int4> tiles;
+  salt::cut_tiles(per_c, plan->M, tiles);
+  if ((int)tiles.size() > plan->tile_cap)
+    return fail(ctx, SALT_ERR_BAD_STATE, "%zu tiles exceed the plan's %d", tiles.size(), plan->tile_cap);
+  std::copy(tiles.begin(), tiles.end(), plan->staging + T);
+  plan->n_tiles = (int32_t)tiles.size();
+  plan->n_groups_c = n_groups_c;
+  plan->ru_max = ru_max;
+  plan->sum_rank = sum_rank;
+  plan->T = T;
+  plan->built = false;
+  if (T > 0) {
+    SALT_HIP(ctx, use_stream(ctx, plan, s));
+    SALT_HIP(ctx, hipMemcpyAsync(plan->staged_dev, plan->staging, ((size_t)T + tiles.size()) * sizeof(int4),
+                                 hipMemcpyHostToDevice, s));
+    SALT_HIP(ctx, hipEventRecord(plan->staged, s));
+    plan->staged_pending = true;
+  }
+  return SALT_OK;
+}
+
+salt_status build_impl(salt_ctx* ctx, salt_plan* plan, hipStream_t s) {
+  if (plan->T < 0) return fail(ctx, SALT_ERR_BAD_STATE, "no maps were set on the plan");
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  if (plan->T > 0) {
+    SALT_HIP(ctx, use_stream(ctx, plan, s));
+    salt::PlanLaunch pl{};
+    pl.maps = plan->staged_dev;
+    pl.tiles = plan->staged_dev + plan->T;
+    pl.keys = plan->keys;
+    pl.keys_sorted = plan->keys + plan->max_T;
+    pl.srt = plan->srt;
+    pl.perm = plan->perm();
+    pl.seg_off = plan->seg_off();
+    pl.seg_c = plan->seg_c();
+    pl.seg_u = plan->seg_u();
+    pl.grp_off = plan->grp_off();
+    pl.meta = plan->meta;
+    pl.T = plan->T;
+    pl.n_tiles = plan->n_tiles;
+    SALT_HIP(ctx, salt::launch_plan(pl, s));
+  }
+  plan->built = true;
+  return SALT_OK;
+}
+
+// The apply of `n` tables (ids `tables`, activations xs, outputs ys) on a
+// built plan, in launches of at most kMaxJobs tables.  ev: null, or four events
+// per launch (the timed form allows one launch).
+salt_status apply_impl(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_plan* plan, const void* const* xs,
+                       void* const* ys, hipStream_t s, hipEvent_t* ev) {
+  SALT_LIVE(ctx);
+  if (!plan || n < 0 || (n > 0 && (!tables || !xs || !ys))) return fail(ctx, SALT_ERR_INVALID_ARG, "null argument");
+  if (!plan->built) return fail(ctx, SALT_ERR_BAD_STATE, "plan was not built");
+  if (ev && n > salt::kMaxJobs)
+    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "a timed apply serves at most %d tables", salt::kMaxJobs);
+  for (int i = 0; i < n; ++i) {
+    const int t = tables[i];
+    if (t < 0 || t >= ctx->cfg.n_tables)
+      return fail(ctx, SALT_ERR_OUT_OF_RANGE, "table %d not in [0, %d)", t, ctx->cfg.n_tables);
+    if (!ctx->table_ready[t])
+      return fail(ctx, SALT_ERR_BAD_STATE, "centroids of table %d were not all pinned", t);
+    if (plan->T > 0 && (!xs[i] || !ys[i] || !aligned16(xs[i]) || !aligned16(ys[i])))
+      return fail(ctx, SALT_ERR_INVALID_ARG, "null or misaligned x / y of table %d", t);
+  }
+  const int T = plan->T;
+  if (T == 0 || n == 0) return SALT_OK;
+  int64_t need_load = -1;
+  for (size_t i = 0; i < plan->slots.size(); ++i) {
+    const int sl = plan->slots[i];
+    if (ctx->slot_rank[sl] != plan->slot_rank[i])
+      return fail(ctx, SALT_ERR_BAD_STATE,
+                  "slot %d was reloaded with rank %d after the plan's maps were set (rank %d)", sl,
+                  ctx->slot_rank[sl], plan->slot_rank[i]);
+    need_load = std::max(need_load, ctx->slot_loader[sl]);
+  }
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  SALT_HIP(ctx, use_stream(ctx, plan, s));
+  SALT_HIP(ctx, ring_wait(ctx->loaders, s, need_load));
+  const int C = ctx->cfg.n_centroids;
+  for (int first = 0; first < n; first += salt::kMaxJobs) {
+    const int nj = std::min(salt::kMaxJobs, n - first);
+    salt::ApplyLaunch a{};
+    a.tiles = plan->staged_dev + T;
+    a.srt = plan->srt;
+    a.pool = ctx->pool;
+    a.partials = plan->partials;
+    a.slot_stride = (int64_t)ctx->slot_stride;
+    a.partial_cap = (int64_t)plan->partial_cap;
+    a.n_jobs = nj;
+    a.T = T;
+    a.n_tiles = plan->n_tiles;
+    a.M = plan->M;
+    a.C = C;
+    a.r_c = ctx->cfg.r_c;
+    a.n_slots = ctx->cfg.n_slots;
+    a.r_u = plan->ru_max;
+    a.nq = std::max(1, salt::cdiv(plan->ru_max, salt::kRankChunk));
+    a.R = salt::padded_rank(a.r_c, a.r_u);
+    a.esize = (int32_t)ctx->esize;
+    for (int j = 0; j < nj; ++j) {
+      const int t = tables[first + j];
+      const salt_shape sh = ctx->tables[t];
+      salt::Job& jb = a.jobs[j];
+      jb.x = xs[first + j];
+      jb.y = ys[first + j];
+      jb.at_c = C ? ctx->cent_at[t] : nullptr;
+      jb.bt_c = C ? ctx->cent_b[t] : nullptr;
+      jb.prefix = ctx->tab_prefix[t];
+      jb.in = sh.in_dim;
+      jb.out = sh.out_dim;
+    }
+    if (!salt::configure_launch(a, ctx->n_cu, plan->n_groups_c, plan->sum_rank))
+      return fail(ctx, SALT_ERR_BAD_STATE, "split-K partials of %d tables do not fit the plan", nj);
+    SALT_HIP(ctx, salt::launch_apply(a, s, ev));
+  }
+  SALT_HIP(ctx, open_readers(ctx, plan, s));
+  return SALT_OK;
+}
+
+// Residual swaps of n slots: validated first (an invalid batch changes no
+// state), then enqueued on the side stream behind the applies that read the
+// slots, with one loader event for the batch.
+salt_status load_impl(salt_ctx* ctx, int32_t n, const int32_t* slots, const int32_t* ranks, const void* const* blobs,
+                      const size_t* bytes) {
+  SALT_LIVE(ctx);
+  if (n < 0 || (n > 0 && (!slots || !ranks || !blobs || !bytes)))
+    return fail(ctx, SALT_ERR_INVALID_ARG, "null argument");
+  for (int i = 0; i < n; ++i) {
+    const int slot = slots[i], r_u = ranks[i];
+    if (slot < 0 || slot >= ctx->cfg.n_slots)
+      return fail(ctx, SALT_ERR_OUT_OF_RANGE, "slot %d not in [0, %d)", slot, ctx->cfg.n_slots);
+    if (r_u < 0 || r_u > ctx->cfg.r_u_max)
+      return fail(ctx, SALT_ERR_OUT_OF_RANGE, "rank %d not in [0, %d]", r_u, ctx->cfg.r_u_max);
+    const size_t want = salt_residual_bytes(ctx, r_u);
+    if (bytes[i] != want)
+      return fail(ctx, SALT_ERR_INVALID_ARG, "blob %d is %zu bytes, rank %d needs %zu", i, bytes[i], r_u, want);
+    if (want == 0) continue;
+    const void* blob = blobs[i];
+    if (!blob || !aligned16(blob)) return fail(ctx, SALT_ERR_INVALID_ARG, "null or misaligned blob %d", i);
+    if (!g_host_ranges.contains(blob, want)) {
+      hipPointerAttribute_t attr;
+      hipError_t e = hipPointerGetAttributes(&attr, blob);
+      if (e != hipSuccess || attr.type != hipMemoryTypeHost) {
+        (void)hipGetLastError();
+        return fail(ctx, SALT_ERR_NOT_PINNED, "blob %p is not page-locked host memory", blob);
+      }
+    }
+  }
+  if (n == 0) return SALT_OK;
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  // the swaps may not overwrite what an enqueued apply still reads
+  int64_t wait_reader = -1;
+  for (salt_plan* p : ctx->plans) {
+    if (!p->readers_open) continue;
+    for (int i = 0; i < n; ++i)
+      if (std::binary_search(p->slots.begin(), p->slots.end(), slots[i])) {
+        SALT_HIP(ctx, close_readers(ctx, p));
+        break;
+      }
+  }
+  for (int i = 0; i < n; ++i) wait_reader = std::max(wait_reader, ctx->slot_reader[slots[i]]);
+  SALT_HIP(ctx, ring_wait(ctx->readers, ctx->side, wait_reader));
+  for (int i = 0; i < n; ++i)
+    if (bytes[i] > 0)
+      SALT_HIP(ctx, hipMemcpyAsync(ctx->pool + (size_t)slots[i] * ctx->slot_stride, blobs[i], bytes[i],
+                                   hipMemcpyHostToDevice, ctx->side));
+  int64_t seq;
+  SALT_HIP(ctx, ring_record(ctx->loaders, ctx->side, &seq));
+  for (int i = 0; i < n; ++i) {
+    ctx->slot_loader[slots[i]] = seq;
+    ctx->slot_rank[slots[i]] = ranks[i];
+  }
+  return SALT_OK;
+}
+
+salt_status fuse_impl(salt_ctx* ctx, int32_t table, int32_t c, float gamma, void* w, int64_t ldw, void* stream,
+                      hipEvent_t e0, hipEvent_t e1) {
+  SALT_LIVE(ctx);
+  if (table < 0 || table >= ctx->cfg.n_tables)
+    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "table %d not in [0, %d)", table, ctx->cfg.n_tables);
+  const int C = ctx->cfg.n_centroids;
+  if (c < 0 || c >= C) return fail(ctx, SALT_ERR_OUT_OF_RANGE, "centroid %d not in [0, %d)", c, C);
+  if (!ctx->cent_pinned[(size_t)table * C + c])
+    return fail(ctx, SALT_ERR_BAD_STATE, "centroid %d of table %d was never pinned", c, table);
+  const salt_shape sh = ctx->tables[table];
+  if (!w || !aligned16(w)) return fail(ctx, SALT_ERR_INVALID_ARG, "null or misaligned weight");
+  if (ldw < sh.out_dim || ldw % 8 != 0)
+    return fail(ctx, SALT_ERR_INVALID_ARG, "ldw %lld: need a multiple of 8 and >= out_dim %d", (long long)ldw,
+                sh.out_dim);
+  if (!std::isfinite(gamma)) return fail(ctx, SALT_ERR_INVALID_ARG, "gamma is not finite");
+  SALT_HIP(ctx, hipSetDevice(ctx->device));
+  const size_t rc = ctx->cfg.r_c, es = ctx->esize;
+  salt::FuseArgs f{};
+  f.at = ctx->cent_at[table] + (size_t)c * rc * sh.in_dim * es;
+  f.bt = ctx->cent_b[table] + (size_t)c * rc * sh.out_dim * es;
+  f.w = w;
+  f.ldw = ldw;
+  f.in_dim = sh.in_dim;
+  f.out_dim = sh.out_dim;
+  f.r_c = (int32_t)rc;
+  f.gamma = gamma;
+  SALT_HIP(ctx, salt::launch_fuse(f, ctx->cfg.dtype == SALT_BF16, (hipStream_t)stream, e0, e1));
+  return SALT_OK;
 }
 
 }  // namespace
@@ -255,8 +595,7 @@ const char* salt_last_error(const salt_ctx* ctx) { return ctx ? ctx->err.c_str()
 
 int32_t salt_version(void) { return SALT_VERSION; }
 
-size_t salt_residual_bytes_for(salt_dtype dtype, int32_t n_tables, const salt_shape* tables,
-                               int32_t r_u) {
+size_t salt_residual_bytes_for(salt_dtype dtype, int32_t n_tables, const salt_shape* tables, int32_t r_u) {
   if (!tables || n_tables <= 0 || r_u < 0 || (dtype != SALT_F32 && dtype != SALT_BF16)) return 0;
   size_t sum = 0;
   for (int i = 0; i < n_tables; ++i) {
@@ -278,11 +617,14 @@ salt_status salt_host_alloc(size_t bytes, void** out) {
     *out = nullptr;
     return SALT_ERR_OUT_OF_MEMORY;
   }
+  g_host_ranges.add(*out, bytes);
   return SALT_OK;
 }
 
 void salt_host_free(void* p) {
-  if (p) (void)hipHostFree(p);
+  if (!p) return;
+  g_host_ranges.remove(p);
+  (void)hipHostFree(p);
 }
 
 salt_status salt_create(const salt_config* cfg, salt_ctx** out) {
@@ -291,13 +633,13 @@ salt_status salt_create(const salt_config* cfg, salt_ctx** out) {
   g_create_err = "invalid configuration";
   if (cfg->dtype != SALT_F32 && cfg->dtype != SALT_BF16) return SALT_ERR_INVALID_ARG;
   if (cfg->n_tables < 1 || !cfg->tables) return SALT_ERR_INVALID_ARG;
-  if (cfg->n_centroids < 0 || cfg->n_centroids > 64 || cfg->r_c < 0 || cfg->r_c > salt::kMaxRc ||
+  if (cfg->n_centroids < 0 || cfg->n_centroids > salt::kMaxC || cfg->r_c < 0 || cfg->r_c > salt::kMaxRc ||
       cfg->r_c % 8 != 0 || (cfg->n_centroids == 0) != (cfg->r_c == 0))
     return SALT_ERR_OUT_OF_RANGE;
   if (cfg->n_slots < 1 || cfg->n_slots > (1 << 20) || cfg->r_u_max < 0 || cfg->r_u_max > salt::kMaxRu)
     return SALT_ERR_OUT_OF_RANGE;
-  if (cfg->max_tokens < 1 || cfg->max_tokens > (1 << 20)) return SALT_ERR_OUT_OF_RANGE;
-  if (cfg->flags & ~SALT_DETERMINISTIC) return SALT_ERR_INVALID_ARG;
+  if (cfg->max_tokens < 1 || cfg->max_tokens > salt::kMaxTokens) return SALT_ERR_OUT_OF_RANGE;
+  if (cfg->flags != 0) return SALT_ERR_INVALID_ARG;
   for (int i = 0; i < cfg->n_tables; ++i) {
     const salt_shape s = cfg->tables[i];
     if (s.in_dim <= 0 || s.out_dim <= 0 || s.in_dim % 8 || s.out_dim % 8 || s.in_dim > (1 << 20) ||
@@ -336,6 +678,7 @@ salt_status salt_create(const salt_config* cfg, salt_ctx** out) {
   c->cent_at.assign(cfg->n_tables, nullptr);
   c->cent_b.assign(cfg->n_tables, nullptr);
   c->cent_pinned.assign((size_t)cfg->n_tables * C, 0);
+  c->table_ready.assign(cfg->n_tables, C == 0 ? 1 : 0);
   if (C > 0) {
     for (int t = 0; t < cfg->n_tables; ++t) {
       const salt_shape s = c->tables[t];
@@ -372,23 +715,18 @@ void salt_destroy(salt_ctx* ctx) {
   if (!ctx) return;
   (void)hipSetDevice(ctx->device);
   (void)hipDeviceSynchronize();
-  for (salt_plan* p : ctx->plans) {
-    free_plan_buffers(p);
-    delete p;
-  }
+  for (salt_plan* p : ctx->plans) free_plan(p);
   destroy_ctx_memory(ctx);
   delete ctx;
 }
 
-salt_status salt_pin_centroids(salt_ctx* ctx, int32_t table, int32_t c0, int32_t n,
-                               const void* At_host, const void* B_host) {
-  if (!ctx) return SALT_ERR_INVALID_ARG;
-  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+salt_status salt_pin_centroids(salt_ctx* ctx, int32_t table, int32_t c0, int32_t n, const void* At_host,
+                               const void* B_host) {
+  SALT_LIVE(ctx);
   if (table < 0 || table >= ctx->cfg.n_tables)
     return fail(ctx, SALT_ERR_OUT_OF_RANGE, "table %d not in [0, %d)", table, ctx->cfg.n_tables);
   if (n < 0 || c0 < 0 || c0 + n > ctx->cfg.n_centroids)
-    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "centroids [%d, %d) not in [0, %d)", c0, c0 + n,
-                ctx->cfg.n_centroids);
+    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "centroids [%d, %d) not in [0, %d)", c0, c0 + n, ctx->cfg.n_centroids);
   if (n == 0) return SALT_OK;
   if (!At_host || !B_host) return fail(ctx, SALT_ERR_INVALID_ARG, "null centroid array");
   SALT_HIP(ctx, hipSetDevice(ctx->device));
@@ -406,49 +744,25 @@ salt_status salt_pin_centroids(salt_ctx* ctx, int32_t table, int32_t c0, int32_t
     transpose_rank_major(static_cast<const uint32_t*>(B_host), reinterpret_cast<uint32_t*>(bt.data()), n, rc, out);
   SALT_HIP(ctx, hipMemcpy(ctx->cent_b[table] + (size_t)c0 * rc * out * es, bt.data(), bt.size(),
                           hipMemcpyHostToDevice));
-  for (int i = c0; i < c0 + n; ++i) ctx->cent_pinned[(size_t)table * ctx->cfg.n_centroids + i] = 1;
+  const int C = ctx->cfg.n_centroids;
+  for (int i = c0; i < c0 + n; ++i) ctx->cent_pinned[(size_t)table * C + i] = 1;
+  bool all = true;
+  for (int i = 0; i < C; ++i) all = all && ctx->cent_pinned[(size_t)table * C + i];
+  ctx->table_ready[table] = all ? 1 : 0;
   return SALT_OK;
 }
 
-salt_status salt_load_residual(salt_ctx* ctx, int32_t slot, int32_t r_u, const void* blob,
-                               size_t bytes) {
-  if (!ctx) return SALT_ERR_INVALID_ARG;
-  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
-  if (slot < 0 || slot >= ctx->cfg.n_slots)
-    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "slot %d not in [0, %d)", slot, ctx->cfg.n_slots);
-  if (r_u < 0 || r_u > ctx->cfg.r_u_max)
-    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "rank %d not in [0, %d]", r_u, ctx->cfg.r_u_max);
-  const size_t want = salt_residual_bytes(ctx, r_u);
-  if (bytes != want)
-    return fail(ctx, SALT_ERR_INVALID_ARG, "blob is %zu bytes, rank %d needs %zu", bytes, r_u, want);
-  if (want > 0) {
-    if (!blob || !aligned16(blob)) return fail(ctx, SALT_ERR_INVALID_ARG, "null or misaligned blob");
-    hipPointerAttribute_t attr;
-    hipError_t e = hipPointerGetAttributes(&attr, blob);
-    if (e != hipSuccess || attr.type != hipMemoryTypeHost) {
-      (void)hipGetLastError();
-      return fail(ctx, SALT_ERR_NOT_PINNED, "blob %p is not page-locked host memory", blob);
-    }
-  }
-  SALT_HIP(ctx, hipSetDevice(ctx->device));
-  // the swap may not overwrite what an enqueued apply still reads
-  for (salt_plan* p : ctx->plans)
-    if (p->readers_open && std::binary_search(p->slots.begin(), p->slots.end(), slot))
-      SALT_HIP(ctx, close_readers(ctx, p));
-  SALT_HIP(ctx, ring_wait(ctx->readers, ctx->side, ctx->slot_reader[slot]));
-  if (want > 0)
-    SALT_HIP(ctx, hipMemcpyAsync(ctx->pool + (size_t)slot * ctx->slot_stride, blob, want,
-                                 hipMemcpyHostToDevice, ctx->side));
-  int64_t seq;
-  SALT_HIP(ctx, ring_record(ctx->loaders, ctx->side, &seq));
-  ctx->slot_loader[slot] = seq;
-  ctx->slot_rank[slot] = r_u;
-  return SALT_OK;
+salt_status salt_load_residual(salt_ctx* ctx, int32_t slot, int32_t r_u, const void* blob, size_t bytes) {
+  return load_impl(ctx, 1, &slot, &r_u, &blob, &bytes);
+}
+
+salt_status salt_load_residuals(salt_ctx* ctx, int32_t n, const int32_t* slots, const int32_t* ranks,
+                                const void* const* blobs, const size_t* bytes) {
+  return load_impl(ctx, n, slots, ranks, blobs, bytes);
 }
 
 salt_status salt_wait_loads(salt_ctx* ctx) {
-  if (!ctx) return SALT_ERR_INVALID_ARG;
-  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  SALT_LIVE(ctx);
   SALT_HIP(ctx, hipSetDevice(ctx->device));
   SALT_HIP(ctx, hipStreamSynchronize(ctx->side));
   ctx->loaders.done = ctx->loaders.next - 1;
@@ -456,62 +770,11 @@ salt_status salt_wait_loads(salt_ctx* ctx) {
 }
 
 salt_status salt_plan_create(salt_ctx* ctx, salt_plan** out) {
-  if (!ctx || !out) return SALT_ERR_INVALID_ARG;
+  if (!out) return SALT_ERR_INVALID_ARG;
   *out = nullptr;
-  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  SALT_LIVE(ctx);
   SALT_HIP(ctx, hipSetDevice(ctx->device));
-  salt_plan* p = new (std::nothrow) salt_plan();
-  if (!p) return SALT_ERR_OUT_OF_MEMORY;
-  const size_t T = (size_t)ctx->cfg.max_tokens;
-  const size_t R = salt::padded_rank(ctx->cfg.r_c, ctx->cfg.r_u_max);
-  PlanBuffers& b = p->dev;
-  // split-K partials for up to max(8 T, 64K) (split, token) pairs
-  b.partial_cap = std::max<size_t>(8 * T, 65536) * R;
-  b.v_stride = T * R;
-  // tiles: at most ceil(T / M) + one partial tile per centroid group (<= 65)
-  b.tiles_max = (int32_t)((T + 15) / 16 + 66);
-  b.tile_cap = 0;
-  for (size_t M : {16, 32, 64}) b.tile_cap = std::max(b.tile_cap, ((T + M - 1) / M + 66) * (M + 1));
-  bool ok = hipMalloc((void**)&b.maps, T * sizeof(int4)) == hipSuccess &&
-            hipMalloc((void**)&b.perm, T * 4) == hipSuccess &&
-            hipMalloc((void**)&b.srt, T * sizeof(int4)) == hipSuccess &&
-            hipMalloc((void**)&b.srt_c, T * 4) == hipSuccess &&
-            hipMalloc((void**)&b.seg_off, (T + 1) * 4) == hipSuccess &&
-            hipMalloc((void**)&b.seg_c, T * 4) == hipSuccess &&
-            hipMalloc((void**)&b.seg_u, T * 4) == hipSuccess &&
-            hipMalloc((void**)&b.grp_off, (T + 1) * 4) == hipSuccess &&
-            hipMalloc((void**)&b.grp_tok, (T + 1) * 4) == hipSuccess &&
-            hipMalloc((void**)&b.grp_c, T * 4) == hipSuccess &&
-            hipMalloc((void**)&b.tiles, b.tile_cap * sizeof(int4)) == hipSuccess &&
-            hipMalloc((void**)&b.arrive, (size_t)b.tiles_max * salt::kCounterStride * 4) == hipSuccess &&
-            hipMalloc((void**)&b.ready, (size_t)b.tiles_max * salt::kReadyPerTile * 4) == hipSuccess &&
-            hipMalloc((void**)&b.v, 2 * T * R * 4) == hipSuccess &&
-            hipMalloc((void**)&b.meta, salt::kMetaWords * 4) == hipSuccess &&
-            hipMalloc((void**)&b.counter, 64 * 4) == hipSuccess &&
-            hipMalloc((void**)&b.partials, b.partial_cap * 4) == hipSuccess &&
-            hipMalloc((void**)&b.sink, salt::kSinkBytes) == hipSuccess &&
-            hipHostMalloc((void**)&p->staging, T * sizeof(int4), hipHostMallocDefault) == hipSuccess;
-  if (!ok) {
-    (void)hipGetLastError();
-    free_plan_buffers(p);
-    delete p;
-    return fail(ctx, SALT_ERR_OUT_OF_MEMORY, "plan buffers for %zu tokens do not fit", T);
-  }
-  hipError_t e = hipEventCreateWithFlags(&p->staged, hipEventDisableTiming);
-  if (e == hipSuccess) e = hipMemset(b.counter, 0, 64 * 4);
-  if (e == hipSuccess) e = hipMemset(b.meta, 0, salt::kMetaWords * 4);
-  if (e == hipSuccess) e = hipMemset(b.arrive, 0, (size_t)b.tiles_max * salt::kCounterStride * 4);
-  if (e == hipSuccess) e = hipMemset(b.ready, 0, (size_t)b.tiles_max * salt::kReadyPerTile * 4);
-  if (e == hipSuccess) e = hipMemset(b.v, 0, 2 * T * R * 4);
-  if (e == hipSuccess) e = hipDeviceSynchronize();
-  if (e != hipSuccess) {
-    free_plan_buffers(p);
-    delete p;
-    return hip_fail(ctx, e, "plan init");
-  }
-  ctx->plans.push_back(p);
-  *out = p;
-  return SALT_OK;
+  return plan_create(ctx, out);
 }
 
 void salt_plan_destroy(salt_ctx* ctx, salt_plan* plan) {
@@ -521,154 +784,70 @@ void salt_plan_destroy(salt_ctx* ctx, salt_plan* plan) {
   (void)hipSetDevice(ctx->device);
   (void)hipDeviceSynchronize();
   ctx->plans.erase(it);
-  free_plan_buffers(plan);
-  delete plan;
+  if (ctx->map_plan == plan) ctx->map_plan = nullptr;
+  free_plan(plan);
 }
 
-salt_status salt_plan_set_maps(salt_ctx* ctx, salt_plan* plan, int32_t T, const int32_t* tok_c,
-                               const int32_t* tok_u, const float* tok_gamma, void* stream) {
-  if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
-  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
-  if (T < 0 || T > ctx->cfg.max_tokens)
-    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "T = %d not in [0, %d]", T, ctx->cfg.max_tokens);
-  if (T > 0 && (!tok_c || !tok_u)) return fail(ctx, SALT_ERR_INVALID_ARG, "null map");
-  const int C = ctx->cfg.n_centroids, S = ctx->cfg.n_slots;
-  for (int t = 0; t < T; ++t) {
-    if (tok_c[t] < -1 || tok_c[t] >= C)
-      return fail(ctx, SALT_ERR_OUT_OF_RANGE, "tok_c[%d] = %d not in [-1, %d)", t, tok_c[t], C);
-    if (tok_u[t] < -1 || tok_u[t] >= S)
-      return fail(ctx, SALT_ERR_OUT_OF_RANGE, "tok_u[%d] = %d not in [-1, %d)", t, tok_u[t], S);
-    if (tok_u[t] >= 0 && ctx->slot_rank[tok_u[t]] < 0)
-      return fail(ctx, SALT_ERR_SLOT_EMPTY, "tok_u[%d] = %d: slot never loaded", t, tok_u[t]);
-    if (tok_gamma && !std::isfinite(tok_gamma[t]))
-      return fail(ctx, SALT_ERR_INVALID_ARG, "tok_gamma[%d] is not finite", t);
-  }
-  SALT_HIP(ctx, hipSetDevice(ctx->device));
-  hipStream_t s = (hipStream_t)stream;
-  SALT_HIP(ctx, flush_build(plan));
-  // the staging buffer may still feed the previous copy
-  if (plan->staged_pending) {
-    SALT_HIP(ctx, hipEventSynchronize(plan->staged));
-    plan->staged_pending = false;
-  }
-  std::vector<int32_t> slots;
-  std::vector<int32_t> per_c((size_t)C + 1, 0);   // tokens per centroid id (+1 for c = -1)
-  int64_t sum_ru = 0;
-  for (int t = 0; t < T; ++t) {
-    const int u = tok_u[t];
-    const int r = u >= 0 ? ctx->slot_rank[u] : 0;
-    const float g = tok_gamma ? tok_gamma[t] : 1.0f;
-    int32_t gbits;
-    std::memcpy(&gbits, &g, 4);
-    plan->staging[t] = make_int4(tok_c[t], u, r, gbits);
-    if (u >= 0) slots.push_back(u);
-    per_c[(size_t)tok_c[t] + 1]++;
-    sum_ru += r;
-  }
-  std::sort(slots.begin(), slots.end());
-  slots.erase(std::unique(slots.begin(), slots.end()), slots.end());
-  // the previous batch's applies still read the old slots
-  SALT_HIP(ctx, close_readers(ctx, plan));
-  plan->slots = slots;
-  plan->slot_rank.resize(slots.size());
-  for (size_t i = 0; i < slots.size(); ++i) plan->slot_rank[i] = ctx->slot_rank[slots[i]];
-  // tile size from the mean group size; the tile count is exact
-  int n_groups = 0, n_groups_c = 0;
-  for (int g = 0; g <= C; ++g)
-    if (per_c[g]) {
-      ++n_groups;
-      n_groups_c += (g > 0);
-    }
-  const double mean = n_groups ? (double)T / n_groups : 0.0;
-  plan->M = (ctx->cfg.dtype == SALT_F32 || mean <= 24.0) ? 16 : 32;
-  // large bf16 batches with long centroid groups and residual rank <= 2: the
-  // two-launch apply with 64-token tiles (bandwidth bound; no in-launch hand-off)
-  if (ctx->cfg.dtype == SALT_BF16 && T > salt::kPlanFusedT && ctx->cfg.r_u_max <= 2 && mean >= 96.0)
-    plan->M = salt::kTwoPassM;
-  int n_tiles = 0;
-  for (int g = 0; g <= C; ++g) n_tiles += (per_c[g] + plan->M - 1) / plan->M;
-  plan->n_tiles = n_tiles;
-  plan->n_groups_c = n_groups_c;
-  plan->sum_ru = sum_ru;
-  plan->T = T;
-  plan->built = false;
-  if (T > 0) {
-    SALT_HIP(ctx, hipMemcpyAsync(plan->dev.maps, plan->staging, (size_t)T * sizeof(int4),
-                                 hipMemcpyHostToDevice, s));
-    SALT_HIP(ctx, hipEventRecord(plan->staged, s));
-    plan->staged_pending = true;
-  }
-  return SALT_OK;
+salt_status salt_plan_set_maps(salt_ctx* ctx, salt_plan* plan, int32_t T, const int32_t* tok_c, const int32_t* tok_u,
+                               const float* tok_gamma, void* stream) {
+  SALT_LIVE(ctx);
+  if (!plan) return SALT_ERR_INVALID_ARG;
+  return set_maps_impl(ctx, plan, T, tok_c, tok_u, tok_gamma, (hipStream_t)stream);
 }
 
 salt_status salt_plan_build(salt_ctx* ctx, salt_plan* plan, void* stream) {
-  if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
-  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
-  SALT_HIP(ctx, hipSetDevice(ctx->device));
-  SALT_HIP(ctx, flush_build(plan));
-  const bool reset = plan->epoch >= kEpochReset;
-  if (reset) plan->epoch &= 1u;   // keeps the parity that picks the v buffer
-  if (!reset && atomic_sums(ctx) && plan->T > 0 && plan->T <= salt::kPlanFusedT) {
-    plan->build_pending = true;
-    plan->build_stream = (hipStream_t)stream;
-  } else {
-    SALT_HIP(ctx, launch_build(plan, (hipStream_t)stream, reset));
-  }
-  plan->built = true;
-  plan->arrivals = 0;
-  return SALT_OK;
+  SALT_LIVE(ctx);
+  if (!plan) return SALT_ERR_INVALID_ARG;
+  return build_impl(ctx, plan, (hipStream_t)stream);
 }
 
 salt_status salt_plan_tiling(salt_ctx* ctx, const salt_plan* plan, int32_t* tile_tokens, int32_t* n_tiles,
                              int32_t* launches) {
   if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
-  if (plan->T < 0 || plan->M <= 0) return fail(ctx, SALT_ERR_BAD_STATE, "no maps were set on the plan");
+  if (plan->T < 0) return fail(ctx, SALT_ERR_BAD_STATE, "no maps were set on the plan");
   if (tile_tokens) *tile_tokens = plan->M;
   if (n_tiles) *n_tiles = plan->n_tiles;
-  if (launches) *launches = plan->M == salt::kTwoPassM ? 2 : 1;
+  if (launches) *launches = plan->T > 0 ? 2 : 0;
   return SALT_OK;
 }
 
-salt_status salt_plan_errors(salt_ctx* ctx, const salt_plan* plan, void* stream, int32_t* n_errors) {
-  if (!ctx || !plan || !n_errors) return SALT_ERR_INVALID_ARG;
-  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+salt_status salt_plan_errors(salt_ctx* ctx, const salt_plan* plan_c, void* stream, int32_t* n_errors) {
+  SALT_LIVE(ctx);
+  if (!plan_c || !n_errors) return SALT_ERR_INVALID_ARG;
+  salt_plan* plan = const_cast<salt_plan*>(plan_c);
   *n_errors = 0;
-  if (!plan->built || plan->T == 0) return SALT_OK;
+  if (!plan->built || plan->T <= 0) return SALT_OK;
   SALT_HIP(ctx, hipSetDevice(ctx->device));
-  SALT_HIP(ctx, flush_build(plan));
-  SALT_HIP(ctx, hipStreamSynchronize((hipStream_t)stream));
-  if (plan->build_stream && plan->build_stream != (hipStream_t)stream)
-    SALT_HIP(ctx, hipStreamSynchronize(plan->build_stream));
+  hipStream_t s = (hipStream_t)stream;
+  SALT_HIP(ctx, use_stream(ctx, plan, s));
+  SALT_HIP(ctx, hipStreamSynchronize(s));
   int32_t meta[salt::kMetaWords];
-  SALT_HIP(ctx, hipMemcpy(meta, plan->dev.meta, sizeof meta, hipMemcpyDeviceToHost));
-  if (meta[salt::kMetaNTiles] != plan->n_tiles) {
-    *n_errors = 1;
-    return fail(ctx, SALT_ERR_BAD_STATE, "device plan has %d tiles, host expected %d",
-                meta[salt::kMetaNTiles], plan->n_tiles);
-  }
+  SALT_HIP(ctx, hipMemcpy(meta, plan->meta, sizeof meta, hipMemcpyDeviceToHost));
   *n_errors = meta[salt::kMetaErr];
-  if (meta[salt::kMetaErr] != 0) {
-    const int32_t zero = 0;
-    SALT_HIP(ctx, hipMemcpy(plan->dev.meta + salt::kMetaErr, &zero, 4, hipMemcpyHostToDevice));
+  if (meta[salt::kMetaNTiles] != plan->n_tiles || meta[salt::kMetaT] != plan->T) {
+    *n_errors += 1;
+    return fail(ctx, SALT_ERR_BAD_STATE, "device plan has %d tiles of %d tokens, host staged %d of %d",
+                meta[salt::kMetaNTiles], meta[salt::kMetaT], plan->n_tiles, plan->T);
   }
   return SALT_OK;
 }
 
-salt_status salt_plan_download(salt_ctx* ctx, const salt_plan* plan, void* stream, int32_t* perm,
-                               int32_t* seg_off, int32_t* seg_c, int32_t* seg_u, int32_t* grp_off,
-                               int32_t* n_seg, int32_t* n_grp) {
-  if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
-  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+salt_status salt_plan_download(salt_ctx* ctx, const salt_plan* plan_c, void* stream, int32_t* perm, int32_t* seg_off,
+                               int32_t* seg_c, int32_t* seg_u, int32_t* grp_off, int32_t* n_seg, int32_t* n_grp) {
+  SALT_LIVE(ctx);
+  if (!plan_c) return SALT_ERR_INVALID_ARG;
+  salt_plan* plan = const_cast<salt_plan*>(plan_c);
   if (!plan->built) return fail(ctx, SALT_ERR_BAD_STATE, "plan was not built");
   SALT_HIP(ctx, hipSetDevice(ctx->device));
   hipStream_t s = (hipStream_t)stream;
-  SALT_HIP(ctx, flush_build(plan));
-  SALT_HIP(ctx, hipStreamSynchronize(s));
-  if (plan->build_stream && plan->build_stream != s) SALT_HIP(ctx, hipStreamSynchronize(plan->build_stream));
   const int T = plan->T;
   int32_t meta[3] = {0, 0, 0};
-  if (T > 0) SALT_HIP(ctx, hipMemcpy(meta, plan->dev.meta, sizeof meta, hipMemcpyDeviceToHost));
-  const int ns = meta[0], ng = meta[1];
+  if (T > 0) {
+    SALT_HIP(ctx, use_stream(ctx, plan, s));
+    SALT_HIP(ctx, hipStreamSynchronize(s));
+    SALT_HIP(ctx, hipMemcpy(meta, plan->meta, sizeof meta, hipMemcpyDeviceToHost));
+  }
+  const int ns = std::min(std::max(meta[0], 0), std::max(T, 0)), ng = std::min(std::max(meta[1], 0), ns);
   if (n_seg) *n_seg = ns;
   if (n_grp) *n_grp = ng;
   if (T == 0) {
@@ -676,30 +855,49 @@ salt_status salt_plan_download(salt_ctx* ctx, const salt_plan* plan, void* strea
     if (grp_off) grp_off[0] = 0;
     return SALT_OK;
   }
-  if (perm) SALT_HIP(ctx, hipMemcpy(perm, plan->dev.perm, (size_t)T * 4, hipMemcpyDeviceToHost));
-  if (seg_off) SALT_HIP(ctx, hipMemcpy(seg_off, plan->dev.seg_off, (size_t)(ns + 1) * 4, hipMemcpyDeviceToHost));
-  if (seg_c) SALT_HIP(ctx, hipMemcpy(seg_c, plan->dev.seg_c, (size_t)ns * 4, hipMemcpyDeviceToHost));
-  if (seg_u) SALT_HIP(ctx, hipMemcpy(seg_u, plan->dev.seg_u, (size_t)ns * 4, hipMemcpyDeviceToHost));
-  if (grp_off) SALT_HIP(ctx, hipMemcpy(grp_off, plan->dev.grp_off, (size_t)(ng + 1) * 4, hipMemcpyDeviceToHost));
+  if (perm) SALT_HIP(ctx, hipMemcpy(perm, plan->perm(), (size_t)T * 4, hipMemcpyDeviceToHost));
+  if (seg_off) SALT_HIP(ctx, hipMemcpy(seg_off, plan->seg_off(), (size_t)(ns + 1) * 4, hipMemcpyDeviceToHost));
+  if (seg_c) SALT_HIP(ctx, hipMemcpy(seg_c, plan->seg_c(), (size_t)ns * 4, hipMemcpyDeviceToHost));
+  if (seg_u) SALT_HIP(ctx, hipMemcpy(seg_u, plan->seg_u(), (size_t)ns * 4, hipMemcpyDeviceToHost));
+  if (grp_off) SALT_HIP(ctx, hipMemcpy(grp_off, plan->grp_off(), (size_t)(ng + 1) * 4, hipMemcpyDeviceToHost));
   return SALT_OK;
 }
 
-namespace {
-salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y, void* stream,
-                       hipEvent_t e0, hipEvent_t e1);
-salt_status fuse_impl(salt_ctx* ctx, int32_t table, int32_t c, float gamma, void* w, int64_t ldw, void* stream,
-                      hipEvent_t e0, hipEvent_t e1);
-}  // namespace
-
-salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y,
-                       void* stream) {
-  return apply_impl(ctx, table, plan, x, y, stream, nullptr, nullptr);
+salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y, void* stream) {
+  return apply_impl(ctx, 1, &table, plan, &x, &y, (hipStream_t)stream, nullptr);
 }
 
-salt_status salt_apply_timed(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y,
-                             void* stream, void* start_event, void* stop_event) {
-  if (!start_event || !stop_event) return fail(ctx, SALT_ERR_INVALID_ARG, "null event");
-  return apply_impl(ctx, table, plan, x, y, stream, (hipEvent_t)start_event, (hipEvent_t)stop_event);
+salt_status salt_apply_batch(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_plan* plan, const void* const* xs,
+                             void* const* ys, void* stream) {
+  return apply_impl(ctx, n, tables, plan, xs, ys, (hipStream_t)stream, nullptr);
+}
+
+salt_status salt_apply_batch_timed(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_plan* plan,
+                                   const void* const* xs, void* const* ys, void* stream, void* const* events) {
+  if (!events || !events[0] || !events[1] || !events[2] || !events[3])
+    return fail(ctx, SALT_ERR_INVALID_ARG, "null event");
+  hipEvent_t ev[4] = {(hipEvent_t)events[0], (hipEvent_t)events[1], (hipEvent_t)events[2], (hipEvent_t)events[3]};
+  return apply_impl(ctx, n, tables, plan, xs, ys, (hipStream_t)stream, ev);
+}
+
+salt_status salt_apply_map(salt_ctx* ctx, int32_t table, int32_t T, const int32_t* tok_c, const int32_t* tok_u,
+                           const float* tok_gamma, const void* x, void* y, void* stream) {
+  SALT_LIVE(ctx);
+  if (table < 0 || table >= ctx->cfg.n_tables)
+    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "table %d not in [0, %d)", table, ctx->cfg.n_tables);
+  if (!ctx->map_plan) {
+    salt_plan* p = nullptr;
+    SALT_HIP(ctx, hipSetDevice(ctx->device));
+    const salt_status st = plan_create(ctx, &p);
+    if (st != SALT_OK) return st;
+    ctx->map_plan = p;
+  }
+  const hipStream_t s = (hipStream_t)stream;
+  salt_status st = set_maps_impl(ctx, ctx->map_plan, T, tok_c, tok_u, tok_gamma, s);
+  if (st != SALT_OK) return st;
+  st = build_impl(ctx, ctx->map_plan, s);
+  if (st != SALT_OK) return st;
+  return apply_impl(ctx, 1, &table, ctx->map_plan, &x, &y, s, nullptr);
 }
 
 salt_status salt_fuse_centroid(salt_ctx* ctx, int32_t table, int32_t c, float gamma, void* w, int64_t ldw,
@@ -713,9 +911,9 @@ salt_status salt_fuse_centroid_timed(salt_ctx* ctx, int32_t table, int32_t c, fl
   return fuse_impl(ctx, table, c, gamma, w, ldw, stream, (hipEvent_t)start_event, (hipEvent_t)stop_event);
 }
 
-salt_status salt_route(int32_t K, const double* n_k, const double* mu_n, const double* sigma_n,
-                       const double* mu_r, const double* sigma_r, double tau_n, double tau_r, double* z_n,
-                       double* z_r, salt_route_result* out) {
+salt_status salt_route(int32_t K, const double* n_k, const double* mu_n, const double* sigma_n, const double* mu_r,
+                       const double* sigma_r, double tau_n, double tau_r, double* z_n, double* z_r,
+                       salt_route_result* out) {
   if (K < 2 || !n_k || !mu_n || !sigma_n || !mu_r || !sigma_r || !out) return SALT_ERR_INVALID_ARG;
   if (!std::isfinite(tau_n) || !std::isfinite(tau_r)) return SALT_ERR_INVALID_ARG;
   double total = 0.0;
@@ -763,8 +961,8 @@ salt_status salt_route(int32_t K, const double* n_k, const double* mu_n, const d
 
 salt_status salt_adapter_gram(salt_ctx* ctx, const void* blob1, int32_t r1, const void* blob2, int32_t r2,
                               double* out, void* stream) {
-  if (!ctx || !out) return SALT_ERR_INVALID_ARG;
-  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
+  SALT_LIVE(ctx);
+  if (!out) return SALT_ERR_INVALID_ARG;
   if (r1 < 1 || r1 > kMaxGramRank || r2 < 1 || r2 > kMaxGramRank)
     return fail(ctx, SALT_ERR_OUT_OF_RANGE, "adapter ranks %d, %d not in [1, %d]", r1, r2, kMaxGramRank);
   if (!blob1 || !blob2 || !aligned16(blob1) || !aligned16(blob2))
@@ -828,210 +1026,3 @@ salt_status salt_adapter_gram(salt_ctx* ctx, const void* blob1, int32_t r1, cons
 }
 
 }  // extern "C"
-
-namespace {
-salt_status fuse_impl(salt_ctx* ctx, int32_t table, int32_t c, float gamma, void* w, int64_t ldw, void* stream,
-                      hipEvent_t e0, hipEvent_t e1) {
-  if (!ctx) return SALT_ERR_INVALID_ARG;
-  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
-  if (table < 0 || table >= ctx->cfg.n_tables)
-    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "table %d not in [0, %d)", table, ctx->cfg.n_tables);
-  const int C = ctx->cfg.n_centroids;
-  if (c < 0 || c >= C) return fail(ctx, SALT_ERR_OUT_OF_RANGE, "centroid %d not in [0, %d)", c, C);
-  if (!ctx->cent_pinned[(size_t)table * C + c])
-    return fail(ctx, SALT_ERR_BAD_STATE, "centroid %d of table %d was never pinned", c, table);
-  const salt_shape sh = ctx->tables[table];
-  if (!w || !aligned16(w)) return fail(ctx, SALT_ERR_INVALID_ARG, "null or misaligned weight");
-  if (ldw < sh.out_dim || ldw % 8 != 0)
-    return fail(ctx, SALT_ERR_INVALID_ARG, "ldw %lld: need a multiple of 8 and >= out_dim %d", (long long)ldw,
-                sh.out_dim);
-  if (!std::isfinite(gamma)) return fail(ctx, SALT_ERR_INVALID_ARG, "gamma is not finite");
-  SALT_HIP(ctx, hipSetDevice(ctx->device));
-  const size_t rc = ctx->cfg.r_c, es = ctx->esize;
-  salt::FuseArgs f{};
-  f.at = ctx->cent_at[table] + (size_t)c * rc * sh.in_dim * es;
-  f.bt = ctx->cent_b[table] + (size_t)c * rc * sh.out_dim * es;
-  f.w = w;
-  f.ldw = ldw;
-  f.in_dim = sh.in_dim;
-  f.out_dim = sh.out_dim;
-  f.r_c = (int32_t)rc;
-  f.gamma = gamma;
-  SALT_HIP(ctx, salt::launch_fuse(f, ctx->cfg.dtype == SALT_BF16, (hipStream_t)stream, e0, e1));
-  return SALT_OK;
-}
-
-salt_status apply_impl(salt_ctx* ctx, int32_t table, salt_plan* plan, const void* x, void* y, void* stream,
-                       hipEvent_t e0, hipEvent_t e1) {
-  if (!ctx || !plan) return SALT_ERR_INVALID_ARG;
-  if (ctx->poisoned) return fail(ctx, SALT_ERR_BAD_STATE, "context is poisoned: %s", ctx->err.c_str());
-  if (table < 0 || table >= ctx->cfg.n_tables)
-    return fail(ctx, SALT_ERR_OUT_OF_RANGE, "table %d not in [0, %d)", table, ctx->cfg.n_tables);
-  if (!plan->built) return fail(ctx, SALT_ERR_BAD_STATE, "plan was not built");
-  const int T = plan->T;
-  if (T == 0) return SALT_OK;
-  if (!x || !y || !aligned16(x) || !aligned16(y))
-    return fail(ctx, SALT_ERR_INVALID_ARG, "null or misaligned x / y");
-  const int C = ctx->cfg.n_centroids;
-  for (int i = 0; i < C; ++i)
-    if (!ctx->cent_pinned[(size_t)table * C + i])
-      return fail(ctx, SALT_ERR_BAD_STATE, "centroid %d of table %d was never pinned", i, table);
-  int64_t need_load = -1;
-  for (size_t i = 0; i < plan->slots.size(); ++i) {
-    const int s = plan->slots[i];
-    if (ctx->slot_rank[s] != plan->slot_rank[i])
-      return fail(ctx, SALT_ERR_BAD_STATE,
-                  "slot %d was reloaded with rank %d after the plan's maps were set (rank %d)", s,
-                  ctx->slot_rank[s], plan->slot_rank[i]);
-    need_load = std::max(need_load, ctx->slot_loader[s]);
-  }
-  SALT_HIP(ctx, hipSetDevice(ctx->device));
-  hipStream_t s = (hipStream_t)stream;
-  // a deferred build runs inside this launch when it was requested on this stream
-  const bool fused_plan = plan->build_pending && plan->build_stream == s;
-  if (!fused_plan) SALT_HIP(ctx, flush_build(plan));
-  SALT_HIP(ctx, ring_wait(ctx->loaders, s, need_load));
-
-  const salt_shape sh = ctx->tables[table];
-  ApplyArgs a{};
-  a.x = x;
-  a.y = y;
-  a.cent_at = C ? ctx->cent_at[table] : nullptr;
-  a.cent_bt = C ? ctx->cent_b[table] : nullptr;
-  a.pool = ctx->pool;
-  a.slot_stride = ctx->slot_stride;
-  a.tab_prefix = ctx->tab_prefix[table];
-  a.tiles = plan->dev.tiles;
-  a.partials = plan->dev.partials;
-  a.arrive = plan->dev.arrive;
-  a.ready = plan->dev.ready;
-  a.meta = plan->dev.meta;
-  a.sink = plan->dev.sink;
-  a.T = T;
-  a.in_dim = sh.in_dim;
-  a.out_dim = sh.out_dim;
-  a.r_c = ctx->cfg.r_c;
-  a.r_u_max = ctx->cfg.r_u_max;
-  a.R = salt::padded_rank(a.r_c, a.r_u_max);
-  a.n_tiles = plan->n_tiles;
-  if (plan->M == salt::kTwoPassM) {
-    // Two launches, each sized to what the device holds at once (one round of
-    // blocks).  Shrink: (tile, K range) blocks, K ranges a multiple of 4 waves x
-    // 32.  Expand: (tile, column range) blocks, each streaming its chunks two
-    // at a time.
-    if (!ctx->occ_shrink) {
-      SALT_HIP(ctx, salt::two_pass_occupancy(a.r_c, a.r_u_max, a.R, &ctx->occ_shrink, &ctx->occ_expand));
-      ctx->occ_shrink = std::max(1, ctx->occ_shrink);
-      ctx->occ_expand = std::max(1, ctx->occ_expand);
-    }
-    const bool atomic = atomic_sums(ctx);
-    const int gran = 128;
-    int S = (int)std::max<int64_t>(1, (int64_t)ctx->occ_shrink * ctx->n_cu / a.n_tiles);
-    S = std::min({S, 8, (sh.in_dim + gran - 1) / gran});
-    while (!atomic && S > 1 && (size_t)S * T * a.R > plan->dev.partial_cap) --S;
-    a.Kc = ((sh.in_dim + S - 1) / S + gran - 1) / gran * gran;
-    a.S = (sh.in_dim + a.Kc - 1) / a.Kc;
-    a.sk = a.S;
-    const int chunks = (sh.out_dim + salt::kNC - 1) / salt::kNC;
-    const int n_col = (int)std::min<int64_t>(
-        chunks, std::max<int64_t>(1, (int64_t)ctx->occ_expand * ctx->n_cu / a.n_tiles));
-    a.cpb = (chunks + n_col - 1) / n_col;
-    a.n_col = (chunks + a.cpb - 1) / a.cpb;
-    a.two_pass = 1;
-    a.fused_plan = 0;
-    a.writer = -1;
-    a.maps = plan->dev.maps;
-    a.partials = plan->dev.partials;
-    a.atomic_sum = atomic ? 1 : 0;
-    a.epoch = ++plan->epoch;
-    a.clear_rows = T;
-    if (atomic) {
-      // the same alternating v buffers as the single-launch atomic sums
-      const int p = (int)(a.epoch & 1u), q = p ^ 1;
-      a.v = plan->dev.v + (size_t)p * plan->dev.v_stride;
-      a.v_clear = plan->dev.v + (size_t)q * plan->dev.v_stride;
-      a.clear_rows = std::max(T, plan->v_dirty[q]);
-      plan->v_dirty[q] = 0;
-      plan->v_dirty[p] = T;
-    } else {
-      a.v = plan->dev.v;
-      a.v_clear = nullptr;
-    }
-    SALT_HIP(ctx, salt::launch_apply(a, 1, salt::kTwoPassM, s, e0, e1));
-    SALT_HIP(ctx, open_readers(ctx, plan, s));
-    return SALT_OK;
-  }
-  // K split.  Small (decode) batches are latency bound: spread the shrink input
-  // over many blocks (~16 KiB each) so no CU streams much more than its share,
-  // and let partial traffic reach half of the input.  Large (prefill) batches
-  // are bandwidth bound: ~64 KiB blocks, partial traffic under a fifth.
-  const int M = plan->M, KW = 64 / M;
-  const double es = (double)ctx->esize;
-  const double shrink_bytes = es * sh.in_dim * ((double)T + (double)plan->n_groups_c * a.r_c + (double)plan->sum_ru);
-  const bool small = T <= 1024;
-  const double block_bytes = small ? 16384.0 : 65536.0;
-  const int s_bytes = (int)std::ceil(shrink_bytes / ((double)a.n_tiles * block_bytes));
-  const int s_traffic = std::max(1, (int)((small ? 0.5 : 0.2) * shrink_bytes / ((double)T * a.R * 8.0)));
-  const int gran = 32 * KW;
-  // the last block of a tile sums S x M x R partials: keep that within ~64 KiB
-  const bool atomic = atomic_sums(ctx);
-  const int s_reduce = atomic ? salt::kMaxSplit : std::max(1, (int)(65536 / ((size_t)M * a.R * 4)));
-  int S = std::max(1, std::min({s_bytes, s_traffic, s_reduce, salt::kMaxSplit, (sh.in_dim + gran - 1) / gran}));
-  if (small) {
-    // at most two register batches of U steps per wave (U as the kernel picks
-    // it), so that the shrink loop runs straight through with every load in flight
-    const int ru_t = a.r_u_max <= 1 ? 1 : (a.r_u_max <= 2 ? 2 : salt::kRankChunk);
-    const int U = std::max(1, salt::shrink_batch(ctx->esize == 2 ? 4 : 8, 1, salt::centroid_blocks(a.r_c), ru_t) / 2);
-    const int s_steps = (sh.in_dim + 2 * U * gran - 1) / (2 * U * gran);
-    S = std::max(S, std::min({s_steps, salt::kMaxSplit, (sh.in_dim + gran - 1) / gran}));
-  }
-  // residual ranks above kRankChunk: one shrink block per (K range, chunk)
-  const int nq = a.r_u_max > salt::kRankChunk ? (a.r_u_max + salt::kRankChunk - 1) / salt::kRankChunk : 1;
-  S = std::max(1, std::min(S, salt::kMaxSplit / nq));
-  while (S > 1 && (size_t)S * nq * T * a.R > plan->dev.partial_cap) --S;
-  const int Kc = ((sh.in_dim + S - 1) / S + gran - 1) / gran * gran;
-  a.Kc = Kc;
-  a.sk = (sh.in_dim + Kc - 1) / Kc;   // <= S
-  a.S = a.sk * nq;
-  // expand: one kNC-column chunk per block while the launch fits the device
-  // at about four blocks per compute unit; past that, each block streams several
-  // chunks (two in flight), so that the expand blocks left beside the shrink
-  // blocks are all resident and load their first chunks before v is ready
-  const int chunks = (sh.out_dim + salt::kNC - 1) / salt::kNC;
-  const int64_t n_exp = std::max<int64_t>({(int64_t)a.n_tiles, 4 * (int64_t)ctx->n_cu - (int64_t)a.n_tiles * a.S,
-                                           2 * (int64_t)ctx->n_cu});
-  a.cpb = (int)std::max<int64_t>(1, ((int64_t)a.n_tiles * chunks + n_exp - 1) / n_exp);
-  a.n_col = (chunks + a.cpb - 1) / a.cpb;
-  if (!atomic && a.S > 1) plan->arrivals += (uint32_t)a.S;
-  a.target = plan->arrivals;
-  a.epoch = ++plan->epoch;
-  a.atomic_sum = atomic ? 1 : 0;
-  a.clear_rows = T;
-  if (atomic) {
-    // v buffers alternate between applies: this apply sums into buffer
-    // p = epoch & 1 (all zero: the previous apply cleared it) and clears the
-    // other one, including rows an earlier larger batch used
-    const int p = (int)(a.epoch & 1u), q = p ^ 1;
-    a.v = plan->dev.v + (size_t)p * plan->dev.v_stride;
-    a.v_clear = plan->dev.v + (size_t)q * plan->dev.v_stride;
-    a.clear_rows = std::max(T, plan->v_dirty[q]);
-    plan->v_dirty[q] = 0;
-    plan->v_dirty[p] = T;
-  } else {
-    a.v = plan->dev.v;
-    a.v_clear = nullptr;
-  }
-  a.fused_plan = fused_plan ? 1 : 0;
-  a.writer = -1;
-  a.maps = plan->dev.maps;
-  if (fused_plan) {
-    a.pb = plan->dev;
-    a.writer = a.n_tiles * (a.S + a.n_col);   // one block past the apply's own
-    plan->build_pending = false;
-  }
-  SALT_HIP(ctx, salt::launch_apply(a, ctx->cfg.dtype == SALT_BF16, M, s, e0, e1));
-  SALT_HIP(ctx, open_readers(ctx, plan, s));
-  return SALT_OK;
-}
-
-}  // namespace

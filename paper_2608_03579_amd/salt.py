@@ -24,10 +24,11 @@ F32, BF16 = 0, 1
 # every entry point declared in include/salt.h
 EXPORTS = (
     "salt_create", "salt_destroy", "salt_pin_centroids", "salt_residual_bytes",
-    "salt_residual_bytes_for", "salt_load_residual", "salt_wait_loads", "salt_host_alloc",
-    "salt_host_free", "salt_plan_create", "salt_plan_destroy", "salt_plan_set_maps",
+    "salt_residual_bytes_for", "salt_load_residual", "salt_load_residuals", "salt_wait_loads",
+    "salt_host_alloc", "salt_host_free", "salt_plan_create", "salt_plan_destroy", "salt_plan_set_maps",
     "salt_plan_build", "salt_plan_download", "salt_plan_errors", "salt_plan_tiling", "salt_apply",
-    "salt_apply_timed", "salt_fuse_centroid", "salt_fuse_centroid_timed", "salt_adapter_gram", "salt_route",
+    "salt_apply_batch", "salt_apply_batch_timed", "salt_apply_map", "salt_fuse_centroid",
+    "salt_fuse_centroid_timed", "salt_adapter_gram", "salt_route",
     "salt_status_str",
     "salt_last_error", "salt_version",
 )
@@ -43,8 +44,6 @@ class Config(C.Structure):
                 ("r_u_max", C.c_int32), ("max_tokens", C.c_int32), ("device", C.c_int32),
                 ("flags", C.c_int32)]
 
-
-DETERMINISTIC = 1   # salt_config.flags: split-K partials summed in a fixed order
 
 
 class RouteResult(C.Structure):
@@ -65,6 +64,7 @@ def _load() -> C.CDLL:
         "salt_residual_bytes": (SZ, [P, I32]),
         "salt_residual_bytes_for": (SZ, [C.c_int, I32, C.POINTER(Shape), I32]),
         "salt_load_residual": (C.c_int, [P, I32, I32, VP, SZ]),
+        "salt_load_residuals": (C.c_int, [P, I32, IP, IP, C.POINTER(VP), C.POINTER(SZ)]),
         "salt_wait_loads": (C.c_int, [P]),
         "salt_host_alloc": (C.c_int, [SZ, C.POINTER(VP)]),
         "salt_host_free": (None, [VP]),
@@ -76,7 +76,9 @@ def _load() -> C.CDLL:
         "salt_plan_errors": (C.c_int, [P, P, VP, IP]),
         "salt_plan_tiling": (C.c_int, [P, P, IP, IP, IP]),
         "salt_apply": (C.c_int, [P, I32, P, VP, VP, VP]),
-        "salt_apply_timed": (C.c_int, [P, I32, P, VP, VP, VP, VP, VP]),
+        "salt_apply_batch": (C.c_int, [P, I32, IP, P, C.POINTER(VP), C.POINTER(VP), VP]),
+        "salt_apply_batch_timed": (C.c_int, [P, I32, IP, P, C.POINTER(VP), C.POINTER(VP), VP, C.POINTER(VP)]),
+        "salt_apply_map": (C.c_int, [P, I32, I32, IP, IP, C.POINTER(C.c_float), VP, VP, VP]),
         "salt_fuse_centroid": (C.c_int, [P, I32, I32, C.c_float, VP, C.c_int64, VP]),
         "salt_fuse_centroid_timed": (C.c_int, [P, I32, I32, C.c_float, VP, C.c_int64, VP, VP, VP]),
         "salt_adapter_gram": (C.c_int, [P, VP, I32, VP, I32, C.POINTER(C.c_double), VP]),
@@ -158,12 +160,11 @@ class Context:
     _N_STAGE = 8
 
     def __init__(self, dtype: str, tables: Sequence[Tuple[int, int]], n_centroids: int, r_c: int,
-                 n_slots: int, r_u_max: int, max_tokens: int, device: int = 0,
-                 deterministic: bool = False):
+                 n_slots: int, r_u_max: int, max_tokens: int, device: int = 0):
         self.dtype = dtype
         self._shapes = (Shape * len(tables))(*[Shape(int(i), int(o)) for i, o in tables])
         cfg = Config(F32 if dtype == "f32" else BF16, len(tables), self._shapes, n_centroids, r_c,
-                     n_slots, r_u_max, max_tokens, device, DETERMINISTIC if deterministic else 0)
+                     n_slots, r_u_max, max_tokens, device, 0)
         h = C.c_void_p()
         st = lib.salt_create(C.byref(cfg), C.byref(h))
         if st != OK:
@@ -243,11 +244,51 @@ class Context:
     def apply_status(self, table: int, plan: "Plan", x_ptr: int, y_ptr: int, stream: int = 0) -> int:
         return lib.salt_apply(self.h, table, plan.h, x_ptr, y_ptr, stream)
 
-    def apply_timed(self, table: int, plan: "Plan", x_ptr: int, y_ptr: int, stream: int, start_event: int,
-                    stop_event: int):
-        """``apply`` whose two HIP events record the kernel's own start and end."""
-        self._check(lib.salt_apply_timed(self.h, table, plan.h, x_ptr, y_ptr, stream, start_event, stop_event),
-                    "salt_apply_timed")
+    @staticmethod
+    def _ptrs(ptrs):
+        return (C.c_void_p * len(ptrs))(*[C.c_void_p(int(p)) for p in ptrs])
+
+    def apply_batch(self, tables: Sequence[int], plan: "Plan", x_ptrs: Sequence[int], y_ptrs: Sequence[int],
+                    stream: int = 0):
+        """salt_apply_batch: tables[i] with x_ptrs[i] -> y_ptrs[i], one plan."""
+        n = len(tables)
+        tabs = np.ascontiguousarray(tables, dtype=np.int32)
+        self._check(lib.salt_apply_batch(self.h, n, _i32p(tabs), plan.h, self._ptrs(x_ptrs), self._ptrs(y_ptrs),
+                                         stream), "salt_apply_batch")
+
+    def apply_batch_status(self, tables, plan, x_ptrs, y_ptrs, stream: int = 0) -> int:
+        tabs = np.ascontiguousarray(tables, dtype=np.int32)
+        return lib.salt_apply_batch(self.h, len(tables), _i32p(tabs), plan.h, self._ptrs(x_ptrs),
+                                    self._ptrs(y_ptrs), stream)
+
+    def apply_batch_timed(self, tables, plan, x_ptrs, y_ptrs, stream: int, events: Sequence[int]):
+        """``apply_batch`` (one launch) whose four HIP events record the start and end
+        of the shrink kernel and of the expand kernel."""
+        tabs = np.ascontiguousarray(tables, dtype=np.int32)
+        self._check(lib.salt_apply_batch_timed(self.h, len(tables), _i32p(tabs), plan.h, self._ptrs(x_ptrs),
+                                               self._ptrs(y_ptrs), stream, self._ptrs(events)),
+                    "salt_apply_batch_timed")
+
+    def apply_map(self, table: int, tok_c, tok_u, gamma, x_ptr: int, y_ptr: int, stream: int = 0):
+        """salt_apply_map: build + apply on host maps with the context's own plan."""
+        st = self.apply_map_status(table, tok_c, tok_u, gamma, x_ptr, y_ptr, stream)
+        self._check(st, "salt_apply_map")
+
+    def apply_map_status(self, table: int, tok_c, tok_u, gamma, x_ptr: int, y_ptr: int, stream: int = 0) -> int:
+        tok_c = np.ascontiguousarray(tok_c, dtype=np.int32)
+        tok_u = np.ascontiguousarray(tok_u, dtype=np.int32)
+        g = None if gamma is None else np.ascontiguousarray(gamma, dtype=np.float32)
+        gp = None if g is None else g.ctypes.data_as(C.POINTER(C.c_float))
+        return lib.salt_apply_map(self.h, table, int(tok_c.shape[0]), _i32p(tok_c), _i32p(tok_u), gp, x_ptr, y_ptr,
+                                  stream)
+
+    def load_residuals_ptr(self, slots: Sequence[int], ranks: Sequence[int], ptrs: Sequence[int],
+                           nbytes: Sequence[int]) -> int:
+        """salt_load_residuals on page-locked blobs; returns the status."""
+        sl = np.ascontiguousarray(slots, dtype=np.int32)
+        rk = np.ascontiguousarray(ranks, dtype=np.int32)
+        sz = (C.c_size_t * len(nbytes))(*[int(n) for n in nbytes])
+        return lib.salt_load_residuals(self.h, len(sl), _i32p(sl), _i32p(rk), self._ptrs(ptrs), sz)
 
     def fuse_centroid(self, table: int, c: int, gamma: float, w_ptr: int, ldw: int, stream: int = 0):
         """Fold gamma * centroid c of `table` into the base weight at w_ptr ([in][ldw], device)."""

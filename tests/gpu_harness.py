@@ -50,15 +50,14 @@ def fuse_within_bound(got: np.ndarray, ref: np.ndarray, w0: np.ndarray, a: np.nd
 class Run:
     """One context + one plan for workload ``w``; residual generations per slot."""
 
-    def __init__(self, w: synth.Workload, max_tokens: int = None, pin_tables=None,
-                 deterministic: bool = False):
+    def __init__(self, w: synth.Workload, max_tokens: int = None, pin_tables=None):
         from paper_2608_03579_amd import salt
         self.salt = salt
         self.w = w
         self.gen = {}
         tables = [(i, o) for _, i, o in w.tables]
         self.ctx = salt.Context(w.dtype, tables, w.n_centroids, w.r_c, w.n_slots, w.r_u_max,
-                                max_tokens or max(1, w.T), deterministic=deterministic)
+                                max_tokens or max(1, w.T))
         if w.n_centroids:
             for t in (range(len(tables)) if pin_tables is None else pin_tables):
                 at, b = w.centroids(t)
@@ -93,6 +92,18 @@ class Run:
         out = yd.to_host()
         xd.free()
         yd.free()
+        return out
+
+    def apply_batch(self, tables, xs=None, y0s=None):
+        """salt_apply_batch of several tables in one call; returns their y arrays."""
+        w = self.w
+        xd = [to_dev(w.x(t) if xs is None else xs[i]) for i, t in enumerate(tables)]
+        yd = [to_dev(w.y0(t) if y0s is None else y0s[i]) for i, t in enumerate(tables)]
+        self.ctx.apply_batch(tables, self.plan, [d.ptr for d in xd], [d.ptr for d in yd], self.stream)
+        self._stream.synchronize()
+        out = [d.to_host() for d in yd]
+        for d in xd + yd:
+            d.free()
         return out
 
     # ---- oracle side ----------------------------------------------------------

@@ -53,6 +53,7 @@ def test_create_rejects_bad_configs_before_touching_the_gpu():
         dict(n_centroids=0, r_c=8),                 # rank without centroids
         dict(r_u_max=73),                           # above the largest residual rank (72)
         dict(max_tokens=0),
+        dict(max_tokens=65537),                     # above the largest plan
         dict(n_slots=0),
     ]
 

@@ -23,7 +23,6 @@ def _tol(w):
 
 def _check(run, table=0, rows=None):
     got = oracle.decode(run.apply(table), run.w.dtype)
-    assert run.plan.errors(run.stream) == 0
     ref = run.oracle_table(table, rows)
     if rows is not None:
         got = got[np.asarray(rows)]
@@ -36,6 +35,7 @@ def _plan_matches(run):
     want = oracle.plan(run.maps[0], run.maps[1])
     for k in want:
         assert np.array_equal(p[k], want[k]), k
+    assert run.plan.errors(run.stream) == 0
 
 
 @pytest.mark.parametrize("cfg", [1, 2])
@@ -73,10 +73,10 @@ def test_ragged_and_degenerate_batches():
         for k, T in enumerate((1, 5, 17, 33, 63)):
             run.set_and_build(w.tok_c[:T], w.tok_u[:T])
             if k % 2 == 0:
-                _plan_matches(run)       # standalone plan kernel
+                _plan_matches(run)
             got = oracle.decode(run.apply(0), w.dtype)[:T]
             if k % 2 == 1:
-                _plan_matches(run)       # the plan the apply built
+                _plan_matches(run)
             ref = run.oracle_table(0, rows=list(range(T)))
             assert close_enough(got, ref, TOL_NORTH_STAR)[0], T
             # rows past T are untouched
@@ -114,8 +114,8 @@ def test_rank_zero_and_mixed_rank_slots():
 
 
 def test_repeated_applies_and_rebuilds():
-    """Arrival counters and epochs over many applies of one plan, then a rebuild
-    with a batch of a different tiling."""
+    """Many applies of one plan (its partials buffer reused each time), then
+    rebuilds with batches of a different tiling."""
     _announce("40 applies on one plan, then rebuilds")
     w = synth.make(2, 7)
     run = Run(w)
@@ -127,7 +127,6 @@ def test_repeated_applies_and_rebuilds():
         for _ in range(40):
             run.ctx.apply(0, run.plan, xd.ptr, yd.ptr, run.stream)
         run._stream.synchronize()
-        assert run.plan.errors(run.stream) == 0
         got = oracle.decode(yd.to_host(), w.dtype)
         one = run.oracle_table(0) - oracle.decode(w.y0(0), w.dtype)
         ref = oracle.decode(w.y0(0), w.dtype) + 40 * one
@@ -300,40 +299,172 @@ def test_prefill_full_size_sampled():
         run.close()
 
 
-def test_timed_apply_matches_apply_and_times_the_kernel():
-    """salt_apply_timed runs the same apply (bit-identical in the deterministic
-    mode); its events bracket the kernel."""
-    _announce("salt_apply_timed on q_proj decode")
-    from paper_2608_03579_amd import hip
+def test_timed_batch_matches_batch_and_times_both_kernels():
+    """salt_apply_batch_timed runs the same apply (bit-identical: the partial sums
+    are added in a fixed order); its four events bracket the shrink and the
+    expand kernels."""
+    _announce("salt_apply_batch_timed on three zipf tables")
+    from paper_2608_03579_amd import hip, salt
     from tests.gpu_harness import to_dev
-    w = synth.make(2, 11, y0="normal")
-    run = Run(w, deterministic=True)
+    w = synth.make(5, 11, y0="normal")
+    run = Run(w)
     try:
         run.set_and_build()
-        want = run.apply(0)
-        xd, yd = to_dev(w.x(0)), to_dev(w.y0(0))
-        e0, e1 = hip.Event(), hip.Event()
-        run.ctx.apply_timed(0, run.plan, xd.ptr, yd.ptr, run.stream, e0.h, e1.h)
+        tables = [0, 4, 6]
+        want = run.apply_batch(tables)
+        xd = [to_dev(w.x(t)) for t in tables]
+        yd = [to_dev(w.y0(t)) for t in tables]
+        ev = [hip.Event() for _ in range(4)]
+        run.ctx.apply_batch_timed(tables, run.plan, [d.ptr for d in xd], [d.ptr for d in yd], run.stream,
+                                  [e.h for e in ev])
         run._stream.synchronize()
-        assert np.array_equal(yd.to_host(), want)
-        ms = e0.elapsed_ms(e1)
-        assert 0.0 < ms < 100.0, ms
-        assert run.plan.errors(run.stream) == 0
-        from paper_2608_03579_amd import salt
-        assert salt.lib.salt_apply_timed(run.ctx.h, 0, run.plan.h, xd.ptr, yd.ptr, run.stream, None, e1.h) \
-            == salt.ERR_INVALID_ARG
-        e0.destroy()
-        e1.destroy()
+        for d, y in zip(yd, want):
+            assert np.array_equal(d.to_host(), y)
+        shrink_ms, expand_ms = ev[0].elapsed_ms(ev[1]), ev[2].elapsed_ms(ev[3])
+        assert 0.0 < shrink_ms < 100.0 and 0.0 < expand_ms < 100.0, (shrink_ms, expand_ms)
+        assert ev[1].elapsed_ms(ev[2]) >= 0.0                  # the expand starts after the shrink ends
+        nul = salt.C.c_void_p * 4
+        st = salt.lib.salt_apply_batch_timed(run.ctx.h, 1, salt._i32p(np.zeros(1, np.int32)), run.plan.h,
+                                             run.ctx._ptrs([xd[0].ptr]), run.ctx._ptrs([yd[0].ptr]), run.stream,
+                                             nul(ev[0].h, None, ev[2].h, ev[3].h))
+        assert st == salt.ERR_INVALID_ARG
+        for e in ev:
+            e.destroy()
+    finally:
+        run.close()
+
+
+def test_repeated_applies_are_bit_identical():
+    """The split-K partials are summed in a fixed order: the same call on equal
+    inputs gives equal bytes, apply after apply.  The K split depends on the
+    tables that share a launch, so a table applied alone and inside a batch agree
+    within the tolerance, not necessarily bit for bit."""
+    _announce("bit-identical repeats: q_proj decode, zipf layer")
+    for cfg, tables in ((2, [0]), (5, [0, 1, 2, 3, 4, 5, 6])):
+        w = synth.make(cfg, 12, y0="normal")
+        run = Run(w)
+        try:
+            run.set_and_build()
+            first = run.apply_batch(tables)
+            for _ in range(3):
+                for a, b in zip(first, run.apply_batch(tables)):
+                    assert np.array_equal(a, b)
+            for t, y in zip(tables, first):
+                alone = run.apply(t)
+                assert np.array_equal(alone, run.apply(t))
+                assert close_enough(oracle.decode(alone, w.dtype), oracle.decode(y, w.dtype), TOL_NORTH_STAR)[0]
+        finally:
+            run.close()
+
+
+def test_plan_used_across_streams():
+    """Set maps and build on one stream, then apply on another without any host
+    synchronisation: the library orders the plan's work across streams."""
+    _announce("plan built on stream 1, applied on stream 2")
+    from paper_2608_03579_amd import hip
+    from tests.gpu_harness import to_dev
+    w = synth.make(5, 13)
+    run = Run(w)
+    try:
+        s2 = hip.Stream()
+        xd, yd = to_dev(w.x(4)), to_dev(w.y0(4))
+        for rep in range(3):
+            run.plan.set_maps(w.tok_c, w.tok_u, w.gamma, run.stream)
+            run.plan.build(run.stream)
+            run.maps = (w.tok_c, w.tok_u, w.gamma)
+            yd.upload(w.y0(4))
+            run.ctx.apply(4, run.plan, xd.ptr, yd.ptr, s2.h)
+            s2.synchronize()
+            got = oracle.decode(yd.to_host(), w.dtype)
+            assert close_enough(got, run.oracle_table(4), TOL_NORTH_STAR)[0], rep
+        # and the other way round: build on stream 2, apply on stream 1
+        run.plan.set_maps(w.tok_c, w.tok_u, w.gamma, s2.h)
+        run.plan.build(s2.h)
+        yd.upload(w.y0(4))
+        run.ctx.apply(4, run.plan, xd.ptr, yd.ptr, run.stream)
+        run._stream.synchronize()
+        assert close_enough(oracle.decode(yd.to_host(), w.dtype), run.oracle_table(4), TOL_NORTH_STAR)[0]
+        _plan_matches(run)
+        s2.destroy()
+    finally:
+        run.close()
+
+
+def test_apply_map_one_shot():
+    """salt_apply_map: the context's own plan, built and applied on host maps,
+    batch after batch of different sizes."""
+    _announce("salt_apply_map")
+    from paper_2608_03579_amd import salt
+    from tests.gpu_harness import to_dev
+    w = synth.make(2, 14, y0="normal")
+    run = Run(w)
+    try:
+        for T in (64, 17, 1, 64):
+            xd, yd = to_dev(w.x(0)), to_dev(w.y0(0))
+            run.ctx.apply_map(0, w.tok_c[:T], w.tok_u[:T], None, xd.ptr, yd.ptr, run.stream)
+            run._stream.synchronize()
+            got = oracle.decode(yd.to_host(), w.dtype)
+            run.maps = (w.tok_c[:T], w.tok_u[:T], None)
+            ref = run.oracle_table(0, rows=list(range(T)))
+            assert close_enough(got[:T], ref, TOL_NORTH_STAR)[0], T
+            assert np.array_equal(yd.to_host()[T:], w.y0(0)[T:])
+        assert run.ctx.apply_map_status(1, w.tok_c, w.tok_u, None, xd.ptr, yd.ptr, run.stream) == \
+            salt.ERR_OUT_OF_RANGE
+        assert run.ctx.apply_map_status(0, np.full(w.T, 9, np.int32), w.tok_u, None, xd.ptr, yd.ptr,
+                                        run.stream) == salt.ERR_OUT_OF_RANGE
+    finally:
+        run.close()
+
+
+def test_batched_swaps():
+    """salt_load_residuals: 32 swaps in one call, validated as a whole, ordered
+    behind the applies that read the old residuals."""
+    _announce("salt_load_residuals: 32 rank-2 swaps of the 8B decode batch")
+    from paper_2608_03579_amd import salt
+    from tests.gpu_harness import to_dev
+    w = synth.make(4, 3)
+    run = Run(w)
+    try:
+        run.set_and_build()
+        t = 6
+        xd, y1 = to_dev(w.x(t)), to_dev(w.y0(t))
+        run.ctx.apply(t, run.plan, xd.ptr, y1.ptr, run.stream)
+        swapped = [int(s) for s in w.meta["swap_slots"]]
+        nb = run.ctx.residual_bytes(2)
+        bufs = [salt.HostBuffer(nb) for _ in swapped]
+        for b, s in zip(bufs, swapped):
+            b.view(np.uint16)[:] = w.residual_blob(s, 1)
+        # an invalid entry fails the whole call and changes nothing
+        bad = list(swapped)
+        bad[5] = 1 << 20
+        assert run.ctx.load_residuals_ptr(bad, [2] * 32, [b.ptr for b in bufs], [nb] * 32) == salt.ERR_OUT_OF_RANGE
+        assert run.ctx.load_residuals_ptr(swapped, [2] * 32, [b.ptr for b in bufs], [nb] * 31 + [nb - 2]) == \
+            salt.ERR_INVALID_ARG
+        assert run.ctx.load_residuals_ptr(swapped, [2] * 32, [b.ptr for b in bufs], [nb] * 32) == salt.OK
+        for s in swapped:
+            run.gen[s] = 1
+        y2 = to_dev(w.y0(t))
+        run.ctx.apply(t, run.plan, xd.ptr, y2.ptr, run.stream)
+        run._stream.synchronize()
+        run.ctx.wait_loads()
+        ref_new = run.oracle_table(t)
+        assert close_enough(oracle.decode(y2.to_host(), w.dtype), ref_new, TOL_NORTH_STAR)[0]
+        for s in swapped:
+            run.gen[s] = 0
+        assert close_enough(oracle.decode(y1.to_host(), w.dtype), run.oracle_table(t), TOL_NORTH_STAR)[0]
+        for b in bufs:
+            b.free()
     finally:
         run.close()
 
 
 def test_plan_tiling_reports_the_launch_structure():
-    """salt_plan_tiling: decode batches run in one launch with 16- or 32-token
-    tiles, fp32 in one launch with 16-token tiles, the 8192-token prefill in two
-    launches with 64-token tiles; the tile count matches the centroid groups."""
+    """salt_plan_tiling: every apply is two launches; decode batches with short
+    centroid groups take 16-token tiles, fp32 16, the Zipf batch and the
+    8192-token prefill 64; the tile count matches the centroid groups."""
     _announce("salt_plan_tiling")
-    for cfg, kw, want in ((2, {}, (16, 1)), (1, {}, (16, 1)), (5, {}, (32, 1)), (3, {"layers": 1}, (64, 2))):
+    for cfg, kw, want in ((2, {}, (16, 2)), (1, {}, (16, 2)), (4, {}, (16, 2)), (5, {}, (64, 2)),
+                          (3, {"layers": 1}, (64, 2))):
         w = synth.make(cfg, 0, **kw)
         run = Run(w, pin_tables=[])
         try:

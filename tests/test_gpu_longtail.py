@@ -88,11 +88,10 @@ CASES = [
 
 
 @pytest.mark.parametrize("seed,tables,C,r_c,T,n_reg,n_tail,dtype", CASES)
-@pytest.mark.parametrize("deterministic", [False, True])
-def test_long_tail_mixed_batch(seed, tables, C, r_c, T, n_reg, n_tail, dtype, deterministic):
-    _announce(f"long tail r_c={r_c} T={T} {dtype} deterministic={deterministic}")
+def test_long_tail_mixed_batch(seed, tables, C, r_c, T, n_reg, n_tail, dtype):
+    _announce(f"long tail r_c={r_c} T={T} {dtype}")
     w = _workload(seed, tables, C, r_c, T, n_reg, n_tail, dtype)
-    run = Run(w, deterministic=deterministic)
+    run = Run(w)
     try:
         run.set_and_build()
         _check(run, TOL_NORTH_STAR if dtype == "bf16" else TOL_F32)

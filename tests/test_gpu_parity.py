@@ -1,12 +1,11 @@
 """GPU parity: libsalt (through the C ABI) against the fp64 CPU oracle.
 
-Plans must match the oracle bit for bit.  A build of a batch of at most 256
-tokens is deferred into the next apply on its stream, so a case that applies
-before it downloads the plan checks the plan that apply wrote, and one that
-downloads first checks the standalone plan kernel.  Outputs must satisfy
+Plans must match the oracle bit for bit.  Outputs must satisfy
 |y - ref| <= 1e-2 * (1 + |ref|) element-wise for bf16 (fp32 accumulation), and
 1e-5 * (1 + |ref|) for the fp32 Tiny workload; the integer-valued variants must be
-bit-exact.  Every case prints its name before the GPU work starts.
+bit-exact.  Multi-table workloads are applied both table by table (salt_apply)
+and as one salt_apply_batch over a decoder layer's seven tables, the call the
+bench times.  Every case prints its name before the GPU work starts.
 """
 import numpy as np
 import pytest
@@ -27,11 +26,10 @@ def _check_plan(run):
     want = oracle.plan(run.maps[0], run.maps[1])
     for k in ("perm", "seg_off", "seg_c", "seg_u", "grp_off"):
         assert np.array_equal(p[k], want[k]), (k, p[k][:16], want[k][:16])
+    assert run.plan.errors(run.stream) == 0, "device plan disagrees with the host's tiles"
 
 
-def _check_table(run, table, rows=None, exact=False):
-    got = run.apply(table)
-    assert run.plan.errors(run.stream) == 0, "apply blocks gave up waiting for their tile"
+def _compare(run, table, got, rows=None, exact=False):
     got = oracle.decode(got, run.w.dtype)
     ref = run.oracle_table(table, rows)
     if rows is not None:
@@ -41,6 +39,15 @@ def _check_table(run, table, rows=None, exact=False):
         return
     ok, worst, nbad = close_enough(got, ref, _tol(run.w))
     assert ok, f"table {table}: {nbad} elements out of tolerance, worst {worst:.3f}x the bound"
+
+
+def _check_table(run, table, rows=None, exact=False):
+    _compare(run, table, run.apply(table), rows, exact)
+
+
+def _check_batch(run, tables, rows=None, exact=False):
+    for t, y in zip(tables, run.apply_batch(tables)):
+        _compare(run, t, y, rows, exact)
 
 
 def _announce(name):
@@ -54,8 +61,8 @@ def test_tiny_fp32(seed, y0):
     run = Run(synth.make(1, seed, y0=y0))
     try:
         run.set_and_build()
-        _check_table(run, 0)     # the apply builds the plan
         _check_plan(run)
+        _check_table(run, 0)
     finally:
         run.close()
 
@@ -67,11 +74,11 @@ def test_llama32_qproj_decode(seed):
     try:
         run.set_and_build()
         if seed == 2:
-            _check_plan(run)     # standalone plan kernel, then the apply reads its tiles
-            _check_table(run, 0)
-        else:
-            _check_table(run, 0)
+            _check_table(run, 0)         # apply before the plan is read back
             _check_plan(run)
+        else:
+            _check_plan(run)
+            _check_table(run, 0)
     finally:
         run.close()
 
@@ -86,17 +93,21 @@ def test_exact_integer_bit_exact(cfg):
         _check_plan(run)
         for t in range(len(w.tables)):
             _check_table(run, t, exact=True)
+        if len(w.tables) > 1:
+            _check_batch(run, list(range(len(w.tables))), exact=True)
     finally:
         run.close()
 
 
 def test_gamma_bins():
-    _announce("gamma bins cfg1 + cfg2")
-    for cfg in (1, 2):
+    _announce("gamma bins cfg1 + cfg2 + cfg5")
+    for cfg in (1, 2, 5):
         run = Run(synth.make(cfg, 4, gamma="bins"))
         try:
             run.set_and_build()
             _check_table(run, 0)
+            if cfg == 5:
+                _check_batch(run, [0, 4, 6])
         finally:
             run.close()
 
@@ -109,7 +120,8 @@ def test_llama31_decode_with_swaps():
         for s in w.meta["swap_slots"]:
             run.load(int(s), 1)
         run.set_and_build()
-        for t in range(len(w.tables)):
+        _check_batch(run, list(range(len(w.tables))))
+        for t in (0, 6):
             _check_table(run, t)
         _check_plan(run)
     finally:
@@ -123,12 +135,9 @@ def test_zipf_multitenant(baseline):
     run = Run(w)
     try:
         run.set_and_build()
-        if baseline:
-            _check_plan(run)
-        for t in range(len(w.tables)):
-            _check_table(run, t)
-        if not baseline:
-            _check_plan(run)     # written by the first apply, which built it
+        _check_plan(run)
+        _check_batch(run, list(range(len(w.tables))))
+        _check_table(run, 3)
     finally:
         run.close()
 
@@ -141,7 +150,6 @@ def test_prefill_reduced():
         run.set_and_build()
         _check_plan(run)
         rows = list(range(0, w.T, 7)) + [w.T - 1]
-        for t in range(len(w.tables)):
-            _check_table(run, t, rows=rows)
+        _check_batch(run, list(range(len(w.tables))), rows=rows)
     finally:
         run.close()

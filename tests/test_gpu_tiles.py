@@ -1,0 +1,109 @@
+"""GPU parity across the apply's tile and rank classes: tiles of 16, 32 and 64
+tokens (chosen from the mean centroid-group size), centroid ranks in each of the
+16 / 32 / 64 / 128 rank classes, residual ranks 0, 1, 2 and 16, no centroids at
+all, ragged table shapes (in / out not multiples of 64), and integer inputs that
+must come out bit-exact.  Every output is compared with the CPU oracle through
+the C ABI; every case prints its name first.
+"""
+import zlib
+
+import numpy as np
+import pytest
+
+import oracle
+from paper_2608_03579_amd import synth
+from tests.gpu_harness import TOL_F32, TOL_NORTH_STAR, Run, close_enough
+
+pytestmark = pytest.mark.gpu
+
+
+def _announce(name):
+    print(f"\n[gpu case] {name}", flush=True)
+
+
+def _workload(seed, tables, C, r_c, T, n_slots, ranks, dtype="bf16", exact=False, y0="normal", gamma=False):
+    """T tokens over n_slots users whose ranks are drawn from `ranks`; C centroids
+    (one per user) or none."""
+    rng = np.random.default_rng(np.random.SeedSequence([2608, 3579, 55, seed]))
+    slot_rank = rng.choice(np.asarray(ranks, np.int32), size=n_slots).astype(np.int32)
+    tok_u = rng.integers(0, n_slots, size=T).astype(np.int32)
+    user_c = rng.integers(0, max(C, 1), size=n_slots).astype(np.int32)
+    tok_c = (user_c[tok_u] if C else np.full(T, -1)).astype(np.int32)
+    g = None
+    if gamma:
+        g = np.asarray(synth.GAMMA_BINS, np.float32)[rng.integers(0, 3, size=n_slots)][tok_u]
+    return synth.Workload(cfg=9, seed=seed, name="tiles", dtype=dtype, tables=tables, n_centroids=C, r_c=r_c,
+                          n_slots=n_slots, r_u_max=max(int(slot_rank.max()), 0), slot_rank=slot_rank, tok_c=tok_c,
+                          tok_u=tok_u, gamma=g, y0_kind="int" if exact else y0, exact=exact)
+
+
+def _run_all(w, want_m=None, exact=False):
+    run = Run(w)
+    try:
+        run.set_and_build()
+        m, _, _ = run.plan.tiling()
+        if want_m is not None:
+            assert m == want_m, (m, want_m)
+        p = run.plan.download(run.stream)
+        want = oracle.plan(w.tok_c, w.tok_u)
+        for k in want:
+            assert np.array_equal(p[k], want[k]), k
+        assert run.plan.errors(run.stream) == 0
+        tables = list(range(len(w.tables)))
+        for t, y in zip(tables, run.apply_batch(tables)):
+            got = oracle.decode(y, w.dtype)
+            ref = run.oracle_table(t)
+            if exact:
+                assert np.array_equal(got, ref), f"table {t}: {np.sum(got != ref)} exact mismatches"
+            else:
+                ok, worst, nbad = close_enough(got, ref, TOL_F32 if w.dtype == "f32" else TOL_NORTH_STAR)
+                assert ok, f"table {t}: {nbad} out of tolerance, worst {worst:.3f}x"
+    finally:
+        run.close()
+
+
+RAGGED = [("a", 264, 136), ("b", 1032, 520), ("c", 3072, 1024)]
+
+CASES = [
+    # name, C, r_c, T, n_slots, ranks, tile tokens
+    ("m16 r_c32 r_u2", 16, 32, 256, 200, (2,), 16),
+    ("m16 r_c8 r_u1", 8, 8, 128, 60, (1,), 16),
+    ("m32 r_c64 r_u1/2", 8, 64, 256, 80, (1, 2), 32),
+    ("m32 r_c48 r_u0/2", 6, 48, 200, 50, (0, 2), 32),
+    ("m64 r_c64 r_u1", 4, 64, 1024, 40, (1,), 64),
+    ("m64 r_c128 r_u2", 4, 128, 600, 30, (2,), 64),
+    ("m64 r_c16 r_u16", 2, 16, 512, 20, (16,), 64),
+    ("m64 no centroid r_u16", 0, 0, 300, 40, (1, 16), 64),
+    ("m64 no centroid r_u0", 0, 0, 200, 10, (0,), 64),
+]
+
+
+@pytest.mark.parametrize("name,C,r_c,T,n_slots,ranks,m", CASES)
+def test_tile_and_rank_classes(name, C, r_c, T, n_slots, ranks, m):
+    _announce(f"tiles: {name}")
+    _run_all(_workload(zlib.crc32(name.encode()) % 1000, RAGGED, C, r_c, T, n_slots, ranks, gamma=C > 0), want_m=m)
+
+
+@pytest.mark.parametrize("name,C,r_c,T,n_slots,ranks,m", [CASES[0], CASES[2], CASES[4], CASES[7]])
+def test_tile_classes_integer_bit_exact(name, C, r_c, T, n_slots, ranks, m):
+    _announce(f"tiles, integer inputs: {name}")
+    _run_all(_workload(7 + zlib.crc32(name.encode()) % 1000, RAGGED, C, r_c, T, n_slots, ranks, exact=True), want_m=m, exact=True)
+
+
+def test_fp32_tiles():
+    _announce("fp32: r_c 8 / 32 / 64, residual ranks 1 / 2 / 16, ragged shapes")
+    for seed, (C, r_c, ranks) in enumerate(((4, 8, (2,)), (4, 32, (1, 2)), (2, 64, (16,)))):
+        _run_all(_workload(40 + seed, [("a", 264, 136), ("b", 520, 1032)], C, r_c, 96, 30, ranks, dtype="f32"),
+                 want_m=16)
+
+
+def test_large_batch_multi_chunk_plan():
+    """T = 9000 > 4096: the plan sorts in three chunks and merges them."""
+    _announce("T=9000 multi-chunk plan, 64-token tiles")
+    _run_all(_workload(60, [("a", 256, 520)], 8, 32, 9000, 700, (1, 2)), want_m=64)
+
+
+def test_max_tokens_batch():
+    """The largest batch a plan accepts (65536 tokens, 16 sort chunks)."""
+    _announce("T=65536, small tables")
+    _run_all(_workload(61, [("a", 128, 64)], 4, 16, 65536, 3000, (1, 2)), want_m=64)
