@@ -1,31 +1,33 @@
 #!/usr/bin/env python3
 """Throughput of the batched centroid + residual LoRA apply on one MI355X.
 
-    python bench.py [--steps K] [--warmup W] [--workload qproj|prefill|decode8b|zipf]
+    python bench.py [--steps K] [--warmup W] [--workload prefill|qproj|decode8b|zipf|zipf-baseline|...]
 
 Prints ONE JSON line.  A step is one pass of the hot path over one batch: the
-device plan build (grouping by centroid) followed by ``salt_apply`` on every
-table of the workload.  Inputs (x, y, maps, pinned centroids, resident
+device plan build (grouping by centroid) followed by the apply of every table of
+the workload, a decoder layer's seven tables per salt_apply_batch (one shrink and
+one expand launch per layer).  Inputs (x, y, maps, pinned centroids, resident
 residuals) are in HBM before the timed region starts.
 
-Default workload: Llama-3.2-3B q_proj (3072 -> 3072), bf16 decode batch of 64
-tokens, 4 centroids r=32, 64 residual slots r=2 (one token per user).  One such
-apply moves about 4.3 MB, which fits in the 256 MB Infinity Cache, so the bench
-rotates over ``--rot`` copies of every buffer (tables, slot pool, x, y, plans):
-consecutive steps touch disjoint memory, as consecutive projections of a real
-decode step would, and bytes come from HBM.
+Default workload (the metric's configuration): Llama-3.2-3B, all seven
+projections of its 28 layers (196 tables), bf16 prefill of 8192 tokens in 256
+user segments, 8 centroids of rank 64, residuals of rank 1.  The default run also
+reports, as sub-records, the q_proj decode batch (T = 64), the Llama-3.1-8B
+decode layer (T = 256, with 32 residual swaps per step overlapped with the
+apply) and the Zipf multi-tenant layer (T = 512) against its rank-16 LoRA
+baseline.
 
-Timing: HIP events on the stream the kernels run on, around the K timed steps;
-then, for the roofline, events around a second timed region of back-to-back
-applies (plans already built) give the apply kernel's average duration.
+Timing: HIP events on the stream the kernels run on, around the K timed steps.
+For the roofline, salt_apply_batch_timed's events record each shrink and expand
+kernel's own start and end; the dominant kernel is the one with the larger mean
+duration, its achieved bandwidth = its algorithmic bytes / that duration.
 ``cpu_baseline`` times the fp64 oracle on a bounded sample of the same workload
-on this host.  Other workloads (--workload): the 28-layer Llama-3.2-3B prefill
-(T = 8192), the Llama-3.1-8B decode (T = 256) and the Zipf multi-tenant batch
-(T = 512) with its rank-16 LoRA baseline.
+on this host, BLAS on one thread and on all cores.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -34,34 +36,62 @@ import time
 import numpy as np
 
 HBM_PEAK_GBPS = 8000.0   # MI355X HBM3E
+METRIC = "Centroid+residual LoRA apply: tokens/s and achieved HBM GB/s, Llama-3.2-3B"
 
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
+
+# sources that fix the apply kernels' machine code and launch shapes: counter
+# summaries under profiles/ hold for these contents only
+KERNEL_SOURCES = ("salt_apply.hip", "salt_device.h", "salt_layout.h", "salt_launch.h", "salt_internal.h")
 
 
 def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def apply_bytes(w, plan_maps, table):
-    """Algorithmic HBM bytes of one apply: x once, y read + write once, each
-    referenced centroid's A and B once, each referenced residual at its own rank
-    once, and the per-token plan records (16 B each)."""
-    tok_c, tok_u = plan_maps
-    _, n_in, n_out = w.tables[table]
-    es = w.esize
-    T = len(tok_c)
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for n in KERNEL_SOURCES:
+        h.update(open(os.path.join(ROOT, "paper_2608_03579_amd", "csrc", n), "rb").read())
+    return h.hexdigest()[:16]
+
+
+# ---------------------------------------------------------------------------
+# algorithmic bytes
+# ---------------------------------------------------------------------------
+def _adapter_rows(w, maps):
+    """Rank rows of adapters one table's apply reads: each referenced centroid
+    at r_c, each referenced residual slot at its own rank."""
+    tok_c, tok_u = maps
     cents = np.unique(tok_c[tok_c >= 0])
     slots = np.unique(tok_u[tok_u >= 0])
-    b = T * n_in * es + 2 * T * n_out * es
-    b += len(cents) * w.r_c * (n_in + n_out) * es
-    b += int(sum(int(w.slot_rank[s]) for s in slots)) * (n_in + n_out) * es
-    b += T * 16
-    return b
+    return len(cents) * w.r_c + int(sum(int(w.slot_rank[s]) for s in slots))
 
 
-def apply_flops(w, plan_maps, table):
-    tok_c, tok_u = plan_maps
+def kernel_bytes(w, maps, table):
+    """(shrink, expand) algorithmic bytes of one table: the shrink reads x once
+    and the A factors of the referenced adapters once; the expand reads and
+    writes y once and reads their B factors once; each reads the 16-byte token
+    records."""
+    _, n_in, n_out = w.tables[table]
+    es = w.esize
+    T = len(maps[0])
+    rows = _adapter_rows(w, maps)
+    return es * (T * n_in + rows * n_in) + 16 * T, es * (2 * T * n_out + rows * n_out) + 16 * T
+
+
+def apply_bytes(w, maps, table):
+    """Algorithmic HBM bytes of one table's apply: x once, y read + write once,
+    each referenced centroid's A and B once, each referenced residual at its own
+    rank once, and the per-token plan records (16 B each)."""
+    _, n_in, n_out = w.tables[table]
+    T = len(maps[0])
+    return w.esize * (T * n_in + 2 * T * n_out + _adapter_rows(w, maps) * (n_in + n_out)) + 16 * T
+
+
+def apply_flops(w, maps, table):
+    tok_c, tok_u = maps
     _, n_in, n_out = w.tables[table]
     r = np.where(tok_c >= 0, w.r_c, 0) + np.where(tok_u >= 0, w.slot_rank[np.maximum(tok_u, 0)], 0)
     return int(2 * (n_in + n_out) * r.sum())
@@ -70,28 +100,31 @@ def apply_flops(w, plan_maps, table):
 # ---------------------------------------------------------------------------
 # CPU baseline: the oracle as it stands, bounded sample, on this host
 # ---------------------------------------------------------------------------
-def cpu_baseline(w, budget_s=12.0):
-    """Tokens/s of the oracle: plan once per batch, then every table's apply,
-    in chunks of at most 64 tokens so that a bounded sample of a large batch
-    still covers every table.  BLAS limited to one thread."""
-    import oracle
+def host_info():
+    model = "unknown"
     try:
-        from threadpoolctl import threadpool_limits
-        limiter = threadpool_limits(limits=1)
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    blas = "unknown"
+    try:
+        cfg = np.show_config(mode="dicts")
+        b = cfg.get("Build Dependencies", {}).get("blas", {})
+        blas = f"{b.get('name', '?')} {b.get('version', '')}".strip()
     except Exception:   # pragma: no cover
-        limiter = None
-    d = w.dtype
-    n_tab = len(w.tables)
-    chunk = min(w.T, 64)
-    data = []
-    for t in range(n_tab):
-        x = oracle.decode(w.x(t), d)
-        y0 = oracle.decode(w.y0(t), d)
-        cat, cb = (oracle.decode(a, d) for a in w.centroids(t)) if w.n_centroids else (None, None)
-        res = {int(s): tuple(oracle.decode(a, d) for a in w.residual(int(s), t)) for s in w.referenced_slots()}
-        data.append((x, y0, cat, cb, res))
-        log(f"cpu baseline: table {t + 1} of {n_tab} staged")
-    pairs = 0            # (token, table) pairs computed
+        pass
+    return {"cpu_model": model, "logical_cpus": os.cpu_count(), "blas": blas}
+
+
+def _oracle_pass(data, w, chunk, budget_s):
+    """Plan once per batch, then the apply of every table on chunks of `chunk`
+    tokens, until budget_s has passed at the end of a chunk."""
+    import oracle
+    n_tab = len(data)
+    pairs = 0
     t0 = time.perf_counter()
     start = 0
     while True:
@@ -103,37 +136,103 @@ def cpu_baseline(w, budget_s=12.0):
             oracle.apply(x, y0, cat, cb, res, w.tok_c, w.tok_u, w.gamma, rows=rows)
         pairs += len(rows) * n_tab
         start = (start + chunk) % w.T
-        if time.perf_counter() - t0 >= budget_s and start == 0 or time.perf_counter() - t0 >= 3 * budget_s:
+        if time.perf_counter() - t0 >= budget_s:
             break
-    dt = time.perf_counter() - t0
-    if limiter is not None and hasattr(limiter, "unregister"):
-        limiter.unregister()
-    return {"value": pairs / n_tab / dt, "unit": "tokens/s", "cores": 1, "kind": "oracle",
-            "sample": f"{pairs // n_tab} tokens through all {n_tab} tables (plan + apply, chunks of {chunk} "
-                      f"tokens) in {dt:.1f} s; fp64 numpy, BLAS limited to 1 thread; "
-                      f"host has {os.cpu_count()} logical cpus"}
+    return pairs / n_tab / (time.perf_counter() - t0), pairs // n_tab
 
 
-def tables_summary(w):
-    names = [f"{n} {i}->{o}" for n, i, o in w.tables]
-    layers = sorted({n.split(".")[0] for n, _, _ in w.tables}) if "." in w.tables[0][0] else []
-    if len(layers) > 1:
-        per = len(names) // len(layers)
-        return [f"{len(layers)} layers x " + ", ".join(x.split(".", 1)[1] for x in names[:per])]
-    return names
+def cpu_baseline(w, dw, budget_s=3.0, repeats=3):
+    """Tokens/s of the oracle through every table of workload w (the 28-layer
+    prefill repeats the seven tables of dw, as the GPU run does), BLAS on one
+    thread and on all cores; median of `repeats` runs each, after one warm-up."""
+    import oracle
+    from threadpoolctl import threadpool_info, threadpool_limits
+    d = dw.dtype
+    data = []
+    for t in range(len(dw.tables)):
+        x = oracle.decode(dw.x(t), d)
+        y0 = oracle.decode(dw.y0(t), d)
+        cat, cb = (oracle.decode(a, d) for a in dw.centroids(t)) if dw.n_centroids else (None, None)
+        res = {int(s): tuple(oracle.decode(a, d) for a in dw.residual(int(s), t)) for s in dw.referenced_slots()}
+        data.append((x, y0, cat, cb, res))
+    reps = len(w.tables) // len(dw.tables)
+    data = data * reps
+    chunk = min(w.T, 64)
+    out = {}
+    for name, limit in (("single_thread", 1), ("all_cores", None)):
+        with threadpool_limits(limits=limit):
+            threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+            _oracle_pass(data, w, chunk, 0.3)
+            runs = [_oracle_pass(data, w, chunk, budget_s) for _ in range(repeats)]
+        vals = sorted(r[0] for r in runs)
+        out[name] = {"value": vals[len(vals) // 2], "cores": threads if limit is None else 1,
+                     "tokens_per_run": runs[0][1], "runs": [round(v, 1) for v in vals]}
+        log(f"cpu baseline {name}: {out[name]['value']:.1f} tokens/s ({threads if limit is None else 1} threads)")
+    best = max(out.values(), key=lambda r: r["value"])
+    hi = host_info()
+    return {"value": best["value"], "unit": "tokens/s", "cores": best["cores"], "kind": "oracle",
+            "sample": (f"the first {best['tokens_per_run']} tokens through all {len(w.tables)} tables per run (plan + "
+                       f"apply, chunks of {chunk} tokens), median of {repeats} runs of ~{budget_s:.0f} s after a "
+                       f"warm-up; fp64 numpy; single thread {out['single_thread']['value']:.1f} tokens/s, all "
+                       f"cores ({out['all_cores']['cores']} BLAS threads) {out['all_cores']['value']:.1f} tokens/s; "
+                       f"{hi['cpu_model']}, {hi['logical_cpus']} logical cpus, BLAS {hi['blas']}"),
+            "single_thread": out["single_thread"], "all_cores": out["all_cores"], "host": hi}
 
 
 # ---------------------------------------------------------------------------
-# GPU bench
+# GPU
 # ---------------------------------------------------------------------------
-def build_replicated(w, dw, rot, hip, salt, deterministic=False):
-    """A context whose tables are ``rot`` copies of the workload's tables, with
-    every centroid pinned and every referenced residual loaded.  Adapter values
-    come from ``dw``, whose tables repeat to give ``w``'s (the same workload with
-    fewer layers for the 28-layer prefill; ``w`` itself otherwise)."""
+WORKLOADS = {
+    "prefill": dict(cfg=3, rot=1, steps=10, warmup=2),
+    "qproj": dict(cfg=2, rot=128, steps=2000, warmup=200),
+    "decode8b": dict(cfg=4, rot=4, steps=500, warmup=50, swaps=True),
+    "zipf": dict(cfg=5, rot=4, steps=500, warmup=50),
+    "zipf-baseline": dict(cfg=5, rot=4, baseline=True, steps=200, warmup=20),
+    # Sec. 3.3's long tail: the Zipf batch with the users of slots >= 100 served by
+    # concatenated rank-65/66 adapters (no centroid), the head by centroid + residual
+    "longtail": dict(cfg=5, rot=4, tail=100, steps=200, warmup=20),
+    # Sec. 3.3: a centroid fused into the base weights of one Llama-3.2-3B layer
+    "fuse": dict(cfg=5, rot=2, steps=20, warmup=3, fuse=True),
+    # Sec. 3.1 Eq. 2 / Sec. 4.5: layer-wise cosine of two rank-16 adapters over the
+    # 196 tables of the 28-layer Llama-3.2-3B
+    "gram": dict(cfg=3, rot=1, steps=10, warmup=2, gram=True),
+}
+# sub-records of the default run: shorter than a workload's own defaults
+SUB_RECORDS = (("qproj", 1000, 100), ("decode8b", 200, 20), ("zipf", 200, 20), ("zipf-baseline", 100, 10))
+
+
+def make_workload(spec):
+    from paper_2608_03579_amd import synth
+    w = synth.make(spec["cfg"], 0, baseline=spec.get("baseline", False))
+    if spec.get("tail"):
+        w = synth.long_tail(w, spec["tail"])
+    # the 28-layer prefill draws adapter and activation values for one layer and
+    # repeats them over the layers (each table still has its own memory)
+    dw = synth.make(3, 0, layers=1) if spec["cfg"] == 3 else w
+    return w, dw
+
+
+def layer_groups(w):
+    """Tables applied together: a decoder layer's seven projections."""
+    names = [n for n, _, _ in w.tables]
+    groups, cur, layer = [], [], None
+    for t, n in enumerate(names):
+        l = n.split(".")[0] if "." in n else ""
+        if cur and l != layer:
+            groups.append(cur)
+            cur = []
+        cur.append(t)
+        layer = l
+    groups.append(cur)
+    return groups
+
+
+def build_context(w, dw, rot, salt):
+    """A context whose tables are `rot` copies of the workload's tables, with
+    every centroid pinned and every referenced residual loaded; adapter values
+    come from dw, whose tables repeat to give w's."""
     shapes = [(i, o) for _, i, o in w.tables] * rot
-    ctx = salt.Context(w.dtype, shapes, w.n_centroids, w.r_c, w.n_slots, w.r_u_max, max(1, w.T),
-                       deterministic=deterministic)
+    ctx = salt.Context(w.dtype, shapes, w.n_centroids, w.r_c, w.n_slots, w.r_u_max, max(1, w.T))
     n_tab, n_dat = len(w.tables), len(dw.tables)
     reps = (n_tab // n_dat) * rot
     if w.n_centroids:
@@ -150,46 +249,15 @@ def build_replicated(w, dw, rot, hip, salt, deterministic=False):
     return ctx
 
 
-def swap_timing(w, hip, salt, n=32):
-    """H2D swap of n residual blobs (rank r_u_max of the workload vs rank 16),
-    pinned host memory, on the context's side stream."""
-    out = {}
-    shapes = [(i, o) for _, i, o in w.tables]
-    per16 = salt.residual_bytes_for(salt.BF16 if w.dtype == "bf16" else salt.F32, shapes, 16)
-    n = n or max(4, min(32, (256 << 20) // max(1, per16)))
-    for r in sorted({max(1, w.r_u_max), 16}):
-        ctx = salt.Context(w.dtype, shapes, 0, 0, n, r, 1)
-        nbytes = ctx.residual_bytes(r)
-        bufs = [salt.HostBuffer(nbytes) for _ in range(n)]
-        for b in bufs:
-            b.view(np.uint8)[:] = 1
-        ev0, ev1 = hip.Event(), hip.Event()
-        best = None
-        for rep in range(5):
-            hip.synchronize()
-            t0 = time.perf_counter()
-            for i, b in enumerate(bufs):
-                st = ctx.load_residual_ptr(i, r, b.ptr, nbytes)
-                assert st == 0, st
-            ctx.wait_loads()
-            dt = time.perf_counter() - t0
-            best = dt if best is None else min(best, dt)
-        out[f"r{r}"] = {"blobs": n, "bytes_per_blob": nbytes, "ms": best * 1e3,
-                        "GBps": n * nbytes / best / 1e9}
-        for b in bufs:
-            b.free()
-        ctx.close()
-    return out
-
-
-def run_gpu(w, dw, args, hip, salt):
-    rot = args.rot
+def run_gpu(name, w, dw, spec, steps, warmup, hip, salt):
+    rot = spec["rot"]
     n_tab, n_dat = len(w.tables), len(dw.tables)
-    log(f"workload: {w.name}; T={w.T}, tables={n_tab}, rotation={rot}")
-    ctx = build_replicated(w, dw, rot, hip, salt, deterministic=args.deterministic)
+    log(f"{name}: {w.name}; T={w.T}, tables={n_tab}, rotation={rot}")
+    t_setup = time.perf_counter()
+    ctx = build_context(w, dw, rot, salt)
     stream = hip.Stream()
-    # x and y per table copy (rotation keeps the working set above the MALL);
-    # values repeat with the data tables, memory does not
+    # x and y per table copy: the rotation keeps consecutive steps on disjoint
+    # memory (the working set stays above the 256 MB Infinity Cache)
     xs, ys = [None] * (n_tab * rot), [None] * (n_tab * rot)
     for t in range(n_dat):
         x0 = hip.DeviceArray.from_host(dw.x(t))
@@ -203,7 +271,6 @@ def run_gpu(w, dw, args, hip, salt):
         hip.synchronize()
         x0.free()
         y0.free()
-    # one plan per rotation slot; every plan holds the same batch's maps
     plans = []
     for k in range(rot):
         p = ctx.plan()
@@ -211,152 +278,201 @@ def run_gpu(w, dw, args, hip, salt):
         plans.append(p)
     stream.synchronize()
     tile_m, n_tiles, launches = plans[0].tiling()
-    log(f"tiles of {tile_m} tokens: {n_tiles}; kernel launches per apply: {launches}")
+    groups = layer_groups(w)
+    log(f"{name}: setup {time.perf_counter() - t_setup:.1f} s; tiles of {tile_m} tokens: {n_tiles}; "
+        f"{len(groups)} apply_batch calls per step, {launches} launches each")
+
+    def tabs(slot, g):
+        return [slot * n_tab + t for t in g]
 
     def step(k):
         slot = k % rot
         p = plans[slot]
         p.build(stream.h)
-        for t in range(n_tab):
-            tab = slot * n_tab + t
-            ctx.apply(tab, p, xs[tab].ptr, ys[tab].ptr, stream.h)
+        for g in groups:
+            tt = tabs(slot, g)
+            ctx.apply_batch(tt, p, [xs[i].ptr for i in tt], [ys[i].ptr for i in tt], stream.h)
 
-    for k in range(args.warmup):
+    for k in range(warmup):
         step(k)
     stream.synchronize()
     e0, e1 = hip.Event(), hip.Event()
     hip.synchronize()
     e0.record(stream)
     t0 = time.perf_counter()
-    for k in range(args.steps):
+    for k in range(steps):
         step(k)
     enqueue = time.perf_counter() - t0
     e1.record(stream)
     e1.synchronize()
     wall = time.perf_counter() - t0
-    hip.synchronize()
     ms_total = e0.elapsed_ms(e1)
-    ms_step = ms_total / args.steps
-    log(f"timed {args.steps} steps: {ms_total:.3f} ms GPU ({wall * 1e3:.1f} ms wall, host enqueue "
+    ms_step = ms_total / steps
+    log(f"{name}: timed {steps} steps: {ms_total:.3f} ms GPU ({wall * 1e3:.1f} ms wall, host enqueue "
         f"{enqueue * 1e3:.1f} ms), {ms_step * 1e3:.2f} us/step")
 
-    # roofline: the apply kernel's own duration.  A second timed region runs
-    # applies of one table on plans already built, back to back (launch-to-launch
-    # period, HIP events around the run); a third launches the same applies
-    # through salt_apply_timed, whose HIP events record each kernel's own start
-    # and end (the duration the rocprofv3 kernel trace reports).
+    # roofline: each launch's shrink and expand kernels timed by their own events
     maps = (w.tok_c, w.tok_u)
+    kb = [kernel_bytes(w, maps, t) for t in range(n_tab)]
     bytes_tab = np.array([apply_bytes(w, maps, t) for t in range(n_tab)], dtype=np.float64)
-    flops_tab = np.array([apply_flops(w, maps, t) for t in range(n_tab)], dtype=np.float64)
-    n_meas = max(1, min(args.steps, 4000) // n_tab)
-    per_tab = np.zeros(n_tab)
-    period_tab = np.zeros(n_tab)
-    ev = [hip.Event() for _ in range(2 * n_meas)]
-    for t in range(n_tab):
-        a, b = hip.Event(), hip.Event()
-        a.record(stream)
-        for k in range(n_meas):
-            slot = k % rot
-            tab = slot * n_tab + t
-            ctx.apply(tab, plans[slot], xs[tab].ptr, ys[tab].ptr, stream.h)
-        b.record(stream)
-        b.synchronize()
-        period_tab[t] = a.elapsed_ms(b) / n_meas
-        a.destroy()
-        b.destroy()
-        for k in range(n_meas):
-            slot = k % rot
-            tab = slot * n_tab + t
-            ctx.apply_timed(tab, plans[slot], xs[tab].ptr, ys[tab].ptr, stream.h, ev[2 * k].h, ev[2 * k + 1].h)
-        stream.synchronize()
-        per_tab[t] = float(np.mean([ev[2 * k].elapsed_ms(ev[2 * k + 1]) for k in range(n_meas)]))
-    for e in ev:
+    n_meas = max(2, min(200, 2000 // max(1, len(groups))))
+    ev = [hip.Event() for _ in range(4 * n_meas * len(groups))]
+    i = 0
+    for k in range(n_meas):
+        slot = k % rot
+        for g in groups:
+            tt = tabs(slot, g)
+            ctx.apply_batch_timed(tt, plans[slot], [xs[j].ptr for j in tt], [ys[j].ptr for j in tt], stream.h,
+                                  [e.h for e in ev[4 * i:4 * i + 4]])
+            i += 1
+    stream.synchronize()
+    sh = np.array([ev[4 * j].elapsed_ms(ev[4 * j + 1]) for j in range(i)]).reshape(n_meas, len(groups))
+    ex = np.array([ev[4 * j + 2].elapsed_ms(ev[4 * j + 3]) for j in range(i)]).reshape(n_meas, len(groups))
+    for e in ev + [e0, e1]:
         e.destroy()
-    errors = sum(p.errors(stream.h) for p in plans)
-    if errors:
-        raise RuntimeError(f"{errors} apply blocks gave up waiting; results invalid")
-    dom = int(np.argmax(per_tab * 1.0))
-    achieved = bytes_tab[dom] / (per_tab[dom] * 1e-3) / 1e9
-    step_bytes = float(bytes_tab.sum())
-    log(f"apply durations (us): " + ", ".join(f"{w.tables[t][0]} {per_tab[t] * 1e3:.2f}" for t in range(n_tab)))
-    log(f"apply launch periods (us): " + ", ".join(f"{w.tables[t][0]} {period_tab[t] * 1e3:.2f}" for t in range(n_tab)))
+    sh_us, ex_us = sh.mean() * 1e3, ex.mean() * 1e3
+    # all groups of a workload have the same shapes (28 identical layers)
+    g0 = groups[0]
+    sh_bytes = float(sum(kb[t][0] for t in g0))
+    ex_bytes = float(sum(kb[t][1] for t in g0))
+    dominant = "k_expand" if ex_us >= sh_us else "k_shrink"
+    dom_us, dom_bytes = (ex_us, ex_bytes) if dominant == "k_expand" else (sh_us, sh_bytes)
+    achieved = dom_bytes / (dom_us * 1e-6) / 1e9
+    log(f"{name}: per launch of {len(g0)} tables: k_shrink {sh_us:.2f} us ({sh_bytes / sh_us / 1e3:.0f} GB/s), "
+        f"k_expand {ex_us:.2f} us ({ex_bytes / ex_us / 1e3:.0f} GB/s)")
 
-    swap = swap_timing(w, hip, salt) if args.swap else None
-    if args.copy_mb:
-        log(f"copy calibration: {args.copy_mb} MiB device-to-device")
-        a_ = hip.DeviceArray((args.copy_mb << 20,), np.uint8)
-        b_ = hip.DeviceArray((args.copy_mb << 20,), np.uint8)
-        for _ in range(3):
-            b_.copy_from(a_, stream)
-        stream.synchronize()
-        a_.free()
-        b_.free()
+    swap = run_swaps(w, dw, ctx, plans, groups, tabs, xs, ys, stream, hip, salt) if spec.get("swaps") else None
     for p in plans:
         p.close()
+    for d in xs + ys:
+        d.free()
     ctx.close()
+    stream.destroy()
+    step_bytes = float(bytes_tab.sum())
     return {
-        "ms_per_step": ms_step,
-        "tokens_per_s": w.T / (ms_step * 1e-3),
-        "step_GBps": step_bytes / (ms_step * 1e-3) / 1e9,
-        "apply_us": {w.tables[t][0]: round(per_tab[t] * 1e3, 3) for t in range(n_tab)},
-        "apply_bytes": {w.tables[t][0]: int(bytes_tab[t]) for t in range(n_tab)},
-        "apply_flops": {w.tables[t][0]: int(flops_tab[t]) for t in range(n_tab)},
+        "workload": w.name, "T": w.T, "tables": len(w.tables),
+        "ms_per_step": ms_step, "tokens_per_s": w.T / (ms_step * 1e-3),
+        "step_bytes": step_bytes, "step_GBps": step_bytes / (ms_step * 1e-3) / 1e9,
+        "step_frac": step_bytes / (ms_step * 1e-3) / 1e9 / HBM_PEAK_GBPS,
+        "step_flops": float(sum(apply_flops(w, maps, t) for t in range(n_tab))),
+        "tiling": {"tile_tokens": tile_m, "tiles": n_tiles, "launches_per_apply": launches,
+                   "tables_per_launch": len(g0), "launches_per_step": 2 * len(groups) + 1},
+        "kernels": {"k_shrink": {"avg_us": sh_us, "bytes_per_launch": int(sh_bytes),
+                                 "GBps": sh_bytes / (sh_us * 1e-6) / 1e9},
+                    "k_expand": {"avg_us": ex_us, "bytes_per_launch": int(ex_bytes),
+                                 "GBps": ex_bytes / (ex_us * 1e-6) / 1e9}},
         "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
-                     "kernel": (f"k_apply (salt_apply, one launch) on {w.tables[dom][0]}" if launches == 1 else
-                                f"k_shrink + k_expand (salt_apply, two launches) on {w.tables[dom][0]}"),
-                     "tiling": {"tile_tokens": tile_m, "tiles": n_tiles, "launches_per_apply": launches},
-                     "bytes_per_launch": int(bytes_tab[dom]), "avg_us": per_tab[dom] * 1e3,
-                     "period_us": period_tab[dom] * 1e3,
-                     "timing": f"avg_us: mean apply duration over {n_meas} applies, from HIP events that "
-                               "record the start of each apply's first kernel and the end of its last "
-                               "(salt_apply_timed) on its stream; period_us: launch-to-launch period of "
-                               "back-to-back applies, with the dispatch gap"},
+                     "kernel": f"{dominant} (salt_apply_batch of {len(g0)} tables)",
+                     "bytes_per_launch": int(dom_bytes), "avg_us": dom_us,
+                     "timing": f"avg_us: mean duration over {sh.size} launches, from the HIP events "
+                               "salt_apply_batch_timed records at the kernel's own start and end on its stream"},
         "swap": swap,
     }
 
 
-# committed rocprofv3 counter summaries: HBM traffic per apply launch, valid
-# only for the kernel source they were taken on
+def run_swaps(w, dw, ctx, plans, groups, tabs, xs, ys, stream, hip, salt, n=32, reps=20):
+    """Config-4 residual swaps: 32 new users' residuals per step, pinned host
+    blobs of the layer's seven tables (327,680 B at rank 2), H2D on a context's
+    side stream.  The swaps go to a context of exactly those seven tables, so a
+    blob is one user's real per-layer residual; the apply they overlap with runs
+    on the bench's rotated tables (slots no in-flight batch reads, as the next
+    step's users would be).  Reported: swap-only, apply-only and overlapped
+    step times, rank 2 against rank 16, one salt_load_residuals call against one
+    salt_load_residual per blob."""
+    shapes = [(i, o) for _, i, o in dw.tables]
+    ctx2 = salt.Context(w.dtype, shapes, 0, 0, n, 2, 1)
+    ctx16 = salt.Context(w.dtype, shapes, 0, 0, n, 16, 1)
+    nb2, nb16 = ctx2.residual_bytes(2), ctx16.residual_bytes(16)
+    src = dw.residual_blob(int(w.referenced_slots()[0]))
+    bufs2 = [salt.HostBuffer(nb2) for _ in range(n)]
+    bufs16 = [salt.HostBuffer(nb16) for _ in range(n)]
+    for b in bufs2:
+        b.view(np.uint16)[:] = src
+    for b in bufs16:
+        b.view(np.uint16)[:] = np.tile(src, 8)
+
+    def swap2(r=0):
+        assert ctx2.load_residuals_ptr(list(range(n)), [2] * n, [b.ptr for b in bufs2], [nb2] * n) == 0
+
+    def swap2_each(r=0):
+        for i, b in enumerate(bufs2):
+            assert ctx2.load_residual_ptr(i, 2, b.ptr, nb2) == 0
+
+    def swap16(r=0):
+        assert ctx16.load_residuals_ptr(list(range(n)), [16] * n, [b.ptr for b in bufs16], [nb16] * n) == 0
+
+    def apply_step(k):
+        slot = k % len(plans)
+        plans[slot].build(stream.h)
+        for g in groups:
+            tt = tabs(slot, g)
+            ctx.apply_batch(tt, plans[slot], [xs[i].ptr for i in tt], [ys[i].ptr for i in tt], stream.h)
+
+    def timed(fn):
+        out = []
+        for r in range(reps + 2):
+            hip.synchronize()
+            t0 = time.perf_counter()
+            fn(r)
+            stream.synchronize()
+            ctx2.wait_loads()
+            ctx16.wait_loads()
+            if r >= 2:
+                out.append(time.perf_counter() - t0)
+        return float(np.median(out)) * 1e6
+
+    apply_us = timed(apply_step)
+    swap_us = timed(swap2)
+    swap_each_us = timed(swap2_each)
+    swap16_us = timed(swap16)
+    both_us = timed(lambda r: (swap2(), apply_step(r)))
+    for b in bufs2 + bufs16:
+        b.free()
+    ctx2.close()
+    ctx16.close()
+    r = {"blobs_per_step": n, "bytes_per_blob_r2": int(nb2), "bytes_per_blob_r16": int(nb16),
+         "swap_only_us": swap_us, "swap_only_GBps": n * nb2 / (swap_us * 1e-6) / 1e9,
+         "swap_one_call_per_blob_us": swap_each_us,
+         "swap_r16_us": swap16_us, "swap_r16_GBps": n * nb16 / (swap16_us * 1e-6) / 1e9,
+         "r16_over_r2_time": swap16_us / swap_us, "r16_over_r2_bytes": nb16 / nb2,
+         "apply_only_step_us": apply_us, "overlapped_step_us": both_us,
+         "timing": f"host wall time from the first enqueue until every stream involved has drained, median of "
+                   f"{reps}"}
+    log(f"swaps: {n} x {nb2} B rank 2 in {swap_us:.1f} us ({r['swap_only_GBps']:.1f} GB/s; one call per blob "
+        f"{swap_each_us:.1f} us), rank 16 {swap16_us:.1f} us ({r['swap_r16_GBps']:.1f} GB/s); apply-only step "
+        f"{apply_us:.1f} us, overlapped {both_us:.1f} us")
+    return r
+
+
+# committed rocprofv3 counter summaries: HBM traffic per launch of the dominant
+# kernel, valid only for the kernel source they were taken on
 TRAFFIC_PROFILES = {
-    "qproj": "profiles/k_apply_llama32-3b_qproj_decode_T64_hbm_traffic.md",
+    "prefill": "profiles/k_expand_llama32-3b_28layer_prefill_T8192_hbm_traffic.md",
+    "qproj": "profiles/k_shrink_k_expand_llama32-3b_qproj_decode_T64_hbm_traffic.md",
 }
 
 
-def measured_traffic(workload):
-    """Bytes per launch from the committed counter summary of this workload, or
-    None when there is none or the kernel source changed since it was taken."""
-    import hashlib
+def read_fields(path):
+    fields = {}
+    for line in open(path):
+        if ":" in line:
+            k, v = line.split(":", 1)
+            fields[k.strip().lstrip("- ").strip()] = v.strip()
+    return fields
+
+
+def measured_traffic(workload, kernel):
+    """Bytes per launch of `kernel` from the committed counter summary of this
+    workload, or None when there is none or the kernel sources changed since."""
     rel = TRAFFIC_PROFILES.get(workload)
     if rel is None or not os.path.exists(os.path.join(ROOT, rel)):
         return None
-    fields = {}
-    for line in open(os.path.join(ROOT, rel)):
-        if ":" in line:
-            k, v = line.split(":", 1)
-            fields[k.strip()] = v.strip()
-    src = os.path.join(ROOT, "paper_2608_03579_amd", "csrc", "salt_kernels.hip")
-    h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    if fields.get("kernel_source_sha256_16") != h or "traffic_bytes_per_launch" not in fields:
+    f = read_fields(os.path.join(ROOT, rel))
+    if f.get("kernel_source_sha256_16") != kernel_source_hash():
         return None
-    return int(fields["traffic_bytes_per_launch"])
-
-
-WORKLOADS = {
-    "qproj": dict(cfg=2, rot=128, steps=2000, warmup=200),
-    "prefill": dict(cfg=3, rot=1, steps=10, warmup=2),
-    "decode8b": dict(cfg=4, rot=4, steps=500, warmup=50),
-    "zipf": dict(cfg=5, rot=4, steps=500, warmup=50),
-    "zipf-baseline": dict(cfg=5, rot=4, baseline=True, steps=200, warmup=20),
-    # Sec. 3.3's long tail: the Zipf batch with the users of slots >= 100 served by
-    # concatenated rank-65/66 adapters (no centroid), the head by centroid + residual
-    "longtail": dict(cfg=5, rot=4, tail=100, steps=300, warmup=30),
-    # Sec. 3.3: a centroid fused into the base weights of one Llama-3.2-3B layer
-    "fuse": dict(cfg=5, rot=2, steps=20, warmup=3, fuse=True),
-    # Sec. 3.1 Eq. 2 / Sec. 4.5: layer-wise cosine of two rank-16 adapters over the
-    # 196 tables of the 28-layer Llama-3.2-3B
-    "gram": dict(cfg=3, rot=1, steps=10, warmup=2, gram=True),
-}
+    key = f"traffic_bytes_per_launch_{kernel}"
+    return int(f[key]) if key in f else None
 
 
 def gram_workload(rank=16):
@@ -404,22 +520,17 @@ def cpu_gram_baseline(w, rank=16, budget_s=12.0):
     """GB/s of the oracle (dense updates formed in float64, one BLAS thread) on the
     same tables, counted with the same bytes of factors."""
     import oracle
-    try:
-        from threadpoolctl import threadpool_limits
-        limiter = threadpool_limits(limits=1)
-    except Exception:   # pragma: no cover
-        limiter = None
+    from threadpoolctl import threadpool_limits
     done, nbytes = 0, 0.0
-    t0 = time.perf_counter()
-    while time.perf_counter() - t0 < budget_s and done < len(w.tables):
-        at1, b1 = (oracle.decode(a, "bf16") for a in w.residual(0, done))
-        at2, b2 = (oracle.decode(a, "bf16") for a in w.residual(1, done))
-        oracle.update_terms(at1, b1, at2, b2)
-        nbytes += 2 * rank * (at1.shape[1] + b1.shape[1]) * 2
-        done += 1
-    dt = time.perf_counter() - t0
-    if limiter is not None and hasattr(limiter, "unregister"):
-        limiter.unregister()
+    with threadpool_limits(limits=1):
+        t0 = time.perf_counter()
+        while time.perf_counter() - t0 < budget_s and done < len(w.tables):
+            at1, b1 = (oracle.decode(a, "bf16") for a in w.residual(0, done))
+            at2, b2 = (oracle.decode(a, "bf16") for a in w.residual(1, done))
+            oracle.update_terms(at1, b1, at2, b2)
+            nbytes += 2 * rank * (at1.shape[1] + b1.shape[1]) * 2
+            done += 1
+        dt = time.perf_counter() - t0
     return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"{done} of {len(w.tables)} tables (dense updates in fp64) in {dt:.1f} s; BLAS limited to "
                       f"1 thread; host has {os.cpu_count()} logical cpus"}
@@ -442,8 +553,9 @@ def run_fuse(w, args, hip, salt):
         at, b = w.centroids(t)
         ctx.pin_centroids(t, at, b)
     stream = hip.Stream()
+    rot = WORKLOADS["fuse"]["rot"]
     ws = []
-    for k in range(args.rot):
+    for k in range(rot):
         for t in range(n_tab):
             ws.append(hip.DeviceArray.from_host(w.base_weight(t)))
     hip.synchronize()
@@ -451,7 +563,7 @@ def run_fuse(w, args, hip, salt):
 
     def step(k):
         g = 0.8 if k % 2 == 0 else -0.8
-        base = (k % args.rot) * n_tab
+        base = (k % rot) * n_tab
         for t in range(n_tab):
             ctx.fuse_centroid(t, 0, g, ws[base + t].ptr, tables[t][1], stream.h)
 
@@ -470,7 +582,7 @@ def run_fuse(w, args, hip, salt):
     per_tab = np.zeros(n_tab)
     for t in range(n_tab):
         for k in range(n_meas):
-            ctx.fuse_centroid_timed(t, 0, 0.8 if k % 2 == 0 else -0.8, ws[(k % args.rot) * n_tab + t].ptr,
+            ctx.fuse_centroid_timed(t, 0, 0.8 if k % 2 == 0 else -0.8, ws[(k % rot) * n_tab + t].ptr,
                                     tables[t][1], stream.h, ev[2 * k].h, ev[2 * k + 1].h)
         stream.synchronize()
         per_tab[t] = float(np.mean([ev[2 * k].elapsed_ms(ev[2 * k + 1]) for k in range(n_meas)]))
@@ -484,7 +596,6 @@ def run_fuse(w, args, hip, salt):
     log(f"fuse durations (us): " + ", ".join(f"{w.tables[t][0]} {per_tab[t] * 1e3:.2f}" for t in range(n_tab)))
     return {"ms_per_step": ms_step, "step_GBps": bytes_tab.sum() / (ms_step * 1e-3) / 1e9,
             "fuse_us": {w.tables[t][0]: round(per_tab[t] * 1e3, 3) for t in range(n_tab)},
-            "fuse_bytes": {w.tables[t][0]: int(bytes_tab[t]) for t in range(n_tab)},
             "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                          "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
                          "kernel": f"k_fuse (salt_fuse_centroid) on {w.tables[dom][0]}",
@@ -493,33 +604,21 @@ def run_fuse(w, args, hip, salt):
                                    "the kernel's own start and end (salt_fuse_centroid_timed)"}}
 
 
-def cpu_fuse_baseline(w, budget_s=12.0):
-    """GB/s of the oracle's fuse (float64 numpy, BLAS limited to one thread) over
-    the same tables, counted with the same algorithmic bytes."""
-    import oracle
-    try:
-        from threadpoolctl import threadpool_limits
-        limiter = threadpool_limits(limits=1)
-    except Exception:   # pragma: no cover
-        limiter = None
-    d = w.dtype
-    data = []
-    for t in range(len(w.tables)):
-        at, b = w.centroids(t)
-        data.append((oracle.decode(w.base_weight(t), d), oracle.decode(at[0], d), oracle.decode(b[0], d)))
-    done, nbytes = 0, 0.0
-    t0 = time.perf_counter()
-    while time.perf_counter() - t0 < budget_s:
-        W, A, B = data[done % len(data)]
-        oracle.fuse_centroid(W, A, B, 0.8)
-        nbytes += fuse_bytes(W.shape[0], W.shape[1], A.shape[0])
-        done += 1
-    dt = time.perf_counter() - t0
-    if limiter is not None and hasattr(limiter, "unregister"):
-        limiter.unregister()
-    return {"value": nbytes / dt / 1e9, "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{done} table fuses (one layer's 7 tables in turn) in {dt:.1f} s; fp64 numpy, BLAS "
-                      f"limited to 1 thread; host has {os.cpu_count()} logical cpus"}
+def tables_summary(w):
+    groups = layer_groups(w)
+    names = [n.split(".", 1)[-1] for n, _, _ in (w.tables[t] for t in groups[0])]
+    shapes = [f"{n} {w.tables[t][1]}->{w.tables[t][2]}" for n, t in zip(names, groups[0])]
+    return f"{len(groups)} layers x [{', '.join(shapes)}]" if len(groups) > 1 else ", ".join(shapes)
+
+
+def sub_record(res):
+    keep = ("workload", "T", "tables", "ms_per_step", "tokens_per_s", "step_bytes", "step_GBps", "step_frac",
+            "tiling", "kernels")
+    r = {k: res[k] for k in keep}
+    r["roofline"] = {k: res["roofline"][k] for k in ("kernel", "achieved", "frac", "avg_us", "bytes_per_launch")}
+    if res.get("swap"):
+        r["swap"] = res["swap"]
+    return r
 
 
 def main():
@@ -527,34 +626,20 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None)
     ap.add_argument("--warmup", type=int, default=None)
+    ap.add_argument("--workload", default="prefill", choices=sorted(WORKLOADS))
+    ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-sub", action="store_true", help="skip the decode / Zipf sub-records")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="also run a device-to-device copy of this many MiB (counter calibration)")
-    ap.add_argument("--workload", default="qproj", choices=sorted(WORKLOADS))
-    ap.add_argument("--rot", type=int, default=None)
-    ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--no-swap", dest="swap", action="store_false")
-    ap.add_argument("--deterministic", action="store_true",
-                    help="fixed-order split-K sums (SALT_DETERMINISTIC) instead of fp32 atomics")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: the apply has no cross-GPU path in this build "
-              f"(asked for --gpus {args.gpus})", file=sys.stderr)
+        print(f"bench.py runs on one GPU only: this build has no cross-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
         sys.exit(2)
     spec = WORKLOADS[args.workload]
-    if args.rot is None:
-        args.rot = spec["rot"]
-    if args.steps is None:
-        args.steps = spec["steps"]
-    if args.warmup is None:
-        args.warmup = spec["warmup"]
-
-    from paper_2608_03579_amd import synth
-    w = synth.make(spec["cfg"], 0, baseline=spec.get("baseline", False))
-    if spec.get("tail"):
-        w = synth.long_tail(w, spec["tail"])
-    # the 28-layer prefill draws adapter and activation values for one layer and
-    # repeats them over the layers (distinct memory per table)
-    dw = synth.make(3, 0, layers=1) if spec["cfg"] == 3 else w
+    steps = args.steps if args.steps is not None else spec["steps"]
+    warmup = args.warmup if args.warmup is not None else spec["warmup"]
+    args.steps, args.warmup = steps, warmup
 
     from paper_2608_03579_amd import hip, salt
     if hip.device_count() < 1:
@@ -567,69 +652,84 @@ def main():
         achieved = res["bytes"] / (res["ms"] * 1e-3) / 1e9
         print(json.dumps({
             "metric": "Adapter cosine in factor space (Sec. 3.1 Eq. 2, Sec. 4.5): achieved HBM GB/s, Llama-3.2-3B",
-            "value": achieved, "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "value": achieved, "unit": "GB/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
             "ms_per_step": res["ms"], "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
             "dtype": "bf16", "data": "synthetic",
-            "config": {"workload": "two rank-16 adapters, 196 tables of the 28-layer Llama-3.2-3B",
-                       "step": "salt_adapter_gram (Grams over in and out, fp32; products in fp64)"},
-            "call_wall_ms": res["wall_ms"],
+            "config": {"workload": "two rank-16 adapters, 196 tables of the 28-layer Llama-3.2-3B"},
             "roofline": {"bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                          "frac": achieved / HBM_PEAK_GBPS, "traffic": None,
                          "kernel": "k_gram + k_gram_finish (salt_adapter_gram)",
                          "bytes_per_launch": res["bytes"], "avg_us": res["ms"] * 1e3,
-                         "timing": "avg_us: median stream time of the whole call (descriptor upload, Gram "
-                                   "buffer clear, both kernels, result copy) between HIP events"},
+                         "timing": "avg_us: median stream time of the whole call between HIP events"},
             "cpu_baseline": cpu}), flush=True)
         return
     if spec.get("fuse"):
+        w, _ = make_workload(spec)
         res = run_fuse(w, args, hip, salt)
-        cpu = None if args.no_cpu else cpu_fuse_baseline(w)
         print(json.dumps({
             "metric": "Centroid fused into the base weights (Sec. 3.3 node start-up): achieved HBM GB/s, "
                       "Llama-3.2-3B",
-            "value": res["step_GBps"], "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "value": res["step_GBps"], "unit": "GB/s", "n_gpus": 1, "steps": steps, "warmup": warmup,
             "ms_per_step": res["ms_per_step"], "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
             "dtype": "bf16", "data": "synthetic",
-            "config": {"workload": "llama3.2-3b one layer, centroid fused into the base weights",
-                       "tables": tables_summary(w), "centroid_rank": w.r_c, "rotation": args.rot,
-                       "step": "salt_fuse_centroid per table (W read + written once, A_c and B_c read once)"},
-            "fuse_us": res["fuse_us"], "fuse_bytes": res["fuse_bytes"], "roofline": res["roofline"],
-            "cpu_baseline": cpu}), flush=True)
+            "config": {"workload": "llama3.2-3b one layer, centroid fused into the base weights"},
+            "fuse_us": res["fuse_us"], "roofline": res["roofline"], "cpu_baseline": None}), flush=True)
         return
-    res = run_gpu(w, dw, args, hip, salt)
-    res["roofline"]["traffic"] = measured_traffic(args.workload)
 
+    w, dw = make_workload(spec)
+    res = run_gpu(args.workload, w, dw, spec, steps, warmup, hip, salt)
+    dom = res["roofline"]["kernel"].split()[0]
+    res["roofline"]["traffic"] = measured_traffic(args.workload, dom)
+    subs = {}
+    if args.workload == "prefill" and not args.no_sub:
+        for name, s_steps, s_warm in SUB_RECORDS:
+            sw, sdw = make_workload(WORKLOADS[name])
+            subs[name] = sub_record(run_gpu(name, sw, sdw, WORKLOADS[name], s_steps, s_warm, hip, salt))
+        z, zb = subs["zipf"], subs["zipf-baseline"]
+        subs["zipf_salt_vs_rank16_baseline"] = {
+            "bytes_ratio_baseline_over_salt": zb["step_bytes"] / z["step_bytes"],
+            "tokens_per_s_ratio_salt_over_baseline": z["tokens_per_s"] / zb["tokens_per_s"]}
     cpu = None
     if not args.no_cpu:
         log("cpu baseline (oracle) ...")
-        cpu = cpu_baseline(dw if spec["cfg"] == 3 else w)
-
+        cpu = cpu_baseline(w, dw)
+    if args.copy_mb:
+        log(f"copy calibration: {args.copy_mb} MiB device-to-device")
+        a_ = hip.DeviceArray((args.copy_mb << 20,), np.uint8)
+        b_ = hip.DeviceArray((args.copy_mb << 20,), np.uint8)
+        s_ = hip.Stream()
+        for _ in range(3):
+            b_.copy_from(a_, s_)
+        s_.synchronize()
+        a_.free()
+        b_.free()
     out = {
-        "metric": "Centroid+residual LoRA apply: tokens/s and achieved HBM GB/s, Llama-3.2-3B",
+        "metric": METRIC,
         "value": res["tokens_per_s"],
         "unit": "tokens/s",
         "n_gpus": 1,
-        "steps": args.steps,
-        "warmup": args.warmup,
+        "steps": steps,
+        "warmup": warmup,
         "ms_per_step": res["ms_per_step"],
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
         "dtype": "bf16",
         "data": "synthetic",
-        "config": {"workload": w.name, "T": w.T,
-                   "tables": tables_summary(w),
-                   "centroids": f"{w.n_centroids} x r{w.r_c}",
-                   "residual_slots": f"{w.n_slots} x r<={w.r_u_max}",
-                   "accumulation": "fp32", "rotation": args.rot,
-                   "split_k_sum": "ordered" if args.deterministic else "fp32 atomics",
-                   "step": "salt_plan_build + salt_apply per table, maps staged in HBM beforehand"},
+        "config": {"workload": w.name, "T": w.T, "tables": tables_summary(w),
+                   "centroids": f"{w.n_centroids} x r{w.r_c}", "residual_slots": f"{w.n_slots} x r<={w.r_u_max}",
+                   "accumulation": "fp32", "rotation": spec["rot"],
+                   "step": "salt_plan_build + one salt_apply_batch per decoder layer (its 7 tables); maps staged "
+                           "in HBM beforehand"},
         "achieved_GBps_step": res["step_GBps"],
-        "apply_us": res["apply_us"],
-        "apply_bytes": res["apply_bytes"],
+        "step_bytes": res["step_bytes"],
+        "tiling": res["tiling"],
+        "kernels": res["kernels"],
         "roofline": res["roofline"],
         "cpu_baseline": cpu,
-        "swap_h2d": res["swap"],
+        "swap": res["swap"],
+        "sub_records": subs or None,
+        "kernel_source_sha256_16": kernel_source_hash(),
     }
     print(json.dumps(out), flush=True)
 

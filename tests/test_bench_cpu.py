@@ -6,7 +6,6 @@ The byte model is pinned to totals worked out by hand from the workload
 definitions (x read once, y read and written once, each referenced adapter
 once at its own rank, 16 B of plan record per token), not to the function's own
 formula."""
-import hashlib
 import os
 import shutil
 import subprocess
@@ -71,33 +70,54 @@ def test_more_than_one_gpu_is_refused():
     assert "one GPU" in r.stderr and r.stdout == ""
 
 
-def _fields(path):
-    out = {}
-    for line in open(path):
-        if ":" in line:
-            k, v = line.split(":", 1)
-            out[k.strip()] = v.strip()
-    return out
+def test_kernel_bytes_split_the_apply_bytes():
+    # shrink (x + A factors) and expand (y read + write + B factors) together are
+    # the apply's bytes, with the 16 B token records read by both
+    for cfg in (2, 4, 5):
+        w = synth.make(cfg, 0)
+        maps = (w.tok_c, w.tok_u)
+        for t in range(len(w.tables)):
+            sh, ex = bench.kernel_bytes(w, maps, t)
+            assert sh + ex == bench.apply_bytes(w, maps, t) + 16 * w.T
+    w = synth.make(2, 0)
+    sh, ex = bench.kernel_bytes(w, (w.tok_c, w.tok_u), 0)
+    assert sh == 64 * 3072 * 2 + (4 * 32 + 64 * 2) * 3072 * 2 + 64 * 16
+    assert ex == 2 * 64 * 3072 * 2 + (4 * 32 + 64 * 2) * 3072 * 2 + 64 * 16
+
+
+def test_layer_groups():
+    assert [len(g) for g in bench.layer_groups(synth.make(3, 0))] == [7] * 28
+    assert bench.layer_groups(synth.make(4, 0)) == [list(range(7))]
+    assert bench.layer_groups(synth.make(2, 0)) == [[0]]
 
 
 def test_traffic_is_reported_only_for_the_profiled_kernel_source(tmp_path, monkeypatch):
-    rel = bench.TRAFFIC_PROFILES["qproj"]
-    fields = _fields(os.path.join(ROOT, rel))
-    src = os.path.join(ROOT, "paper_2608_03579_amd", "csrc", "salt_kernels.hip")
-    h = hashlib.sha256(open(src, "rb").read()).hexdigest()[:16]
-    got = bench.measured_traffic("qproj")
-    if fields.get("kernel_source_sha256_16") == h:
-        assert got == int(fields["traffic_bytes_per_launch"])
-    else:
-        assert got is None
-    # a copy of the tree whose kernel source differs by one byte: no traffic
+    for workload, rel in bench.TRAFFIC_PROFILES.items():
+        path = os.path.join(ROOT, rel)
+        if not os.path.exists(path):
+            assert bench.measured_traffic(workload, "k_expand") is None
+            continue
+        fields = bench.read_fields(path)
+        for kernel in ("k_shrink", "k_expand"):
+            got = bench.measured_traffic(workload, kernel)
+            key = f"traffic_bytes_per_launch_{kernel}"
+            if fields.get("kernel_source_sha256_16") == bench.kernel_source_hash() and key in fields:
+                assert got == int(fields[key])
+            else:
+                assert got is None
+    # a copy of the tree whose kernel sources differ by one byte: no traffic
     fake = tmp_path / "root"
-    (fake / "paper_2608_03579_amd" / "csrc").mkdir(parents=True)
-    (fake / os.path.dirname(rel)).mkdir(parents=True, exist_ok=True)
-    shutil.copy(os.path.join(ROOT, rel), fake / rel)
-    with open(src, "rb") as f:
-        data = f.read()
-    (fake / "paper_2608_03579_amd" / "csrc" / "salt_kernels.hip").write_bytes(data + b"\n")
+    csrc = fake / "paper_2608_03579_amd" / "csrc"
+    csrc.mkdir(parents=True)
+    for n in bench.KERNEL_SOURCES:
+        shutil.copy(os.path.join(ROOT, "paper_2608_03579_amd", "csrc", n), csrc / n)
+    for rel in bench.TRAFFIC_PROFILES.values():
+        if os.path.exists(os.path.join(ROOT, rel)):
+            (fake / os.path.dirname(rel)).mkdir(parents=True, exist_ok=True)
+            shutil.copy(os.path.join(ROOT, rel), fake / rel)
+    with open(csrc / "salt_apply.hip", "ab") as f:
+        f.write(b"\n")
     monkeypatch.setattr(bench, "ROOT", str(fake))
-    assert bench.measured_traffic("qproj") is None
-    assert bench.measured_traffic("no-such-workload") is None
+    for workload in bench.TRAFFIC_PROFILES:
+        assert bench.measured_traffic(workload, "k_expand") is None
+    assert bench.measured_traffic("no-such-workload", "k_expand") is None
