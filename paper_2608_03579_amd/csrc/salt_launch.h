@@ -15,13 +15,13 @@
 namespace salt {
 
 // Tokens per tile, from the mean size of the batch's centroid groups: short
-// groups (decode batches) take 16-token tiles, long ones (prefill) 64.  fp32
-// contexts always use 16.
+// groups (decode batches) take 16-token tiles, groups of up to ~100 tokens 32,
+// long ones (prefill) 64.  fp32 contexts always use 16.
 inline int choose_tile_tokens(int esize, int T, int n_groups) {
   if (esize == 4 || n_groups <= 0) return 16;
   const double mean = (double)T / n_groups;
   if (mean <= 24.0) return 16;
-  if (mean <= 48.0) return 32;
+  if (mean <= 96.0) return 32;
   return 64;
 }
 
@@ -62,24 +62,30 @@ inline int max_tiles(int T, int C) { return cdiv(T, 16) + C + 1; }
 // of a one-range shrink do not fit.
 inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t sum_rank) {
   const int TB = a.M / 16, KW = kWaves / TB, CW = kWaves / TB;
-  const int target = 4 * std::max(1, n_cu);
+  const int target = 8 * std::max(1, n_cu);        // blocks per launch: a few rounds of the whole device
   const double es = (double)a.esize;
+  const double adapters = (double)n_groups_c * a.r_c + (double)sum_rank;
   int64_t sum_in = 0, sum_out = 0;
   for (int j = 0; j < a.n_jobs; ++j) {
     sum_in += a.jobs[j].in;
     sum_out += a.jobs[j].out;
   }
+  // shrink: one K-range length for the whole launch, so that blocks of every
+  // table carry about the same work, sized for ~target blocks; each table's
+  // split is capped so that its partials (written, then read) stay within a
+  // tenth of its bytes
+  const int gran = kStepK * KW;
   const double pairs = (double)a.n_tiles * a.nq;
+  const int kc_target = std::max(gran, cdiv((int)std::ceil((double)sum_in * pairs / target), gran) * gran);
   const double part_row = 8.0 * a.T * a.R;        // bytes of one K range's partials, written and read
   std::vector<int> S(a.n_jobs);
   for (int j = 0; j < a.n_jobs; ++j) {
     const Job& jb = a.jobs[j];
-    const double adapters = (double)n_groups_c * a.r_c + (double)sum_rank;
     const double bytes = es * ((double)a.T * (jb.in + 2.0 * jb.out) + adapters * (jb.in + jb.out));
-    const int s_blocks = (int)std::ceil((double)target * jb.in / ((double)sum_in * pairs));
+    const int s_balance = cdiv(jb.in, kc_target);
     const int s_traffic = std::max(1, (int)(0.1 * bytes / part_row));
-    const int s_max = cdiv(jb.in, kStepK * KW);
-    S[j] = std::max(1, std::min({s_blocks, s_traffic, s_max}));
+    const int s_max = cdiv(jb.in, gran);
+    S[j] = std::max(1, std::min({s_balance, s_traffic, s_max}));
   }
   // partials must fit: shrink the largest split until they do
   auto total = [&]() {
@@ -96,23 +102,21 @@ inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t s
   }
   int64_t poff = 0;
   int sb = 0, eb = 0;
-  const int e_target = 4 * std::max(1, n_cu);
   for (int j = 0; j < a.n_jobs; ++j) {
     Job& jb = a.jobs[j];
-    const int gran = kStepK * KW;
     jb.Kc = cdiv(cdiv(jb.in, S[j]), gran) * gran;
     jb.S = cdiv(jb.in, jb.Kc);
     jb.poff = poff;
     poff += (int64_t)jb.S * a.T * a.R;
-    // column blocks: about e_target over the launch, no more than keep the
-    // tile's partial re-reads within a quarter of the expand's own bytes
-    const double adapters = (double)n_groups_c * a.r_c + (double)sum_rank;
+    // expand: column blocks in proportion to out for ~target blocks; each
+    // block first reads its tile's partials (from L2), which should not pass
+    // the block's own bytes
     const double e_bytes = es * (2.0 * a.T * jb.out + adapters * jb.out);
     const double reread = 4.0 * jb.S * a.T * a.R;
-    const int n_blocks = (int)std::lround((double)e_target * jb.out / ((double)sum_out * a.n_tiles));
-    const int n_traffic = std::max(1, (int)(0.25 * e_bytes / reread));
+    const int n_blocks = (int)std::lround((double)target * jb.out / ((double)sum_out * a.n_tiles));
+    const int n_traffic = std::max(1, (int)(e_bytes / reread));
     const int n_max = cdiv(jb.out, kChunkCols * CW);
-    int n_col = std::max(1, std::min({n_blocks, n_traffic, n_max}));
+    const int n_col = std::max(1, std::min({n_blocks, n_traffic, n_max}));
     const int cgran = kChunkCols * CW;
     jb.cpb = cdiv(cdiv(jb.out, n_col), cgran) * cgran;
     jb.n_col = cdiv(jb.out, jb.cpb);

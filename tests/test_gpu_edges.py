@@ -463,7 +463,7 @@ def test_plan_tiling_reports_the_launch_structure():
     centroid groups take 16-token tiles, fp32 16, the Zipf batch and the
     8192-token prefill 64; the tile count matches the centroid groups."""
     _announce("salt_plan_tiling")
-    for cfg, kw, want in ((2, {}, (16, 2)), (1, {}, (16, 2)), (4, {}, (16, 2)), (5, {}, (64, 2)),
+    for cfg, kw, want in ((2, {}, (16, 2)), (1, {}, (16, 2)), (4, {}, (16, 2)), (5, {}, (32, 2)),
                           (3, {"layers": 1}, (64, 2))):
         w = synth.make(cfg, 0, **kw)
         run = Run(w, pin_tables=[])
