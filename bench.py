@@ -249,7 +249,7 @@ def build_context(w, dw, rot, salt):
     return ctx
 
 
-def run_gpu(name, w, dw, spec, steps, warmup, hip, salt):
+def run_gpu(name, w, dw, spec, steps, warmup, hip, salt, meas=None):
     rot = spec["rot"]
     n_tab, n_dat = len(w.tables), len(dw.tables)
     log(f"{name}: {w.name}; T={w.T}, tables={n_tab}, rotation={rot}")
@@ -315,7 +315,7 @@ def run_gpu(name, w, dw, spec, steps, warmup, hip, salt):
     maps = (w.tok_c, w.tok_u)
     kb = [kernel_bytes(w, maps, t) for t in range(n_tab)]
     bytes_tab = np.array([apply_bytes(w, maps, t) for t in range(n_tab)], dtype=np.float64)
-    n_meas = max(2, min(200, 2000 // max(1, len(groups))))
+    n_meas = meas or max(2, min(200, 2000 // max(1, len(groups))))
     ev = [hip.Event() for _ in range(4 * n_meas * len(groups))]
     i = 0
     for k in range(n_meas):
@@ -629,6 +629,7 @@ def main():
     ap.add_argument("--workload", default="prefill", choices=sorted(WORKLOADS))
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-sub", action="store_true", help="skip the decode / Zipf sub-records")
+    ap.add_argument("--meas", type=int, default=None, help="timed launches per table group for the roofline")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="also run a device-to-device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -677,7 +678,7 @@ def main():
         return
 
     w, dw = make_workload(spec)
-    res = run_gpu(args.workload, w, dw, spec, steps, warmup, hip, salt)
+    res = run_gpu(args.workload, w, dw, spec, steps, warmup, hip, salt, args.meas)
     dom = res["roofline"]["kernel"].split()[0]
     res["roofline"]["traffic"] = measured_traffic(args.workload, dom)
     subs = {}

@@ -26,6 +26,7 @@
 #include <hip/hip_ext.h>
 
 #include <algorithm>
+#include <atomic>
 
 #include "salt_device.h"
 #include "salt_internal.h"
@@ -47,11 +48,6 @@ template <int M>
 constexpr int waves_along() { return kWaves / (M / 16); }
 template <typename E, int M, int NB>
 constexpr bool staged() { return sizeof(E) == 2 && M > 16 && NB > 0; }
-// Register batches: block-steps (shrink) or block-chunks (expand) whose loads
-// are issued together; two batches alternate, so one is in flight while the
-// other computes.
-template <typename E, int M, int NB, int RU>
-constexpr int batch_len() { return (M == 64 && NB <= 4 && RU <= 2) ? 2 : 1; }
 // Staged rows carry 8 elements of padding: consecutive rows then start 4 LDS
 // banks apart, so a fragment read (16 rows x 16 bytes per 8-lane phase) hits
 // every bank once.
@@ -61,60 +57,74 @@ template <int NB>
 constexpr int stage_row_b() { return 16 * NB + 8; }
 template <int NB, int RU>
 constexpr int shrink_wc() { return 16 * NB + RU; }
+// Block-steps (shrink) or block-chunks (expand) per batch: the loads of one
+// batch are in flight while the previous batch computes.  One: a second step
+// per batch costs more in occupancy (registers) than it gains in loads in
+// flight on every workload measured.
+template <typename E, int M, int NB, int RU>
+constexpr int depth() { return 1; }
 
-__device__ __forceinline__ uint4 sel(bool p, uint4 v) { return p ? v : make_uint4(0u, 0u, 0u, 0u); }
-__device__ __forceinline__ Ops<float>::Vec sel(bool p, Ops<float>::Vec v) { return p ? v : Ops<float>::zero(); }
 
 // ---------------------------------------------------------------------------
 // shrink
 // ---------------------------------------------------------------------------
 // Wave w takes token block mb = w % TB and the kStepK-wide steps kq, kq + KW, ...
 // (kq = w / TB) of the block's K range: block-step j covers steps j KW .. j KW +
-// KW - 1, one per K quarter.  A lane holds token (lane & 15) of its block and the
-// 16 consecutive k at 16 (lane >> 4) of a step, as two 8-element vectors h = 0,
-// 1; MFMA h multiplies vector h of x and of A_c, so the two MFMAs of a step
-// together cover its 64 k.  Every load is issued unconditionally at an address
-// inside the block's own data (a step past the wave's last re-reads that last
-// step, the ragged end of K re-reads the last full vector, a token without a
-// centroid or residual term reads its own x row), and masked by a select, so
-// that the compiler's waits on outstanding loads count them exactly and a batch
-// stays in flight while the other one computes.
+// KW - 1, one per K quarter.  A lane holds token (lane & 15) of its block and,
+// of a step, the two 8-element vectors h = 0, 1 at k = 8 (lane >> 4) + kPiece h:
+// one load instruction then reads 64 contiguous bytes of each token row.  MFMA
+// h multiplies vector h of x and of A_c, so the two MFMAs of a step together
+// cover its 64 k.
+//
+// x and A_c are read through buffer resources (a masked lane reads at kOob and
+// gets zeros); the residual rows through per-lane pointers fixed for the whole
+// block (a lane without that residual row points at the zero page).  Block-step
+// j + 1's per-lane operands are loaded while block-step j computes; with a
+// staged A_c, block-step j + 2's A_c slice is loaded while block-step j + 1's is
+// written into the other half of the LDS stage, so every wait is for loads that
+// were issued a whole block-step earlier.
 template <typename E, int M, int NB, int RU>
 __global__ void __launch_bounds__(kThreads) k_shrink(const ApplyLaunch a) {
   using O = Ops<E>;
   using Vec = typename O::Vec;
+  constexpr int ES = sizeof(E);
   constexpr int TB = M / 16, KW = waves_along<M>(), WC = shrink_wc<NB, RU>();
   constexpr bool kStage = staged<E, M, NB>();
-  constexpr int U = batch_len<E, M, NB, RU>();
   constexpr int NBL = NB > 0 ? NB : 1;
   constexpr int SR = stage_row_a<M>();                       // elements per staged A_c row
   constexpr int NCV = kStage ? NB * KW / 2 : 1;              // staged A_c vectors per thread and block-step
-  constexpr int NAC = kStage ? NCV : 2 * NBL;                // A_c vectors per lane and step
-  constexpr int RUP = RU <= 2 ? RU : 1;                      // residual ranks in the pipelined batch (wider: read in place)
+  constexpr int NAC = kStage ? 1 : 2 * NBL;                  // per-lane A_c vectors per step (unstaged)
+  constexpr int RUP = RU <= 2 ? RU : 0;                      // residual ranks in the pipelined operands
+  constexpr int U = depth<E, M, NB, RU>();
   extern __shared__ __attribute__((aligned(16))) char lds[];
   float* s_red = reinterpret_cast<float*>(lds);              // [KW][M][WC], after the K loop
   E* s_a = reinterpret_cast<E*>(lds);                        // [2][U][16 NB][SR], during the K loop
 
-  const int b = blockIdx.x;
-  const Job& jb = a.jobs[job_of_shrink(a, b)];
-  const ShrinkCoord sc = shrink_coord(a, jb, b);
+  const Job& jb = a.jobs[job_of_shrink(a, blockIdx.x)];
+  const ShrinkCoord sc = shrink_coord(a, jb, blockIdx.x);
   const TileHdr th = clamp_tile(a, a.tiles[sc.tau]);
   if (th.n <= 0) return;                                     // (no tile is empty; the whole block leaves)
+  const int in = jb.in;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int mb = wave % TB, kq = wave / TB, row = lane & 15, g = lane >> 4;
   const int kt = mb * 16 + row;                              // this lane's token within the tile
   const TokRec tr = clamp_tok(a, a.srt[tile_pos(th, kt)], kt < th.n);
-  // x row of the tile's first token: the address of loads whose value is
-  // masked (it is read by the tile anyway, and differs from the lane's own
-  // operands, so each such load stays a plain unconditional load)
-  const int t0 = clamp_tok(a, a.srt[th.i0], true).t;
   const int r0 = sc.q * kRankChunk;                          // first residual rank of this block
   const bool has_c = NB > 0 && th.c >= 0 && sc.q == 0;
-  const E* x = reinterpret_cast<const E*>(jb.x);
-  const E* atc = reinterpret_cast<const E*>(jb.at_c);
   const int klo = k_lo(jb, sc.s), khi = k_hi(jb, sc.s), nst = k_steps(jb, sc.s);
   const int nbs = cdiv(nst, KW);                             // block-steps
-  const int klast = imax(klo, khi - 8);                      // last whole vector of the K range
+  const int klast = imax(0, in - 8);                         // last whole vector of a row
+
+  const Rsrc rx = make_rsrc(jb.x, (uint32_t)((int64_t)a.T * in * ES));
+  const Rsrc rac = make_rsrc(has_c ? static_cast<const char*>(jb.at_c) + (int64_t)th.c * a.r_c * in * ES : nullptr,
+                             has_c ? (uint32_t)((int64_t)a.r_c * in * ES) : 0u);
+  const uint32_t xrow = tr.tok ? (uint32_t)tr.t * (uint32_t)(in * ES) : kOob;
+  // residual rows r0 + jj of this lane's slot (the zero page where there is none)
+  const char* au[RUP > 0 ? RUP : 1];
+#pragma unroll
+  for (int jj = 0; jj < RUP; ++jj)
+    au[jj] = (tr.res && r0 + jj < tr.r) ? a.pool + atu_byte(a, jb, tr.u, tr.r, r0 + jj, 0) : a.zeros;
+  const char* au_wide = tr.res ? a.pool + atu_byte(a, jb, tr.u, tr.r, r0, 0) : a.zeros;
 
   f32x4 acc[NBL];
 #pragma unroll
@@ -123,76 +133,72 @@ __global__ void __launch_bounds__(kThreads) k_shrink(const ApplyLaunch a) {
 #pragma unroll
   for (int j = 0; j < RU; ++j) accu[j] = 0.f;
 
-  struct Batch {
-    Vec ac[U][NAC];
+  // the per-lane operands of a batch: block-steps j0 .. j0 + U - 1
+  struct Ops1 {
     Vec x[U][2];
-    Vec u[U][RUP][2];
+    Vec u[U][RUP > 0 ? RUP : 1][2];
+    Vec ac[U][NAC];
   };
-  // first k of this wave's step in block-step j (past the end: its last step)
-  auto step_k = [&](int j) { return klo + imin(j * KW + kq, nst - 1) * kStepK; };
-  auto load = [&](Batch& B, int j0) {
+  // first k of this lane's vectors in block-step j (a step past the K range
+  // reads nothing: its x offsets are out of range)
+  auto lane_k = [&](int j) { return klo + (j * KW + kq) * kStepK + 8 * g; };
+  auto load = [&](Ops1& B, int j0) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int j = j0 + u;
-      const int kb = step_k(j) + 16 * g;
-      if constexpr (kStage) {
-        // the block's A_c slice of block-step j: 16 NB rows x 64 KW k, one 16-byte
-        // piece per (thread, q); rows are whole 128 KW-byte runs of global memory
-        const int kj = klo + imin(j, nbs - 1) * kStepK * KW;
+      const int j = j0 + u, kb = lane_k(j);
+      const bool step_ok = j * KW + kq < nst;
 #pragma unroll
-        for (int q = 0; q < NCV; ++q) {
-          const int L = q * kThreads + tid, r = L / (8 * KW), c16 = L % (8 * KW);
-          const int kk = imin(kj + 8 * c16, klast);
-          const E* p = has_c ? atc + atc_off(a, jb, th.c, r, kk) : x + x_off(a, jb, t0, kk);
-          B.ac[u][q] = O::load(p);
-        }
-      } else if constexpr (NB > 0) {
+      for (int h = 0; h < 2; ++h) {
+        const int k = kb + kPiece * h;
+        B.x[u][h] = O::bload(rx, oob_unless(step_ok && k + 8 <= khi, xrow + (uint32_t)(k * ES)));
+      }
+#pragma unroll
+      for (int jj = 0; jj < RUP; ++jj)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          B.u[u][jj][h] = O::load(reinterpret_cast<const E*>(au[jj] + imin(kb + kPiece * h, klast) * ES));
+      if constexpr (!kStage && NB > 0) {
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
           for (int h = 0; h < 2; ++h) {
-            const int kk = imin(kb + 8 * h, klast);
-            const E* p = has_c ? atc + atc_off(a, jb, th.c, 16 * nb + row, kk) : x + x_off(a, jb, t0, kk);
-            B.ac[u][2 * nb + h] = O::load(p);
+            const int k = kb + kPiece * h, r = 16 * nb + row;
+            B.ac[u][2 * nb + h] =
+                O::bload(rac, oob_unless(step_ok && r < a.r_c && k + 8 <= khi, (uint32_t)((r * in + k) * ES)));
           }
       }
-#pragma unroll
-      for (int h = 0; h < 2; ++h) B.x[u][h] = O::load(x + x_off(a, jb, tr.t, imin(kb + 8 * h, klast)));
-#pragma unroll
-      for (int jj = 0; jj < RUP; ++jj)
-#pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int kk = imin(kb + 8 * h, klast);
-          const E* p = tr.res ? reinterpret_cast<const E*>(a.pool + atu_byte(a, jb, tr.u, tr.r, r0 + jj, kk))
-                              : x + x_off(a, jb, t0, kk);
-          B.u[u][jj][h] = O::load(p);
-        }
     }
   };
-  // the staged copy of a batch's A_c slices (rows past r_c and k past the range
-  // are zero)
-  auto stage = [&](const Batch& B, int half, int j0) {
+  // the block's A_c slice of block-step j (16 NB ranks x 64 KW k), one 16-byte
+  // piece per (thread, q); ranks past r_c and k past the range read as zero
+  Vec stg[U][NCV];
+  auto load_stage = [&](int j0) {
     if constexpr (kStage) {
 #pragma unroll
       for (int u = 0; u < U; ++u) {
-        const int kj = klo + imin(j0 + u, nbs - 1) * kStepK * KW;
+        const int kj = klo + (j0 + u) * kStepK * KW;
 #pragma unroll
         for (int q = 0; q < NCV; ++q) {
-          const int L = q * kThreads + tid, r = L / (8 * KW), c16 = L % (8 * KW);
-          const bool ok = r < a.r_c && kj + 8 * c16 + 8 <= khi;
-          *reinterpret_cast<Vec*>(s_a + ((size_t)(half * U + u) * 16 * NB + r) * SR + 8 * c16) = sel(ok, B.ac[u][q]);
+          const int L = q * kThreads + tid, r = L / (8 * KW), k = kj + 8 * (L % (8 * KW));
+          stg[u][q] = O::bload(rac, oob_unless(r < a.r_c && k + 8 <= khi, (uint32_t)((r * in + k) * ES)));
         }
       }
     }
   };
-  auto compute = [&](const Batch& B, int half, int j0) {
+  auto write_stage = [&](int half) {
+    if constexpr (kStage) {
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int q = 0; q < NCV; ++q) {
+          const int L = q * kThreads + tid, r = L / (8 * KW), c16 = L % (8 * KW);
+          *reinterpret_cast<Vec*>(s_a + ((size_t)(half * U + u) * 16 * NB + r) * SR + 8 * c16) = stg[u][q];
+        }
+    }
+  };
+  auto compute = [&](const Ops1& B, int half) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int j = j0 + u, st = j * KW + kq;
-      const int kb = klo + imin(st, nst - 1) * kStepK + 16 * g;
-      Vec xv[2];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) xv[h] = sel(st < nst && kb + 8 * h + 8 <= khi, B.x[u][h]);
       if constexpr (NB > 0) {
         if (has_c) {
 #pragma unroll
@@ -202,74 +208,76 @@ __global__ void __launch_bounds__(kThreads) k_shrink(const ApplyLaunch a) {
               Vec af;
               if constexpr (kStage)
                 af = *reinterpret_cast<const Vec*>(s_a + ((size_t)(half * U + u) * 16 * NB + 16 * nb + row) * SR +
-                                                   kq * kStepK + 16 * g + 8 * h);
+                                                   kq * kStepK + 8 * g + kPiece * h);
               else
                 af = B.ac[u][2 * nb + h];
-              acc[nb] = O::mma(xv[h], af, acc[nb]);
+              acc[nb] = O::mma(B.x[u][h], af, acc[nb]);
             }
         }
       }
       if constexpr (RU <= 2) {
 #pragma unroll
-        for (int jj = 0; jj < RU; ++jj) {
-          const bool live = tr.res && r0 + jj < tr.r;
+        for (int jj = 0; jj < RU; ++jj)
 #pragma unroll
-          for (int h = 0; h < 2; ++h) accu[jj] = O::dot(xv[h], sel(live, B.u[u][jj][h]), accu[jj]);
+          for (int h = 0; h < 2; ++h) accu[jj] = O::dot(B.x[u][h], B.u[u][jj][h], accu[jj]);
+      }
+    }
+  };
+  // wide residual ranks: the step's rows of 8 ranks at a time, read in place
+  // (U is 1 for wide ranks)
+  auto compute_wide = [&](const Ops1& B, int j) {
+    if constexpr (RU > 2) {
+      static_assert(U == 1, "wide residual ranks run one block-step per batch");
+      const int kb = lane_k(j);
+      const int64_t rs = (int64_t)in * ES;
+#pragma unroll
+      for (int j8 = 0; j8 < RU; j8 += 8) {
+        Vec uv[8][2];
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          const char* base = (tr.res && r0 + j8 + jj < tr.r) ? au_wide + (j8 + jj) * rs : a.zeros;
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+            uv[jj][h] = O::load(reinterpret_cast<const E*>(base + imin(kb + kPiece * h, klast) * ES));
         }
-      } else {
-        // wide residual ranks: this step's rows of 8 ranks at a time, loaded together here
 #pragma unroll
-        for (int j8 = 0; j8 < RU; j8 += 8) {
-          Vec uv[8][2];
+        for (int jj = 0; jj < 8; ++jj)
 #pragma unroll
-          for (int jj = 0; jj < 8; ++jj)
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-              const int kk = imin(kb + 8 * h, klast);
-              const E* p = tr.res ? reinterpret_cast<const E*>(a.pool + atu_byte(a, jb, tr.u, tr.r, r0 + j8 + jj, kk))
-                                  : x + x_off(a, jb, t0, kk);
-              uv[jj][h] = O::load(p);
-            }
-#pragma unroll
-          for (int jj = 0; jj < 8; ++jj) {
-            const bool live = tr.res && r0 + j8 + jj < tr.r;
-#pragma unroll
-            for (int h = 0; h < 2; ++h) accu[j8 + jj] = O::dot(xv[h], sel(live, uv[jj][h]), accu[j8 + jj]);
-          }
-        }
+          for (int h = 0; h < 2; ++h) accu[j8 + jj] = O::dot(B.x[0][h], uv[jj][h], accu[j8 + jj]);
       }
     }
   };
 
-  Batch A;
-  if constexpr (sizeof(E) == 4) {
-    // fp32: one register batch, loaded then used (its vectors are twice as wide)
-    for (int j0 = 0; j0 < nbs; j0 += U) {
-      load(A, j0);
-      compute(A, 0, j0);
+  Ops1 A;
+  if constexpr (ES == 4) {
+    // fp32: one set of operands, loaded then used (its vectors are twice as wide)
+    for (int j = 0; j < nbs; ++j) {
+      load(A, j);
+      compute(A, 0);
+      compute_wide(A, j);
     }
   } else {
-  Batch Bb;
-  load(A, 0);
-  if constexpr (kStage) {
-    stage(A, 0, 0);
-    __syncthreads();
-  }
-  for (int j0 = 0; j0 < nbs; j0 += 2 * U) {
-    load(Bb, j0 + U);
-    compute(A, 0, j0);
-    if constexpr (kStage) {
-      stage(Bb, 1, j0 + U);
-      __syncthreads();
+    Ops1 Bb;
+    load_stage(0);
+    load(A, 0);
+    write_stage(0);
+    load_stage(U);
+    if constexpr (kStage) __syncthreads();
+    for (int j = 0; j < nbs; j += 2 * U) {
+      load(Bb, j + U);
+      write_stage(1);
+      load_stage(j + 2 * U);
+      compute(A, 0);
+      compute_wide(A, j);
+      if constexpr (kStage) __syncthreads();
+      if (j + U >= nbs) break;                               // (block-uniform)
+      load(A, j + 2 * U);
+      write_stage(0);
+      load_stage(j + 3 * U);
+      compute(Bb, 1);
+      compute_wide(Bb, j + U);
+      if constexpr (kStage) __syncthreads();
     }
-    if (j0 + U >= nbs) break;                                // (block-uniform)
-    load(A, j0 + 2 * U);
-    compute(Bb, 1, j0 + U);
-    if constexpr (kStage) {
-      stage(A, 0, j0 + 2 * U);
-      __syncthreads();
-    }
-  }
   }
   if constexpr (kStage) __syncthreads();                     // s_red reuses the stages
 
@@ -299,23 +307,25 @@ __global__ void __launch_bounds__(kThreads) k_shrink(const ApplyLaunch a) {
   const int ncent = sc.q == 0 ? a.r_c : 0;
   const int nres = imax(0, imin(RU, a.r_u - r0));
   const int ncols = ncent + nres;
-  for (int idx = tid; idx < th.n * ncols; idx += kThreads) {
-    const int k = idx / ncols, cc = idx - k * ncols;
-    float v = 0.f;
-    int col;
-    if (cc < ncent) {
-      col = cc;
-      if (has_c) {
+  const Rsrc rp = make_rsrc(a.partials + jb.poff, (uint32_t)((int64_t)jb.S * a.T * a.R * 4));
+  for (int k = wave; k < th.n; k += kWaves) {
+    for (int cc = lane; cc < ncols; cc += 64) {
+      float v = 0.f;
+      int col;
+      if (cc < ncent) {
+        col = cc;
+        if (has_c) {
 #pragma unroll
-        for (int w = 0; w < KW; ++w) v += s_red[((size_t)w * M + k) * WC + cc];
+          for (int w = 0; w < KW; ++w) v += s_red[((size_t)w * M + k) * WC + cc];
+        }
+      } else {
+        const int j = cc - ncent;
+        col = a.r_c + r0 + j;
+#pragma unroll
+        for (int w = 0; w < KW; ++w) v += s_red[((size_t)w * M + k) * WC + 16 * NB + j];
       }
-    } else {
-      const int j = cc - ncent;
-      col = a.r_c + r0 + j;
-#pragma unroll
-      for (int w = 0; w < KW; ++w) v += s_red[((size_t)w * M + k) * WC + 16 * NB + j];
+      buf_store_f32(rp, (uint32_t)(part_off(a, jb, sc.s, th.i0 + k, col) - jb.poff) * 4u, v);
     }
-    a.partials[part_off(a, jb, sc.s, th.i0 + k, col)] = v;
   }
 }
 
@@ -326,123 +336,189 @@ __global__ void __launch_bounds__(kThreads) k_shrink(const ApplyLaunch a) {
 // j CW + cq (cq = w / TB) of the block's columns.  Per chunk the centroid part is
 // four 16 x 16 MFMA tiles D[col][token] = Bt_c[col][:] . v_c[token][:]; A-operand
 // row i of tile b4 is column expand_col(col0, i, b4), so that output lane (token
-// = lane & 15, g = lane >> 4) holds the 16 consecutive columns col0 + 16 g + 0..15
-// of its token: y is read and written as 32 contiguous bytes (bf16) per lane.  A
-// staged B_c chunk keeps the columns in that MFMA order (LDS row of column o:
-// 64 (o / 64) + 16 b4 + i), so a fragment read takes 16 consecutive rows.  Loads
-// are unconditional and masked by selects as in the shrink.
+// = lane & 15, g = lane >> 4) holds the columns col0 + 8 g + kPiece h + 0..7, h =
+// 0, 1, of its token: each y load or store instruction covers 64 contiguous bytes
+// (bf16) of every token row.  A staged B_c chunk keeps the columns in that MFMA
+// order (LDS row of column o: 64 (o / 64) + 16 b4 + i), so a fragment read takes
+// 16 consecutive rows.
+// y and B_c go through buffer resources (masked lanes load zeros at kOob, and
+// their stores are dropped), the residual rows through per-lane pointers; the
+// loads are pipelined one block-chunk ahead as in the shrink.
 template <typename E, int M, int NB, int RU>
-__global__ void __launch_bounds__(kThreads) k_expand(const ApplyLaunch a) {
+__device__ __forceinline__ void expand_segment(const ApplyLaunch& a, const ExpandSeg& sg, char* lds) {
   using O = Ops<E>;
   using Vec = typename O::Vec;
-  constexpr bool kBf16 = sizeof(E) == 2;
+  constexpr int ES = sizeof(E);
+  constexpr bool kBf16 = ES == 2;
   constexpr int TB = M / 16, CW = waves_along<M>(), KS = (NB + 1) / 2;
   constexpr bool kStage = staged<E, M, NB>();
-  constexpr int U = batch_len<E, M, NB, RU>();
   constexpr int KSL = KS > 0 ? KS : 1;
   constexpr int SRB = stage_row_b<NB>();                     // elements per staged B_c row (one column)
   constexpr int NCV = kStage ? CW * NB / 2 : 1;              // staged B_c vectors per thread and block-chunk
-  constexpr int NBC = kStage ? NCV : 4 * KSL;                // B_c vectors per lane and chunk
-  constexpr int RUP = RU <= 2 ? RU : 1;                      // residual ranks in the pipelined batch (wider: read in place)
-  extern __shared__ __attribute__((aligned(16))) char lds[];
+  constexpr int NBC = kStage ? 1 : 4 * KSL;                  // per-lane B_c vectors per chunk (unstaged)
+  constexpr int RUP = RU <= 2 ? RU : 0;                      // residual ranks in the pipelined operands
+  constexpr int U = depth<E, M, NB, RU>();
   float* s_v = reinterpret_cast<float*>(lds);                // [M][R] v of the tile
-  E* s_b = reinterpret_cast<E*>(lds + sizeof(float) * (size_t)M * a.R);   // [2][U][64 CW][SRB]
 
-  const int b = blockIdx.x;
-  const Job& jb = a.jobs[job_of_expand(a, b)];
-  const ExpandCoord ec = expand_coord(a, jb, b);
-  const TileHdr th = clamp_tile(a, a.tiles[ec.tau]);
-  if (th.n <= 0) return;
+  const Job& jb = a.jobs[sg.job];
+  const TileHdr th = clamp_tile(a, a.tiles[sg.tau]);
+  if (th.n <= 0) return;                                     // (no tile is empty)
+  const int out = jb.out;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int R = a.R, VW = imin(a.r_c + a.r_u, R);
   const int mb = wave % TB, cq = wave / TB, row = lane & 15, g = lane >> 4;
   const int kt = mb * 16 + row;                              // this lane's token within the tile
   const TokRec tr = clamp_tok(a, a.srt[tile_pos(th, kt)], kt < th.n);
-  const int t0 = clamp_tok(a, a.srt[th.i0], true).t;       // masked loads read this token's y row
   const bool has_c = NB > 0 && th.c >= 0;
-  E* y = reinterpret_cast<E*>(jb.y);
-  const E* btc = reinterpret_cast<const E*>(jb.bt_c);
-  const int clo = c_lo(jb, ec.cb), chi = c_hi(jb, ec.cb), nch = c_chunks(jb, ec.cb);
+  // the segment's columns: block-chunks [j0, j1) of the tile
+  const int clo = imin(out, sg.j0 * jb.cpb), chi = imin(out, sg.j1 * jb.cpb);
+  const int nch = cdiv(chi - clo, kChunkCols);               // 64-column chunks
   const int nbj = cdiv(nch, CW);                             // block-chunks
-  const int clast = imax(clo, chi - 8);
+  const int olast = imax(0, out - 8);
+  // residual ranks past the first chunk (long-tail adapters) are read from s_v
+  // inside the column loop, so the stage then sits after it; otherwise s_v is
+  // dead once v is in registers and the stage takes its place
+  const bool long_tail = RU == kRankChunk && a.r_u > RU;
+  E* s_b = reinterpret_cast<E*>(lds + (long_tail ? sizeof(float) * (size_t)M * R : 0));   // [2][U][64 CW][SRB]
 
-  struct Batch {
-    Vec bc[U][NBC];
+  const Rsrc ry = make_rsrc(jb.y, (uint32_t)((int64_t)a.T * out * ES));
+  const Rsrc rb = make_rsrc(has_c ? static_cast<const char*>(jb.bt_c) + (int64_t)th.c * out * a.r_c * ES : nullptr,
+                            has_c ? (uint32_t)((int64_t)out * a.r_c * ES) : 0u);
+  const uint32_t yrow = tr.tok ? (uint32_t)tr.t * (uint32_t)(out * ES) : kOob;
+  const char* bu[RUP > 0 ? RUP : 1];
+#pragma unroll
+  for (int jj = 0; jj < RUP; ++jj)
+    bu[jj] = (tr.res && jj < tr.r) ? a.pool + bu_byte(a, jb, tr.u, tr.r, jj, 0) : a.zeros;
+  const char* bu_wide = tr.res ? a.pool + bu_byte(a, jb, tr.u, tr.r, 0, 0) : a.zeros;
+
+  // the per-lane operands of a batch: block-chunks j0 .. j0 + U - 1
+  struct Ops1 {
     Vec y[U][2];
-    Vec u[U][RUP][2];
+    Vec u[U][RUP > 0 ? RUP : 1][2];
+    Vec bc[U][NBC];
   };
-  auto chunk_col = [&](int j) { return clo + imin(j * CW + cq, nch - 1) * kChunkCols; };
-  auto load = [&](Batch& B, int j0) {
+  // this lane's first column in block-chunk j
+  auto lane_col = [&](int j) { return clo + (j * CW + cq) * kChunkCols + 8 * g; };
+  auto y_off = [&](int j, int h) {
+    const int col = lane_col(j) + kPiece * h;
+    return oob_unless(j * CW + cq < nch && col + 8 <= chi, yrow + (uint32_t)(col * ES));
+  };
+  auto load = [&](Ops1& B, int j0) {
 #pragma unroll
     for (int u = 0; u < U; ++u) {
-      const int j = j0 + u;
-      const int cl = chunk_col(j) + 16 * g;
-      if constexpr (kStage) {
-        // the block's B_c chunk of block-chunk j: columns [cj, cj + 64 CW), all
-        // r_c ranks of each, contiguous in global memory
-        const int cj = clo + imin(j, nbj - 1) * kChunkCols * CW;
+      const int j = j0 + u, cl = lane_col(j);
 #pragma unroll
-        for (int q = 0; q < NCV; ++q) {
-          const int e = 8 * (q * kThreads + tid);            // element of the chunk
-          const int o = cj + e / imax(a.r_c, 8), rk = e % imax(a.r_c, 8);
-          const E* p = has_c ? btc + btc_off(a, jb, th.c, o, rk) : y + y_off(a, jb, t0, imin(cl, clast));
-          B.bc[u][q] = O::load(p);
-        }
-      } else if constexpr (NB > 0) {
-#pragma unroll
-        for (int b4 = 0; b4 < 4; ++b4)
-#pragma unroll
-          for (int ks = 0; ks < KS; ++ks)
-          {
-            const E* p = has_c ? btc + btc_off(a, jb, th.c, expand_col(chunk_col(j), row, b4), 32 * ks + 8 * g)
-                               : y + y_off(a, jb, t0, imin(cl, clast));
-            B.bc[u][b4 * KS + ks] = O::load(p);
-          }
-      }
-#pragma unroll
-      for (int h = 0; h < 2; ++h) B.y[u][h] = O::load(y + y_off(a, jb, tr.t, imin(cl + 8 * h, clast)));
+      for (int h = 0; h < 2; ++h) B.y[u][h] = O::bload(ry, y_off(j, h));
 #pragma unroll
       for (int jj = 0; jj < RUP; ++jj)
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-          const int cc = imin(cl + 8 * h, clast);
-          const E* p = tr.res ? reinterpret_cast<const E*>(a.pool + bu_byte(a, jb, tr.u, tr.r, jj, cc))
-                              : y + y_off(a, jb, t0, cc);
-          B.u[u][jj][h] = O::load(p);
+        for (int h = 0; h < 2; ++h)
+          B.u[u][jj][h] = O::load(reinterpret_cast<const E*>(bu[jj] + imin(cl + kPiece * h, olast) * ES));
+      if constexpr (!kStage && NB > 0) {
+        const bool chunk_ok = j * CW + cq < nch;
+        const int col0 = clo + (j * CW + cq) * kChunkCols;
+#pragma unroll
+        for (int b4 = 0; b4 < 4; ++b4)
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            const int o = expand_col(col0, row, b4), rk = 32 * ks + 8 * g;
+            B.bc[u][b4 * KS + ks] =
+                O::bload(rb, oob_unless(chunk_ok && o < chi && rk < a.r_c, (uint32_t)((o * a.r_c + rk) * ES)));
+          }
+      }
+    }
+  };
+  // the block's B_c chunk of block-chunk j: columns [cj, cj + 64 CW), all r_c
+  // ranks of each, contiguous in global memory; thread piece q holds the 8
+  // ranks from st_rk[q] of chunk column st_oc[q] (fixed for the block)
+  Vec stg[U][NCV];
+  int st_oc[NCV], st_rk[NCV];
+  if constexpr (kStage) {
+    const int rc8 = imax(a.r_c, 8);
+#pragma unroll
+    for (int q = 0; q < NCV; ++q) {
+      const int e = 8 * (q * kThreads + tid);
+      st_oc[q] = e / rc8;
+      st_rk[q] = e - st_oc[q] * rc8;
+    }
+  }
+  auto load_stage = [&](int j0) {
+    if constexpr (kStage) {
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int cj = clo + (j0 + u) * kChunkCols * CW;
+#pragma unroll
+        for (int q = 0; q < NCV; ++q) {
+          const bool ok = st_oc[q] < kChunkCols * CW && cj + st_oc[q] < chi;
+          stg[u][q] = O::bload(rb, oob_unless(ok, (uint32_t)(((cj + st_oc[q]) * a.r_c + st_rk[q]) * ES)));
         }
+      }
+    }
+  };
+  auto write_stage = [&](int half) {
+    if constexpr (kStage) {
+#pragma unroll
+      for (int q = 0; q < NCV; ++q) {
+        const int oc = st_oc[q];
+        if (oc < kChunkCols * CW) {
+          const int o = oc & 63;
+          const int r = (oc >> 6) * 64 + (2 * (o >> 5) + ((o >> 2) & 1)) * 16 + 4 * ((o >> 3) & 3) + (o & 3);
+#pragma unroll
+          for (int u = 0; u < U; ++u)
+            *reinterpret_cast<Vec*>(s_b + ((size_t)(half * U + u) * 64 * CW + r) * SRB + st_rk[q]) = stg[u][q];
+        }
+      }
     }
   };
 
   // first loads (they need no v), then v of the tile: the K ranges' partials
   // summed in order
-  Batch A;
+  Ops1 A;
+  load_stage(0);
   load(A, 0);
-  for (int idx = tid; idx < M * VW; idx += kThreads) {
-    const int k = idx / VW, col = idx - k * VW;
-    float v = 0.f;
-    if (k < th.n) {
-      const int p = th.i0 + k;
-      int s = 0;
-      for (; s + 4 <= jb.S; s += 4) {
-        const float p0 = a.partials[part_off(a, jb, s, p, col)];
-        const float p1 = a.partials[part_off(a, jb, s + 1, p, col)];
-        const float p2 = a.partials[part_off(a, jb, s + 2, p, col)];
-        const float p3 = a.partials[part_off(a, jb, s + 3, p, col)];
-        v += p0;
-        v += p1;
-        v += p2;
-        v += p3;
+  {
+    // the tile's rows of one K range are contiguous: (n R / 4) float4 from row
+    // i0; per pass, thread t sums float4 q0 + t and q0 + t + kThreads over the
+    // K ranges in order, with four K ranges' loads in flight at a time (rows
+    // past n read zero)
+    const Rsrc rp = make_rsrc(a.partials + jb.poff, (uint32_t)((int64_t)jb.S * a.T * a.R * 4));
+    const uint32_t sstride = (uint32_t)a.T * (uint32_t)R * 4u;
+    const uint32_t tile0 = (uint32_t)th.i0 * (uint32_t)R * 4u;
+    const int n4 = th.n * R / 4, m4 = M * R / 4;
+    constexpr int QMAX = 2;                                  // float4 per thread and pass
+    for (int q0 = tid; q0 < m4; q0 += QMAX * kThreads) {
+      float4 v[QMAX];
+      uint32_t off[QMAX];
+#pragma unroll
+      for (int i = 0; i < QMAX; ++i) {
+        const int q = q0 + i * kThreads;
+        v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        off[i] = oob_unless(q < n4, tile0 + 16u * (uint32_t)q);
       }
-      for (; s < jb.S; ++s) v += a.partials[part_off(a, jb, s, p, col)];
-    }
-    s_v[k * R + col] = v;
-  }
-  if constexpr (kStage) {
-    // the staged rows' rank padding [r_c, 16 NB) reads as zero
-    const int padr = 16 * NB - a.r_c;
-    for (int i = tid; i < 2 * U * 64 * CW * padr; i += kThreads) {
-      const int r = i / padr, k = a.r_c + i % padr;
-      s_b[(size_t)r * SRB + k] = E(0);
+      int sl = 0;
+      for (; sl + 4 <= jb.S; sl += 4) {
+        float4 p[4][QMAX];
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+#pragma unroll
+          for (int i = 0; i < QMAX; ++i) p[d][i] = buf_load_f32x4(rp, off[i] + (uint32_t)(sl + d) * sstride);
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+#pragma unroll
+          for (int i = 0; i < QMAX; ++i) v[i] = f4_add(v[i], p[d][i]);
+      }
+      for (; sl < jb.S; ++sl) {
+        float4 p[QMAX];
+#pragma unroll
+        for (int i = 0; i < QMAX; ++i) p[i] = buf_load_f32x4(rp, off[i] + (uint32_t)sl * sstride);
+#pragma unroll
+        for (int i = 0; i < QMAX; ++i) v[i] = f4_add(v[i], p[i]);
+      }
+#pragma unroll
+      for (int i = 0; i < QMAX; ++i) {
+        const int q = q0 + i * kThreads;
+        if (q < m4) reinterpret_cast<float4*>(s_v)[q] = v[i];
+      }
     }
   }
   __syncthreads();
@@ -454,12 +530,13 @@ __global__ void __launch_bounds__(kThreads) k_expand(const ApplyLaunch a) {
   Vec vhi[KSL], vlo[KSL];
 #pragma unroll
   for (int ks = 0; ks < KS; ++ks) {
-    float f[8];
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const int j = 32 * ks + 8 * g + e;
-      f[e] = (tr.tok && j < a.r_c) ? vrow[j] * gam : 0.f;
+    // (r_c is a multiple of 8: a group of 8 ranks is wholly inside or past it)
+    float4 va = make_float4(0.f, 0.f, 0.f, 0.f), vb = va;
+    if (tr.tok && 32 * ks + 8 * g < a.r_c) {
+      va = reinterpret_cast<const float4*>(vrow + 32 * ks + 8 * g)[0];
+      vb = reinterpret_cast<const float4*>(vrow + 32 * ks + 8 * g)[1];
     }
+    float f[8] = {va.x * gam, va.y * gam, va.z * gam, va.w * gam, vb.x * gam, vb.y * gam, vb.z * gam, vb.w * gam};
     if constexpr (kBf16) {
       uint32_t h[8], l[8];
 #pragma unroll
@@ -478,147 +555,140 @@ __global__ void __launch_bounds__(kThreads) k_expand(const ApplyLaunch a) {
   float vu[RU];
 #pragma unroll
   for (int jj = 0; jj < RU; ++jj) vu[jj] = (tr.res && jj < tr.r) ? vrow[a.r_c + jj] : 0.f;
-
-  auto stage = [&](const Batch& B, int half, int j0) {
-    if constexpr (kStage) {
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int cj = clo + imin(j0 + u, nbj - 1) * kChunkCols * CW;
-#pragma unroll
-        for (int q = 0; q < NCV; ++q) {
-          const int e = 8 * (q * kThreads + tid);
-          const int rc8 = imax(a.r_c, 8);
-          const int oc = e / rc8, rk = e % rc8;              // column of the chunk, first rank
-          if (oc < 64 * CW) {
-            const int o = oc & 63;
-            const int r = (oc >> 6) * 64 + ((o >> 2) & 3) * 16 + (o >> 4) * 4 + (o & 3);
-            const bool ok = cj + oc < chi;
-            *reinterpret_cast<Vec*>(s_b + ((size_t)(half * U + u) * 64 * CW + r) * SRB + rk) = sel(ok, B.bc[u][q]);
-          }
-        }
-      }
-    }
-  };
-  auto compute = [&](const Batch& B, int half, int j0) {
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int j = j0 + u, ch = j * CW + cq;
-      const int cl = chunk_col(j) + 16 * g;
-      bool cv[2];
-#pragma unroll
-      for (int h = 0; h < 2; ++h) cv[h] = ch < nch && tr.tok && cl + 8 * h + 8 <= chi;
-      f32x4 d[4];
-#pragma unroll
-      for (int b4 = 0; b4 < 4; ++b4) d[b4] = f32x4{0.f, 0.f, 0.f, 0.f};
-      if constexpr (NB > 0) {
-        if (has_c) {
-#pragma unroll
-          for (int b4 = 0; b4 < 4; ++b4)
-#pragma unroll
-            for (int ks = 0; ks < KS; ++ks) {
-              Vec bf;
-              if constexpr (kStage)
-                bf = *reinterpret_cast<const Vec*>(s_b + ((size_t)(half * U + u) * 64 * CW + cq * 64 + b4 * 16 + row) *
-                                                       SRB + 32 * ks + 8 * g);
-              else
-                bf = B.bc[u][b4 * KS + ks];
-              d[b4] = O::mma(bf, vhi[ks], d[b4]);
-              if constexpr (kBf16) d[b4] = O::mma(bf, vlo[ks], d[b4]);
-            }
-        }
-      }
-      float yf[16];
-      O::to_f32(B.y[u][0], yf);
-      O::to_f32(B.y[u][1], yf + 8);
-#pragma unroll
-      for (int b4 = 0; b4 < 4; ++b4)
-#pragma unroll
-        for (int e = 0; e < 4; ++e) yf[4 * b4 + e] += d[b4][e];
-      if constexpr (RU <= 2) {
-#pragma unroll
-        for (int jj = 0; jj < RU; ++jj) {
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            float bu[8];
-            O::to_f32(B.u[u][jj][h], bu);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) yf[8 * h + e] = fmaf(vu[jj], bu[e], yf[8 * h + e]);
-          }
-        }
-      } else {
-        // wide residual ranks: this chunk's columns of 8 ranks at a time, loaded together here
-#pragma unroll
-        for (int j8 = 0; j8 < RU; j8 += 8) {
-          Vec bv[8][2];
-#pragma unroll
-          for (int jj = 0; jj < 8; ++jj)
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-              const int cc = imin(cl + 8 * h, clast);
-              const E* p = tr.res ? reinterpret_cast<const E*>(a.pool + bu_byte(a, jb, tr.u, tr.r, j8 + jj, cc))
-                                  : y + y_off(a, jb, t0, cc);
-              bv[jj][h] = O::load(p);
-            }
-#pragma unroll
-          for (int jj = 0; jj < 8; ++jj) {
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-              float bu[8];
-              O::to_f32(bv[jj][h], bu);
-#pragma unroll
-              for (int e = 0; e < 8; ++e) yf[8 * h + e] = fmaf(vu[j8 + jj], bu[e], yf[8 * h + e]);
-            }
-          }
-        }
-      }
-      // residual ranks past the first chunk (long-tail adapters): read here
-      if (RU == kRankChunk && tr.res && tr.r > RU) {
-        for (int rho = RU; rho < tr.r; ++rho) {
-          const float vr = vrow[a.r_c + rho];
-#pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            float bu[8];
-            O::to_f32(O::load(reinterpret_cast<const E*>(a.pool + bu_byte(a, jb, tr.u, tr.r, rho,
-                                                                          imin(cl + 8 * h, clast)))), bu);
-#pragma unroll
-            for (int e = 0; e < 8; ++e) yf[8 * h + e] = fmaf(vr, bu[e], yf[8 * h + e]);
-          }
-        }
-      }
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-        if (cv[h]) O::store(y + y_off(a, jb, tr.t, cl + 8 * h), yf + 8 * h);
-    }
-  };
-
-  if constexpr (sizeof(E) == 4) {
-    compute(A, 0, 0);
-    for (int j0 = U; j0 < nbj; j0 += U) {
-      load(A, j0);
-      compute(A, 0, j0);
-    }
-    return;
-  } else {
-  Batch Bb;
   if constexpr (kStage) {
-    stage(A, 0, 0);
+    __syncthreads();
+    // the staged rows' rank padding [r_c, 16 NB) reads as zero
+    const int padr = 16 * NB - a.r_c;
+    for (int i = tid; i < 2 * U * 64 * CW * padr; i += kThreads) {
+      const int r = i / padr, k = a.r_c + i % padr;
+      s_b[(size_t)r * SRB + k] = E(0);
+    }
+    write_stage(0);
+    load_stage(U);
     __syncthreads();
   }
-  for (int j0 = 0; j0 < nbj; j0 += 2 * U) {
-    load(Bb, j0 + U);
-    compute(A, 0, j0);
-    if constexpr (kStage) {
-      stage(Bb, 1, j0 + U);
-      __syncthreads();
+
+  auto compute1 = [&](const Ops1& B, int half, int u, int j) {
+    const int cl = lane_col(j);
+    f32x4 d[4];
+#pragma unroll
+    for (int b4 = 0; b4 < 4; ++b4) d[b4] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (NB > 0) {
+      if (has_c) {
+#pragma unroll
+        for (int b4 = 0; b4 < 4; ++b4)
+#pragma unroll
+          for (int ks = 0; ks < KS; ++ks) {
+            Vec bf;
+            if constexpr (kStage)
+              bf = *reinterpret_cast<const Vec*>(s_b + ((size_t)(half * U + u) * 64 * CW + cq * 64 + b4 * 16 + row) *
+                                                     SRB + 32 * ks + 8 * g);
+            else
+              bf = B.bc[u][b4 * KS + ks];
+            d[b4] = O::mma(bf, vhi[ks], d[b4]);
+            if constexpr (kBf16) d[b4] = O::mma(bf, vlo[ks], d[b4]);
+          }
+      }
     }
-    if (j0 + U >= nbj) break;                                // (block-uniform)
-    load(A, j0 + 2 * U);
-    compute(Bb, 1, j0 + U);
-    if constexpr (kStage) {
-      stage(A, 0, j0 + 2 * U);
-      __syncthreads();
+    float yf[16];
+    O::to_f32(B.y[u][0], yf);
+    O::to_f32(B.y[u][1], yf + 8);
+#pragma unroll
+    for (int b4 = 0; b4 < 4; ++b4)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) yf[4 * b4 + e] += d[b4][e];
+    if constexpr (RU <= 2) {
+#pragma unroll
+      for (int jj = 0; jj < RU; ++jj)
+#pragma unroll
+        for (int h = 0; h < 2; ++h) {
+          float b[8];
+          O::to_f32(B.u[u][jj][h], b);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) yf[8 * h + e] = fmaf(vu[jj], b[e], yf[8 * h + e]);
+        }
+    } else {
+      // wide residual ranks: this chunk's columns of 8 ranks at a time, read in place
+      const int64_t rs = (int64_t)out * ES;
+#pragma unroll
+      for (int j8 = 0; j8 < RU; j8 += 8) {
+        Vec bv[8][2];
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          const char* base = (tr.res && j8 + jj < tr.r) ? bu_wide + (j8 + jj) * rs : a.zeros;
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+            bv[jj][h] = O::load(reinterpret_cast<const E*>(base + imin(cl + kPiece * h, olast) * ES));
+        }
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj)
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            float b[8];
+            O::to_f32(bv[jj][h], b);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) yf[8 * h + e] = fmaf(vu[j8 + jj], b[e], yf[8 * h + e]);
+          }
+      }
+      if (long_tail && tr.res && tr.r > RU) {
+        for (int rho = RU; rho < tr.r; ++rho) {
+          const float vr = vrow[a.r_c + rho];
+          const char* base = bu_wide + rho * rs;
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            float b[8];
+            O::to_f32(O::load(reinterpret_cast<const E*>(base + imin(cl + kPiece * h, olast) * ES)), b);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) yf[8 * h + e] = fmaf(vr, b[e], yf[8 * h + e]);
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < 2; ++h) O::bstore(ry, y_off(j, h), yf + 8 * h);
+  };
+  auto compute = [&](const Ops1& B, int half, int j0) {
+#pragma unroll
+    for (int u = 0; u < U; ++u) compute1(B, half, u, j0 + u);
+  };
+
+  if constexpr (ES == 4) {
+    compute(A, 0, 0);
+    for (int j = U; j < nbj; j += U) {
+      load(A, j);
+      compute(A, 0, j);
+    }
+  } else {
+    Ops1 Bb;
+    for (int j = 0; j < nbj; j += 2 * U) {
+      load(Bb, j + U);
+      write_stage(1);
+      load_stage(j + 2 * U);
+      compute(A, 0, j);
+      if constexpr (kStage) __syncthreads();
+      if (j + U >= nbj) break;                               // (block-uniform)
+      load(A, j + 2 * U);
+      write_stage(0);
+      load_stage(j + 3 * U);
+      compute(Bb, 1, j + U);
+      if constexpr (kStage) __syncthreads();
     }
   }
+}
+
+// One round of blocks; block b walks its contiguous share of the launch's work
+// items segment by segment (a segment: the block-chunks of one tile).  Every
+// segment starts behind a block barrier, so its LDS writes never meet the
+// previous segment's reads.
+template <typename E, int M, int NB, int RU>
+__global__ void __launch_bounds__(kThreads) k_expand(const ApplyLaunch a) {
+  extern __shared__ __attribute__((aligned(16))) char lds[];
+  const int end = expand_begin(a, blockIdx.x + 1, gridDim.x);
+  for (int pos = expand_begin(a, blockIdx.x, gridDim.x); pos < end;) {
+    const ExpandSeg sg = expand_seg(a, pos, end);
+    __syncthreads();
+    expand_segment<E, M, NB, RU>(a, sg, lds);
+    pos += sg.j1 - sg.j0;                                    // (>= 1)
   }
 }
 
@@ -635,22 +705,43 @@ void launch_k(K kernel, int blocks, size_t lds, hipStream_t s, const ApplyLaunch
 template <typename E, int M, int NB, int RU>
 size_t shrink_lds() {
   const size_t red = sizeof(float) * (size_t)waves_along<M>() * M * shrink_wc<NB, RU>();
-  const size_t stg = staged<E, M, NB>() ? sizeof(E) * 2 * batch_len<E, M, NB, RU>() * 16 * NB * stage_row_a<M>() : 0;
+  const size_t stg = staged<E, M, NB>() ? sizeof(E) * 2 * depth<E, M, NB, RU>() * 16 * NB * stage_row_a<M>() : 0;
   return red > stg ? red : stg;
 }
 template <typename E, int M, int NB, int RU>
-size_t expand_lds(int R) {
-  const size_t stg = staged<E, M, NB>() ? sizeof(E) * 2 * batch_len<E, M, NB, RU>() * 64 * waves_along<M>() *
-                                              stage_row_b<NB>()
-                                        : 0;
-  return sizeof(float) * (size_t)M * R + stg;
+size_t expand_lds(int R, int r_u) {
+  const size_t stg =
+      staged<E, M, NB>() ? sizeof(E) * 2 * depth<E, M, NB, RU>() * 64 * waves_along<M>() * stage_row_b<NB>() : 0;
+  const size_t sv = sizeof(float) * (size_t)M * R;
+  // the stage takes the place of v unless long-tail ranks read v in the column loop
+  return (RU == kRankChunk && r_u > RU) ? sv + stg : std::max(sv, stg);
+}
+
+// Blocks of `kernel` with `lds` bytes of LDS that one compute unit holds at once
+// (cached per kernel for the last LDS size asked).
+template <typename K>
+int resident_blocks(K kernel, size_t lds) {
+  static std::atomic<uint64_t> cache{0};                     // (lds << 32) | blocks
+  const uint64_t c = cache.load(std::memory_order_relaxed);
+  if (c != 0 && (c >> 32) == (uint64_t)lds) return (int)(c & 0xffffffffu);
+  int n = 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(kernel), kThreads, lds) !=
+          hipSuccess ||
+      n < 1) {
+    (void)hipGetLastError();
+    n = 1;
+  }
+  cache.store(((uint64_t)lds << 32) | (uint32_t)n, std::memory_order_relaxed);
+  return n;
 }
 
 template <typename E, int M, int NB, int RU>
 hipError_t launch_mnr(const ApplyLaunch& a, hipStream_t s, hipEvent_t* ev) {
   launch_k(k_shrink<E, M, NB, RU>, a.shrink_blocks, shrink_lds<E, M, NB, RU>(), s, a, ev ? ev[0] : nullptr,
            ev ? ev[1] : nullptr);
-  launch_k(k_expand<E, M, NB, RU>, a.expand_blocks, expand_lds<E, M, NB, RU>(a.R), s, a, ev ? ev[2] : nullptr,
+  const size_t lds = expand_lds<E, M, NB, RU>(a.R, a.r_u);
+  const int round = resident_blocks(k_expand<E, M, NB, RU>, lds) * std::max(1, a.n_cu);
+  launch_k(k_expand<E, M, NB, RU>, std::min(a.expand_items, round), lds, s, a, ev ? ev[2] : nullptr,
            ev ? ev[3] : nullptr);
   return hipGetLastError();
 }
@@ -676,7 +767,7 @@ hipError_t launch_m(const ApplyLaunch& a, hipStream_t s, hipEvent_t* ev) {
 
 hipError_t launch_apply(const ApplyLaunch& a, hipStream_t s, hipEvent_t* ev) {
   if (a.T <= 0 || a.n_tiles <= 0 || a.n_jobs <= 0) return hipSuccess;
-  if (a.n_jobs > kMaxJobs || a.shrink_blocks <= 0 || a.expand_blocks <= 0 || a.r_c > kMaxRc || a.r_u > kMaxRu)
+  if (a.n_jobs > kMaxJobs || a.shrink_blocks <= 0 || a.expand_items <= 0 || a.r_c > kMaxRc || a.r_u > kMaxRu)
     return hipErrorInvalidValue;
   if (a.esize == 4) {
     if (a.M != 16) return hipErrorInvalidValue;
@@ -704,9 +795,10 @@ hipError_t kernels_init(int device) {
   hipError_t e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, device);
   if (e != hipSuccess) return e;
   const int R = padded_rank(kMaxRc, kMaxRu);
-  const size_t need_expand = std::max({expand_lds<uint16_t, 64, 8, kRankChunk>(R), expand_lds<uint16_t, 32, 8, kRankChunk>(R),
-                                       expand_lds<uint16_t, 64, 4, 2>(padded_rank(64, 2)),
-                                       expand_lds<uint16_t, 32, 4, 2>(padded_rank(64, 2))});
+  const size_t need_expand = std::max({expand_lds<uint16_t, 64, 8, kRankChunk>(R, kMaxRu),
+                                       expand_lds<uint16_t, 32, 8, kRankChunk>(R, kMaxRu),
+                                       expand_lds<uint16_t, 64, 4, 2>(padded_rank(64, 2), 2),
+                                       expand_lds<uint16_t, 32, 4, 2>(padded_rank(64, 2), 2)});
   const size_t need_shrink = std::max({shrink_lds<uint16_t, 64, 8, kRankChunk>(), shrink_lds<uint16_t, 32, 8, kRankChunk>(),
                                        shrink_lds<uint16_t, 64, 4, 2>(), shrink_lds<uint16_t, 32, 4, 2>()});
   const size_t need_plan = sizeof(uint64_t) * kSortChunk + 256;

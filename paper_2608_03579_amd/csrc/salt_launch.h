@@ -54,7 +54,7 @@ inline void cut_tiles(const std::vector<int>& per_c, int M, std::vector<int4>& t
 // Largest number of tiles a batch of T tokens over C centroids can cut into.
 inline int max_tiles(int T, int C) { return cdiv(T, 16) + C + 1; }
 
-// K ranges, column blocks and block offsets of launch `a`, whose jobs (in,
+// K ranges, expand block-chunks and work offsets of launch `a`, whose jobs (in,
 // out, prefix, pointers) and batch fields (T, M, n_tiles, C, r_c, r_u, nq, R,
 // esize, partial_cap) are set.  n_groups_c: centroids the batch references;
 // sum_rank: residual ranks summed over the slots it references (both for the
@@ -65,11 +65,8 @@ inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t s
   const int target = 8 * std::max(1, n_cu);        // blocks per launch: a few rounds of the whole device
   const double es = (double)a.esize;
   const double adapters = (double)n_groups_c * a.r_c + (double)sum_rank;
-  int64_t sum_in = 0, sum_out = 0;
-  for (int j = 0; j < a.n_jobs; ++j) {
-    sum_in += a.jobs[j].in;
-    sum_out += a.jobs[j].out;
-  }
+  int64_t sum_in = 0;
+  for (int j = 0; j < a.n_jobs; ++j) sum_in += a.jobs[j].in;
   // shrink: one K-range length for the whole launch, so that blocks of every
   // table carry about the same work, sized for ~target blocks; each table's
   // split is capped so that its partials (written, then read) stay within a
@@ -87,13 +84,19 @@ inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t s
     const int s_max = cdiv(jb.in, gran);
     S[j] = std::max(1, std::min({s_balance, s_traffic, s_max}));
   }
-  // partials must fit: shrink the largest split until they do
+  // partials must fit, and each table's region stays below kMaxBufferBytes:
+  // shrink the largest split until they do
   auto total = [&]() {
     int64_t t = 0;
     for (int j = 0; j < a.n_jobs; ++j) t += (int64_t)S[j] * a.T * a.R;
     return t;
   };
-  while (total() > a.partial_cap) {
+  auto too_big = [&]() {
+    for (int j = 0; j < a.n_jobs; ++j)
+      if ((int64_t)S[j] * a.T * a.R * 4 >= kMaxBufferBytes) return true;
+    return false;
+  };
+  while (total() > a.partial_cap || too_big()) {
     int jm = 0;
     for (int j = 1; j < a.n_jobs; ++j)
       if (S[j] > S[jm]) jm = j;
@@ -108,17 +111,9 @@ inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t s
     jb.S = cdiv(jb.in, jb.Kc);
     jb.poff = poff;
     poff += (int64_t)jb.S * a.T * a.R;
-    // expand: column blocks in proportion to out for ~target blocks; each
-    // block first reads its tile's partials (from L2), which should not pass
-    // the block's own bytes
-    const double e_bytes = es * (2.0 * a.T * jb.out + adapters * jb.out);
-    const double reread = 4.0 * jb.S * a.T * a.R;
-    const int n_blocks = (int)std::lround((double)target * jb.out / ((double)sum_out * a.n_tiles));
-    const int n_traffic = std::max(1, (int)(e_bytes / reread));
-    const int n_max = cdiv(jb.out, kChunkCols * CW);
-    const int n_col = std::max(1, std::min({n_blocks, n_traffic, n_max}));
-    const int cgran = kChunkCols * CW;
-    jb.cpb = cdiv(cdiv(jb.out, n_col), cgran) * cgran;
+    // expand: work items of one block-chunk (kChunkCols per wave along the
+    // columns); the launch splits them evenly over one round of blocks
+    jb.cpb = kChunkCols * CW;
     jb.n_col = cdiv(jb.out, jb.cpb);
     jb.shrink_base = sb;
     jb.expand_base = eb;
@@ -126,7 +121,7 @@ inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t s
     eb += a.n_tiles * jb.n_col;
   }
   a.shrink_blocks = sb;
-  a.expand_blocks = eb;
+  a.expand_items = eb;
   return true;
 }
 

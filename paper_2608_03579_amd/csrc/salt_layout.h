@@ -38,6 +38,7 @@ constexpr int kMaxRu = 72;           // largest residual rank (long-tail concate
 constexpr int kMaxC = 64;            // largest centroid library
 constexpr int kMaxTokens = 65536;    // largest batch of one plan
 constexpr int kSortChunk = 4096;     // keys one plan block sorts in LDS
+constexpr int64_t kMaxBufferBytes = (int64_t)1 << 31;   // bound of every buffer an apply kernel addresses with 32-bit offsets
 
 SALT_HD int imin(int a, int b) { return a < b ? a : b; }
 SALT_HD int imax(int a, int b) { return a > b ? a : b; }
@@ -67,10 +68,10 @@ struct Job {
   int32_t in, out;
   int32_t S;               // K ranges of the shrink
   int32_t Kc;              // length of one K range (a multiple of kStepK)
-  int32_t cpb;             // output columns of one expand block (a multiple of kChunkCols)
-  int32_t n_col;           // expand blocks per tile
+  int32_t cpb;             // output columns of one expand block-chunk (kChunkCols x the waves along the columns)
+  int32_t n_col;           // expand block-chunks per tile: cdiv(out, cpb)
   int32_t shrink_base;     // first shrink block of this job
-  int32_t expand_base;     // first expand block of this job
+  int32_t expand_base;     // first expand work item of this job
 };
 
 struct ApplyLaunch {
@@ -79,6 +80,7 @@ struct ApplyLaunch {
   const int4* srt;         // [T] token records in sorted order
   const char* pool;        // residual slot pool
   float* partials;         // split-K partial sums
+  const char* zeros;       // zero page: >= max(in, out) * esize bytes of zeros (read in place of missing residual rows)
   int64_t slot_stride;     // bytes between slots
   int64_t partial_cap;     // floats of `partials`
   int32_t n_jobs;
@@ -92,7 +94,8 @@ struct ApplyLaunch {
   int32_t R;               // partial row stride, padded_rank(r_c, r_u)
   int32_t esize;           // bytes per element (2: bf16, 4: fp32)
   int32_t shrink_blocks;
-  int32_t expand_blocks;
+  int32_t expand_items;    // expand work items: sum over jobs of n_tiles x n_col
+  int32_t n_cu;            // compute units of the device (sizes the expand grid)
 };
 
 struct TileHdr {
@@ -141,31 +144,45 @@ SALT_HD int job_of_expand(const ApplyLaunch& a, int b) {
   return j;
 }
 
-// Shrink block b of job j: tile tau, K range s, residual rank chunk q.
+// Shrink item i of job j: tile tau, K range s, residual rank chunk q
+// (items of a job: (q, s, tau) with tau fastest).
 struct ShrinkCoord {
   int tau, s, q;
 };
-SALT_HD ShrinkCoord shrink_coord(const ApplyLaunch& a, const Job& jb, int b) {
-  const int local = b - jb.shrink_base;
-  const int per_tile = jb.S * a.nq;
+SALT_HD ShrinkCoord shrink_coord(const ApplyLaunch& a, const Job& jb, int item) {
+  const int local = item - jb.shrink_base;
   ShrinkCoord c;
-  c.tau = iclamp(local / per_tile, 0, a.n_tiles - 1);
-  const int rem = local - (local / per_tile) * per_tile;
-  c.q = rem / jb.S;
-  c.s = rem - c.q * jb.S;
+  c.tau = local % a.n_tiles;
+  const int rest = local / a.n_tiles;
+  c.s = rest % jb.S;
+  c.q = iclamp(rest / jb.S, 0, a.nq - 1);
   return c;
 }
 
-// Expand block b of job j: tile tau, column block cb.
-struct ExpandCoord {
-  int tau, cb;
+// Expand work items: (job, tile, block-chunk), job-major, then tile, block-chunk
+// fastest; block-chunk bc of a job covers columns [bc cpb, min(out, (bc + 1)
+// cpb)).  A launch of G blocks gives block b the contiguous items [b N / G,
+// (b + 1) N / G), N = expand_items, so every block carries the same number of
+// block-chunks (to within one) and walks them tile by tile, reading a tile's v
+// once per visit.
+SALT_HD int expand_begin(const ApplyLaunch& a, int b, int G) {
+  return (int)((int64_t)iclamp(b, 0, G) * a.expand_items / imax(G, 1));
+}
+// Block-chunks [j0, j1) of tile tau of job `job`: the run of items that starts at
+// item pos and ends at the tile's last block-chunk or at item end, whichever
+// comes first (pos < end).
+struct ExpandSeg {
+  int job, tau, j0, j1;
 };
-SALT_HD ExpandCoord expand_coord(const ApplyLaunch& a, const Job& jb, int b) {
-  const int local = b - jb.expand_base;
-  ExpandCoord c;
-  c.tau = iclamp(local / jb.n_col, 0, a.n_tiles - 1);
-  c.cb = local - (local / jb.n_col) * jb.n_col;
-  return c;
+SALT_HD ExpandSeg expand_seg(const ApplyLaunch& a, int pos, int end) {
+  ExpandSeg sg;
+  sg.job = job_of_expand(a, pos);
+  const Job& jb = a.jobs[sg.job];
+  const int local = imax(0, pos - jb.expand_base), nc = imax(jb.n_col, 1);
+  sg.tau = iclamp(local / nc, 0, a.n_tiles - 1);
+  sg.j0 = local - (local / nc) * nc;
+  sg.j1 = imin(nc, sg.j0 + imax(1, end - pos));
+  return sg;
 }
 
 // ---- element offsets (in elements of the context dtype unless stated) --------------
@@ -212,15 +229,17 @@ SALT_HD int k_lo(const Job& jb, int s) { return imin(jb.in, s * jb.Kc); }
 SALT_HD int k_hi(const Job& jb, int s) { return imin(jb.in, (s + 1) * jb.Kc); }
 SALT_HD int k_steps(const Job& jb, int s) { return cdiv(k_hi(jb, s) - k_lo(jb, s), kStepK); }
 
-// Column block cb of a job: [c_lo, c_hi), in kChunkCols-wide chunks shared by
-// the cw waves along the columns.
-SALT_HD int c_lo(const Job& jb, int cb) { return imin(jb.out, cb * jb.cpb); }
-SALT_HD int c_hi(const Job& jb, int cb) { return imin(jb.out, (cb + 1) * jb.cpb); }
-SALT_HD int c_chunks(const Job& jb, int cb) { return cdiv(c_hi(jb, cb) - c_lo(jb, cb), kChunkCols); }
+// Elements between the two 8-element vectors a lane holds of a 64-wide shrink
+// step or expand chunk: lane group g holds g 8 + 0..7 and kPiece + g 8 + 0..7,
+// so that the four groups' vector h covers 32 contiguous elements.
+constexpr int kPiece = 32;
 
 // Output column of expand A-operand row i (lane & 15) in column block b4 of a
 // 64-column chunk starting at col0: arranged so that MFMA output lane (token,
-// g) holds the 16 consecutive columns col0 + 16 g + 0..15.
-SALT_HD int expand_col(int col0, int i, int b4) { return col0 + (i >> 2) * 16 + b4 * 4 + (i & 3); }
+// g), which receives rows 4 g + e of tile b4, holds columns col0 + 8 g + kPiece h
+// + 4 (b4 & 1) + e with h = b4 >> 1, i.e. the vectors col0 + 8 g + kPiece h + 0..7.
+SALT_HD int expand_col(int col0, int i, int b4) {
+  return col0 + kPiece * (b4 >> 1) + 8 * (i >> 2) + 4 * (b4 & 1) + (i & 3);
+}
 
 }  // namespace salt

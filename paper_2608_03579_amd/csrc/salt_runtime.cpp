@@ -124,6 +124,7 @@ struct salt_ctx {
   std::vector<uint8_t> table_ready;      // per table: every centroid pinned
   char* pool = nullptr;
   size_t slot_stride = 0;
+  char* zeros = nullptr;                 // zero page of max(in, out) * esize bytes, never written after set-up
   hipStream_t side = nullptr;
   // bookkeeping
   std::vector<int32_t> slot_rank;        // -1 = never loaded
@@ -265,6 +266,7 @@ void destroy_ctx_memory(salt_ctx* c) {
   for (char* p : c->cent_b)
     if (p) (void)hipFree(p);
   if (c->pool) (void)hipFree(c->pool);
+  if (c->zeros) (void)hipFree(c->zeros);
   for (hipEvent_t e : c->readers.ev)
     if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : c->loaders.ev)
@@ -454,6 +456,7 @@ salt_status apply_impl(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_pla
     a.srt = plan->srt;
     a.pool = ctx->pool;
     a.partials = plan->partials;
+    a.zeros = ctx->zeros;
     a.slot_stride = (int64_t)ctx->slot_stride;
     a.partial_cap = (int64_t)plan->partial_cap;
     a.n_jobs = nj;
@@ -467,6 +470,7 @@ salt_status apply_impl(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_pla
     a.nq = std::max(1, salt::cdiv(plan->ru_max, salt::kRankChunk));
     a.R = salt::padded_rank(a.r_c, a.r_u);
     a.esize = (int32_t)ctx->esize;
+    a.n_cu = ctx->n_cu;
     for (int j = 0; j < nj; ++j) {
       const int t = tables[first + j];
       const salt_shape sh = ctx->tables[t];
@@ -645,6 +649,12 @@ salt_status salt_create(const salt_config* cfg, salt_ctx** out) {
     if (s.in_dim <= 0 || s.out_dim <= 0 || s.in_dim % 8 || s.out_dim % 8 || s.in_dim > (1 << 20) ||
         s.out_dim > (1 << 20))
       return SALT_ERR_INVALID_ARG;
+    // x and y of a full batch are each addressed with 32-bit byte offsets
+    const int64_t esz = cfg->dtype == SALT_F32 ? 4 : 2;
+    if ((int64_t)cfg->max_tokens * std::max(s.in_dim, s.out_dim) * esz >= salt::kMaxBufferBytes) {
+      g_create_err = "max_tokens x max(in_dim, out_dim) x element size must stay below 2 GiB";
+      return SALT_ERR_OUT_OF_RANGE;
+    }
   }
   salt_ctx* c = new (std::nothrow) salt_ctx();
   if (!c) return SALT_ERR_OUT_OF_MEMORY;
@@ -689,6 +699,16 @@ salt_status salt_create(const salt_config* cfg, salt_ctx** out) {
       }
     }
   }
+  size_t max_dim = 8;
+  for (const salt_shape& s : c->tables) max_dim = std::max<size_t>(max_dim, std::max(s.in_dim, s.out_dim));
+  const size_t zero_bytes = round_up(max_dim * c->esize, kAlign);
+  if (hipMalloc((void**)&c->zeros, zero_bytes) != hipSuccess) {
+    (void)hipGetLastError();
+    return bail(SALT_ERR_OUT_OF_MEMORY, hipSuccess, "");
+  }
+  e = hipMemset(c->zeros, 0, zero_bytes);
+  if (e == hipSuccess) e = hipDeviceSynchronize();
+  if (e != hipSuccess) return bail(SALT_ERR_HIP, e, "zero page");
   c->slot_stride = round_up(std::max<size_t>(1, salt_residual_bytes(c, cfg->r_u_max)), kAlign);
   if (hipMalloc((void**)&c->pool, c->slot_stride * (size_t)cfg->n_slots) != hipSuccess) {
     (void)hipGetLastError();

@@ -59,14 +59,20 @@ def build() -> str:
         with open(os.path.join(src, n), "w") as f:
             f.write(text)
     srcs = [os.path.join(src, n) for n in SOURCES] + [os.path.join(SHIM, "harness.cpp")]
-    cmd = [CLANG, "-std=c++17", "-O1", "-g", "-fsanitize=address", "-fno-omit-frame-pointer", "-w",
-           f"-I{SHIM}", f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}", "-x", "c++", *srcs, "-o", exe + ".tmp"]
+    flags = ["-std=c++17", "-O1", "-g", "-fsanitize=address", "-fno-omit-frame-pointer", "-w"]
     for old in os.listdir(BUILD):
         if old.startswith("harness-"):
             os.remove(os.path.join(BUILD, old))
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        raise RuntimeError("host build of libsalt failed:\n" + res.stderr[-6000:])
+    # one compiler process per source, then one link
+    objs = [os.path.join(src, os.path.basename(s) + ".o") for s in srcs]
+    procs = [subprocess.Popen([CLANG, *flags, f"-I{SHIM}", f"-I{os.path.join(ROOT, 'include')}", f"-I{CSRC}",
+                               "-x", "c++", "-c", s, "-o", o], stdout=subprocess.PIPE, stderr=subprocess.PIPE,
+                              text=True) for s, o in zip(srcs, objs)]
+    errs = [(p.communicate()[1], p.returncode) for p in procs]
+    res = subprocess.run([CLANG, *flags, *objs, "-o", exe + ".tmp"], capture_output=True, text=True)
+    if any(rc for _, rc in errs) or res.returncode != 0:
+        msg = "".join(e for e, rc in errs if rc) + res.stderr
+        raise RuntimeError("host build of libsalt failed:\n" + msg[-6000:])
     os.replace(exe + ".tmp", exe)
     return exe
 

@@ -404,6 +404,49 @@ inline float salt_cpu_fdot2_bf16(salt_cpu_bf16x2 a, salt_cpu_bf16x2 b, float c, 
   return (float)((double)c + (double)(float)a[0] * (double)(float)b[0] + (double)(float)a[1] * (double)(float)b[1]);
 }
 
+// ---- raw buffer resources ------------------------------------------------------------
+// (base, size in bytes); an access at an offset >= size reads zero and a store
+// there is dropped, as the hardware range check does.  An access that starts
+// inside the buffer but ends past it is a kernel bug here (the kernels never
+// make one) and aborts the run.
+struct salt_cpu_rsrc {
+  const char* base;
+  uint32_t n;
+};
+typedef unsigned int salt_cpu_u32x4 __attribute__((ext_vector_type(4)));
+inline salt_cpu_rsrc salt_cpu_make_rsrc(void* p, short, int n, int) { return salt_cpu_rsrc{(const char*)p, (uint32_t)n}; }
+inline bool salt_cpu_buf_in(salt_cpu_rsrc r, int off, int soff, uint32_t size) {
+  const uint32_t o = (uint32_t)off + (uint32_t)soff;
+  if (o >= r.n) return false;
+  if (o + size > r.n || o + size < o) {
+    fprintf(stderr, "buffer access [%u, %u) straddles the end of a %u-byte buffer\n", o, o + size, r.n);
+    abort();
+  }
+  return true;
+}
+inline salt_cpu_u32x4 salt_cpu_buf_load_b128(salt_cpu_rsrc r, int off, int soff, int) {
+  salt_cpu_u32x4 v = {0u, 0u, 0u, 0u};
+  if (salt_cpu_buf_in(r, off, soff, 16)) memcpy(&v, r.base + (uint32_t)off + (uint32_t)soff, 16);
+  return v;
+}
+inline unsigned salt_cpu_buf_load_b32(salt_cpu_rsrc r, int off, int soff, int) {
+  unsigned v = 0u;
+  if (salt_cpu_buf_in(r, off, soff, 4)) memcpy(&v, r.base + (uint32_t)off + (uint32_t)soff, 4);
+  return v;
+}
+inline void salt_cpu_buf_store_b128(salt_cpu_u32x4 v, salt_cpu_rsrc r, int off, int soff, int) {
+  if (salt_cpu_buf_in(r, off, soff, 16)) memcpy(const_cast<char*>(r.base) + (uint32_t)off + (uint32_t)soff, &v, 16);
+}
+inline void salt_cpu_buf_store_b32(unsigned v, salt_cpu_rsrc r, int off, int soff, int) {
+  if (salt_cpu_buf_in(r, off, soff, 4)) memcpy(const_cast<char*>(r.base) + (uint32_t)off + (uint32_t)soff, &v, 4);
+}
+#define __amdgpu_buffer_rsrc_t salt_cpu_rsrc
+#define __builtin_amdgcn_make_buffer_rsrc salt_cpu_make_rsrc
+#define __builtin_amdgcn_raw_buffer_load_b128 salt_cpu_buf_load_b128
+#define __builtin_amdgcn_raw_buffer_load_b32 salt_cpu_buf_load_b32
+#define __builtin_amdgcn_raw_buffer_store_b128 salt_cpu_buf_store_b128
+#define __builtin_amdgcn_raw_buffer_store_b32 salt_cpu_buf_store_b32
+
 #define __builtin_amdgcn_mfma_f32_16x16x32_bf16 salt_cpu_mfma_bf16
 #define __builtin_amdgcn_mfma_f32_16x16x4f32 salt_cpu_mfma_f32
 #define __builtin_amdgcn_fdot2_f32_bf16 salt_cpu_fdot2_bf16
@@ -413,6 +456,11 @@ inline hipError_t hipGetLastError() { return hipSuccess; }
 inline const char* hipGetErrorString(hipError_t e) { return e == hipSuccess ? "no error" : "cpu runtime error"; }
 inline hipError_t hipSetDevice(int d) { return d == 0 ? hipSuccess : hipErrorInvalidDevice; }
 inline hipError_t hipDeviceSynchronize() { return hipSuccess; }
+template <typename F>
+inline hipError_t hipOccupancyMaxActiveBlocksPerMultiprocessor(int* n, F, int, size_t) {
+  *n = 2;
+  return hipSuccess;
+}
 inline hipError_t hipDeviceGetAttribute(int* v, hipDeviceAttribute_t a, int) {
   *v = a == hipDeviceAttributeMultiprocessorCount ? salt_cpu::g_n_cu : 160 * 1024;
   return hipSuccess;
