@@ -226,6 +226,26 @@ SALT_API salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, c
 SALT_API salt_status salt_apply_batch(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_plan* plan,
                                       const void* const* xs, void* const* ys, void* stream);
 
+/* salt_apply_batch for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * same arguments and kernels, but the launches keep their split-K partial sums
+ * in a static device array of the library (64 MiB per device, set up by
+ * salt_create) instead of the plan's buffer, whose capacity still bounds the
+ * K split.  The call allocates nothing and calls no allocating routine.
+ * Whenever the plan's partial capacity (two K ranges per token row of a
+ * 16-table launch; max_tokens x padded(r_c + r_u) <= 512 Ki) fits the array,
+ * the launches are exactly those of salt_apply_batch and y is bit-identical;
+ * beyond that a launch may split K more coarsely (same accuracy bound).  The
+ * array is shared by every salt_apply_batch_noalloc on the device: calls whose
+ * work overlaps in time (on different streams) race on it and give wrong y;
+ * calls on one stream are ordered and safe.  Every partial a launch reads was
+ * written by that launch, so nothing needs clearing.  SALT_ERR_OUT_OF_RANGE
+ * (nothing enqueued) if a launch's partials cannot fit even with one K range
+ * per table: T x padded(r_c + r_u) floats per table of the launch must total
+ * at most 16 Mi. */
+SALT_API salt_status salt_apply_batch_noalloc(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_plan* plan,
+                                              const void* const* xs, void* const* ys, void* stream);
+
 /* salt_apply_batch for measurement (n <= 16: one launch): events[0] and
  * events[1] (hipEvent_t, timing enabled) record the start and end of the
  * shrink kernel, events[2] and events[3] those of the expand kernel

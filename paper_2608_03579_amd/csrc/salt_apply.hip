@@ -27,6 +27,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <mutex>
 
 #include "salt_device.h"
 #include "salt_internal.h"
@@ -785,12 +786,25 @@ hipError_t launch_apply(const ApplyLaunch& a, hipStream_t s, hipEvent_t* ev) {
 
 namespace salt {
 
+// Device scratch of salt_apply_batch_noalloc: the split-K partial sums of its
+// launches.  Each device that runs the library holds its own copy until the
+// process ends; its device address is resolved once per device, in
+// kernels_init, and only that address is ever handed to a kernel.
+static __device__ __align__(256) float scratch[kScratchFloats];
+
+namespace {
+std::mutex g_init_mu;
+bool g_init_done[kMaxDevices] = {};
+float* g_scratch[kMaxDevices] = {};
+}  // namespace
+
 // Per-device set-up: checks that a workgroup may hold the LDS the apply and
-// plan kernels ask for (the expand of 64-token tiles at the largest ranks).
+// plan kernels ask for (the expand of 64-token tiles at the largest ranks), and
+// resolves this device's copy of the scratch array.  Call with `device` current.
 hipError_t kernels_init(int device) {
-  static bool done[64] = {};
-  if (device < 0 || device >= 64) return hipErrorInvalidDevice;
-  if (done[device]) return hipSuccess;
+  if (device < 0 || device >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> g(g_init_mu);
+  if (g_init_done[device]) return hipSuccess;
   int lds_max = 0;
   hipError_t e = hipDeviceGetAttribute(&lds_max, hipDeviceAttributeMaxSharedMemoryPerBlock, device);
   if (e != hipSuccess) return e;
@@ -804,8 +818,19 @@ hipError_t kernels_init(int device) {
   const size_t need_plan = sizeof(uint64_t) * kSortChunk + 256;
   const size_t need = std::max(need_expand, std::max(need_shrink, need_plan));
   if ((size_t)lds_max < need) return hipErrorInvalidConfiguration;
-  done[device] = true;
+  float* p = nullptr;
+  e = hipGetSymbolAddress(reinterpret_cast<void**>(&p), HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return e;
+  if (!p) return hipErrorInvalidSymbol;
+  g_scratch[device] = p;
+  g_init_done[device] = true;
   return hipSuccess;
+}
+
+float* static_scratch(int device) {
+  if (device < 0 || device >= kMaxDevices) return nullptr;
+  std::lock_guard<std::mutex> g(g_init_mu);
+  return g_init_done[device] ? g_scratch[device] : nullptr;
 }
 
 }  // namespace salt

@@ -65,6 +65,12 @@ struct GramArgs {
 constexpr int centroid_blocks(int r_c) { return r_c == 0 ? 0 : (r_c <= 32 ? 2 : (r_c <= 64 ? 4 : 8)); }
 
 hipError_t kernels_init(int device);
+// Floats of the static device scratch that salt_apply_batch_noalloc's launches
+// keep their split-K partials in (64 MiB per device).
+constexpr size_t kScratchFloats = (size_t)16 << 20;
+constexpr int kMaxDevices = 64;
+// This device's copy of the scratch (resolved by kernels_init), or null.
+float* static_scratch(int device);
 hipError_t launch_plan(const PlanLaunch& a, hipStream_t s);
 // The apply: k_shrink then k_expand on s.  ev (may be null): four HIP events
 // that record the start and end of the shrink kernel (ev[0], ev[1]) and of the

@@ -418,8 +418,10 @@ salt_status build_impl(salt_ctx* ctx, salt_plan* plan, hipStream_t s) {
 // The apply of `n` tables (ids `tables`, activations xs, outputs ys) on a
 // built plan, in launches of at most kMaxJobs tables.  ev: null, or four events
 // per launch (the timed form allows one launch).
+// `scratch`: the launches keep their split-K partials in the device's static
+// scratch (salt_apply_batch_noalloc) instead of the plan's own buffer.
 salt_status apply_impl(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_plan* plan, const void* const* xs,
-                       void* const* ys, hipStream_t s, hipEvent_t* ev) {
+                       void* const* ys, hipStream_t s, hipEvent_t* ev, bool scratch = false) {
   SALT_LIVE(ctx);
   if (!plan || n < 0 || (n > 0 && (!tables || !xs || !ys))) return fail(ctx, SALT_ERR_INVALID_ARG, "null argument");
   if (!plan->built) return fail(ctx, SALT_ERR_BAD_STATE, "plan was not built");
@@ -445,6 +447,15 @@ salt_status apply_impl(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_pla
                   ctx->slot_rank[sl], plan->slot_rank[i]);
     need_load = std::max(need_load, ctx->slot_loader[sl]);
   }
+  float* partials = plan->partials;
+  int64_t partial_cap = (int64_t)plan->partial_cap;
+  if (scratch) {
+    // the plan's own capacity where it is smaller, so that the launch (and its
+    // K split) is the one salt_apply_batch makes whenever the plan's fits
+    partials = salt::static_scratch(ctx->device);
+    partial_cap = std::min(partial_cap, (int64_t)salt::kScratchFloats);
+    if (!partials) return fail(ctx, SALT_ERR_BAD_STATE, "the static scratch of device %d is not set up", ctx->device);
+  }
   SALT_HIP(ctx, hipSetDevice(ctx->device));
   SALT_HIP(ctx, use_stream(ctx, plan, s));
   SALT_HIP(ctx, ring_wait(ctx->loaders, s, need_load));
@@ -455,10 +466,10 @@ salt_status apply_impl(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_pla
     a.tiles = plan->staged_dev + T;
     a.srt = plan->srt;
     a.pool = ctx->pool;
-    a.partials = plan->partials;
+    a.partials = partials;
     a.zeros = ctx->zeros;
     a.slot_stride = (int64_t)ctx->slot_stride;
-    a.partial_cap = (int64_t)plan->partial_cap;
+    a.partial_cap = partial_cap;
     a.n_jobs = nj;
     a.T = T;
     a.n_tiles = plan->n_tiles;
@@ -483,8 +494,13 @@ salt_status apply_impl(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_pla
       jb.in = sh.in_dim;
       jb.out = sh.out_dim;
     }
-    if (!salt::configure_launch(a, ctx->n_cu, plan->n_groups_c, plan->sum_rank))
+    if (!salt::configure_launch(a, ctx->n_cu, plan->n_groups_c, plan->sum_rank)) {
+      if (scratch)
+        return fail(ctx, SALT_ERR_OUT_OF_RANGE,
+                    "split-K partials of %d tables x %d tokens x %d ranks exceed the static scratch (%zu floats)", nj,
+                    T, a.R, salt::kScratchFloats);
       return fail(ctx, SALT_ERR_BAD_STATE, "split-K partials of %d tables do not fit the plan", nj);
+    }
     SALT_HIP(ctx, salt::launch_apply(a, s, ev));
   }
   SALT_HIP(ctx, open_readers(ctx, plan, s));
@@ -890,6 +906,11 @@ salt_status salt_apply(salt_ctx* ctx, int32_t table, salt_plan* plan, const void
 salt_status salt_apply_batch(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_plan* plan, const void* const* xs,
                              void* const* ys, void* stream) {
   return apply_impl(ctx, n, tables, plan, xs, ys, (hipStream_t)stream, nullptr);
+}
+
+salt_status salt_apply_batch_noalloc(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_plan* plan,
+                                     const void* const* xs, void* const* ys, void* stream) {
+  return apply_impl(ctx, n, tables, plan, xs, ys, (hipStream_t)stream, nullptr, true);
 }
 
 salt_status salt_apply_batch_timed(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_plan* plan,

@@ -27,7 +27,7 @@ EXPORTS = (
     "salt_residual_bytes_for", "salt_load_residual", "salt_load_residuals", "salt_wait_loads",
     "salt_host_alloc", "salt_host_free", "salt_plan_create", "salt_plan_destroy", "salt_plan_set_maps",
     "salt_plan_build", "salt_plan_download", "salt_plan_errors", "salt_plan_tiling", "salt_apply",
-    "salt_apply_batch", "salt_apply_batch_timed", "salt_apply_map", "salt_fuse_centroid",
+    "salt_apply_batch", "salt_apply_batch_noalloc", "salt_apply_batch_timed", "salt_apply_map", "salt_fuse_centroid",
     "salt_fuse_centroid_timed", "salt_adapter_gram", "salt_route",
     "salt_status_str",
     "salt_last_error", "salt_version",
@@ -77,6 +77,7 @@ def _load() -> C.CDLL:
         "salt_plan_tiling": (C.c_int, [P, P, IP, IP, IP]),
         "salt_apply": (C.c_int, [P, I32, P, VP, VP, VP]),
         "salt_apply_batch": (C.c_int, [P, I32, IP, P, C.POINTER(VP), C.POINTER(VP), VP]),
+        "salt_apply_batch_noalloc": (C.c_int, [P, I32, IP, P, C.POINTER(VP), C.POINTER(VP), VP]),
         "salt_apply_batch_timed": (C.c_int, [P, I32, IP, P, C.POINTER(VP), C.POINTER(VP), VP, C.POINTER(VP)]),
         "salt_apply_map": (C.c_int, [P, I32, I32, IP, IP, C.POINTER(C.c_float), VP, VP, VP]),
         "salt_fuse_centroid": (C.c_int, [P, I32, I32, C.c_float, VP, C.c_int64, VP]),
@@ -255,6 +256,17 @@ class Context:
         tabs = np.ascontiguousarray(tables, dtype=np.int32)
         self._check(lib.salt_apply_batch(self.h, n, _i32p(tabs), plan.h, self._ptrs(x_ptrs), self._ptrs(y_ptrs),
                                          stream), "salt_apply_batch")
+
+    def apply_batch_noalloc(self, tables: Sequence[int], plan: "Plan", x_ptrs: Sequence[int],
+                            y_ptrs: Sequence[int], stream: int = 0):
+        """salt_apply_batch_noalloc: salt_apply_batch with the partials in the
+        library's static device scratch (no allocation)."""
+        self._check(self.apply_batch_noalloc_status(tables, plan, x_ptrs, y_ptrs, stream), "salt_apply_batch_noalloc")
+
+    def apply_batch_noalloc_status(self, tables, plan, x_ptrs, y_ptrs, stream: int = 0) -> int:
+        tabs = np.ascontiguousarray(tables, dtype=np.int32)
+        return lib.salt_apply_batch_noalloc(self.h, len(tables), _i32p(tabs), plan.h, self._ptrs(x_ptrs),
+                                            self._ptrs(y_ptrs), stream)
 
     def apply_batch_status(self, tables, plan, x_ptrs, y_ptrs, stream: int = 0) -> int:
         tabs = np.ascontiguousarray(tables, dtype=np.int32)

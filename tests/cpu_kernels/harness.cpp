@@ -8,7 +8,8 @@
 //   n_loads, then per load: slot, rank, blob bytes (rank * sum(in + out) * esize)
 //   n_batches, then per batch:
 //     mode (0: set_maps + build + apply_batch on the context's plan 0 .. n_plans-1;
-//           1: salt_apply_map, one table), plan index,
+//           1: salt_apply_map, one table; 2: as 0 with salt_apply_batch_noalloc),
+//     plan index,
 //     T, has_gamma, tok_c [T], tok_u [T], gamma (float32) [T] if has_gamma,
 //     n_jobs, tables [n_jobs], then per job x bytes [T][in], y0 bytes [T][out]
 // Output per batch: status of set_maps, build, apply, plan_errors; n_errors,
@@ -153,7 +154,8 @@ int main(int argc, char** argv) {
       s_set = salt_plan_set_maps(ctx, p, T, tc.data(), tu.data(), has_gamma ? gm.data() : nullptr, nullptr);
       if (s_set == SALT_OK) s_build = salt_plan_build(ctx, p, nullptr);
       if (s_set == SALT_OK && s_build == SALT_OK) {
-        s_apply = salt_apply_batch(ctx, nj, tabs.data(), p, xs.data(), ys.data(), nullptr);
+        s_apply = mode == 2 ? salt_apply_batch_noalloc(ctx, nj, tabs.data(), p, xs.data(), ys.data(), nullptr)
+                            : salt_apply_batch(ctx, nj, tabs.data(), p, xs.data(), ys.data(), nullptr);
         s_err = salt_plan_errors(ctx, p, nullptr, &n_err);
         (void)salt_plan_tiling(ctx, p, &tile_m, &n_tiles, nullptr);
         (void)salt_plan_download(ctx, p, nullptr, perm.data(), seg_off.data(), seg_c.data(), seg_u.data(),

@@ -43,6 +43,7 @@
 #define __forceinline__ inline
 #define __launch_bounds__(...)
 #define __shared__ static
+#define __align__(n) __attribute__((aligned(n)))
 
 struct int4 {
   int x, y, z, w;
@@ -86,6 +87,7 @@ typedef enum {
   hipErrorOutOfMemory = 2,
   hipErrorInvalidConfiguration = 9,
   hipErrorInvalidDevice = 101,
+  hipErrorInvalidSymbol = 13,
   hipErrorLaunchFailure = 719
 } hipError_t;
 typedef struct salt_cpu_stream* hipStream_t;
@@ -452,6 +454,12 @@ inline void salt_cpu_buf_store_b32(unsigned v, salt_cpu_rsrc r, int off, int sof
 #define __builtin_amdgcn_fdot2_f32_bf16 salt_cpu_fdot2_bf16
 
 // ---- runtime API (synchronous) -------------------------------------------------------
+// a file-scope __device__ array is a host array here; its "device address" is its address
+#define HIP_SYMBOL(x) (&(x))
+inline hipError_t hipGetSymbolAddress(void** p, const void* sym) {
+  *p = const_cast<void*>(sym);
+  return hipSuccess;
+}
 inline hipError_t hipGetLastError() { return hipSuccess; }
 inline const char* hipGetErrorString(hipError_t e) { return e == hipSuccess ? "no error" : "cpu runtime error"; }
 inline hipError_t hipSetDevice(int d) { return d == 0 ? hipSuccess : hipErrorInvalidDevice; }
