@@ -39,14 +39,26 @@ namespace {
 // ---------------------------------------------------------------------------
 // shared shapes
 // ---------------------------------------------------------------------------
-// M tokens per tile = TB token blocks of 16.  A block's 4 waves split as
+// M tokens per tile = TB token blocks of 16.  A block has waves_of(M) waves:
+// four for tiles of up to 64 tokens, one per token block beyond.  They split as
 // (token block, K quarter) in the shrink and (token block, column phase) in the
-// expand: KW = CW = 4 / TB.  With TB > 1 (32- and 64-token tiles, bf16) several
-// waves need the same centroid operand at the same time (A_c in the shrink, B_c
-// in the expand); the block then loads it once, cooperatively, into an LDS
-// stage from which each wave reads its MFMA fragments.
+// expand: KW = CW = waves / TB.  With TB > 1 (32-, 64- and 128-token tiles,
+// bf16) several waves need the same centroid operand at the same time (A_c in
+// the shrink, B_c in the expand); the block then loads it once, cooperatively,
+// into an LDS stage from which each wave reads its MFMA fragments, so the
+// operand is read from L2 once per M tokens.
 template <int M>
-constexpr int waves_along() { return kWaves / (M / 16); }
+constexpr int waves_along() { return waves_of(M) / (M / 16); }
+template <int M>
+constexpr int threads_of() { return 64 * waves_of(M); }
+// Waves per SIMD the kernels for 128-token tiles are compiled for (two blocks
+// of 8 waves per compute unit) where their registers fit that without
+// spilling: r_c <= 32 with residual ranks up to 2, r_c <= 64 with rank 1.
+// Other kernels keep the compiler's choice.
+template <typename E, int M, int NB, int RU>
+constexpr int min_waves() {
+  return (sizeof(E) == 2 && M == 128 && ((NB <= 2 && RU <= 2) || (NB <= 4 && RU <= 1))) ? 4 : 1;
+}
 template <typename E, int M, int NB>
 constexpr bool staged() { return sizeof(E) == 2 && M > 16 && NB > 0; }
 // Staged rows carry 8 elements of padding: consecutive rows then start 4 LDS
@@ -85,7 +97,8 @@ constexpr int depth() { return 1; }
 // written into the other half of the LDS stage, so every wait is for loads that
 // were issued a whole block-step earlier.
 template <typename E, int M, int NB, int RU>
-__global__ void __launch_bounds__(kThreads) k_shrink(const ApplyLaunch a) {
+__global__ void __launch_bounds__(threads_of<M>()) __attribute__((amdgpu_waves_per_eu(min_waves<E, M, NB, RU>(), 8)))
+k_shrink(const ApplyLaunch a) {
   using O = Ops<E>;
   using Vec = typename O::Vec;
   constexpr int ES = sizeof(E);
@@ -93,7 +106,9 @@ __global__ void __launch_bounds__(kThreads) k_shrink(const ApplyLaunch a) {
   constexpr bool kStage = staged<E, M, NB>();
   constexpr int NBL = NB > 0 ? NB : 1;
   constexpr int SR = stage_row_a<M>();                       // elements per staged A_c row
-  constexpr int NCV = kStage ? NB * KW / 2 : 1;              // staged A_c vectors per thread and block-step
+  constexpr int NT = threads_of<M>(), NW = waves_of(M);
+  constexpr int PIECES = 16 * NB * 8 * KW;                   // 16-byte pieces of a block-step's A_c slice
+  constexpr int NCV = kStage ? (PIECES + NT - 1) / NT : 1;   // staged A_c vectors per thread and block-step
   constexpr int NAC = kStage ? 1 : 2 * NBL;                  // per-lane A_c vectors per step (unstaged)
   constexpr int RUP = RU <= 2 ? RU : 0;                      // residual ranks in the pipelined operands
   constexpr int U = depth<E, M, NB, RU>();
@@ -103,7 +118,7 @@ __global__ void __launch_bounds__(kThreads) k_shrink(const ApplyLaunch a) {
 
   const Job& jb = a.jobs[job_of_shrink(a, blockIdx.x)];
   const ShrinkCoord sc = shrink_coord(a, jb, blockIdx.x);
-  const TileHdr th = clamp_tile(a, a.tiles[sc.tau]);
+  const TileHdr th = shrink_tile(a, sc.tau);
   if (th.n <= 0) return;                                     // (no tile is empty; the whole block leaves)
   const int in = jb.in;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -180,8 +195,8 @@ __global__ void __launch_bounds__(kThreads) k_shrink(const ApplyLaunch a) {
         const int kj = klo + (j0 + u) * kStepK * KW;
 #pragma unroll
         for (int q = 0; q < NCV; ++q) {
-          const int L = q * kThreads + tid, r = L / (8 * KW), k = kj + 8 * (L % (8 * KW));
-          stg[u][q] = O::bload(rac, oob_unless(r < a.r_c && k + 8 <= khi, (uint32_t)((r * in + k) * ES)));
+          const int L = q * NT + tid, r = L / (8 * KW), k = kj + 8 * (L % (8 * KW));
+          stg[u][q] = O::bload(rac, oob_unless(L < PIECES && r < a.r_c && k + 8 <= khi, (uint32_t)((r * in + k) * ES)));
         }
       }
     }
@@ -192,8 +207,8 @@ __global__ void __launch_bounds__(kThreads) k_shrink(const ApplyLaunch a) {
       for (int u = 0; u < U; ++u)
 #pragma unroll
         for (int q = 0; q < NCV; ++q) {
-          const int L = q * kThreads + tid, r = L / (8 * KW), c16 = L % (8 * KW);
-          *reinterpret_cast<Vec*>(s_a + ((size_t)(half * U + u) * 16 * NB + r) * SR + 8 * c16) = stg[u][q];
+          const int L = q * NT + tid, r = L / (8 * KW), c16 = L % (8 * KW);
+          if (L < PIECES) *reinterpret_cast<Vec*>(s_a + ((size_t)(half * U + u) * 16 * NB + r) * SR + 8 * c16) = stg[u][q];
         }
     }
   };
@@ -309,7 +324,7 @@ __global__ void __launch_bounds__(kThreads) k_shrink(const ApplyLaunch a) {
   const int nres = imax(0, imin(RU, a.r_u - r0));
   const int ncols = ncent + nres;
   const Rsrc rp = make_rsrc(a.partials + jb.poff, (uint32_t)((int64_t)jb.S * a.T * a.R * 4));
-  for (int k = wave; k < th.n; k += kWaves) {
+  for (int k = wave; k < th.n; k += NW) {
     for (int cc = lane; cc < ncols; cc += 64) {
       float v = 0.f;
       int col;
@@ -355,14 +370,15 @@ __device__ __forceinline__ void expand_segment(const ApplyLaunch& a, const Expan
   constexpr bool kStage = staged<E, M, NB>();
   constexpr int KSL = KS > 0 ? KS : 1;
   constexpr int SRB = stage_row_b<NB>();                     // elements per staged B_c row (one column)
-  constexpr int NCV = kStage ? CW * NB / 2 : 1;              // staged B_c vectors per thread and block-chunk
+  constexpr int NT = threads_of<M>();
+  constexpr int NCV = kStage ? (128 * CW * NB + NT - 1) / NT : 1;   // staged B_c vectors per thread and block-chunk
   constexpr int NBC = kStage ? 1 : 4 * KSL;                  // per-lane B_c vectors per chunk (unstaged)
   constexpr int RUP = RU <= 2 ? RU : 0;                      // residual ranks in the pipelined operands
   constexpr int U = depth<E, M, NB, RU>();
   float* s_v = reinterpret_cast<float*>(lds);                // [M][R] v of the tile
 
   const Job& jb = a.jobs[sg.job];
-  const TileHdr th = clamp_tile(a, a.tiles[sg.tau]);
+  const TileHdr th = expand_tile(a, sg.tau);
   if (th.n <= 0) return;                                     // (no tile is empty)
   const int out = jb.out;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -438,7 +454,7 @@ __device__ __forceinline__ void expand_segment(const ApplyLaunch& a, const Expan
     const int rc8 = imax(a.r_c, 8);
 #pragma unroll
     for (int q = 0; q < NCV; ++q) {
-      const int e = 8 * (q * kThreads + tid);
+      const int e = 8 * (q * NT + tid);
       st_oc[q] = e / rc8;
       st_rk[q] = e - st_oc[q] * rc8;
     }
@@ -479,7 +495,7 @@ __device__ __forceinline__ void expand_segment(const ApplyLaunch& a, const Expan
   load(A, 0);
   {
     // the tile's rows of one K range are contiguous: (n R / 4) float4 from row
-    // i0; per pass, thread t sums float4 q0 + t and q0 + t + kThreads over the
+    // i0; per pass, thread t sums float4 q0 + t and q0 + t + NT over the
     // K ranges in order, with four K ranges' loads in flight at a time (rows
     // past n read zero)
     const Rsrc rp = make_rsrc(a.partials + jb.poff, (uint32_t)((int64_t)jb.S * a.T * a.R * 4));
@@ -487,12 +503,12 @@ __device__ __forceinline__ void expand_segment(const ApplyLaunch& a, const Expan
     const uint32_t tile0 = (uint32_t)th.i0 * (uint32_t)R * 4u;
     const int n4 = th.n * R / 4, m4 = M * R / 4;
     constexpr int QMAX = 2;                                  // float4 per thread and pass
-    for (int q0 = tid; q0 < m4; q0 += QMAX * kThreads) {
+    for (int q0 = tid; q0 < m4; q0 += QMAX * NT) {
       float4 v[QMAX];
       uint32_t off[QMAX];
 #pragma unroll
       for (int i = 0; i < QMAX; ++i) {
-        const int q = q0 + i * kThreads;
+        const int q = q0 + i * NT;
         v[i] = make_float4(0.f, 0.f, 0.f, 0.f);
         off[i] = oob_unless(q < n4, tile0 + 16u * (uint32_t)q);
       }
@@ -517,7 +533,7 @@ __device__ __forceinline__ void expand_segment(const ApplyLaunch& a, const Expan
       }
 #pragma unroll
       for (int i = 0; i < QMAX; ++i) {
-        const int q = q0 + i * kThreads;
+        const int q = q0 + i * NT;
         if (q < m4) reinterpret_cast<float4*>(s_v)[q] = v[i];
       }
     }
@@ -560,7 +576,7 @@ __device__ __forceinline__ void expand_segment(const ApplyLaunch& a, const Expan
     __syncthreads();
     // the staged rows' rank padding [r_c, 16 NB) reads as zero
     const int padr = 16 * NB - a.r_c;
-    for (int i = tid; i < 2 * U * 64 * CW * padr; i += kThreads) {
+    for (int i = tid; i < 2 * U * 64 * CW * padr; i += NT) {
       const int r = i / padr, k = a.r_c + i % padr;
       s_b[(size_t)r * SRB + k] = E(0);
     }
@@ -682,7 +698,8 @@ __device__ __forceinline__ void expand_segment(const ApplyLaunch& a, const Expan
 // segment starts behind a block barrier, so its LDS writes never meet the
 // previous segment's reads.
 template <typename E, int M, int NB, int RU>
-__global__ void __launch_bounds__(kThreads) k_expand(const ApplyLaunch a) {
+__global__ void __launch_bounds__(threads_of<M>()) __attribute__((amdgpu_waves_per_eu(min_waves<E, M, NB, RU>(), 8)))
+k_expand(const ApplyLaunch a) {
   extern __shared__ __attribute__((aligned(16))) char lds[];
   const int end = expand_begin(a, blockIdx.x + 1, gridDim.x);
   for (int pos = expand_begin(a, blockIdx.x, gridDim.x); pos < end;) {
@@ -697,10 +714,10 @@ __global__ void __launch_bounds__(kThreads) k_expand(const ApplyLaunch a) {
 // launch
 // ---------------------------------------------------------------------------
 template <typename K>
-void launch_k(K kernel, int blocks, size_t lds, hipStream_t s, const ApplyLaunch& a, hipEvent_t e0,
+void launch_k(K kernel, int blocks, int threads, size_t lds, hipStream_t s, const ApplyLaunch& a, hipEvent_t e0,
               hipEvent_t e1) {
-  if (e0 || e1) hipExtLaunchKernelGGL(kernel, dim3(blocks), dim3(kThreads), (uint32_t)lds, s, e0, e1, 0u, a);
-  else hipLaunchKernelGGL(kernel, dim3(blocks), dim3(kThreads), lds, s, a);
+  if (e0 || e1) hipExtLaunchKernelGGL(kernel, dim3(blocks), dim3(threads), (uint32_t)lds, s, e0, e1, 0u, a);
+  else hipLaunchKernelGGL(kernel, dim3(blocks), dim3(threads), lds, s, a);
 }
 
 template <typename E, int M, int NB, int RU>
@@ -721,12 +738,12 @@ size_t expand_lds(int R, int r_u) {
 // Blocks of `kernel` with `lds` bytes of LDS that one compute unit holds at once
 // (cached per kernel for the last LDS size asked).
 template <typename K>
-int resident_blocks(K kernel, size_t lds) {
+int resident_blocks(K kernel, int threads, size_t lds) {
   static std::atomic<uint64_t> cache{0};                     // (lds << 32) | blocks
   const uint64_t c = cache.load(std::memory_order_relaxed);
   if (c != 0 && (c >> 32) == (uint64_t)lds) return (int)(c & 0xffffffffu);
   int n = 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(kernel), kThreads, lds) !=
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&n, reinterpret_cast<const void*>(kernel), threads, lds) !=
           hipSuccess ||
       n < 1) {
     (void)hipGetLastError();
@@ -738,11 +755,14 @@ int resident_blocks(K kernel, size_t lds) {
 
 template <typename E, int M, int NB, int RU>
 hipError_t launch_mnr(const ApplyLaunch& a, hipStream_t s, hipEvent_t* ev) {
-  launch_k(k_shrink<E, M, NB, RU>, a.shrink_blocks, shrink_lds<E, M, NB, RU>(), s, a, ev ? ev[0] : nullptr,
-           ev ? ev[1] : nullptr);
+  constexpr int NT = threads_of<M>();
+  constexpr int MS = M > 64 ? 64 : M;                         // tokens per shrink tile
+  if (a.MS != MS) return hipErrorInvalidValue;
+  launch_k(k_shrink<E, MS, NB, RU>, a.shrink_blocks, threads_of<MS>(), shrink_lds<E, MS, NB, RU>(), s, a,
+           ev ? ev[0] : nullptr, ev ? ev[1] : nullptr);
   const size_t lds = expand_lds<E, M, NB, RU>(a.R, a.r_u);
-  const int round = resident_blocks(k_expand<E, M, NB, RU>, lds) * std::max(1, a.n_cu);
-  launch_k(k_expand<E, M, NB, RU>, std::min(a.expand_items, round), lds, s, a, ev ? ev[2] : nullptr,
+  const int round = resident_blocks(k_expand<E, M, NB, RU>, NT, lds) * std::max(1, a.n_cu);
+  launch_k(k_expand<E, M, NB, RU>, std::min(a.expand_items, round), NT, lds, s, a, ev ? ev[2] : nullptr,
            ev ? ev[3] : nullptr);
   return hipGetLastError();
 }
@@ -778,6 +798,7 @@ hipError_t launch_apply(const ApplyLaunch& a, hipStream_t s, hipEvent_t* ev) {
     case 16: return launch_m<uint16_t, 16>(a, s, ev);
     case 32: return launch_m<uint16_t, 32>(a, s, ev);
     case 64: return launch_m<uint16_t, 64>(a, s, ev);
+    case 128: return launch_m<uint16_t, 128>(a, s, ev);
     default: return hipErrorInvalidValue;
   }
 }
@@ -811,9 +832,12 @@ hipError_t kernels_init(int device) {
   const int R = padded_rank(kMaxRc, kMaxRu);
   const size_t need_expand = std::max({expand_lds<uint16_t, 64, 8, kRankChunk>(R, kMaxRu),
                                        expand_lds<uint16_t, 32, 8, kRankChunk>(R, kMaxRu),
+                                       expand_lds<uint16_t, 128, 8, kRankChunk>(R, kMaxRu),
+                                       expand_lds<uint16_t, 128, 4, 2>(padded_rank(64, 2), 2),
                                        expand_lds<uint16_t, 64, 4, 2>(padded_rank(64, 2), 2),
                                        expand_lds<uint16_t, 32, 4, 2>(padded_rank(64, 2), 2)});
-  const size_t need_shrink = std::max({shrink_lds<uint16_t, 64, 8, kRankChunk>(), shrink_lds<uint16_t, 32, 8, kRankChunk>(),
+  const size_t need_shrink = std::max({shrink_lds<uint16_t, 128, 8, kRankChunk>(),
+                                       shrink_lds<uint16_t, 64, 8, kRankChunk>(), shrink_lds<uint16_t, 32, 8, kRankChunk>(),
                                        shrink_lds<uint16_t, 64, 4, 2>(), shrink_lds<uint16_t, 32, 4, 2>()});
   const size_t need_plan = sizeof(uint64_t) * kSortChunk + 256;
   const size_t need = std::max(need_expand, std::max(need_shrink, need_plan));

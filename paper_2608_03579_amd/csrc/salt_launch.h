@@ -16,19 +16,25 @@ namespace salt {
 
 // Tokens per tile, from the mean size of the batch's centroid groups: short
 // groups (decode batches) take 16-token tiles, groups of up to ~100 tokens 32,
-// long ones (prefill) 64.  fp32 contexts always use 16.
-inline int choose_tile_tokens(int esize, int T, int n_groups) {
+// up to ~400 tokens 64, longer ones (prefill) 128 when there is a centroid
+// operand, which each block stages once per tile: the larger the tile, the
+// fewer times it is read.  fp32 contexts always use 16.
+inline int choose_tile_tokens(int esize, int T, int n_groups, bool centroids) {
   if (esize == 4 || n_groups <= 0) return 16;
   const double mean = (double)T / n_groups;
   if (mean <= 24.0) return 16;
   if (mean <= 96.0) return 32;
-  return 64;
+  if (mean <= 384.0 || !centroids) return 64;
+  return 128;
 }
 
 // Tiles of a batch from the token counts of its centroid groups, per_c[c + 1]
 // for c = -1 .. C - 1 (the sorted order puts c = -1 first).  A group of n tokens
-// becomes ceil(n / M) tiles of near-equal size, the first n mod k of them one
-// token longer.  Tiles are contiguous in sorted order and cover [0, T).
+// becomes k = ceil(n / M) tiles: for tiles of up to 64 tokens of near-equal
+// size, the first n mod k of them one token longer; for larger tiles
+// k - 1 full tiles and the remainder (the expand of 128-token tiles splits
+// its work by column chunks, not by tiles, so their sizes need not match).
+// Tiles are contiguous in sorted order and cover [0, T).
 inline void cut_tiles(const std::vector<int>& per_c, int M, std::vector<int4>& tiles) {
   tiles.clear();
   int start = 0;
@@ -38,7 +44,7 @@ inline void cut_tiles(const std::vector<int>& per_c, int M, std::vector<int4>& t
     const int k = cdiv(n, M), base = n / k, extra = n % k;
     int p = start;
     for (int i = 0; i < k; ++i) {
-      const int len = base + (i < extra ? 1 : 0);
+      const int len = M > 64 ? imin(M, n - i * M) : base + (i < extra ? 1 : 0);
       int4 t;
       t.x = p;
       t.y = len;
@@ -55,13 +61,13 @@ inline void cut_tiles(const std::vector<int>& per_c, int M, std::vector<int4>& t
 inline int max_tiles(int T, int C) { return cdiv(T, 16) + C + 1; }
 
 // K ranges, expand block-chunks and work offsets of launch `a`, whose jobs (in,
-// out, prefix, pointers) and batch fields (T, M, n_tiles, C, r_c, r_u, nq, R,
+// out, prefix, pointers) and batch fields (T, M, n_tiles, MS, n_stiles, C, r_c, r_u, nq, R,
 // esize, partial_cap) are set.  n_groups_c: centroids the batch references;
 // sum_rank: residual ranks summed over the slots it references (both for the
 // byte counts that bound the partial traffic).  Returns false if the partials
 // of a one-range shrink do not fit.
 inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t sum_rank) {
-  const int TB = a.M / 16, KW = kWaves / TB, CW = kWaves / TB;
+  const int KW = waves_of(a.MS) / (a.MS / 16), CW = waves_of(a.M) / (a.M / 16);
   const int target = 8 * std::max(1, n_cu);        // blocks per launch: a few rounds of the whole device
   const double es = (double)a.esize;
   const double adapters = (double)n_groups_c * a.r_c + (double)sum_rank;
@@ -72,7 +78,7 @@ inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t s
   // split is capped so that its partials (written, then read) stay within a
   // tenth of its bytes
   const int gran = kStepK * KW;
-  const double pairs = (double)a.n_tiles * a.nq;
+  const double pairs = (double)shrink_tiles(a) * a.nq;
   const int kc_target = std::max(gran, cdiv((int)std::ceil((double)sum_in * pairs / target), gran) * gran);
   const double part_row = 8.0 * a.T * a.R;        // bytes of one K range's partials, written and read
   std::vector<int> S(a.n_jobs);
@@ -117,7 +123,7 @@ inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t s
     jb.n_col = cdiv(jb.out, jb.cpb);
     jb.shrink_base = sb;
     jb.expand_base = eb;
-    sb += a.n_tiles * jb.S * a.nq;
+    sb += shrink_tiles(a) * jb.S * a.nq;
     eb += a.n_tiles * jb.n_col;
   }
   a.shrink_blocks = sb;

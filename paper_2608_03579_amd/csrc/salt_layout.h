@@ -27,8 +27,7 @@ struct int4 {
 namespace salt {
 
 // ---- fixed shapes -----------------------------------------------------------
-constexpr int kThreads = 256;        // threads of an apply block (4 waves of 64)
-constexpr int kWaves = 4;
+constexpr int kWaves = 4;            // waves of an apply block for tiles of up to 64 tokens
 constexpr int kStepK = 64;           // k elements one wave takes per shrink step
 constexpr int kChunkCols = 64;       // output columns one wave takes per expand chunk
 constexpr int kMaxJobs = 16;         // tables one apply launch serves
@@ -44,6 +43,10 @@ SALT_HD int imin(int a, int b) { return a < b ? a : b; }
 SALT_HD int imax(int a, int b) { return a > b ? a : b; }
 SALT_HD int iclamp(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
 SALT_HD int cdiv(int a, int b) { return (a + b - 1) / b; }
+
+// Waves of an apply block for tiles of M tokens: four, or one per 16-token
+// block beyond 64 tokens.
+SALT_HD constexpr int waves_of(int M) { return M > 64 ? M / 16 : kWaves; }
 
 // Row stride of the split-K partials: r_c + r_u rounded up to whole float4s.
 SALT_HD int padded_rank(int r_c, int r_u) {
@@ -86,6 +89,9 @@ struct ApplyLaunch {
   int32_t n_jobs;
   int32_t T;
   int32_t n_tiles;
+  const int4* stiles;      // [n_stiles] the shrink's tiles (the expand's tiles unless those exceed 64 tokens)
+  int32_t n_stiles;
+  int32_t MS;              // tokens per shrink tile (min(M, 64))
   int32_t M;               // tokens per tile (16, 32 or 64)
   int32_t C, r_c;
   int32_t n_slots;
@@ -108,12 +114,12 @@ struct TokRec {
   bool res;                // has a residual term (slot >= 0, rank > 0)
 };
 
-// The header of tile `tau` with every field clamped: 0 <= i0 < T,
-// 0 <= n <= min(M, T - i0), -1 <= c < C.
-SALT_HD TileHdr clamp_tile(const ApplyLaunch& a, int4 h) {
+// A tile header with every field clamped: 0 <= i0 < T, 0 <= n <= min(M, T -
+// i0), -1 <= c < C (M: the tile size of the list it comes from).
+SALT_HD TileHdr clamp_tile(const ApplyLaunch& a, int4 h, int M) {
   TileHdr r;
   r.i0 = iclamp(h.x, 0, imax(a.T - 1, 0));
-  r.n = iclamp(h.y, 0, imin(a.M, a.T - r.i0));
+  r.n = iclamp(h.y, 0, imin(M, a.T - r.i0));
   r.c = (a.r_c > 0) ? iclamp(h.z, -1, a.C - 1) : -1;
   return r;
 }
@@ -144,19 +150,26 @@ SALT_HD int job_of_expand(const ApplyLaunch& a, int b) {
   return j;
 }
 
-// Shrink item i of job j: tile tau, K range s, residual rank chunk q
+// Shrink item i of job j: shrink tile tau, K range s, residual rank chunk q
 // (items of a job: (q, s, tau) with tau fastest).
 struct ShrinkCoord {
   int tau, s, q;
 };
+SALT_HD int shrink_tiles(const ApplyLaunch& a) { return a.n_stiles; }
 SALT_HD ShrinkCoord shrink_coord(const ApplyLaunch& a, const Job& jb, int item) {
-  const int local = item - jb.shrink_base;
+  const int local = item - jb.shrink_base, nt = imax(shrink_tiles(a), 1);
   ShrinkCoord c;
-  c.tau = local % a.n_tiles;
-  const int rest = local / a.n_tiles;
+  c.tau = local % nt;
+  const int rest = local / nt;
   c.s = rest % jb.S;
   c.q = iclamp(rest / jb.S, 0, a.nq - 1);
   return c;
+}
+SALT_HD TileHdr shrink_tile(const ApplyLaunch& a, int tau) {
+  return clamp_tile(a, a.stiles[iclamp(tau, 0, a.n_stiles - 1)], a.MS);
+}
+SALT_HD TileHdr expand_tile(const ApplyLaunch& a, int tau) {
+  return clamp_tile(a, a.tiles[iclamp(tau, 0, a.n_tiles - 1)], a.M);
 }
 
 // Expand work items: (job, tile, block-chunk), job-major, then tile, block-chunk

@@ -71,7 +71,7 @@ HostRanges g_host_ranges;
 
 struct salt_plan {
   // device buffers, sized for max_tokens
-  int4* staged_dev = nullptr;       // [max_T + tile_cap]: the batch's maps [T], then its tiles
+  int4* staged_dev = nullptr;       // [max_T + 2 tile_cap]: the batch's maps [T], its tiles, its shrink tiles
   uint64_t* keys = nullptr;         // [2][max_T]
   int4* srt = nullptr;              // [max_T]
   int32_t* ints = nullptr;          // perm [max_T], seg_off / grp_off [max_T + 1], seg_c / seg_u [max_T]
@@ -88,6 +88,8 @@ struct salt_plan {
   bool built = false;
   int32_t M = 16;                   // tokens per tile
   int32_t n_tiles = 0;
+  int32_t MS = 16;                  // tokens per shrink tile
+  int32_t n_stiles = 0;             // shrink tiles: 0 when they are the tiles themselves
   int32_t n_groups_c = 0;           // centroids referenced
   int32_t ru_max = 0;               // largest residual rank referenced
   int64_t sum_rank = 0;             // ranks summed over the distinct referenced slots
@@ -289,7 +291,7 @@ salt_status plan_create(salt_ctx* ctx, salt_plan** out) {
   p->max_T = (int32_t)T;
   p->tile_cap = salt::max_tiles((int)T, ctx->cfg.n_centroids);
   p->partial_cap = plan_partial_cap(T, R);
-  const size_t staged = T + (size_t)p->tile_cap;
+  const size_t staged = T + 2 * (size_t)p->tile_cap;
   bool ok = hipMalloc((void**)&p->staged_dev, staged * sizeof(int4)) == hipSuccess &&
             hipMalloc((void**)&p->keys, 2 * T * sizeof(uint64_t)) == hipSuccess &&
             hipMalloc((void**)&p->srt, T * sizeof(int4)) == hipSuccess &&
@@ -368,13 +370,20 @@ salt_status set_maps_impl(salt_ctx* ctx, salt_plan* plan, int32_t T, const int32
       ++n_groups;
       n_groups_c += (g > 0);
     }
-  plan->M = salt::choose_tile_tokens((int)ctx->esize, T, n_groups);
-  std::vector<int4> tiles;
+  plan->M = salt::choose_tile_tokens((int)ctx->esize, T, n_groups, n_groups_c > 0);
+  // tiles of more than 64 tokens serve the expand only; the shrink then runs
+  // its own 64-token tiles of the same sorted order
+  std::vector<int4> tiles, stiles;
   salt::cut_tiles(per_c, plan->M, tiles);
-  if ((int)tiles.size() > plan->tile_cap)
-    return fail(ctx, SALT_ERR_BAD_STATE, "%zu tiles exceed the plan's %d", tiles.size(), plan->tile_cap);
+  plan->MS = std::min(plan->M, 64);
+  if (plan->MS != plan->M) salt::cut_tiles(per_c, plan->MS, stiles);
+  if ((int)tiles.size() > plan->tile_cap || (int)stiles.size() > plan->tile_cap)
+    return fail(ctx, SALT_ERR_BAD_STATE, "%zu tiles exceed the plan's %d", std::max(tiles.size(), stiles.size()),
+                plan->tile_cap);
   std::copy(tiles.begin(), tiles.end(), plan->staging + T);
+  std::copy(stiles.begin(), stiles.end(), plan->staging + T + tiles.size());
   plan->n_tiles = (int32_t)tiles.size();
+  plan->n_stiles = (int32_t)stiles.size();
   plan->n_groups_c = n_groups_c;
   plan->ru_max = ru_max;
   plan->sum_rank = sum_rank;
@@ -382,8 +391,8 @@ salt_status set_maps_impl(salt_ctx* ctx, salt_plan* plan, int32_t T, const int32
   plan->built = false;
   if (T > 0) {
     SALT_HIP(ctx, use_stream(ctx, plan, s));
-    SALT_HIP(ctx, hipMemcpyAsync(plan->staged_dev, plan->staging, ((size_t)T + tiles.size()) * sizeof(int4),
-                                 hipMemcpyHostToDevice, s));
+    SALT_HIP(ctx, hipMemcpyAsync(plan->staged_dev, plan->staging,
+                                 ((size_t)T + tiles.size() + stiles.size()) * sizeof(int4), hipMemcpyHostToDevice, s));
     SALT_HIP(ctx, hipEventRecord(plan->staged, s));
     plan->staged_pending = true;
   }
@@ -408,7 +417,7 @@ salt_status build_impl(salt_ctx* ctx, salt_plan* plan, hipStream_t s) {
     pl.grp_off = plan->grp_off();
     pl.meta = plan->meta;
     pl.T = plan->T;
-    pl.n_tiles = plan->n_tiles;
+    pl.n_tiles = plan->n_tiles + plan->n_stiles;              // both lists, checked alike
     SALT_HIP(ctx, salt::launch_plan(pl, s));
   }
   plan->built = true;
@@ -464,6 +473,9 @@ salt_status apply_impl(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_pla
     const int nj = std::min(salt::kMaxJobs, n - first);
     salt::ApplyLaunch a{};
     a.tiles = plan->staged_dev + T;
+    a.stiles = plan->n_stiles ? plan->staged_dev + T + plan->n_tiles : a.tiles;
+    a.n_stiles = plan->n_stiles ? plan->n_stiles : plan->n_tiles;
+    a.MS = plan->MS;
     a.srt = plan->srt;
     a.pool = ctx->pool;
     a.partials = partials;
@@ -860,10 +872,10 @@ salt_status salt_plan_errors(salt_ctx* ctx, const salt_plan* plan_c, void* strea
   int32_t meta[salt::kMetaWords];
   SALT_HIP(ctx, hipMemcpy(meta, plan->meta, sizeof meta, hipMemcpyDeviceToHost));
   *n_errors = meta[salt::kMetaErr];
-  if (meta[salt::kMetaNTiles] != plan->n_tiles || meta[salt::kMetaT] != plan->T) {
+  if (meta[salt::kMetaNTiles] != plan->n_tiles + plan->n_stiles || meta[salt::kMetaT] != plan->T) {
     *n_errors += 1;
     return fail(ctx, SALT_ERR_BAD_STATE, "device plan has %d tiles of %d tokens, host staged %d of %d",
-                meta[salt::kMetaNTiles], meta[salt::kMetaT], plan->n_tiles, plan->T);
+                meta[salt::kMetaNTiles], meta[salt::kMetaT], plan->n_tiles + plan->n_stiles, plan->T);
   }
   return SALT_OK;
 }

@@ -42,6 +42,7 @@
 #define __host__
 #define __forceinline__ inline
 #define __launch_bounds__(...)
+#define amdgpu_waves_per_eu(...)   // an occupancy hint for the GPU compiler only
 #define __shared__ static
 #define __align__(n) __attribute__((aligned(n)))
 

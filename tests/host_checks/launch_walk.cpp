@@ -40,7 +40,7 @@ int main() {
     }
     int n_groups = 0;
     for (int g = 1; g <= C; ++g) n_groups += per_c[g] > 0;
-    const int M = choose_tile_tokens(esize, T, std::max(1, n_groups + (per_c[0] > 0)));
+    const int M = choose_tile_tokens(esize, T, std::max(1, n_groups + (per_c[0] > 0)), n_groups > 0);
     std::vector<int4> tiles;
     cut_tiles(per_c, M, tiles);
     if ((int)tiles.size() > max_tiles(T, C)) fail("more tiles than max_tiles", tiles.size(), max_tiles(T, C));
@@ -62,6 +62,12 @@ int main() {
     a.n_jobs = std::uniform_int_distribution<int>(1, kMaxJobs)(rng);
     a.T = T;
     a.n_tiles = (int)tiles.size();
+    a.tiles = tiles.data();
+    a.MS = M > 64 ? 64 : M;
+    std::vector<int4> stiles;
+    if (a.MS != M) cut_tiles(per_c, a.MS, stiles);
+    a.stiles = a.MS != M ? stiles.data() : tiles.data();
+    a.n_stiles = a.MS != M ? (int)stiles.size() : a.n_tiles;
     a.M = M;
     a.C = C;
     a.r_c = C ? 8 << (rng() % 5) : 0;
@@ -87,7 +93,7 @@ int main() {
       const int item = b;
       const int j = job_of_shrink(a, item);
       const ShrinkCoord sc = shrink_coord(a, a.jobs[j], item);
-      if (sc.tau < 0 || sc.tau >= a.n_tiles || sc.s < 0 || sc.s >= a.jobs[j].S) fail("shrink coord", trial, b);
+      if (sc.tau < 0 || sc.tau >= shrink_tiles(a) || sc.s < 0 || sc.s >= a.jobs[j].S) fail("shrink coord", trial, b);
       if (!sh.insert({j, sc.tau, sc.s, sc.q}).second) fail("shrink item twice", trial, b);
     }
     // expand: the item ranges of G blocks, walked segment by segment as the
@@ -109,7 +115,7 @@ int main() {
     int64_t want_sh = 0, want_ex = 0, poff = 0;
     for (int j = 0; j < a.n_jobs; ++j) {
       const Job& jb = a.jobs[j];
-      want_sh += (int64_t)a.n_tiles * jb.S * a.nq;
+      want_sh += (int64_t)shrink_tiles(a) * jb.S * a.nq;
       want_ex += (int64_t)a.n_tiles * jb.n_col;
       if (jb.Kc % kStepK || jb.cpb % kChunkCols || jb.n_col * jb.cpb < jb.out || (jb.n_col - 1) * jb.cpb >= jb.out)
         fail("range granularity", trial, j);
@@ -124,6 +130,17 @@ int main() {
     }
     if (poff > a.partial_cap) fail("partials overflow", trial, poff, a.partial_cap);
     if ((int64_t)sh.size() != want_sh || (int64_t)ex.size() != want_ex) fail("items missing", trial);
+    // the shrink's tiles cover the batch like the expand's: contiguous, inside
+    // one centroid group each, at most MS tokens
+    {
+      int pos2 = 0;
+      for (int t = 0; t < a.n_stiles; ++t) {
+        const TileHdr h = shrink_tile(a, t);
+        if (h.i0 != pos2 || h.n < 1 || h.n > a.MS || h.n != a.stiles[t].y) fail("shrink tile", trial, t, h.i0);
+        pos2 += h.n;
+      }
+      if (pos2 != T) fail("shrink tiles do not cover the batch", trial, pos2, T);
+    }
   }
   std::printf("ok\n");
   return 0;

@@ -460,11 +460,11 @@ def test_batched_swaps():
 
 def test_plan_tiling_reports_the_launch_structure():
     """salt_plan_tiling: every apply is two launches; decode batches with short
-    centroid groups take 16-token tiles, fp32 16, the Zipf batch and the
-    8192-token prefill 64; the tile count matches the centroid groups."""
+    centroid groups take 16-token tiles, fp32 16, the Zipf batch 32 and the
+    8192-token prefill 128; the tile count matches the centroid groups."""
     _announce("salt_plan_tiling")
     for cfg, kw, want in ((2, {}, (16, 2)), (1, {}, (16, 2)), (4, {}, (16, 2)), (5, {}, (32, 2)),
-                          (3, {"layers": 1}, (64, 2))):
+                          (3, {"layers": 1}, (128, 2))):
         w = synth.make(cfg, 0, **kw)
         run = Run(w, pin_tables=[])
         try:

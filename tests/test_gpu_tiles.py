@@ -1,5 +1,5 @@
-"""GPU parity across the apply's tile and rank classes: tiles of 16, 32 and 64
-tokens (chosen from the mean centroid-group size), centroid ranks in each of the
+"""GPU parity across the apply's tile and rank classes: tiles of 16, 32, 64 and
+128 tokens (chosen from the mean centroid-group size), centroid ranks in each of the
 16 / 32 / 64 / 128 rank classes, residual ranks 0, 1, 2 and 16, no centroids at
 all, ragged table shapes (in / out not multiples of 64), and integer inputs that
 must come out bit-exact.  Every output is compared with the CPU oracle through
@@ -75,6 +75,10 @@ CASES = [
     ("m64 r_c16 r_u16", 2, 16, 512, 20, (16,), 64),
     ("m64 no centroid r_u16", 0, 0, 300, 40, (1, 16), 64),
     ("m64 no centroid r_u0", 0, 0, 200, 10, (0,), 64),
+    ("m128 r_c64 r_u1/2", 2, 64, 1024, 40, (1, 2), 128),
+    ("m128 r_c32 r_u2", 2, 32, 900, 30, (2,), 128),
+    ("m128 r_c128 r_u1", 2, 128, 1024, 40, (1,), 128),
+    ("m64 no centroid, long group, r_u16", 0, 0, 600, 20, (1, 16), 64),
 ]
 
 
@@ -84,7 +88,7 @@ def test_tile_and_rank_classes(name, C, r_c, T, n_slots, ranks, m):
     _run_all(_workload(zlib.crc32(name.encode()) % 1000, RAGGED, C, r_c, T, n_slots, ranks, gamma=C > 0), want_m=m)
 
 
-@pytest.mark.parametrize("name,C,r_c,T,n_slots,ranks,m", [CASES[0], CASES[2], CASES[4], CASES[7]])
+@pytest.mark.parametrize("name,C,r_c,T,n_slots,ranks,m", [CASES[0], CASES[2], CASES[4], CASES[7], CASES[9]])
 def test_tile_classes_integer_bit_exact(name, C, r_c, T, n_slots, ranks, m):
     _announce(f"tiles, integer inputs: {name}")
     _run_all(_workload(7 + zlib.crc32(name.encode()) % 1000, RAGGED, C, r_c, T, n_slots, ranks, exact=True), want_m=m, exact=True)
@@ -99,11 +103,11 @@ def test_fp32_tiles():
 
 def test_large_batch_multi_chunk_plan():
     """T = 9000 > 4096: the plan sorts in three chunks and merges them."""
-    _announce("T=9000 multi-chunk plan, 64-token tiles")
-    _run_all(_workload(60, [("a", 256, 520)], 8, 32, 9000, 700, (1, 2)), want_m=64)
+    _announce("T=9000 multi-chunk plan, 128-token tiles")
+    _run_all(_workload(60, [("a", 256, 520)], 8, 32, 9000, 700, (1, 2)), want_m=128)
 
 
 def test_max_tokens_batch():
     """The largest batch a plan accepts (65536 tokens, 16 sort chunks)."""
     _announce("T=65536, small tables")
-    _run_all(_workload(61, [("a", 128, 64)], 4, 16, 65536, 3000, (1, 2)), want_m=64)
+    _run_all(_workload(61, [("a", 128, 64)], 4, 16, 65536, 3000, (1, 2)), want_m=128)

@@ -3,7 +3,7 @@ AddressSanitizer (tests/cpu_build.py), against the fp64 oracle: every global and
 LDS access of the shrink / expand / plan kernels is checked by the sanitizer, and
 the outputs must meet the same bounds as on the GPU (bf16 1e-2 * (1 + |ref|),
 fp32 1e-5 * (1 + |ref|), integer inputs bit-exact).  The cases cover each tile
-size (16 / 32 / 64 tokens, LDS-staged or not), fp32, residual ranks 0 / 1 / 2 / 16,
+size (16 / 32 / 64 / 128 tokens, LDS-staged or not), fp32, residual ranks 0 / 1 / 2 / 16,
 no centroid, and long-tail concatenated adapters (ranks 17 / 18 and 33 / 34, the
 latter on LDS-staged 64-token tiles)."""
 import numpy as np
@@ -79,3 +79,8 @@ def test_expand_blocks_walk_many_tiles(tmp_path):
     walking the block-chunks of many tiles and tables in turn (integer inputs,
     bit-exact)."""
     _check(tile_workload(4, RAGGED, 8, 64, 256, 80, (1, 2), exact=True), tmp_path, 32, exact=True, n_cu=1)
+
+
+def test_m128_tiles_eight_wave_blocks(tmp_path):
+    """128-token tiles: blocks of 8 waves share one staged centroid operand."""
+    _check(tile_workload(12, RAGGED, 2, 64, 1024, 40, (1,), exact=True), tmp_path, 128, exact=True)
