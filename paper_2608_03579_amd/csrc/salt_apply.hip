@@ -784,7 +784,32 @@ hipError_t launch_m(const ApplyLaunch& a, hipStream_t s, hipEvent_t* ev) {
   }
 }
 
+template <typename E, int MS>
+int shrink_round_m(const ApplyLaunch& a) {
+  auto round = [&](auto kernel, size_t lds) { return resident_blocks(kernel, threads_of<MS>(), lds) * std::max(1, a.n_cu); };
+  const int nb = centroid_blocks(a.r_c);
+  const int ru = a.r_u <= 1 ? 1 : (a.r_u <= 2 ? 2 : kRankChunk);
+#define SALT_ROUND(NB_, RU_) \
+  if (nb == NB_ && ru == RU_) return round(k_shrink<E, MS, NB_, RU_>, shrink_lds<E, MS, NB_, RU_>());
+  SALT_ROUND(0, 1) SALT_ROUND(0, 2) SALT_ROUND(0, kRankChunk)
+  SALT_ROUND(2, 1) SALT_ROUND(2, 2) SALT_ROUND(2, kRankChunk)
+  SALT_ROUND(4, 1) SALT_ROUND(4, 2) SALT_ROUND(4, kRankChunk)
+  SALT_ROUND(8, 1) SALT_ROUND(8, 2) SALT_ROUND(8, kRankChunk)
+#undef SALT_ROUND
+  return 0;
+}
+
 }  // namespace
+
+int shrink_round_blocks(const ApplyLaunch& a) {
+  if (a.esize == 4) return shrink_round_m<float, 16>(a);
+  switch (a.MS) {
+    case 16: return shrink_round_m<uint16_t, 16>(a);
+    case 32: return shrink_round_m<uint16_t, 32>(a);
+    case 64: return shrink_round_m<uint16_t, 64>(a);
+    default: return 0;
+  }
+}
 
 hipError_t launch_apply(const ApplyLaunch& a, hipStream_t s, hipEvent_t* ev) {
   if (a.T <= 0 || a.n_tiles <= 0 || a.n_jobs <= 0) return hipSuccess;

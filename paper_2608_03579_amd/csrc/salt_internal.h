@@ -76,6 +76,9 @@ hipError_t launch_plan(const PlanLaunch& a, hipStream_t s);
 // that record the start and end of the shrink kernel (ev[0], ev[1]) and of the
 // expand kernel (ev[2], ev[3]); null entries are skipped.
 hipError_t launch_apply(const ApplyLaunch& a, hipStream_t s, hipEvent_t* ev);
+// Shrink blocks of launch `a` (esize, M, MS, r_c, r_u set) that one round of the
+// device holds at once: the kernel's occupancy per compute unit x n_cu.
+int shrink_round_blocks(const ApplyLaunch& a);
 // e0 / e1: if set, HIP events that record the fuse kernel's own start and end.
 hipError_t launch_fuse(const FuseArgs& f, int bf16, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 // k_gram then k_gram_finish on s; max_in / max_out: largest in / out over the tables.

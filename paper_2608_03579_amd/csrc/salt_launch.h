@@ -66,7 +66,8 @@ inline int max_tiles(int T, int C) { return cdiv(T, 16) + C + 1; }
 // sum_rank: residual ranks summed over the slots it references (both for the
 // byte counts that bound the partial traffic).  Returns false if the partials
 // of a one-range shrink do not fit.
-inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t sum_rank) {
+// shrink_round: shrink blocks one round of the device holds at once (0: unknown).
+inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t sum_rank, int shrink_round = 0) {
   const int KW = waves_of(a.MS) / (a.MS / 16), CW = waves_of(a.M) / (a.M / 16);
   const int target = 8 * std::max(1, n_cu);        // blocks per launch: a few rounds of the whole device
   const double es = (double)a.esize;
@@ -81,14 +82,36 @@ inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t s
   const double pairs = (double)shrink_tiles(a) * a.nq;
   const int kc_target = std::max(gran, cdiv((int)std::ceil((double)sum_in * pairs / target), gran) * gran);
   const double part_row = 8.0 * a.T * a.R;        // bytes of one K range's partials, written and read
-  std::vector<int> S(a.n_jobs);
+  std::vector<int> S(a.n_jobs), s_cap(a.n_jobs);
   for (int j = 0; j < a.n_jobs; ++j) {
     const Job& jb = a.jobs[j];
     const double bytes = es * ((double)a.T * (jb.in + 2.0 * jb.out) + adapters * (jb.in + jb.out));
-    const int s_balance = cdiv(jb.in, kc_target);
     const int s_traffic = std::max(1, (int)(0.1 * bytes / part_row));
-    const int s_max = cdiv(jb.in, gran);
-    S[j] = std::max(1, std::min({s_balance, s_traffic, s_max}));
+    s_cap[j] = std::max(1, std::min(s_traffic, cdiv(jb.in, gran)));
+    S[j] = std::max(1, std::min(cdiv(jb.in, kc_target), s_cap[j]));
+  }
+  // Shrink tiles of 64 tokens (long groups, many tokens): each block is long,
+  // so a round of the device that is only partly filled costs real time.  The
+  // K-range length is then the one that minimises (rounds of blocks) x (the
+  // longest range); ties go to the longer length (fewer partials).
+  if (a.MS >= 64 && shrink_round > 0) {
+    int max_in = 0;
+    for (int j = 0; j < a.n_jobs; ++j) max_in = std::max(max_in, a.jobs[j].in);
+    double best = 0.0;
+    for (int kc = gran; kc < max_in + gran; kc += gran) {
+      int64_t blocks = 0;
+      int longest = 0;
+      for (int j = 0; j < a.n_jobs; ++j) {
+        const int sj = std::max(1, std::min(cdiv(a.jobs[j].in, kc), s_cap[j]));
+        blocks += (int64_t)shrink_tiles(a) * a.nq * sj;
+        longest = std::max(longest, cdiv(cdiv(a.jobs[j].in, sj), gran) * gran);
+      }
+      const double est = (double)((blocks + shrink_round - 1) / shrink_round) * longest;
+      if (best == 0.0 || est <= best) {
+        best = est;
+        for (int j = 0; j < a.n_jobs; ++j) S[j] = std::max(1, std::min(cdiv(a.jobs[j].in, kc), s_cap[j]));
+      }
+    }
   }
   // partials must fit, and each table's region stays below kMaxBufferBytes:
   // shrink the largest split until they do

@@ -506,7 +506,7 @@ salt_status apply_impl(salt_ctx* ctx, int32_t n, const int32_t* tables, salt_pla
       jb.in = sh.in_dim;
       jb.out = sh.out_dim;
     }
-    if (!salt::configure_launch(a, ctx->n_cu, plan->n_groups_c, plan->sum_rank)) {
+    if (!salt::configure_launch(a, ctx->n_cu, plan->n_groups_c, plan->sum_rank, salt::shrink_round_blocks(a))) {
       if (scratch)
         return fail(ctx, SALT_ERR_OUT_OF_RANGE,
                     "split-K partials of %d tables x %d tokens x %d ranks exceed the static scratch (%zu floats)", nj,

@@ -84,7 +84,7 @@ int main() {
       a.jobs[j].prefix = prefix;
       prefix += a.jobs[j].in + a.jobs[j].out;
     }
-    if (!configure_launch(a, 256, n_groups, (int64_t)a.r_u * 50)) {
+    if (!configure_launch(a, 256, n_groups, (int64_t)a.r_u * 50, (trial % 2) ? 64 + (int)(rng() % 3000) : 0)) {
       if (a.partial_cap >= (int64_t)a.n_jobs * T * a.R) fail("configure_launch refused a launch that fits", trial);
       continue;
     }
