@@ -317,6 +317,8 @@ def run_gpu(name, w, dw, spec, steps, warmup, hip, salt, meas=None):
     bytes_tab = np.array([apply_bytes(w, maps, t) for t in range(n_tab)], dtype=np.float64)
     n_meas = meas or max(2, min(200, 2000 // max(1, len(groups))))
     ev = [hip.Event() for _ in range(4 * n_meas * len(groups))]
+    for p in plans[:n_meas]:
+        p.build(stream.h)  # a short timed run may not have built every rotated plan
     i = 0
     for k in range(n_meas):
         slot = k % rot
@@ -450,6 +452,8 @@ def run_swaps(w, dw, ctx, plans, groups, tabs, xs, ys, stream, hip, salt, n=32, 
 TRAFFIC_PROFILES = {
     "prefill": "profiles/k_expand_llama32-3b_28layer_prefill_T8192_hbm_traffic.md",
     "qproj": "profiles/k_shrink_k_expand_llama32-3b_qproj_decode_T64_hbm_traffic.md",
+    "decode8b": "profiles/k_shrink_k_expand_llama31-8b_decode_T256_trace_traffic.md",
+    "zipf": "profiles/k_shrink_k_expand_llama32-3b_zipf_T512_trace_traffic.md",
 }
 
 
@@ -611,11 +615,12 @@ def tables_summary(w):
     return f"{len(groups)} layers x [{', '.join(shapes)}]" if len(groups) > 1 else ", ".join(shapes)
 
 
-def sub_record(res):
+def sub_record(name, res):
     keep = ("workload", "T", "tables", "ms_per_step", "tokens_per_s", "step_bytes", "step_GBps", "step_frac",
             "tiling", "kernels")
     r = {k: res[k] for k in keep}
     r["roofline"] = {k: res["roofline"][k] for k in ("kernel", "achieved", "frac", "avg_us", "bytes_per_launch")}
+    r["roofline"]["traffic"] = measured_traffic(name, res["roofline"]["kernel"].split()[0])
     if res.get("swap"):
         r["swap"] = res["swap"]
     return r
@@ -685,7 +690,7 @@ def main():
     if args.workload == "prefill" and not args.no_sub:
         for name, s_steps, s_warm in SUB_RECORDS:
             sw, sdw = make_workload(WORKLOADS[name])
-            subs[name] = sub_record(run_gpu(name, sw, sdw, WORKLOADS[name], s_steps, s_warm, hip, salt))
+            subs[name] = sub_record(name, run_gpu(name, sw, sdw, WORKLOADS[name], s_steps, s_warm, hip, salt))
         z, zb = subs["zipf"], subs["zipf-baseline"]
         subs["zipf_salt_vs_rank16_baseline"] = {
             "bytes_ratio_baseline_over_salt": zb["step_bytes"] / z["step_bytes"],
