@@ -864,7 +864,7 @@ hipError_t kernels_init(int device) {
   const size_t need_shrink = std::max({shrink_lds<uint16_t, 128, 8, kRankChunk>(),
                                        shrink_lds<uint16_t, 64, 8, kRankChunk>(), shrink_lds<uint16_t, 32, 8, kRankChunk>(),
                                        shrink_lds<uint16_t, 64, 4, 2>(), shrink_lds<uint16_t, 32, 4, 2>()});
-  const size_t need_plan = sizeof(uint64_t) * kSortChunk + 256;
+  const size_t need_plan = (sizeof(uint64_t) + sizeof(int) + 1) * kSortChunk + 256;
   const size_t need = std::max(need_expand, std::max(need_shrink, need_plan));
   if ((size_t)lds_max < need) return hipErrorInvalidConfiguration;
   float* p = nullptr;

@@ -28,7 +28,8 @@ struct PlanLaunch {
   int32_t* grp_off;     // [T + 1]
   int32_t* meta;        // [kMetaWords]
   int32_t T;
-  int32_t n_tiles;
+  int32_t n_tiles;      // tiles [0, n_list0) and [n_list0, n_tiles): two lists, each covering [0, T)
+  int32_t n_list0;      // (== n_tiles: one list)
 };
 
 // One centroid fused into a base weight: W <- rne(W + gamma * A_c B_c).

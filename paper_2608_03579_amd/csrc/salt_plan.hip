@@ -4,8 +4,9 @@
 // unique, so the order, the segments (runs of equal (centroid, slot)) and the
 // groups (runs of equal centroid) are unique and bit-exact.
 //
-//   k_plan_sort:   one block per chunk of kSortChunk tokens sorts its keys in LDS
-//                  (bitonic network).  A batch of one chunk is finished in the
+//   k_plan_sort:   one block per chunk of kSortChunk tokens sorts its keys
+//                  (bitonic network: in-wave steps on registers, the others in
+//                  LDS).  A batch of one chunk is finished in the
 //                  same block; larger batches write their sorted chunks.
 //   k_plan_merge:  (more than one chunk) a key's place is its place in its own
 //                  chunk plus, for every other chunk, the number of keys below
@@ -35,13 +36,17 @@ __device__ __forceinline__ int key_c(uint64_t k) { return (int)(k >> 42) - 1; }
 __device__ __forceinline__ int key_u(uint64_t k) { return (int)((k >> 21) & kTokMask) - 1; }
 __device__ __forceinline__ int key_tok(uint64_t k) { return (int)(k & kTokMask); }
 
-// Sorted record at place p: token t of key k with its slot, rank and gamma.
-__device__ __forceinline__ void write_place(const PlanLaunch& a, int p, uint64_t k) {
+// Sorted record at place p: token t of key k with its slot (from the key), rank
+// r and gamma bits gb.
+__device__ __forceinline__ void write_record(const PlanLaunch& a, int p, uint64_t k, int r, int gb) {
   const int t = iclamp(key_tok(k), 0, a.T - 1);
-  const int4 m = a.maps[t];
   const int q = iclamp(p, 0, a.T - 1);
-  a.srt[q] = make_int4(t, m.y, m.z, m.w);
+  a.srt[q] = make_int4(t, key_u(k), r, gb);
   a.perm[q] = t;
+}
+__device__ __forceinline__ void write_place(const PlanLaunch& a, int p, uint64_t k) {
+  const int4 m = a.maps[iclamp(key_tok(k), 0, a.T - 1)];
+  write_record(a, p, k, m.z, m.w);
 }
 
 // Exclusive block-wide prefix of two counts (1024 threads); totals to all.
@@ -111,16 +116,22 @@ __device__ void plan_finish(const PlanLaunch& a, const uint64_t* keys, int* s_w)
       ++es;
     }
   }
-  // tiles staged by the host: each must hold tokens of its own centroid only
+  // tiles staged by the host: each list covers [0, T) with consecutive tiles,
+  // and each tile holds tokens of its own centroid only, which for sorted keys
+  // (centroid first) holds exactly when its first and last keys carry it
   int bad = 0;
   for (int tau = tid; tau < a.n_tiles; tau += kPlanThreads) {
     const int4 h = a.tiles[tau];
     const int i0 = iclamp(h.x, 0, T - 1), n = iclamp(h.y, 0, T - i0);
-    if (n != h.y || i0 != h.x || n <= 0) {
-      ++bad;
-      continue;
+    const bool first = tau == 0 || tau == a.n_list0, last = tau == a.n_tiles - 1 || tau == a.n_list0 - 1;
+    int start = 0;
+    if (!first) {
+      const int4 g = a.tiles[tau - 1];
+      start = g.x + g.y;
     }
-    for (int k = 0; k < n; ++k) bad += key_c(keys[i0 + k]) != h.z;
+    if (n != h.y || i0 != h.x || n <= 0 || i0 != start || (last && i0 + n != T) || key_c(keys[i0]) != h.z ||
+        key_c(keys[i0 + n - 1]) != h.z)
+      ++bad;
   }
   if (bad) atomicAdd(a.meta + kMetaErr, bad);
   if (tid == 0) {
@@ -133,8 +144,24 @@ __device__ void plan_finish(const PlanLaunch& a, const uint64_t* keys, int* s_w)
   }
 }
 
+// Keys a thread of k_plan_sort holds at most: places tid + kPlanThreads e.
+constexpr int kKeysPerThread = kSortChunk / kPlanThreads;
+static_assert(kSortChunk % kPlanThreads == 0, "a sort chunk is whole keys per thread");
+
+// One compare-exchange step of the bitonic network (merge size k, distance j <
+// 64) on the key x at place p, whose partner p ^ j is lane ^ j of the same
+// wave: the pair ends ascending when (p & k) == 0 and descending otherwise, so
+// the lower place keeps the smaller key exactly when the two conditions agree.
+__device__ __forceinline__ uint64_t exchange_in_wave(uint64_t x, int p, int j, int k) {
+  const uint64_t y = __shfl_xor(x, j);
+  const bool keep_min = ((p & k) == 0) == ((p & j) == 0);
+  return keep_min == (x < y) ? x : y;
+}
+
 __global__ void __launch_bounds__(kPlanThreads) k_plan_sort(const PlanLaunch a) {
   __shared__ uint64_t s_keys[kSortChunk];
+  __shared__ int s_gb[kSortChunk];                   // gamma bits and rank of the chunk's tokens,
+  __shared__ uint8_t s_r[kSortChunk];                // for the records of a one-chunk batch
   __shared__ int s_w[64];
   const int tid = threadIdx.x;
   const int base = blockIdx.x * kSortChunk;
@@ -143,35 +170,70 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_sort(const PlanLaunch a) 
   // the network spans the smallest power of two >= cnt (padding keys sort last)
   int n2 = 2;
   while (n2 < cnt) n2 <<= 1;
-  for (int i = tid; i < n2; i += kPlanThreads) {
-    uint64_t k = kPad;
-    if (i < cnt) {
-      const int4 m = a.maps[base + i];
-      k = plan_key(m.x, m.y, base + i);
+  // Bitonic sort, ascending.  Thread tid holds the places tid + kPlanThreads e,
+  // e < ne; steps whose partners lie within a wave (distance j < 64) run on
+  // registers through lane shuffles, in the waves that hold places; steps of a
+  // larger distance run in LDS, one pair per thread, with a block barrier after
+  // each.  (All loop bounds and the wave test are uniform over a wave.)
+  const int ne = imax(1, n2 / kPlanThreads);
+  const bool holds = (tid & ~63) < n2;
+  uint64_t r[kKeysPerThread];
+#pragma unroll
+  for (int e = 0; e < kKeysPerThread; ++e) {
+    const int p = tid + kPlanThreads * e;
+    r[e] = kPad;
+    if (e < ne && p < cnt) {
+      const int4 m = a.maps[base + p];
+      r[e] = plan_key(m.x, m.y, base + p);
+      s_gb[p] = m.w;
+      s_r[p] = (uint8_t)iclamp(m.z, 0, 255);
     }
-    s_keys[i] = k;
   }
-  __syncthreads();
-  // bitonic sort, ascending
   for (int k = 2; k <= n2; k <<= 1) {
-    for (int j = k >> 1; j > 0; j >>= 1) {
-      for (int i = tid; i < n2 / 2; i += kPlanThreads) {
-        const int lo = ((i & ~(j - 1)) << 1) | (i & (j - 1)), hi = lo + j;
-        const uint64_t x = s_keys[lo], y = s_keys[hi];
-        const bool up = (lo & k) == 0;
-        if ((x > y) == up) {
-          s_keys[lo] = y;
-          s_keys[hi] = x;
-        }
-      }
+    if (k / 2 >= 64) {
+#pragma unroll
+      for (int e = 0; e < kKeysPerThread; ++e)
+        if (e < ne && tid + kPlanThreads * e < n2) s_keys[tid + kPlanThreads * e] = r[e];
       __syncthreads();
+      for (int j = k >> 1; j >= 64; j >>= 1) {
+        for (int i = tid; i < n2 / 2; i += kPlanThreads) {
+          const int lo = ((i & ~(j - 1)) << 1) | (i & (j - 1)), hi = lo + j;
+          const uint64_t x = s_keys[lo], y = s_keys[hi];
+          if ((x > y) == ((lo & k) == 0)) {
+            s_keys[lo] = y;
+            s_keys[hi] = x;
+          }
+        }
+        __syncthreads();
+      }
+#pragma unroll
+      for (int e = 0; e < kKeysPerThread; ++e)
+        if (e < ne && tid + kPlanThreads * e < n2) r[e] = s_keys[tid + kPlanThreads * e];
+    }
+    if (holds) {
+      for (int j = imin(k >> 1, 32); j > 0; j >>= 1) {
+#pragma unroll
+        for (int e = 0; e < kKeysPerThread; ++e)
+          if (e < ne) r[e] = exchange_in_wave(r[e], tid + kPlanThreads * e, j, k);
+      }
     }
   }
   if (gridDim.x == 1) {
-    for (int i = tid; i < cnt; i += kPlanThreads) write_place(a, i, s_keys[i]);
+    // (a thread writes the places it alone read last)
+#pragma unroll
+    for (int e = 0; e < kKeysPerThread; ++e)
+      if (e < ne && tid + kPlanThreads * e < n2) s_keys[tid + kPlanThreads * e] = r[e];
+    __syncthreads();
+    for (int i = tid; i < cnt; i += kPlanThreads) {
+      const uint64_t k = s_keys[i];
+      const int t = iclamp(key_tok(k), 0, cnt - 1);   // (one chunk: base is 0)
+      write_record(a, i, k, s_r[t], s_gb[t]);
+    }
     plan_finish(a, s_keys, s_w);
   } else {
-    for (int i = tid; i < cnt; i += kPlanThreads) a.keys[base + i] = s_keys[i];
+#pragma unroll
+    for (int e = 0; e < kKeysPerThread; ++e)
+      if (e < ne && tid + kPlanThreads * e < cnt) a.keys[base + tid + kPlanThreads * e] = r[e];
   }
 }
 

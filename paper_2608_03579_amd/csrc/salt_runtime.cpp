@@ -418,6 +418,7 @@ salt_status build_impl(salt_ctx* ctx, salt_plan* plan, hipStream_t s) {
     pl.meta = plan->meta;
     pl.T = plan->T;
     pl.n_tiles = plan->n_tiles + plan->n_stiles;              // both lists, checked alike
+    pl.n_list0 = plan->n_tiles;
     SALT_HIP(ctx, salt::launch_plan(pl, s));
   }
   plan->built = true;
