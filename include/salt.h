@@ -123,7 +123,10 @@ SALT_API size_t salt_residual_bytes_for(salt_dtype dtype, int32_t n_tables, cons
  *         for each table in order, At_u[r_u][in] followed by B_u[r_u][out];
  *         bytes must equal salt_residual_bytes(ctx, r_u).  r_u == 0 empties the
  *         residual term of the slot (bytes == 0, blob may be NULL).
- * Asynchronous: one hipMemcpyAsync on the context's side stream.  The copy first
+ * Asynchronous, on the context's side stream: a blob inside memory from
+ * salt_host_alloc is read by the device directly (the gather kernel of
+ * salt_load_residuals); any other page-locked blob takes one hipMemcpyAsync.
+ * The copy first
  * waits for every enqueued salt_apply whose plan references this slot, so an
  * in-flight apply still sees the slot's previous residual.  Every later
  * salt_apply whose plan references the slot waits for this copy.  The blob must
@@ -143,14 +146,18 @@ SALT_API salt_status salt_load_residual(salt_ctx* ctx, int32_t slot, int32_t r_u
  * salt_load_residual would do them one by one, but validated as a whole first
  * (an invalid entry fails the call and changes no state) and ordered with one
  * event for the whole batch.  Blobs inside memory from salt_host_alloc need no
- * pointer query.  A slot listed twice receives its last blob. */
+ * pointer query; when every blob of the call lies in such memory and no slot
+ * repeats, one kernel per 64 blobs reads them all over PCIe into their slots
+ * (no per-blob DMA set-up), else each blob takes its own hipMemcpyAsync, in
+ * order.  A slot listed twice receives its last blob. */
 SALT_API salt_status salt_load_residuals(salt_ctx* ctx, int32_t n, const int32_t* slots, const int32_t* ranks,
                                          const void* const* blobs, const size_t* bytes);
 
 /* Block the host until every residual swap enqueued so far has completed. */
 SALT_API salt_status salt_wait_loads(salt_ctx* ctx);
 
-/* Page-locked host buffers for residual blobs (hipHostMalloc / hipHostFree). */
+/* Page-locked host buffers for residual blobs (hipHostMalloc / hipHostFree),
+ * mapped for the device so that swaps can read them in place. */
 SALT_API salt_status salt_host_alloc(size_t bytes, void** out);
 SALT_API void salt_host_free(void* p);
 

@@ -14,7 +14,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libsalt.so")
-SOURCES = [os.path.join(CSRC, f) for f in ("salt_plan.hip", "salt_apply.hip", "salt_fuse_gram.hip", "salt_runtime.cpp")]
+SOURCES = [os.path.join(CSRC, f) for f in ("salt_plan.hip", "salt_apply.hip", "salt_fuse_gram.hip", "salt_swap.hip", "salt_runtime.cpp")]
 ARCH = "gfx950"
 
 BUILD_DIR = os.path.join(HERE, "_build")

@@ -62,6 +62,17 @@ struct GramArgs {
   double* out;              // [n_tables][3], device
 };
 
+// Residual blobs one swap launch gathers from mapped page-locked host memory:
+// blob i is vecs[i] 16-byte vectors from src[i] (a device-visible host address)
+// into dst[i] (its slot in the pool).
+constexpr int kSwapMax = 64;
+struct SwapArgs {
+  const uint4* src[kSwapMax];
+  uint4* dst[kSwapMax];
+  int64_t vecs[kSwapMax];
+  int32_t n;
+};
+
 // 16-rank blocks of the centroid a shrink lane holds for rank r_c (r_c <= 16 * result).
 constexpr int centroid_blocks(int r_c) { return r_c == 0 ? 0 : (r_c <= 32 ? 2 : (r_c <= 64 ? 4 : 8)); }
 
@@ -83,6 +94,8 @@ int shrink_round_blocks(const ApplyLaunch& a);
 // e0 / e1: if set, HIP events that record the fuse kernel's own start and end.
 hipError_t launch_fuse(const FuseArgs& f, int bf16, hipStream_t s, hipEvent_t e0, hipEvent_t e1);
 // k_gram then k_gram_finish on s; max_in / max_out: largest in / out over the tables.
+// k_swap_gather on s: every blob of a (n <= kSwapMax) in one launch.
+hipError_t launch_swap(const SwapArgs& a, hipStream_t s);
 hipError_t launch_gram(const GramArgs& a, int max_in, int max_out, int bf16, hipStream_t s);
 
 }  // namespace salt

@@ -37,29 +37,49 @@ struct EventRing {
   int64_t done = -1;  // all sequences <= done have completed
 };
 
-// Page-locked ranges handed out by salt_host_alloc: a blob inside one of them
-// needs no pointer query before its swap.
+// Page-locked ranges handed out by salt_host_alloc, with the address under
+// which the device reads each (null if it has none): a blob inside one of them
+// needs no pointer query before its swap, and one with a device view can be
+// gathered by a kernel.
+struct HostRange {
+  uintptr_t start;
+  size_t size;
+  uintptr_t dev;
+};
 struct HostRanges {
   std::mutex mu;
-  std::vector<std::pair<uintptr_t, size_t>> r;   // sorted by start
-  bool contains(const void* p, size_t n) {
+  std::vector<HostRange> r;   // sorted by start
+  // The range holding [p, p + n), or null (call with mu held).
+  const HostRange* find(const void* p, size_t n) const {
     const uintptr_t a = reinterpret_cast<uintptr_t>(p);
-    std::lock_guard<std::mutex> g(mu);
-    auto it = std::upper_bound(r.begin(), r.end(), std::make_pair(a, ~(size_t)0));
-    if (it == r.begin()) return false;
+    auto it = std::upper_bound(r.begin(), r.end(), a, [](uintptr_t x, const HostRange& h) { return x < h.start; });
+    if (it == r.begin()) return nullptr;
     --it;
-    return a >= it->first && a - it->first <= it->second && n <= it->second - (a - it->first);
+    return (a >= it->start && a - it->start <= it->size && n <= it->size - (a - it->start)) ? &*it : nullptr;
   }
-  void add(void* p, size_t n) {
+  bool contains(const void* p, size_t n) {
     std::lock_guard<std::mutex> g(mu);
-    auto v = std::make_pair(reinterpret_cast<uintptr_t>(p), n);
-    r.insert(std::upper_bound(r.begin(), r.end(), v), v);
+    return find(p, n) != nullptr;
+  }
+  // Device address of host bytes [p, p + n), or null.
+  const void* device_view(const void* p, size_t n) {
+    std::lock_guard<std::mutex> g(mu);
+    const HostRange* h = find(p, n);
+    if (!h || !h->dev) return nullptr;
+    return reinterpret_cast<const void*>(h->dev + (reinterpret_cast<uintptr_t>(p) - h->start));
+  }
+  void add(void* p, size_t n, void* dev) {
+    std::lock_guard<std::mutex> g(mu);
+    const HostRange v{reinterpret_cast<uintptr_t>(p), n, reinterpret_cast<uintptr_t>(dev)};
+    r.insert(std::upper_bound(r.begin(), r.end(), v.start,
+                              [](uintptr_t x, const HostRange& h) { return x < h.start; }),
+             v);
   }
   void remove(void* p) {
     std::lock_guard<std::mutex> g(mu);
     const uintptr_t a = reinterpret_cast<uintptr_t>(p);
     for (auto it = r.begin(); it != r.end(); ++it)
-      if (it->first == a) {
+      if (it->start == a) {
         r.erase(it);
         return;
       }
@@ -563,10 +583,37 @@ salt_status load_impl(salt_ctx* ctx, int32_t n, const int32_t* slots, const int3
   }
   for (int i = 0; i < n; ++i) wait_reader = std::max(wait_reader, ctx->slot_reader[slots[i]]);
   SALT_HIP(ctx, ring_wait(ctx->readers, ctx->side, wait_reader));
-  for (int i = 0; i < n; ++i)
-    if (bytes[i] > 0)
-      SALT_HIP(ctx, hipMemcpyAsync(ctx->pool + (size_t)slots[i] * ctx->slot_stride, blobs[i], bytes[i],
-                                   hipMemcpyHostToDevice, ctx->side));
+  // One gather kernel per kSwapMax blobs when every blob has a device view and
+  // no slot repeats; otherwise one DMA copy per blob, in order (so that a slot
+  // listed twice receives its last blob).
+  std::vector<const void*> views((size_t)n, nullptr);
+  bool gather = true;
+  for (int i = 0; i < n && gather; ++i)
+    if (bytes[i] > 0) gather = (views[(size_t)i] = g_host_ranges.device_view(blobs[i], bytes[i])) != nullptr;
+  if (gather) {
+    std::vector<int32_t> sorted(slots, slots + n);
+    std::sort(sorted.begin(), sorted.end());
+    gather = std::adjacent_find(sorted.begin(), sorted.end()) == sorted.end();
+  }
+  if (gather) {
+    salt::SwapArgs g{};
+    for (int i = 0; i < n; ++i) {
+      if (bytes[i] == 0) continue;
+      g.src[g.n] = static_cast<const uint4*>(views[(size_t)i]);
+      g.dst[g.n] = reinterpret_cast<uint4*>(ctx->pool + (size_t)slots[i] * ctx->slot_stride);
+      g.vecs[g.n] = (int64_t)(bytes[i] / 16);                 // (bytes: rank x sum of multiples of 8 x esize)
+      if (++g.n == salt::kSwapMax) {
+        SALT_HIP(ctx, salt::launch_swap(g, ctx->side));
+        g.n = 0;
+      }
+    }
+    SALT_HIP(ctx, salt::launch_swap(g, ctx->side));
+  } else {
+    for (int i = 0; i < n; ++i)
+      if (bytes[i] > 0)
+        SALT_HIP(ctx, hipMemcpyAsync(ctx->pool + (size_t)slots[i] * ctx->slot_stride, blobs[i], bytes[i],
+                                     hipMemcpyHostToDevice, ctx->side));
+  }
   int64_t seq;
   SALT_HIP(ctx, ring_record(ctx->loaders, ctx->side, &seq));
   for (int i = 0; i < n; ++i) {
@@ -650,7 +697,13 @@ salt_status salt_host_alloc(size_t bytes, void** out) {
     *out = nullptr;
     return SALT_ERR_OUT_OF_MEMORY;
   }
-  g_host_ranges.add(*out, bytes);
+  // the address under which the device reads the buffer (swaps gather from it)
+  void* dev = nullptr;
+  if (hipHostGetDevicePointer(&dev, *out, 0) != hipSuccess) {
+    (void)hipGetLastError();
+    dev = nullptr;
+  }
+  g_host_ranges.add(*out, bytes, dev);
   return SALT_OK;
 }
 

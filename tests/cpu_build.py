@@ -12,6 +12,7 @@ Test infrastructure only.
 """
 from __future__ import annotations
 
+import fcntl
 import hashlib
 import os
 import shutil
@@ -26,7 +27,7 @@ ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(ROOT, "paper_2608_03579_amd", "csrc")
 SHIM = os.path.join(HERE, "cpu_kernels")
 BUILD = os.path.join(SHIM, "_build")
-SOURCES = ("salt_plan.hip", "salt_apply.hip", "salt_fuse_gram.hip", "salt_runtime.cpp")
+SOURCES = ("salt_plan.hip", "salt_apply.hip", "salt_fuse_gram.hip", "salt_swap.hip", "salt_runtime.cpp")
 HEADERS = ("salt_device.h", "salt_internal.h", "salt_layout.h", "salt_launch.h")
 DYN_LDS = "extern __shared__ __attribute__((aligned(16))) char lds[];"
 CLANG = "/opt/rocm/llvm/bin/clang++"
@@ -47,9 +48,21 @@ def _digest() -> str:
 
 
 def build() -> str:
+    """The harness for the current sources, built once; concurrent test
+    processes wait on a lock file while one of them builds."""
     exe = os.path.join(BUILD, "harness-" + _digest())
     if os.path.exists(exe):
         return exe
+    os.makedirs(BUILD, exist_ok=True)
+    with open(os.path.join(BUILD, ".lock"), "w") as lk:
+        fcntl.flock(lk, fcntl.LOCK_EX)
+        try:
+            return exe if os.path.exists(exe) else _build(exe)
+        finally:
+            fcntl.flock(lk, fcntl.LOCK_UN)
+
+
+def _build(exe: str) -> str:
     src = os.path.join(BUILD, "src")
     shutil.rmtree(src, ignore_errors=True)
     os.makedirs(src)
@@ -61,7 +74,7 @@ def build() -> str:
     srcs = [os.path.join(src, n) for n in SOURCES] + [os.path.join(SHIM, "harness.cpp")]
     flags = ["-std=c++17", "-O1", "-g", "-fsanitize=address", "-fno-omit-frame-pointer", "-w"]
     for old in os.listdir(BUILD):
-        if old.startswith("harness-"):
+        if old.startswith("harness-") and old != os.path.basename(exe):
             os.remove(os.path.join(BUILD, old))
     # one compiler process per source, then one link
     objs = [os.path.join(src, os.path.basename(s) + ".o") for s in srcs]

@@ -492,6 +492,12 @@ inline hipError_t hipHostMalloc(T** p, size_t n, unsigned f) {
   return hipHostMalloc(reinterpret_cast<void**>(p), n, f);
 }
 inline hipError_t hipHostFree(void* p) { return hipFree(p); }
+inline hipError_t hipHostGetDevicePointer(void** d, void* h, unsigned) {
+  const salt_cpu::Alloc* al = salt_cpu::find(h);
+  if (!al || !al->host) return hipErrorInvalidValue;
+  *d = h;
+  return hipSuccess;
+}
 inline hipError_t hipMemcpy(void* d, const void* s, size_t n, hipMemcpyKind) {
   if (n) memcpy(d, s, n);
   return hipSuccess;
