@@ -458,6 +458,55 @@ def test_batched_swaps():
         run.close()
 
 
+def test_swap_paths_many_blobs_and_a_repeated_slot():
+    """salt_load_residuals past one gather launch (100 blobs from salt_host_alloc
+    memory: launches of 64 and 36), then a call that lists a slot twice (ordered
+    DMA copies: the last blob wins); after each, an apply that reads the swapped
+    slots is compared with the oracle."""
+    _announce("salt_load_residuals: 100 gathered swaps, then a slot listed twice")
+    from paper_2608_03579_amd import salt
+    from tests.gpu_harness import to_dev
+    w = synth.make(4, 5)
+    run = Run(w)
+    bufs = []
+    try:
+        run.set_and_build()
+        slots = [int(s) for s in w.referenced_slots() if int(w.slot_rank[s]) == 2][:100]
+        assert len(slots) == 100
+        nb = run.ctx.residual_bytes(2)
+        bufs = [salt.HostBuffer(nb) for _ in slots]
+        for b, s in zip(bufs, slots):
+            b.view(np.uint16)[:] = w.residual_blob(s, 1)
+        assert run.ctx.load_residuals_ptr(slots, [2] * 100, [b.ptr for b in bufs], [nb] * 100) == salt.OK
+        for s in slots:
+            run.gen[s] = 1
+        t = 2
+        xd = to_dev(w.x(t))
+
+        def check():
+            y = to_dev(w.y0(t))
+            run.ctx.apply(t, run.plan, xd.ptr, y.ptr, run.stream)
+            run._stream.synchronize()
+            run.ctx.wait_loads()
+            ok, worst, nbad = close_enough(oracle.decode(y.to_host(), w.dtype), run.oracle_table(t), TOL_NORTH_STAR)
+            assert ok, f"{nbad} out of tolerance, worst {worst:.3f}x"
+
+        check()
+        s0 = slots[0]
+        b2, b3 = salt.HostBuffer(nb), salt.HostBuffer(nb)
+        bufs += [b2, b3]
+        b2.view(np.uint16)[:] = w.residual_blob(s0, 2)
+        b3.view(np.uint16)[:] = w.residual_blob(s0, 3)
+        assert run.ctx.load_residuals_ptr([s0, slots[1], s0], [2, 2, 2], [b2.ptr, bufs[1].ptr, b3.ptr],
+                                          [nb] * 3) == salt.OK
+        run.gen[s0] = 3
+        check()
+    finally:
+        run.close()
+        for b in bufs:
+            b.free()
+
+
 def test_plan_tiling_reports_the_launch_structure():
     """salt_plan_tiling: every apply is two launches; decode batches with short
     centroid groups take 16-token tiles, fp32 16, the Zipf batch 32 and the

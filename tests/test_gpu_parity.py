@@ -153,3 +153,25 @@ def test_prefill_reduced():
         _check_batch(run, list(range(len(w.tables))), rows=rows)
     finally:
         run.close()
+
+
+def test_prefill_full_layer_sampled():
+    """One Llama-3.2-3B layer at the prefill's full size (T = 8192, 8 centroids of
+    rank 64, 256 users of rank 1) in the launch configuration the bench times:
+    128-token expand tiles over 64-token shrink tiles, one salt_apply_batch of the
+    layer's 7 tables.  The plan is compared whole; outputs on sampled rows (every
+    61st token and the last), which the oracle computes one by one."""
+    _announce("cfg3 prefill, one layer at T=8192, salt_apply_batch of 7 tables, sampled rows")
+    w = synth.make(3, 0, layers=1)
+    assert w.T == 8192
+    run = Run(w)
+    try:
+        run.set_and_build()
+        m, _, launches = run.plan.tiling()
+        assert (m, launches) == (128, 2)
+        _check_plan(run)
+        rows = list(range(0, w.T, 61)) + [w.T - 1]
+        _check_batch(run, list(range(len(w.tables))), rows=rows)
+    finally:
+        run.close()
+
