@@ -157,7 +157,8 @@ SALT_API salt_status salt_load_residuals(salt_ctx* ctx, int32_t n, const int32_t
 SALT_API salt_status salt_wait_loads(salt_ctx* ctx);
 
 /* Page-locked host buffers for residual blobs (hipHostMalloc / hipHostFree),
- * mapped for the device so that swaps can read them in place. */
+ * mapped for the device current at the call, so that swaps of a context on that
+ * device can read them in place (on another device they take DMA copies). */
 SALT_API salt_status salt_host_alloc(size_t bytes, void** out);
 SALT_API void salt_host_free(void* p);
 

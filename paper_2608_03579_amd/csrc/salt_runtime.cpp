@@ -44,7 +44,8 @@ struct EventRing {
 struct HostRange {
   uintptr_t start;
   size_t size;
-  uintptr_t dev;
+  uintptr_t dev;      // device address of start, valid on device `device`
+  int device;
 };
 struct HostRanges {
   std::mutex mu;
@@ -61,16 +62,16 @@ struct HostRanges {
     std::lock_guard<std::mutex> g(mu);
     return find(p, n) != nullptr;
   }
-  // Device address of host bytes [p, p + n), or null.
-  const void* device_view(const void* p, size_t n) {
+  // Address under which `device` reads host bytes [p, p + n), or null.
+  const void* device_view(const void* p, size_t n, int device) {
     std::lock_guard<std::mutex> g(mu);
     const HostRange* h = find(p, n);
-    if (!h || !h->dev) return nullptr;
+    if (!h || !h->dev || h->device != device) return nullptr;
     return reinterpret_cast<const void*>(h->dev + (reinterpret_cast<uintptr_t>(p) - h->start));
   }
-  void add(void* p, size_t n, void* dev) {
+  void add(void* p, size_t n, void* dev, int device) {
     std::lock_guard<std::mutex> g(mu);
-    const HostRange v{reinterpret_cast<uintptr_t>(p), n, reinterpret_cast<uintptr_t>(dev)};
+    const HostRange v{reinterpret_cast<uintptr_t>(p), n, reinterpret_cast<uintptr_t>(dev), device};
     r.insert(std::upper_bound(r.begin(), r.end(), v.start,
                               [](uintptr_t x, const HostRange& h) { return x < h.start; }),
              v);
@@ -589,7 +590,8 @@ salt_status load_impl(salt_ctx* ctx, int32_t n, const int32_t* slots, const int3
   std::vector<const void*> views((size_t)n, nullptr);
   bool gather = true;
   for (int i = 0; i < n && gather; ++i)
-    if (bytes[i] > 0) gather = (views[(size_t)i] = g_host_ranges.device_view(blobs[i], bytes[i])) != nullptr;
+    if (bytes[i] > 0)
+      gather = (views[(size_t)i] = g_host_ranges.device_view(blobs[i], bytes[i], ctx->device)) != nullptr;
   if (gather) {
     std::vector<int32_t> sorted(slots, slots + n);
     std::sort(sorted.begin(), sorted.end());
@@ -697,13 +699,15 @@ salt_status salt_host_alloc(size_t bytes, void** out) {
     *out = nullptr;
     return SALT_ERR_OUT_OF_MEMORY;
   }
-  // the address under which the device reads the buffer (swaps gather from it)
+  // the address under which the current device reads the buffer (swaps of a
+  // context on that device gather from it)
   void* dev = nullptr;
-  if (hipHostGetDevicePointer(&dev, *out, 0) != hipSuccess) {
+  int device = -1;
+  if (hipGetDevice(&device) != hipSuccess || hipHostGetDevicePointer(&dev, *out, 0) != hipSuccess) {
     (void)hipGetLastError();
     dev = nullptr;
   }
-  g_host_ranges.add(*out, bytes, dev);
+  g_host_ranges.add(*out, bytes, dev, device);
   return SALT_OK;
 }
 
