@@ -331,8 +331,9 @@ SALT_API salt_status salt_fuse_centroid_timed(salt_ctx* ctx, int32_t table, int3
  *       r1, r2 in [1, 256]; a centroid is passed the same way.
  *   out: host, [n_tables][3] doubles: Tr(dW1^T dW2), ||dW1||_F^2, ||dW2||_F^2 per table.
  * The Grams accumulate in fp32 (MFMA over in and over out), their elementwise
- * products in fp64.  Allocates temporary device memory, enqueues on `stream`
- * and synchronises it before returning.  Errors: SALT_ERR_OUT_OF_RANGE (rank),
+ * products in fp64.  Keeps its device scratch in the context (allocated on the
+ * first call, grown when a call needs more, freed by salt_destroy), enqueues on
+ * `stream` and synchronises it before returning (the results are host values).  Errors: SALT_ERR_OUT_OF_RANGE (rank),
  * SALT_ERR_INVALID_ARG (null or misaligned pointer), SALT_ERR_OUT_OF_MEMORY. */
 SALT_API salt_status salt_adapter_gram(salt_ctx* ctx, const void* blob1, int32_t r1, const void* blob2,
                                        int32_t r2, double* out, void* stream);

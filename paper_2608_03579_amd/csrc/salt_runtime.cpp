@@ -148,6 +148,8 @@ struct salt_ctx {
   char* pool = nullptr;
   size_t slot_stride = 0;
   char* zeros = nullptr;                 // zero page of max(in, out) * esize bytes, never written after set-up
+  char* gram = nullptr;                  // salt_adapter_gram's device scratch, grown on demand
+  size_t gram_bytes = 0;
   hipStream_t side = nullptr;
   // bookkeeping
   std::vector<int32_t> slot_rank;        // -1 = never loaded
@@ -290,6 +292,7 @@ void destroy_ctx_memory(salt_ctx* c) {
     if (p) (void)hipFree(p);
   if (c->pool) (void)hipFree(c->pool);
   if (c->zeros) (void)hipFree(c->zeros);
+  if (c->gram) (void)hipFree(c->gram);
   for (hipEvent_t e : c->readers.ev)
     if (e) (void)hipEventDestroy(e);
   for (hipEvent_t e : c->loaders.ev)
@@ -1108,31 +1111,32 @@ salt_status salt_adapter_gram(salt_ctx* ctx, const void* blob1, int32_t r1, cons
   a.g_22 = p2 * p2;
   a.g_side = (size_t)a.g_12 + a.g_11 + a.g_22;
   a.g_table = 2 * a.g_side;
-  const size_t g_bytes = sizeof(float) * a.g_table * nt;
-  void* tabs_d = nullptr;
-  void* g_d = nullptr;
-  void* out_d = nullptr;
-  auto release = [&]() {
-    if (tabs_d) (void)hipFree(tabs_d);
-    if (g_d) (void)hipFree(g_d);
-    if (out_d) (void)hipFree(out_d);
-  };
-  if (hipMalloc(&tabs_d, sizeof(salt::GramTable) * nt) != hipSuccess || hipMalloc(&g_d, g_bytes) != hipSuccess ||
-      hipMalloc(&out_d, sizeof(double) * 3 * nt) != hipSuccess) {
-    (void)hipGetLastError();
-    release();
-    return fail(ctx, SALT_ERR_OUT_OF_MEMORY, "adapter Gram scratch (%zu bytes)", g_bytes);
+  // one scratch buffer per context: table records, then the Grams, then the
+  // results (each region 256-byte aligned); it grows to the largest call so far
+  auto up = [](size_t n) { return (n + 255) / 256 * 256; };
+  const size_t tabs_bytes = up(sizeof(salt::GramTable) * nt), g_bytes = up(sizeof(float) * a.g_table * nt);
+  const size_t need = tabs_bytes + g_bytes + sizeof(double) * 3 * nt;
+  if (need > ctx->gram_bytes) {
+    // (the previous buffer is idle: every earlier call synchronised its stream)
+    if (ctx->gram) (void)hipFree(ctx->gram);
+    ctx->gram = nullptr;
+    ctx->gram_bytes = 0;
+    if (hipMalloc((void**)&ctx->gram, need) != hipSuccess) {
+      (void)hipGetLastError();
+      ctx->gram = nullptr;
+      return fail(ctx, SALT_ERR_OUT_OF_MEMORY, "adapter Gram scratch (%zu bytes)", need);
+    }
+    ctx->gram_bytes = need;
   }
-  a.tabs = static_cast<const salt::GramTable*>(tabs_d);
-  a.g = static_cast<float*>(g_d);
-  a.out = static_cast<double*>(out_d);
-  hipError_t e = hipMemcpyAsync(tabs_d, tabs.data(), sizeof(salt::GramTable) * nt, hipMemcpyHostToDevice, s);
-  if (e == hipSuccess) e = hipMemsetAsync(g_d, 0, g_bytes, s);
-  if (e == hipSuccess) e = salt::launch_gram(a, max_in, max_out, ctx->cfg.dtype == SALT_BF16, s);
-  if (e == hipSuccess) e = hipMemcpyAsync(out, out_d, sizeof(double) * 3 * nt, hipMemcpyDeviceToHost, s);
-  if (e == hipSuccess) e = hipStreamSynchronize(s);
-  release();
-  SALT_HIP(ctx, e);
+  char* tabs_d = ctx->gram;
+  a.tabs = reinterpret_cast<const salt::GramTable*>(tabs_d);
+  a.g = reinterpret_cast<float*>(tabs_d + tabs_bytes);
+  a.out = reinterpret_cast<double*>(tabs_d + tabs_bytes + g_bytes);
+  SALT_HIP(ctx, hipMemcpyAsync(tabs_d, tabs.data(), sizeof(salt::GramTable) * nt, hipMemcpyHostToDevice, s));
+  SALT_HIP(ctx, hipMemsetAsync(a.g, 0, sizeof(float) * a.g_table * nt, s));
+  SALT_HIP(ctx, salt::launch_gram(a, max_in, max_out, ctx->cfg.dtype == SALT_BF16, s));
+  SALT_HIP(ctx, hipMemcpyAsync(out, a.out, sizeof(double) * 3 * nt, hipMemcpyDeviceToHost, s));
+  SALT_HIP(ctx, hipStreamSynchronize(s));
   return SALT_OK;
 }
 

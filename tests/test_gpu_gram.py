@@ -127,6 +127,25 @@ def test_gram_integer_factors_bit_exact():
         ctx.close()
 
 
+def test_gram_scratch_grown_and_reused():
+    """Calls on one context: ranks 4 / 6, then 48 / 64 (the context's scratch
+    grows), then 4 / 6 again (it is reused); each result against the oracle."""
+    _announce("adapter gram: one context, scratch grown and reused")
+    tables = [("a", 520, 776), ("b", 3072, 1024)]
+    runs = [_workload(tables, [4, 2], "bf16"), _workload(tables, [48, 16], "bf16"), _workload(tables, [4, 2], "bf16")]
+    ctx = _ctx(runs[0])
+    try:
+        for w, (r1, extra) in zip(runs, ((4, 2), (48, 16), (4, 2))):
+            b1, r1_, b2, r2 = _related(w, r1, extra)
+            d1, d2 = to_dev(b1), to_dev(b2)
+            try:
+                _check(w, b1, r1_, b2, r2, ctx.adapter_gram(d1.ptr, r1_, d2.ptr, r2))
+            finally:
+                d1.free(); d2.free()
+    finally:
+        ctx.close()
+
+
 def test_gram_errors():
     _announce("adapter gram error paths")
     from paper_2608_03579_amd import salt
