@@ -639,7 +639,7 @@ def main():
                     help="also run a device-to-device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only: this build has no cross-GPU path (asked for --gpus {args.gpus})",
+        print(f"bench.py runs on one GPU only: libsalt has no cross-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
         sys.exit(2)
     spec = WORKLOADS[args.workload]

@@ -29,9 +29,10 @@ Sec. 3.3 also lets a node fold one scaled centroid into its base weight at
 start-up (``fuse_centroid``: ``W_base + gamma * A_c B_c``) and then add only the
 residual per request.
 
-Readings where the paper is silent are listed in the design doc (orientation of A/B,
-gamma scaling only the centroid, the canonical segment order, -1 meaning "term
-absent").
+Where the paper is silent this oracle reads it as follows: A is in x r and B is
+r x out for row vectors (y += x A B); gamma scales only the centroid term; the
+segment order is (centroid, slot, token) ascending with -1 first; an id of -1
+means the term is absent.
 """
 from __future__ import annotations
 

@@ -10,7 +10,7 @@ import numpy as np
 import oracle
 from paper_2608_03579_amd import synth
 
-TOL_NORTH_STAR = 1e-2      # |y - ref| <= 1e-2 * (1 + |ref|) for bf16 outputs
+TOL_BF16 = 1e-2      # |y - ref| <= 1e-2 * (1 + |ref|) for bf16 outputs
 TOL_F32 = 1e-5             # fp32 Tiny config: fp32 accumulation of K <= 256 terms
 
 

@@ -9,7 +9,7 @@ import pytest
 
 import oracle
 from paper_2608_03579_amd import synth
-from tests.gpu_harness import TOL_NORTH_STAR, close_enough
+from tests.gpu_harness import TOL_BF16, close_enough
 
 
 def to_bf16_values(a):
@@ -37,7 +37,7 @@ def test_gate_rejects_planted_mistakes(cfg, kw):
     t = 0
     rows = list(range(min(w.T, 48)))
     ref = outputs(w, t, w.tok_c, w.tok_u, w.gamma, rows=rows)
-    assert close_enough(to_bf16_values(ref), ref, TOL_NORTH_STAR)[0]
+    assert close_enough(to_bf16_values(ref), ref, TOL_BF16)[0]
     C, S = w.n_centroids, w.n_slots
     mutants = {
         "y unchanged": oracle.decode(w.y0(t), w.dtype)[rows],
@@ -56,7 +56,7 @@ def test_gate_rejects_planted_mistakes(cfg, kw):
     if w.gamma is not None:
         mutants["gamma ignored"] = outputs(w, t, w.tok_c, w.tok_u, None, rows=rows)
     for name, m in mutants.items():
-        passed, worst, nbad = close_enough(to_bf16_values(m), ref, TOL_NORTH_STAR)
+        passed, worst, nbad = close_enough(to_bf16_values(m), ref, TOL_BF16)
         assert not passed, f"cfg {cfg}: the gate accepts '{name}' (worst {worst:.2f}x)"
 
 

@@ -8,7 +8,7 @@ import pytest
 
 import oracle
 from paper_2608_03579_amd import synth
-from tests.gpu_harness import TOL_F32, TOL_NORTH_STAR, Run, close_enough
+from tests.gpu_harness import TOL_F32, TOL_BF16, Run, close_enough
 
 pytestmark = pytest.mark.gpu
 
@@ -18,7 +18,7 @@ def _announce(name):
 
 
 def _tol(w):
-    return TOL_F32 if w.dtype == "f32" else TOL_NORTH_STAR
+    return TOL_F32 if w.dtype == "f32" else TOL_BF16
 
 
 def _check(run, table=0, rows=None):
@@ -78,7 +78,7 @@ def test_ragged_and_degenerate_batches():
             if k % 2 == 1:
                 _plan_matches(run)
             ref = run.oracle_table(0, rows=list(range(T)))
-            assert close_enough(got, ref, TOL_NORTH_STAR)[0], T
+            assert close_enough(got, ref, TOL_BF16)[0], T
             # rows past T are untouched
             assert np.array_equal(run.apply(0)[T:], w.y0(0)[T:])
         # one centroid for everyone: a group spanning several tiles
@@ -131,7 +131,7 @@ def test_repeated_applies_and_rebuilds():
         one = run.oracle_table(0) - oracle.decode(w.y0(0), w.dtype)
         ref = oracle.decode(w.y0(0), w.dtype) + 40 * one
         # 40 bf16 roundings of the running y: allow 40x the per-step bound
-        assert np.all(np.abs(got - ref) <= 40 * TOL_NORTH_STAR * (1 + np.abs(ref)))
+        assert np.all(np.abs(got - ref) <= 40 * TOL_BF16 * (1 + np.abs(ref)))
         for seed in (8, 9):
             w2 = synth.make(2, seed)
             run.set_and_build(w2.tok_c, w2.tok_u)
@@ -217,9 +217,9 @@ def test_swap_is_ordered_after_inflight_apply():
         for s in swapped:
             run.gen[s] = 0
         ref1 = run.oracle_table(t)
-        assert close_enough(got1, ref1, TOL_NORTH_STAR)[0]
-        assert close_enough(got2, ref2, TOL_NORTH_STAR)[0]
-        assert not close_enough(got1, ref2, TOL_NORTH_STAR)[0]
+        assert close_enough(got1, ref1, TOL_BF16)[0]
+        assert close_enough(got2, ref2, TOL_BF16)[0]
+        assert not close_enough(got1, ref2, TOL_BF16)[0]
     finally:
         run.close()
 
@@ -253,7 +253,7 @@ def test_swap_waits_for_applies_of_replaced_maps_and_other_streams():
         for s in swapped:
             run.gen[s] = 0
         ref1 = run.oracle_table(t)
-        assert close_enough(got1, ref1, TOL_NORTH_STAR)[0], "swap overtook an apply of the replaced maps"
+        assert close_enough(got1, ref1, TOL_BF16)[0], "swap overtook an apply of the replaced maps"
         # (2) the plan applied on a second stream, then the swap back to generation 0
         run.plan.set_maps(w.tok_c, w.tok_u, w.gamma, run.stream)
         run.plan.build(run.stream)
@@ -273,8 +273,8 @@ def test_swap_waits_for_applies_of_replaced_maps_and_other_streams():
         for s in swapped:
             run.gen[s] = 1                           # what both applies read (run.load set 0)
         ref_gen1 = run.oracle_table(t)
-        assert close_enough(oracle.decode(y2.to_host(), w.dtype), ref_gen1, TOL_NORTH_STAR)[0]
-        assert close_enough(oracle.decode(y3.to_host(), w.dtype), ref_gen1, TOL_NORTH_STAR)[0]
+        assert close_enough(oracle.decode(y2.to_host(), w.dtype), ref_gen1, TOL_BF16)[0]
+        assert close_enough(oracle.decode(y3.to_host(), w.dtype), ref_gen1, TOL_BF16)[0]
         other.destroy()
     finally:
         run.close()
@@ -352,7 +352,7 @@ def test_repeated_applies_are_bit_identical():
             for t, y in zip(tables, first):
                 alone = run.apply(t)
                 assert np.array_equal(alone, run.apply(t))
-                assert close_enough(oracle.decode(alone, w.dtype), oracle.decode(y, w.dtype), TOL_NORTH_STAR)[0]
+                assert close_enough(oracle.decode(alone, w.dtype), oracle.decode(y, w.dtype), TOL_BF16)[0]
         finally:
             run.close()
 
@@ -376,14 +376,14 @@ def test_plan_used_across_streams():
             run.ctx.apply(4, run.plan, xd.ptr, yd.ptr, s2.h)
             s2.synchronize()
             got = oracle.decode(yd.to_host(), w.dtype)
-            assert close_enough(got, run.oracle_table(4), TOL_NORTH_STAR)[0], rep
+            assert close_enough(got, run.oracle_table(4), TOL_BF16)[0], rep
         # and the other way round: build on stream 2, apply on stream 1
         run.plan.set_maps(w.tok_c, w.tok_u, w.gamma, s2.h)
         run.plan.build(s2.h)
         yd.upload(w.y0(4))
         run.ctx.apply(4, run.plan, xd.ptr, yd.ptr, run.stream)
         run._stream.synchronize()
-        assert close_enough(oracle.decode(yd.to_host(), w.dtype), run.oracle_table(4), TOL_NORTH_STAR)[0]
+        assert close_enough(oracle.decode(yd.to_host(), w.dtype), run.oracle_table(4), TOL_BF16)[0]
         _plan_matches(run)
         s2.destroy()
     finally:
@@ -406,7 +406,7 @@ def test_apply_map_one_shot():
             got = oracle.decode(yd.to_host(), w.dtype)
             run.maps = (w.tok_c[:T], w.tok_u[:T], None)
             ref = run.oracle_table(0, rows=list(range(T)))
-            assert close_enough(got[:T], ref, TOL_NORTH_STAR)[0], T
+            assert close_enough(got[:T], ref, TOL_BF16)[0], T
             assert np.array_equal(yd.to_host()[T:], w.y0(0)[T:])
         assert run.ctx.apply_map_status(1, w.tok_c, w.tok_u, None, xd.ptr, yd.ptr, run.stream) == \
             salt.ERR_OUT_OF_RANGE
@@ -448,10 +448,10 @@ def test_batched_swaps():
         run._stream.synchronize()
         run.ctx.wait_loads()
         ref_new = run.oracle_table(t)
-        assert close_enough(oracle.decode(y2.to_host(), w.dtype), ref_new, TOL_NORTH_STAR)[0]
+        assert close_enough(oracle.decode(y2.to_host(), w.dtype), ref_new, TOL_BF16)[0]
         for s in swapped:
             run.gen[s] = 0
-        assert close_enough(oracle.decode(y1.to_host(), w.dtype), run.oracle_table(t), TOL_NORTH_STAR)[0]
+        assert close_enough(oracle.decode(y1.to_host(), w.dtype), run.oracle_table(t), TOL_BF16)[0]
         for b in bufs:
             b.free()
     finally:
@@ -488,7 +488,7 @@ def test_swap_paths_many_blobs_and_a_repeated_slot():
             run.ctx.apply(t, run.plan, xd.ptr, y.ptr, run.stream)
             run._stream.synchronize()
             run.ctx.wait_loads()
-            ok, worst, nbad = close_enough(oracle.decode(y.to_host(), w.dtype), run.oracle_table(t), TOL_NORTH_STAR)
+            ok, worst, nbad = close_enough(oracle.decode(y.to_host(), w.dtype), run.oracle_table(t), TOL_BF16)
             assert ok, f"{nbad} out of tolerance, worst {worst:.3f}x"
 
         check()

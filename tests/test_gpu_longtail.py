@@ -15,7 +15,7 @@ import pytest
 
 import oracle
 from paper_2608_03579_amd import synth
-from tests.gpu_harness import TOL_F32, TOL_NORTH_STAR, Run, close_enough
+from tests.gpu_harness import TOL_F32, TOL_BF16, Run, close_enough
 
 pytestmark = pytest.mark.gpu
 
@@ -72,7 +72,7 @@ def _both_ways(run, n_reg, n_tail):
         x = w.x(t)[np.concatenate([np.arange(n_tail), np.arange(n_tail)])]
         y0 = w.y0(t)[np.concatenate([np.arange(n_tail), np.arange(n_tail)])]
         got = oracle.decode(run.apply(t, x=x, y0=y0), w.dtype)
-        ok, worst, nbad = close_enough(got[n_tail:], got[:n_tail], TOL_NORTH_STAR if w.dtype == "bf16" else TOL_F32)
+        ok, worst, nbad = close_enough(got[n_tail:], got[:n_tail], TOL_BF16 if w.dtype == "bf16" else TOL_F32)
         assert ok, f"table {t}: concatenated twin differs ({nbad}, worst {worst:.3f}x)"
         assert T == got.shape[0]
 
@@ -94,7 +94,7 @@ def test_long_tail_mixed_batch(seed, tables, C, r_c, T, n_reg, n_tail, dtype):
     run = Run(w)
     try:
         run.set_and_build()
-        _check(run, TOL_NORTH_STAR if dtype == "bf16" else TOL_F32)
+        _check(run, TOL_BF16 if dtype == "bf16" else TOL_F32)
         _both_ways(run, n_reg, n_tail)
     finally:
         run.close()

@@ -12,13 +12,13 @@ import pytest
 
 import oracle
 from paper_2608_03579_amd import synth
-from tests.gpu_harness import TOL_F32, TOL_NORTH_STAR, Run, close_enough
+from tests.gpu_harness import TOL_F32, TOL_BF16, Run, close_enough
 
 pytestmark = pytest.mark.gpu
 
 
 def _tol(w):
-    return TOL_F32 if w.dtype == "f32" else TOL_NORTH_STAR
+    return TOL_F32 if w.dtype == "f32" else TOL_BF16
 
 
 def _check_plan(run):

@@ -12,7 +12,7 @@ import pytest
 
 import oracle
 from paper_2608_03579_amd import synth
-from tests.gpu_harness import TOL_F32, TOL_NORTH_STAR, Run, close_enough
+from tests.gpu_harness import TOL_F32, TOL_BF16, Run, close_enough
 
 pytestmark = pytest.mark.gpu
 
@@ -56,7 +56,7 @@ def _run_all(w, want_m=None, exact=False):
             if exact:
                 assert np.array_equal(got, ref), f"table {t}: {np.sum(got != ref)} exact mismatches"
             else:
-                ok, worst, nbad = close_enough(got, ref, TOL_F32 if w.dtype == "f32" else TOL_NORTH_STAR)
+                ok, worst, nbad = close_enough(got, ref, TOL_F32 if w.dtype == "f32" else TOL_BF16)
                 assert ok, f"table {t}: {nbad} out of tolerance, worst {worst:.3f}x"
     finally:
         run.close()
