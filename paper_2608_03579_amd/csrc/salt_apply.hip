@@ -647,17 +647,32 @@ __device__ __forceinline__ void expand_segment(const ApplyLaunch& a, const Expan
             for (int e = 0; e < 8; ++e) yf[8 * h + e] = fmaf(vu[j8 + jj], b[e], yf[8 * h + e]);
           }
       }
-      if (long_tail && tr.res && tr.r > RU) {
-        for (int rho = RU; rho < tr.r; ++rho) {
-          const float vr = vrow[a.r_c + rho];
-          const char* base = bu_wide + rho * rs;
+      if (long_tail) {
+        // ranks past the first chunk (their v from s_v), eight rows at a time up
+        // to the batch's largest rank, so that eight rows' loads are in flight
+        // together; a lane past its own rank reads the zero page with a zero v
+        for (int r8 = RU; r8 < a.r_u; r8 += 8) {
+          Vec bv[8][2];
+          float vr[8];
 #pragma unroll
-          for (int h = 0; h < 2; ++h) {
-            float b[8];
-            O::to_f32(O::load(reinterpret_cast<const E*>(base + imin(cl + kPiece * h, olast) * ES)), b);
+          for (int jj = 0; jj < 8; ++jj) {
+            const int rho = r8 + jj;
+            const bool ok = tr.res && rho < tr.r;
+            const char* base = ok ? bu_wide + rho * rs : a.zeros;
+            vr[jj] = ok ? vrow[a.r_c + rho] : 0.f;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) yf[8 * h + e] = fmaf(vr, b[e], yf[8 * h + e]);
+            for (int h = 0; h < 2; ++h)
+              bv[jj][h] = O::load(reinterpret_cast<const E*>(base + imin(cl + kPiece * h, olast) * ES));
           }
+#pragma unroll
+          for (int jj = 0; jj < 8; ++jj)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              float b[8];
+              O::to_f32(bv[jj][h], b);
+#pragma unroll
+              for (int e = 0; e < 8; ++e) yf[8 * h + e] = fmaf(vr[jj], b[e], yf[8 * h + e]);
+            }
         }
       }
     }
