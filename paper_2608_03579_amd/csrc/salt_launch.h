@@ -4,6 +4,7 @@
 // same code.
 #pragma once
 
+#include <stddef.h>
 #include <stdint.h>
 
 #include <algorithm>
@@ -55,6 +56,18 @@ inline void cut_tiles(const std::vector<int>& per_c, int M, std::vector<int4>& t
     }
     start += n;
   }
+}
+
+// Split-K partial floats a plan of up to T tokens holds (rows of R floats): two
+// K ranges per token row for a full launch of kMaxJobs tables, or one if that
+// would pass 256 MiB; small batches get up to 16 Mi floats (64 MiB, at most 64
+// ranges per table), so that a decode launch can split K finely enough to fill
+// the device.
+inline size_t plan_partial_cap(size_t T, size_t R) {
+  const size_t two = 2 * (size_t)kMaxJobs * T * R;
+  const size_t small = std::min((size_t)16 << 20, 64 * (size_t)kMaxJobs * T * R);
+  if (two < small) return small;
+  return two * 4 <= ((size_t)256 << 20) ? two : (size_t)kMaxJobs * T * R;
 }
 
 // Largest number of tiles a batch of T tokens over C centroids can cut into.

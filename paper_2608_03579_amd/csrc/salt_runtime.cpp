@@ -300,13 +300,6 @@ void destroy_ctx_memory(salt_ctx* c) {
   if (c->side) (void)hipStreamDestroy(c->side);
 }
 
-// Partial capacity of a plan: two K ranges per token row for a full launch of
-// kMaxJobs tables, or one if that would pass 256 MiB.
-size_t plan_partial_cap(size_t T, size_t R) {
-  const size_t two = 2 * (size_t)salt::kMaxJobs * T * R;
-  return two * 4 <= ((size_t)256 << 20) ? two : (size_t)salt::kMaxJobs * T * R;
-}
-
 salt_status plan_create(salt_ctx* ctx, salt_plan** out) {
   salt_plan* p = new (std::nothrow) salt_plan();
   if (!p) return fail(ctx, SALT_ERR_OUT_OF_MEMORY, "plan");
@@ -314,7 +307,7 @@ salt_status plan_create(salt_ctx* ctx, salt_plan** out) {
   const size_t R = salt::padded_rank(ctx->cfg.r_c, ctx->cfg.r_u_max);
   p->max_T = (int32_t)T;
   p->tile_cap = salt::max_tiles((int)T, ctx->cfg.n_centroids);
-  p->partial_cap = plan_partial_cap(T, R);
+  p->partial_cap = salt::plan_partial_cap(T, R);
   const size_t staged = T + 2 * (size_t)p->tile_cap;
   bool ok = hipMalloc((void**)&p->staged_dev, staged * sizeof(int4)) == hipSuccess &&
             hipMalloc((void**)&p->keys, 2 * T * sizeof(uint64_t)) == hipSuccess &&
