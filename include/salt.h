@@ -167,7 +167,9 @@ SALT_API void salt_host_free(void* p);
  * requests by their centroid): tokens ordered by (centroid id, residual slot,
  * token index) ascending, -1 first.  Built once per batch on the device, then
  * reused by every table's apply.  A plan owns device buffers sized for
- * max_tokens, including the apply's scratch (split-K partials): the work of one
+ * max_tokens, including the apply's scratch (split-K partials: two K ranges per
+ * token row of a 16-table launch, or up to 64 MiB for small batches so that
+ * their launches can split K finely enough to fill the device): the work of one
  * plan is ordered by the library, also across streams (a call on a stream other
  * than the one of the plan's last work first waits for that work), so several
  * streams that run concurrently need one plan each.
@@ -241,7 +243,8 @@ SALT_API salt_status salt_apply_batch(salt_ctx* ctx, int32_t n, const int32_t* t
  * salt_create) instead of the plan's buffer, whose capacity still bounds the
  * K split.  The call allocates nothing and calls no allocating routine.
  * Whenever the plan's partial capacity (two K ranges per token row of a
- * 16-table launch; max_tokens x padded(r_c + r_u) <= 512 Ki) fits the array,
+ * 16-table launch, raised to up to 16 Mi floats for small batches; it fits the
+ * array when max_tokens x padded(r_c + r_u) <= 512 Ki) fits the array,
  * the launches are exactly those of salt_apply_batch and y is bit-identical;
  * beyond that a launch may split K more coarsely (same accuracy bound).  The
  * array is shared by every salt_apply_batch_noalloc on the device: calls whose
