@@ -49,7 +49,9 @@ __device__ __forceinline__ void write_place(const PlanLaunch& a, int p, uint64_t
   write_record(a, p, k, m.z, m.w);
 }
 
-// Exclusive block-wide prefix of two counts (1024 threads); totals to all.
+// Exclusive block-wide prefix of two counts (NT threads, at most 16 waves);
+// totals to all.
+template <int NT>
 __device__ __forceinline__ void block_scan2(int c0, int c1, int& e0, int& e1, int& t0, int& t1, int* s_w) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   int i0 = c0, i1 = c1;
@@ -68,7 +70,7 @@ __device__ __forceinline__ void block_scan2(int c0, int c1, int& e0, int& e1, in
   __syncthreads();
   if (threadIdx.x == 0) {
     int r0 = 0, r1 = 0;
-    for (int w = 0; w < kPlanThreads / 64; ++w) {
+    for (int w = 0; w < NT / 64; ++w) {
       const int v0 = s_w[w], v1 = s_w[32 + w];
       s_w[w] = r0;
       s_w[32 + w] = r1;
@@ -87,11 +89,12 @@ __device__ __forceinline__ void block_scan2(int c0, int c1, int& e0, int& e1, in
 }
 
 // Segments and groups of the sorted keys keys[0, T) (LDS or global memory),
-// the meta words, and the check of the host's tiles.  One block of 1024 threads;
+// the meta words, and the check of the host's tiles.  One block of NT threads;
 // thread i takes places [i per, (i + 1) per).
+template <int NT>
 __device__ void plan_finish(const PlanLaunch& a, const uint64_t* keys, int* s_w) {
   const int T = a.T, tid = threadIdx.x;
-  const int per = cdiv(T, kPlanThreads);
+  const int per = cdiv(T, NT);
   const int p0 = imin(T, tid * per), p1 = imin(T, p0 + per);
   auto seg_start = [&](int p) { return p == 0 || (keys[p] >> 21) != (keys[p - 1] >> 21); };
   auto grp_start = [&](int p) { return p == 0 || (keys[p] >> 42) != (keys[p - 1] >> 42); };
@@ -101,7 +104,7 @@ __device__ void plan_finish(const PlanLaunch& a, const uint64_t* keys, int* s_w)
     ng += grp_start(p);
   }
   int es, eg, n_seg, n_grp;
-  block_scan2(ns, ng, es, eg, n_seg, n_grp, s_w);
+  block_scan2<NT>(ns, ng, es, eg, n_seg, n_grp, s_w);
   for (int p = p0; p < p1; ++p) {
     const uint64_t k = keys[p];
     if (grp_start(p)) {
@@ -120,7 +123,7 @@ __device__ void plan_finish(const PlanLaunch& a, const uint64_t* keys, int* s_w)
   // and each tile holds tokens of its own centroid only, which for sorted keys
   // (centroid first) holds exactly when its first and last keys carry it
   int bad = 0;
-  for (int tau = tid; tau < a.n_tiles; tau += kPlanThreads) {
+  for (int tau = tid; tau < a.n_tiles; tau += NT) {
     const int4 h = a.tiles[tau];
     const int i0 = iclamp(h.x, 0, T - 1), n = iclamp(h.y, 0, T - i0);
     const bool first = tau == 0 || tau == a.n_list0, last = tau == a.n_tiles - 1 || tau == a.n_list0 - 1;
@@ -144,8 +147,6 @@ __device__ void plan_finish(const PlanLaunch& a, const uint64_t* keys, int* s_w)
   }
 }
 
-// Keys a thread of k_plan_sort holds at most: places tid + kPlanThreads e.
-constexpr int kKeysPerThread = kSortChunk / kPlanThreads;
 static_assert(kSortChunk % kPlanThreads == 0, "a sort chunk is whole keys per thread");
 
 // One compare-exchange step of the bitonic network (merge size k, distance j <
@@ -158,29 +159,35 @@ __device__ __forceinline__ uint64_t exchange_in_wave(uint64_t x, int p, int j, i
   return keep_min == (x < y) ? x : y;
 }
 
-__global__ void __launch_bounds__(kPlanThreads) k_plan_sort(const PlanLaunch a) {
-  __shared__ uint64_t s_keys[kSortChunk];
-  __shared__ int s_gb[kSortChunk];                   // gamma bits and rank of the chunk's tokens,
-  __shared__ uint8_t s_r[kSortChunk];                // for the records of a one-chunk batch
+// One block of NT threads per chunk of at most NC = NT * KPT keys: NT = 1024
+// for batches of more than 512 tokens (KPT = 4, a chunk of kSortChunk keys),
+// otherwise the smallest of 64, 256 or 512 threads that holds the batch (KPT = 1).
+template <int NT>
+__global__ void __launch_bounds__(NT) k_plan_sort(const PlanLaunch a) {
+  constexpr int KPT = NT == kPlanThreads ? kSortChunk / kPlanThreads : 1;   // keys per thread, at most
+  constexpr int NC = NT * KPT;
+  __shared__ uint64_t s_keys[NC];
+  __shared__ int s_gb[NC];                   // gamma bits and rank of the chunk's tokens,
+  __shared__ uint8_t s_r[NC];                // for the records of a one-chunk batch
   __shared__ int s_w[64];
   const int tid = threadIdx.x;
-  const int base = blockIdx.x * kSortChunk;
-  const int cnt = imin(kSortChunk, a.T - base);
+  const int base = blockIdx.x * NC;
+  const int cnt = imin(NC, a.T - base);
   if (tid == 0 && blockIdx.x == 0) a.meta[kMetaErr] = 0;
   // the network spans the smallest power of two >= cnt (padding keys sort last)
   int n2 = 2;
   while (n2 < cnt) n2 <<= 1;
-  // Bitonic sort, ascending.  Thread tid holds the places tid + kPlanThreads e,
+  // Bitonic sort, ascending.  Thread tid holds the places tid + NT e,
   // e < ne; steps whose partners lie within a wave (distance j < 64) run on
   // registers through lane shuffles, in the waves that hold places; steps of a
   // larger distance run in LDS, one pair per thread, with a block barrier after
   // each.  (All loop bounds and the wave test are uniform over a wave.)
-  const int ne = imax(1, n2 / kPlanThreads);
+  const int ne = imax(1, n2 / NT);
   const bool holds = (tid & ~63) < n2;
-  uint64_t r[kKeysPerThread];
+  uint64_t r[KPT];
 #pragma unroll
-  for (int e = 0; e < kKeysPerThread; ++e) {
-    const int p = tid + kPlanThreads * e;
+  for (int e = 0; e < KPT; ++e) {
+    const int p = tid + NT * e;
     r[e] = kPad;
     if (e < ne && p < cnt) {
       const int4 m = a.maps[base + p];
@@ -192,11 +199,11 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_sort(const PlanLaunch a) 
   for (int k = 2; k <= n2; k <<= 1) {
     if (k / 2 >= 64) {
 #pragma unroll
-      for (int e = 0; e < kKeysPerThread; ++e)
-        if (e < ne && tid + kPlanThreads * e < n2) s_keys[tid + kPlanThreads * e] = r[e];
+      for (int e = 0; e < KPT; ++e)
+        if (e < ne && tid + NT * e < n2) s_keys[tid + NT * e] = r[e];
       __syncthreads();
       for (int j = k >> 1; j >= 64; j >>= 1) {
-        for (int i = tid; i < n2 / 2; i += kPlanThreads) {
+        for (int i = tid; i < n2 / 2; i += NT) {
           const int lo = ((i & ~(j - 1)) << 1) | (i & (j - 1)), hi = lo + j;
           const uint64_t x = s_keys[lo], y = s_keys[hi];
           if ((x > y) == ((lo & k) == 0)) {
@@ -207,33 +214,33 @@ __global__ void __launch_bounds__(kPlanThreads) k_plan_sort(const PlanLaunch a) 
         __syncthreads();
       }
 #pragma unroll
-      for (int e = 0; e < kKeysPerThread; ++e)
-        if (e < ne && tid + kPlanThreads * e < n2) r[e] = s_keys[tid + kPlanThreads * e];
+      for (int e = 0; e < KPT; ++e)
+        if (e < ne && tid + NT * e < n2) r[e] = s_keys[tid + NT * e];
     }
     if (holds) {
       for (int j = imin(k >> 1, 32); j > 0; j >>= 1) {
 #pragma unroll
-        for (int e = 0; e < kKeysPerThread; ++e)
-          if (e < ne) r[e] = exchange_in_wave(r[e], tid + kPlanThreads * e, j, k);
+        for (int e = 0; e < KPT; ++e)
+          if (e < ne) r[e] = exchange_in_wave(r[e], tid + NT * e, j, k);
       }
     }
   }
   if (gridDim.x == 1) {
     // (a thread writes the places it alone read last)
 #pragma unroll
-    for (int e = 0; e < kKeysPerThread; ++e)
-      if (e < ne && tid + kPlanThreads * e < n2) s_keys[tid + kPlanThreads * e] = r[e];
+    for (int e = 0; e < KPT; ++e)
+      if (e < ne && tid + NT * e < n2) s_keys[tid + NT * e] = r[e];
     __syncthreads();
-    for (int i = tid; i < cnt; i += kPlanThreads) {
+    for (int i = tid; i < cnt; i += NT) {
       const uint64_t k = s_keys[i];
       const int t = iclamp(key_tok(k), 0, cnt - 1);   // (one chunk: base is 0)
       write_record(a, i, k, s_r[t], s_gb[t]);
     }
-    plan_finish(a, s_keys, s_w);
+    plan_finish<NT>(a, s_keys, s_w);
   } else {
 #pragma unroll
-    for (int e = 0; e < kKeysPerThread; ++e)
-      if (e < ne && tid + kPlanThreads * e < cnt) a.keys[base + tid + kPlanThreads * e] = r[e];
+    for (int e = 0; e < KPT; ++e)
+      if (e < ne && tid + NT * e < cnt) a.keys[base + tid + NT * e] = r[e];
   }
 }
 
@@ -267,7 +274,7 @@ __global__ void __launch_bounds__(256) k_plan_merge(const PlanLaunch a) {
 
 __global__ void __launch_bounds__(kPlanThreads) k_plan_finish(const PlanLaunch a) {
   __shared__ int s_w[64];
-  plan_finish(a, a.keys_sorted, s_w);
+  plan_finish<kPlanThreads>(a, a.keys_sorted, s_w);
 }
 
 }  // namespace
@@ -276,7 +283,10 @@ hipError_t launch_plan(const PlanLaunch& a, hipStream_t s) {
   if (a.T <= 0) return hipSuccess;
   if (a.T > kMaxTokens) return hipErrorInvalidValue;
   const int nch = cdiv(a.T, kSortChunk);
-  hipLaunchKernelGGL(k_plan_sort, dim3(nch), dim3(kPlanThreads), 0, s, a);
+  if (a.T <= 64) hipLaunchKernelGGL(k_plan_sort<64>, dim3(1), dim3(64), 0, s, a);
+  else if (a.T <= 256) hipLaunchKernelGGL(k_plan_sort<256>, dim3(1), dim3(256), 0, s, a);
+  else if (a.T <= 512) hipLaunchKernelGGL(k_plan_sort<512>, dim3(1), dim3(512), 0, s, a);
+  else hipLaunchKernelGGL(k_plan_sort<kPlanThreads>, dim3(nch), dim3(kPlanThreads), 0, s, a);
   if (nch > 1) {
     hipLaunchKernelGGL(k_plan_merge, dim3(cdiv(a.T, 256)), dim3(256), 0, s, a);
     hipLaunchKernelGGL(k_plan_finish, dim3(1), dim3(kPlanThreads), 0, s, a);
