@@ -40,7 +40,8 @@ namespace {
 // shared shapes
 // ---------------------------------------------------------------------------
 // M tokens per tile = TB token blocks of 16.  A block has waves_of(M) waves:
-// four for tiles of up to 64 tokens, one per token block beyond.  They split as
+// four for tiles of up to 32 tokens, eight for 64, one per token block beyond
+// (waves_of in salt_layout.h).  They split as
 // (token block, K quarter) in the shrink and (token block, column phase) in the
 // expand: KW = CW = waves / TB.  With TB > 1 (32-, 64- and 128-token tiles,
 // bf16) several waves need the same centroid operand at the same time (A_c in

@@ -103,11 +103,31 @@ inline bool configure_launch(ApplyLaunch& a, int n_cu, int n_groups_c, int64_t s
     s_cap[j] = std::max(1, std::min(s_traffic, cdiv(jb.in, gran)));
     S[j] = std::max(1, std::min(cdiv(jb.in, kc_target), s_cap[j]));
   }
-  // Shrink tiles of 64 tokens (long groups, many tokens): each block is long,
-  // so a round of the device that is only partly filled costs real time.  The
-  // K-range length is then the one that minimises (rounds of blocks) x (the
-  // longest range); ties go to the longer length (fewer partials).
+  // Shrink tiles of 64 tokens (long groups, many tokens).  If one K range as
+  // long as the smallest table's K already gives a round of the device's
+  // blocks, K is split no finer: tables with more K take ranges of about that
+  // length (blocks of equal length), and a finer split would only add partials
+  // for the expand to sum.  Otherwise each block is long, so a round of the
+  // device that is only partly filled costs real time: the K-range length is
+  // then the one that minimises (rounds of blocks) x (the longest range); ties
+  // go to the longer length (fewer partials).
+  bool fills = false;
   if (a.MS >= 64 && shrink_round > 0) {
+    int min_in = a.jobs[0].in;
+    for (int j = 1; j < a.n_jobs; ++j) min_in = std::min(min_in, a.jobs[j].in);
+    const int kc = cdiv(min_in, gran) * gran;
+    int64_t blocks = 0;
+    std::vector<int> Sm(a.n_jobs);
+    for (int j = 0; j < a.n_jobs; ++j) {
+      Sm[j] = std::max(1, std::min(cdiv(a.jobs[j].in, kc), s_cap[j]));
+      blocks += (int64_t)shrink_tiles(a) * a.nq * Sm[j];
+    }
+    if (blocks >= shrink_round) {
+      S = Sm;
+      fills = true;
+    }
+  }
+  if (a.MS >= 64 && shrink_round > 0 && !fills) {
     int max_in = 0;
     for (int j = 0; j < a.n_jobs; ++j) max_in = std::max(max_in, a.jobs[j].in);
     double best = 0.0;

@@ -27,7 +27,7 @@ struct int4 {
 namespace salt {
 
 // ---- fixed shapes -----------------------------------------------------------
-constexpr int kWaves = 4;            // waves of an apply block for tiles of up to 64 tokens
+constexpr int kWaves = 4;            // waves of an apply block for tiles of up to 32 tokens
 constexpr int kStepK = 64;           // k elements one wave takes per shrink step
 constexpr int kChunkCols = 64;       // output columns one wave takes per expand chunk
 constexpr int kMaxJobs = 16;         // tables one apply launch serves
@@ -44,9 +44,10 @@ SALT_HD int imax(int a, int b) { return a > b ? a : b; }
 SALT_HD int iclamp(int v, int lo, int hi) { return v < lo ? lo : (v > hi ? hi : v); }
 SALT_HD int cdiv(int a, int b) { return (a + b - 1) / b; }
 
-// Waves of an apply block for tiles of M tokens: four, or one per 16-token
-// block beyond 64 tokens.
-SALT_HD constexpr int waves_of(int M) { return M > 64 ? M / 16 : kWaves; }
+// Waves of an apply block for tiles of M tokens: four for up to 32 tokens,
+// eight for 64 (two per 16-token block: two K halves in the shrink, two column
+// phases in the expand), one per 16-token block beyond.
+SALT_HD constexpr int waves_of(int M) { return M > 64 ? M / 16 : (M == 64 ? 2 * kWaves : kWaves); }
 
 // Row stride of the split-K partials: r_c + r_u rounded up to whole float4s.
 SALT_HD int padded_rank(int r_c, int r_u) {
